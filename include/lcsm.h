@@ -1,0 +1,148 @@
+/*
+ * lcsm.h -- C ABI of the relaxed online long-convolution library for AMD
+ * MI355X (gfx950).
+ *
+ * Operation (Oncescu et al., "Flash Inference", arXiv 2410.12982):
+ * for every layer m < M, batch row b < B and channel d < D the library
+ * evaluates, online, the causal long convolution of Eq. (onlineConv)
+ *
+ *     z^m_t[b,d] = sum_{s=0}^{t} y^m_s[b,d] * h[m,d,t-s],   t = 0..L-1
+ *
+ * (0-indexed), where y^m_t is handed in at step t and z^m_t is returned at
+ * the same step, before y^m_{t+1} exists.  The work is tiled as in Alg. 1 /
+ * Alg. 3: at step t the diagonal term y_t h_0 completes z_t (the "red
+ * cell"); then, with i = t+1 and U the largest power of two dividing i, the
+ * contribution of y[i-U, i) to z[i, i+U) (the "gray tile", Eq. taus, lags
+ * 1..2U-1) is added for all layers in one batch.  Small tiles run as a direct
+ * Toeplitz product, large ones as a 2U-point cyclic FFT with filter spectra
+ * precomputed per tile size (Lemma 1, App. B).  When L is not a power of two
+ * the destination window is clipped at L.
+ *
+ * Conventions
+ *  - Every float pointer is a DEVICE pointer to fp32 data unless stated.
+ *  - Every call that touches the device is asynchronous on the stream given
+ *    to lcsm_init; buffers handed in must stay valid until the stream has
+ *    passed the call.
+ *  - Return values: LCSM_OK (0) or a negative LCSM_E* code.  No call throws
+ *    or aborts.  Arguments are validated before any device work is queued.
+ *  - A context is not thread safe; distinct contexts are independent.
+ */
+#ifndef LCSM_H
+#define LCSM_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Error codes. */
+#define LCSM_OK 0
+#define LCSM_EINVAL (-1)  /* bad argument: null pointer, size < 1 or too large */
+#define LCSM_ENOMEM (-2)  /* workspace too small, or the library's allocation failed */
+#define LCSM_EDEVICE (-3) /* a HIP runtime call or kernel launch failed; the context is faulted */
+#define LCSM_EDONE (-4)   /* all L positions have been emitted; nothing was queued */
+#define LCSM_ESTATE (-5)  /* call out of sequence, or the context is faulted (see lcsm_reset) */
+
+/* Tile kinds reported by lcsm_plan_tile. */
+#define LCSM_TILE_NONE 0    /* no gray tile after this step (t = L-1) */
+#define LCSM_TILE_DIRECT 1  /* direct Toeplitz kernel */
+#define LCSM_TILE_FFT 2     /* 2U-point FFT, one LDS-resident pass */
+#define LCSM_TILE_FFT_HBM 3 /* 2U-point FFT, multi-pass through HBM scratch */
+
+/* Tuning options.  A NULL pointer, or a field left at 0, selects the
+ * library default. */
+typedef struct lcsm_options {
+  int direct_max_u;  /* tiles with U <= direct_max_u use the direct kernel (power of two, >= 1) */
+  int lds_fft_max_n; /* FFT tiles with 2U <= lds_fft_max_n run in one LDS pass (power of two) */
+  int reserved[6];   /* must be zero */
+} lcsm_options;
+
+typedef struct lcsm_ctx lcsm_ctx;
+
+/* Device bytes of the workspace a context of this shape needs (state
+ * M*L*B*D fp32, filters M*L*D fp32, filter spectra of the FFT tile sizes, FFT
+ * scratch and a few small buffers).  Host only: touches no device.
+ * Errors: LCSM_EINVAL for sizes < 1, M*B*D >= 2^31, L >= 2^30 or bad options. */
+int lcsm_workspace_bytes(int M, int B, int D, int L, const lcsm_options* opt, size_t* bytes);
+
+/* Create a context (Alg. 3's state: all activations zero, position t = 0).
+ *   filters   device, [M][D][L] fp32: h[m,d,k] is the lag-k tap of layer m,
+ *             channel d (the filter rho^m of the paper, one per channel).
+ *             Copied (and re-laid out) during the call's stream work; the
+ *             caller may free it once the stream has passed lcsm_init.
+ *   stream    hipStream_t to queue all work on; NULL = the null stream.
+ *   workspace device buffer of at least lcsm_workspace_bytes bytes, 256-byte
+ *             aligned, owned by the caller and kept alive until
+ *             lcsm_destroy; NULL makes the library allocate (and free) it.
+ * Initialisation computes the filter spectra of every FFT tile size
+ * (App. B).  Errors: LCSM_EINVAL, LCSM_ENOMEM, LCSM_EDEVICE; *out is NULL
+ * on failure. */
+int lcsm_init(lcsm_ctx** out, const float* filters, int M, int B, int D, int L, void* stream,
+              void* workspace, size_t workspace_bytes, const lcsm_options* opt);
+
+/* One position for all layers (Alg. 3 with the layers' inputs given):
+ *   y_t  device [M][B][D]: the inputs y^m_t of every layer at position t.
+ *   z_t  device [M][B][D]: receives z^m_t = fmaf(h[m,d,0], y^m_t, acc^m_t),
+ *        where acc^m_t is the sum of all earlier contributions.
+ * Then queues the gray tiles of i = t+1 for all layers and advances t.
+ * y_t and z_t may not overlap each other or the workspace.
+ * Errors: LCSM_EDONE once t = L; LCSM_ESTATE after a fault or between
+ * lcsm_step_layer calls; LCSM_EINVAL for null pointers. */
+int lcsm_step(lcsm_ctx* ctx, const float* y_t, float* z_t);
+
+/* One position for all layers with the library's built-in elementwise chain
+ * standing in for the blocks and the sampler of Alg. 3:
+ *   y^0_0 = x^0_0,  y^0_t = 0.5 tanh(z^{M-1}_{t-1}) + x^0_t  (t >= 1),
+ *   y^m_t = 0.5 tanh(z^{m-1}_t) + x^m_t                      (m >= 1).
+ *   x_t  device [M][B][D] additive inputs;  z_t  device [M][B][D] outputs.
+ * The last layer's z_{t-1} is kept inside the context.  Same errors as
+ * lcsm_step. */
+int lcsm_step_chain(lcsm_ctx* ctx, const float* x_t, float* z_t);
+
+/* Red cell of one layer at the current position (the inner loop of Alg. 2 /
+ * Alg. 3, for callers that run their own block between layers):
+ *   y, z device [B][D].  Layers must be stepped in order 0..M-1, each once,
+ *   and then lcsm_advance called.  Errors: LCSM_ESTATE when out of order. */
+int lcsm_step_layer(lcsm_ctx* ctx, int layer, const float* y, float* z);
+
+/* Gray tiles of i = t+1 for all layers, after lcsm_step_layer has run for
+ * every layer at position t; advances t.  Errors: LCSM_ESTATE otherwise. */
+int lcsm_advance(lcsm_ctx* ctx);
+
+/* Run n consecutive lcsm_step calls: step k reads y + k*y_stride and writes
+ * z + k*z_stride (strides in floats).  Equivalent to the loop of single
+ * steps, with one host call.  Errors as lcsm_step; stops at the first. */
+int lcsm_run(lcsm_ctx* ctx, int n, const float* y, size_t y_stride, float* z, size_t z_stride);
+
+/* Restart at position 0 with all activations zero; keeps filters and
+ * spectra and clears a fault.  Errors: LCSM_EDEVICE. */
+int lcsm_reset(lcsm_ctx* ctx);
+
+/* Current position t (the next step emits z_t).  Host only. */
+int lcsm_position(const lcsm_ctx* ctx, int* t);
+
+/* Host-only schedule query, no context needed: the gray tile queued after
+ * step t of a length-L run.  *i = t+1, *U = largest power of two dividing i,
+ * the tile reads y[i-U, i) and adds into z[i, i + *dst_len) with
+ * *dst_len = min(U, L-i); *kind is the LCSM_TILE_* the library uses for it
+ * with these options and shape.  For t = L-1 *kind = LCSM_TILE_NONE and the
+ * other outputs are 0.  Errors: LCSM_EINVAL. */
+int lcsm_plan_tile(int M, int B, int D, int L, const lcsm_options* opt, int t, int* i, int* U,
+                   int* dst_len, int* kind);
+
+/* Release the context and, if the library allocated it, the workspace.
+ * Waits for the context's stream.  NULL is ignored. */
+void lcsm_destroy(lcsm_ctx* ctx);
+
+/* Static description of an error code. */
+const char* lcsm_strerror(int code);
+
+/* Text of the last error recorded on this context ("" if none). */
+const char* lcsm_last_error(const lcsm_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LCSM_H */

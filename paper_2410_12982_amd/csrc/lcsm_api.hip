@@ -1,0 +1,337 @@
+// C ABI of the relaxed online convolution library: context, workspace,
+// argument checks and the per-step tile scheduler (Alg. 1 / Alg. 3).
+#include <stdio.h>
+#include <string.h>
+
+#include <new>
+
+#include "lcsm.h"
+#include "lcsm_internal.h"
+
+using lcsm::Shape;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr int kDefaultDirectMaxU = 1 << 30;  // every tile direct until FFT tiles are selected
+constexpr int kDefaultLdsFftMaxN = 2048;
+
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+bool is_pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
+
+int lowbit(int i) { return i & -i; }
+
+struct Options {
+  int direct_max_u;
+  int lds_fft_max_n;
+};
+
+int resolve_options(const lcsm_options* o, Options* r) {
+  r->direct_max_u = kDefaultDirectMaxU;
+  r->lds_fft_max_n = kDefaultLdsFftMaxN;
+  if (!o) return LCSM_OK;
+  for (int k = 0; k < 6; ++k)
+    if (o->reserved[k] != 0) return LCSM_EINVAL;
+  if (o->direct_max_u < 0 || o->lds_fft_max_n < 0) return LCSM_EINVAL;
+  if (o->direct_max_u) {
+    if (!is_pow2(o->direct_max_u)) return LCSM_EINVAL;
+    r->direct_max_u = o->direct_max_u;
+  }
+  if (o->lds_fft_max_n) {
+    if (!is_pow2(o->lds_fft_max_n)) return LCSM_EINVAL;
+    r->lds_fft_max_n = o->lds_fft_max_n;
+  }
+  return LCSM_OK;
+}
+
+int check_shape(int M, int B, int D, int L) {
+  if (M < 1 || B < 1 || D < 1 || L < 1) return LCSM_EINVAL;
+  if ((long long)M * B * D >= (1LL << 31)) return LCSM_EINVAL;
+  if (L >= (1 << 30)) return LCSM_EINVAL;
+  return LCSM_OK;
+}
+
+// Offsets of the workspace sections, in bytes.
+struct Layout {
+  size_t S, Hf, prev, total;
+};
+
+Layout layout_for(const Shape& s, const Options&) {
+  Layout ly{};
+  size_t off = 0;
+  ly.S = off;
+  off = align_up(off + sizeof(float) * (size_t)s.M * s.L * s.BD);
+  ly.Hf = off;
+  off = align_up(off + sizeof(float) * (size_t)s.M * s.L * s.D);
+  ly.prev = off;
+  off = align_up(off + sizeof(float) * (size_t)s.BD);
+  ly.total = off;
+  return ly;
+}
+
+int tile_kind(const Options& o, int U) {
+  if (U <= 0) return LCSM_TILE_NONE;
+  if (U <= o.direct_max_u) return LCSM_TILE_DIRECT;
+  return (2 * U <= o.lds_fft_max_n) ? LCSM_TILE_FFT : LCSM_TILE_FFT_HBM;
+}
+
+}  // namespace
+
+struct lcsm_ctx {
+  Shape s;
+  Options opt;
+  Layout ly;
+  hipStream_t stream;
+  int device;
+  bool owns_ws;
+  char* ws;
+  size_t ws_bytes;
+  float* S;
+  float* Hf;
+  float* prev;
+  int t;            // next position to emit
+  int layers_done;  // lcsm_step_layer progress at position t
+  bool faulted;
+  char msg[256];
+};
+
+namespace {
+
+int fail(lcsm_ctx* c, int code, const char* what, hipError_t e) {
+  if (e != hipSuccess) {
+    snprintf(c->msg, sizeof(c->msg), "%s: %s", what, hipGetErrorString(e));
+    c->faulted = true;
+    return LCSM_EDEVICE;
+  }
+  snprintf(c->msg, sizeof(c->msg), "%s", what);
+  return code;
+}
+
+// Gray tile of i = t+1 for all layers, when it was not fused into the red
+// launch.
+hipError_t launch_tile(lcsm_ctx* c, int i, int U, int dst_len) {
+  const int kind = tile_kind(c->opt, U);
+  if (kind == LCSM_TILE_DIRECT)
+    return lcsm::launch_direct_tile(c->S, c->Hf, c->s, i, U, dst_len, c->stream);
+  return hipErrorNotSupported;
+}
+
+int step_common(lcsm_ctx* c, const float* in, float* z, bool chain) {
+  if (!c) return LCSM_EINVAL;
+  if (!in || !z) return fail(c, LCSM_EINVAL, "null input or output pointer", hipSuccess);
+  if (c->faulted) return LCSM_ESTATE;
+  if (c->layers_done != 0) return fail(c, LCSM_ESTATE, "step during a per-layer position", hipSuccess);
+  if (c->t >= c->s.L) return LCSM_EDONE;
+  const int t = c->t, i = t + 1;
+  const int U = (i < c->s.L) ? lowbit(i) : 0;
+  const int dst_len = U ? (U < c->s.L - i ? U : c->s.L - i) : 0;
+  const int kind = tile_kind(c->opt, U);
+  const bool fuse = (kind == LCSM_TILE_DIRECT && U <= lcsm::kFusedMaxU);
+  hipError_t e;
+  if (chain)
+    e = lcsm::launch_chain_fused(in, z, c->S, c->Hf, c->prev, c->s, t, fuse ? U : 0, dst_len,
+                                 c->stream);
+  else
+    e = lcsm::launch_step_fused(in, z, c->S, c->Hf, c->s, t, fuse ? U : 0, dst_len, c->stream);
+  if (e != hipSuccess) return fail(c, LCSM_EDEVICE, "red-cell launch", e);
+  if (!fuse && kind != LCSM_TILE_NONE) {
+    e = launch_tile(c, i, U, dst_len);
+    if (e != hipSuccess) return fail(c, LCSM_EDEVICE, "gray-tile launch", e);
+  }
+  c->t = t + 1;
+  return LCSM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int lcsm_workspace_bytes(int M, int B, int D, int L, const lcsm_options* opt, size_t* bytes) {
+  if (!bytes) return LCSM_EINVAL;
+  int r = check_shape(M, B, D, L);
+  if (r) return r;
+  Options o;
+  if ((r = resolve_options(opt, &o))) return r;
+  const Shape s{M, B, D, L, B * D};
+  *bytes = layout_for(s, o).total;
+  return LCSM_OK;
+}
+
+int lcsm_init(lcsm_ctx** out, const float* filters, int M, int B, int D, int L, void* stream,
+              void* workspace, size_t workspace_bytes, const lcsm_options* opt) {
+  if (!out) return LCSM_EINVAL;
+  *out = nullptr;
+  if (!filters) return LCSM_EINVAL;
+  int r = check_shape(M, B, D, L);
+  if (r) return r;
+  Options o;
+  if ((r = resolve_options(opt, &o))) return r;
+  const Shape s{M, B, D, L, B * D};
+  const Layout ly = layout_for(s, o);
+  if (workspace) {
+    if (workspace_bytes < ly.total) return LCSM_ENOMEM;
+    if (((uintptr_t)workspace) % kAlign) return LCSM_EINVAL;
+  }
+  lcsm_ctx* c = new (std::nothrow) lcsm_ctx();
+  if (!c) return LCSM_ENOMEM;
+  c->s = s;
+  c->opt = o;
+  c->ly = ly;
+  c->stream = (hipStream_t)stream;
+  c->msg[0] = 0;
+  if (hipGetDevice(&c->device) != hipSuccess) {
+    delete c;
+    return LCSM_EDEVICE;
+  }
+  if (workspace) {
+    c->ws = (char*)workspace;
+    c->ws_bytes = workspace_bytes;
+    c->owns_ws = false;
+  } else {
+    void* p = nullptr;
+    if (hipMalloc(&p, ly.total) != hipSuccess) {
+      (void)hipGetLastError();
+      delete c;
+      return LCSM_ENOMEM;
+    }
+    c->ws = (char*)p;
+    c->ws_bytes = ly.total;
+    c->owns_ws = true;
+  }
+  c->S = (float*)(c->ws + ly.S);
+  c->Hf = (float*)(c->ws + ly.Hf);
+  c->prev = (float*)(c->ws + ly.prev);
+  hipError_t e = lcsm::launch_transpose_filters(filters, c->Hf, s, c->stream);
+  if (e == hipSuccess) e = lcsm::launch_zero(c->S, (size_t)s.M * s.L * s.BD, c->stream);
+  if (e == hipSuccess) e = lcsm::launch_zero(c->prev, (size_t)s.BD, c->stream);
+  if (e != hipSuccess) {
+    if (c->owns_ws) (void)hipFree(c->ws);
+    delete c;
+    return LCSM_EDEVICE;
+  }
+  c->t = 0;
+  c->layers_done = 0;
+  c->faulted = false;
+  *out = c;
+  return LCSM_OK;
+}
+
+int lcsm_step(lcsm_ctx* ctx, const float* y_t, float* z_t) {
+  return step_common(ctx, y_t, z_t, false);
+}
+
+int lcsm_step_chain(lcsm_ctx* ctx, const float* x_t, float* z_t) {
+  return step_common(ctx, x_t, z_t, true);
+}
+
+int lcsm_step_layer(lcsm_ctx* c, int layer, const float* y, float* z) {
+  if (!c) return LCSM_EINVAL;
+  if (!y || !z) return fail(c, LCSM_EINVAL, "null input or output pointer", hipSuccess);
+  if (c->faulted) return LCSM_ESTATE;
+  if (c->t >= c->s.L) return LCSM_EDONE;
+  if (layer != c->layers_done)
+    return fail(c, LCSM_ESTATE, "layers must be stepped in order 0..M-1", hipSuccess);
+  hipError_t e = lcsm::launch_red_layer(y, z, c->S, c->Hf, c->s, layer, c->t, c->stream);
+  if (e != hipSuccess) return fail(c, LCSM_EDEVICE, "red-cell launch", e);
+  c->layers_done = layer + 1;
+  return LCSM_OK;
+}
+
+int lcsm_advance(lcsm_ctx* c) {
+  if (!c) return LCSM_EINVAL;
+  if (c->faulted) return LCSM_ESTATE;
+  if (c->t >= c->s.L) return LCSM_EDONE;
+  if (c->layers_done != c->s.M)
+    return fail(c, LCSM_ESTATE, "lcsm_advance before every layer was stepped", hipSuccess);
+  const int i = c->t + 1;
+  if (i < c->s.L) {
+    const int U = lowbit(i);
+    const int dst_len = U < c->s.L - i ? U : c->s.L - i;
+    hipError_t e = launch_tile(c, i, U, dst_len);
+    if (e != hipSuccess) return fail(c, LCSM_EDEVICE, "gray-tile launch", e);
+  }
+  c->layers_done = 0;
+  c->t = i;
+  return LCSM_OK;
+}
+
+int lcsm_run(lcsm_ctx* c, int n, const float* y, size_t y_stride, float* z, size_t z_stride) {
+  if (!c) return LCSM_EINVAL;
+  if (n < 0) return fail(c, LCSM_EINVAL, "negative step count", hipSuccess);
+  for (int k = 0; k < n; ++k) {
+    const int r = step_common(c, y + (size_t)k * y_stride, z + (size_t)k * z_stride, false);
+    if (r) return r;
+  }
+  return LCSM_OK;
+}
+
+int lcsm_reset(lcsm_ctx* c) {
+  if (!c) return LCSM_EINVAL;
+  hipError_t e = lcsm::launch_zero(c->S, (size_t)c->s.M * c->s.L * c->s.BD, c->stream);
+  if (e == hipSuccess) e = lcsm::launch_zero(c->prev, (size_t)c->s.BD, c->stream);
+  if (e != hipSuccess) return fail(c, LCSM_EDEVICE, "reset", e);
+  c->t = 0;
+  c->layers_done = 0;
+  c->faulted = false;
+  c->msg[0] = 0;
+  return LCSM_OK;
+}
+
+int lcsm_position(const lcsm_ctx* c, int* t) {
+  if (!c || !t) return LCSM_EINVAL;
+  *t = c->t;
+  return LCSM_OK;
+}
+
+int lcsm_plan_tile(int M, int B, int D, int L, const lcsm_options* opt, int t, int* i, int* U,
+                   int* dst_len, int* kind) {
+  if (!i || !U || !dst_len || !kind) return LCSM_EINVAL;
+  int r = check_shape(M, B, D, L);
+  if (r) return r;
+  Options o;
+  if ((r = resolve_options(opt, &o))) return r;
+  if (t < 0 || t >= L) return LCSM_EINVAL;
+  const int ii = t + 1;
+  if (ii >= L) {
+    *i = *U = *dst_len = 0;
+    *kind = LCSM_TILE_NONE;
+    return LCSM_OK;
+  }
+  const int u = lowbit(ii);
+  *i = ii;
+  *U = u;
+  *dst_len = u < L - ii ? u : L - ii;
+  *kind = tile_kind(o, u);
+  return LCSM_OK;
+}
+
+void lcsm_destroy(lcsm_ctx* c) {
+  if (!c) return;
+  (void)hipStreamSynchronize(c->stream);
+  if (c->owns_ws) (void)hipFree(c->ws);
+  delete c;
+}
+
+const char* lcsm_strerror(int code) {
+  switch (code) {
+    case LCSM_OK:
+      return "ok";
+    case LCSM_EINVAL:
+      return "invalid argument";
+    case LCSM_ENOMEM:
+      return "workspace too small or allocation failed";
+    case LCSM_EDEVICE:
+      return "HIP runtime or kernel launch error";
+    case LCSM_EDONE:
+      return "all positions already emitted";
+    case LCSM_ESTATE:
+      return "call out of sequence or context faulted";
+    default:
+      return "unknown error code";
+  }
+}
+
+const char* lcsm_last_error(const lcsm_ctx* c) { return c ? c->msg : ""; }
+
+}  // extern "C"

@@ -1,0 +1,310 @@
+// Red cells and direct (Toeplitz) gray tiles of the relaxed online
+// convolution, for gfx950.
+//
+// Layout: state S[m][t][c] with c = b*D + d (time-major, one B*D slab per
+// position and layer), filters Hf[m][k][d] (lag-major).  A thread owns one
+// column (m, c): every element it writes has no other writer in the launch,
+// so results are deterministic and no atomics are used.  Consecutive threads
+// take consecutive c, so every row access of a wavefront is one contiguous
+// 256-byte segment.
+//
+// Red cell (Alg. 1 red line, Alg. 3 inner loop): z_t = fmaf(h_0, y_t, acc_t),
+// then the slot of position t is overwritten with y_t (the in-place storage
+// of Sec. 3.3: b^l_t lives in a^l_t's slot until it is consumed).
+//
+// Gray tile (Eq. taus) for i = t+1, side U: for j < dst_len,
+//   S[i+j] += sum_{k<U} y[i-U+k] * h[U+j-k]     (lags 1..2U-1).
+#include "lcsm_internal.h"
+
+namespace lcsm {
+namespace {
+
+constexpr int kThreads = 256;
+
+// One column per thread.  RED: do the red cell at position t first (the
+// tile's newest input y_t then comes from the register, not from memory).
+// U == 0: no tile.  1 <= U <= kFusedMaxU: the tile i = t+1 is computed
+// whole by the thread (U outputs from U inputs and 2U-1 lags).
+template <int U, bool RED>
+__global__ __launch_bounds__(kThreads) void k_step_fused(const float* __restrict__ y,
+                                                        float* __restrict__ z,
+                                                        float* __restrict__ S,
+                                                        const float* __restrict__ Hf, int M, int L,
+                                                        int BD, int D, int t, int dst_len) {
+  const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (e >= (int64_t)M * BD) return;
+  const int m = (int)(e / BD);
+  const int c = (int)(e - (int64_t)m * BD);
+  const int d = c % D;
+  float* col = S + (size_t)m * L * BD + c;
+  const float* hc = Hf + (size_t)m * L * D + d;
+  const size_t rs = (size_t)BD;
+
+  constexpr int NY = U > 0 ? U : 1;
+  constexpr int NH = U > 0 ? 2 * U : 1;
+  float yb[NY];
+  float hh[NH];
+  const bool tile = (U > 0) && (dst_len > 0);
+  if constexpr (U > 0) {
+    if (tile) {
+      // Operands of the tile are issued before the red cell's store so their
+      // latency overlaps it.  Rows t+1-U .. t-1 already hold inputs.
+#pragma unroll
+      for (int k = 0; k < U - 1; ++k) yb[k] = col[(size_t)(t + 1 - U + k) * rs];
+#pragma unroll
+      for (int l = 1; l < 2 * U; ++l) hh[l] = (l < L) ? hc[(size_t)l * D] : 0.f;
+    }
+  }
+  float yt;
+  if constexpr (RED) {
+    yt = y[e];
+    const float acc = col[(size_t)t * rs];
+    z[e] = fmaf(hc[0], yt, acc);
+    col[(size_t)t * rs] = yt;
+  } else {
+    yt = col[(size_t)t * rs];
+  }
+  if constexpr (U > 0) {
+    if (tile) {
+      yb[U - 1] = yt;
+#pragma unroll
+      for (int j = 0; j < U; ++j) {
+        if (j < dst_len) {
+          float o = 0.f;
+#pragma unroll
+          for (int k = 0; k < U; ++k) o = fmaf(yb[k], hh[U + j - k], o);
+          col[(size_t)(t + 1 + j) * rs] += o;
+        }
+      }
+    }
+  }
+}
+
+// The chained input rule (lcsm_step_chain) fused with red cells and, for
+// 1 <= U <= kFusedMaxU, the gray tiles.  One thread per (b, d) column walks
+// the layers in order, since y^m_t depends on z^{m-1}_t.
+template <int U>
+__global__ __launch_bounds__(kThreads) void k_chain_fused(const float* __restrict__ x,
+                                                         float* __restrict__ z,
+                                                         float* __restrict__ S,
+                                                         const float* __restrict__ Hf,
+                                                         float* __restrict__ prev, int M, int L,
+                                                         int BD, int D, int t, int dst_len) {
+  const int c = blockIdx.x * kThreads + threadIdx.x;
+  if (c >= BD) return;
+  const int d = c % D;
+  const size_t rs = (size_t)BD;
+  constexpr int NY = U > 0 ? U : 1;
+  constexpr int NH = U > 0 ? 2 * U : 1;
+  const bool tile = (U > 0) && (dst_len > 0);
+  float zl = (t > 0) ? prev[c] : 0.f;  // z^{M-1}_{t-1}, then z^{m-1}_t
+  for (int m = 0; m < M; ++m) {
+    float* col = S + (size_t)m * L * BD + c;
+    const float* hc = Hf + (size_t)m * L * D + d;
+    float yb[NY];
+    float hh[NH];
+    if constexpr (U > 0) {
+      if (tile) {
+#pragma unroll
+        for (int k = 0; k < U - 1; ++k) yb[k] = col[(size_t)(t + 1 - U + k) * rs];
+#pragma unroll
+        for (int l = 1; l < 2 * U; ++l) hh[l] = (l < L) ? hc[(size_t)l * D] : 0.f;
+      }
+    }
+    const float xv = x[(size_t)m * BD + c];
+    const float yv = (m == 0 && t == 0) ? xv : fmaf(0.5f, tanhf(zl), xv);
+    const float acc = col[(size_t)t * rs];
+    const float zv = fmaf(hc[0], yv, acc);
+    z[(size_t)m * BD + c] = zv;
+    col[(size_t)t * rs] = yv;
+    zl = zv;
+    if constexpr (U > 0) {
+      if (tile) {
+        yb[U - 1] = yv;
+#pragma unroll
+        for (int j = 0; j < U; ++j) {
+          if (j < dst_len) {
+            float o = 0.f;
+#pragma unroll
+            for (int k = 0; k < U; ++k) o = fmaf(yb[k], hh[U + j - k], o);
+            col[(size_t)(t + 1 + j) * rs] += o;
+          }
+        }
+      }
+    }
+  }
+  prev[c] = zl;
+}
+
+// Red cell of one layer.
+__global__ __launch_bounds__(kThreads) void k_red_layer(const float* __restrict__ y,
+                                                       float* __restrict__ z,
+                                                       float* __restrict__ Sm,
+                                                       const float* __restrict__ Hm, int BD, int D,
+                                                       int t) {
+  const int c = blockIdx.x * kThreads + threadIdx.x;
+  if (c >= BD) return;
+  float* p = Sm + (size_t)t * BD + c;
+  const float yt = y[c];
+  z[c] = fmaf(Hm[c % D], yt, *p);
+  *p = yt;
+}
+
+// Direct gray tile for U >= J (U a multiple of J): thread = (column c,
+// output chunk j0 .. j0+J-1, layer m).  The J lags needed at input k form a
+// window that slides down by one per k, so each step loads one input and one
+// new lag.
+template <int J>
+__global__ __launch_bounds__(kThreads) void k_direct_tile(float* __restrict__ S,
+                                                         const float* __restrict__ Hf, int L,
+                                                         int BD, int D, int i, int U,
+                                                         int dst_len) {
+  const int c = blockIdx.x * kThreads + threadIdx.x;
+  const int j0 = blockIdx.y * J;
+  const int m = blockIdx.z;
+  if (c >= BD || j0 >= dst_len) return;
+  const int d = c % D;
+  const size_t rs = (size_t)BD;
+  float* col = S + (size_t)m * L * BD + c;
+  const float* hc = Hf + (size_t)m * L * D + d;
+
+  float acc[J];
+  float w[J];  // w[jj] = h[U + j0 + jj - k] at input k
+#pragma unroll
+  for (int jj = 0; jj < J; ++jj) {
+    acc[jj] = 0.f;
+    const int lag = U + j0 + jj;
+    w[jj] = (lag < L) ? hc[(size_t)lag * D] : 0.f;
+  }
+  const float* ysrc = col + (size_t)(i - U) * rs;
+  for (int k = 0; k < U; ++k) {
+    const float yk = ysrc[(size_t)k * rs];
+#pragma unroll
+    for (int jj = 0; jj < J; ++jj) acc[jj] = fmaf(yk, w[jj], acc[jj]);
+#pragma unroll
+    for (int jj = J - 1; jj > 0; --jj) w[jj] = w[jj - 1];
+    const int lag = U + j0 - k - 1;  // >= j0 >= 0
+    w[0] = (k + 1 < U) ? hc[(size_t)lag * D] : 0.f;
+  }
+  float* dst = col + (size_t)(i + j0) * rs;
+#pragma unroll
+  for (int jj = 0; jj < J; ++jj)
+    if (j0 + jj < dst_len) dst[(size_t)jj * rs] += acc[jj];
+}
+
+__global__ __launch_bounds__(kThreads) void k_transpose(const float* __restrict__ src,
+                                                       float* __restrict__ dst, int D, int L) {
+  // src [D][L] -> dst [L][D] for layer blockIdx.z; 32x32 tiles, padded LDS
+  __shared__ float tile[32][33];
+  const size_t off = (size_t)blockIdx.z * D * L;
+  const int l0 = blockIdx.x * 32, d0 = blockIdx.y * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 32 x 8
+  for (int r = ty; r < 32; r += 8) {
+    const int d = d0 + r, l = l0 + tx;
+    if (d < D && l < L) tile[r][tx] = src[off + (size_t)d * L + l];
+  }
+  __syncthreads();
+  for (int r = ty; r < 32; r += 8) {
+    const int l = l0 + r, d = d0 + tx;
+    if (d < D && l < L) dst[off + (size_t)l * D + d] = tile[tx][r];
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void k_zero(float* __restrict__ p, size_t n) {
+  const size_t stride = (size_t)gridDim.x * kThreads;
+  for (size_t k = (size_t)blockIdx.x * kThreads + threadIdx.x; k < n; k += stride) p[k] = 0.f;
+}
+
+inline unsigned blocks_for(int64_t n) { return (unsigned)((n + kThreads - 1) / kThreads); }
+
+template <bool RED>
+hipError_t dispatch_fused(int U, const float* y, float* z, float* S, const float* Hf,
+                          const Shape& s, int t, int dst_len, hipStream_t st) {
+  const dim3 grid(blocks_for((int64_t)s.M * s.BD)), block(kThreads);
+#define LCSM_FUSED_CASE(UU)                                                                  \
+  case UU:                                                                                   \
+    hipLaunchKernelGGL((k_step_fused<UU, RED>), grid, block, 0, st, y, z, S, Hf, s.M, s.L, \
+                       s.BD, s.D, t, dst_len);                                               \
+    break;
+  switch (U) {
+    LCSM_FUSED_CASE(0)
+    LCSM_FUSED_CASE(1)
+    LCSM_FUSED_CASE(2)
+    LCSM_FUSED_CASE(4)
+    LCSM_FUSED_CASE(8)
+    LCSM_FUSED_CASE(16)
+    LCSM_FUSED_CASE(32)
+    default:
+      return hipErrorInvalidValue;
+  }
+#undef LCSM_FUSED_CASE
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_transpose_filters(const float* src, float* dst, const Shape& s, hipStream_t st) {
+  const dim3 grid((s.L + 31) / 32, (s.D + 31) / 32, s.M);
+  hipLaunchKernelGGL(k_transpose, grid, dim3(kThreads), 0, st, src, dst, s.D, s.L);
+  return hipGetLastError();
+}
+
+hipError_t launch_step_fused(const float* y, float* z, float* S, const float* Hf, const Shape& s,
+                             int t, int U, int dst_len, hipStream_t st) {
+  return dispatch_fused<true>(U, y, z, S, Hf, s, t, dst_len, st);
+}
+
+hipError_t launch_chain_fused(const float* x, float* z, float* S, const float* Hf, float* prev,
+                              const Shape& s, int t, int U, int dst_len, hipStream_t st) {
+  const dim3 grid(blocks_for(s.BD)), block(kThreads);
+#define LCSM_CHAIN_CASE(UU)                                                                   \
+  case UU:                                                                                    \
+    hipLaunchKernelGGL((k_chain_fused<UU>), grid, block, 0, st, x, z, S, Hf, prev, s.M, s.L, \
+                       s.BD, s.D, t, dst_len);                                                \
+    break;
+  switch (U) {
+    LCSM_CHAIN_CASE(0)
+    LCSM_CHAIN_CASE(1)
+    LCSM_CHAIN_CASE(2)
+    LCSM_CHAIN_CASE(4)
+    LCSM_CHAIN_CASE(8)
+    LCSM_CHAIN_CASE(16)
+    LCSM_CHAIN_CASE(32)
+    default:
+      return hipErrorInvalidValue;
+  }
+#undef LCSM_CHAIN_CASE
+  return hipGetLastError();
+}
+
+hipError_t launch_red_layer(const float* y, float* z, float* S, const float* Hf, const Shape& s,
+                            int layer, int t, hipStream_t st) {
+  float* Sm = S + (size_t)layer * s.L * s.BD;
+  const float* Hm = Hf + (size_t)layer * s.L * s.D;
+  hipLaunchKernelGGL(k_red_layer, dim3(blocks_for(s.BD)), dim3(kThreads), 0, st, y, z, Sm, Hm,
+                     s.BD, s.D, t);
+  return hipGetLastError();
+}
+
+hipError_t launch_direct_tile(float* S, const float* Hf, const Shape& s, int i, int U, int dst_len,
+                              hipStream_t st) {
+  if (dst_len <= 0) return hipSuccess;
+  if (U <= kFusedMaxU) {
+    // small tiles: whole tile per thread; position t = i-1 already holds y
+    return dispatch_fused<false>(U, nullptr, nullptr, S, Hf, s, i - 1, dst_len, st);
+  }
+  const dim3 grid(blocks_for(s.BD), (dst_len + kDirectJ - 1) / kDirectJ, s.M);
+  hipLaunchKernelGGL(k_direct_tile<kDirectJ>, grid, dim3(kThreads), 0, st, S, Hf, s.L, s.BD, s.D,
+                     i, U, dst_len);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero(float* p, size_t n, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  size_t blocks = (n + kThreads - 1) / kThreads;
+  if (blocks > 8192) blocks = 8192;
+  hipLaunchKernelGGL(k_zero, dim3((unsigned)blocks), dim3(kThreads), 0, st, p, n);
+  return hipGetLastError();
+}
+
+}  // namespace lcsm

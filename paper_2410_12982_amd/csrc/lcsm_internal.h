@@ -1,0 +1,45 @@
+// Internal declarations shared by the library's HIP sources (not installed).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace lcsm {
+
+// Shape of one context.  State rows are indexed [m][t][b*D + d] (time-major:
+// one position of one layer is a contiguous B*D slab), filters [m][k][d].
+struct Shape {
+  int M, B, D, L;
+  int BD;  // B * D
+};
+
+// Largest tile side handled by the fused red+direct kernels.
+constexpr int kFusedMaxU = 32;
+// Output chunk of the generic direct tile kernel (U >= kDirectJ).
+constexpr int kDirectJ = 16;
+
+// [M][D][L] -> [M][L][D]
+hipError_t launch_transpose_filters(const float* src, float* dst, const Shape& s, hipStream_t st);
+
+// Red cells of all layers at position t; when 1 <= U <= kFusedMaxU the gray
+// tile i = t+1 (side U, dst_len outputs) is fused in.  U == 0: red only.
+hipError_t launch_step_fused(const float* y, float* z, float* S, const float* Hf, const Shape& s,
+                             int t, int U, int dst_len, hipStream_t st);
+
+// Same with the elementwise tanh chain as input rule (see lcsm_step_chain).
+hipError_t launch_chain_fused(const float* x, float* z, float* S, const float* Hf, float* prev,
+                              const Shape& s, int t, int U, int dst_len, hipStream_t st);
+
+// Red cell of one layer at position t.
+hipError_t launch_red_layer(const float* y, float* z, float* S, const float* Hf, const Shape& s,
+                            int layer, int t, hipStream_t st);
+
+// Direct gray tile of all layers: y rows [i-U, i) -> z rows [i, i+dst_len).
+hipError_t launch_direct_tile(float* S, const float* Hf, const Shape& s, int i, int U, int dst_len,
+                              hipStream_t st);
+
+// Fill n floats with zero (a kernel, so it is safe under graph capture).
+hipError_t launch_zero(float* p, size_t n, hipStream_t st);
+
+}  // namespace lcsm

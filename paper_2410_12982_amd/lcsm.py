@@ -1,0 +1,250 @@
+"""Python binding of the C ABI in ``include/lcsm.h`` (ctypes).
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels of ``liblcsm.so``.  PyTorch supplies device memory (the workspace and
+the caller's tensors) and the stream.  If the library has not been built the
+import of this module fails; there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "liblcsm.so")
+
+LCSM_OK = 0
+LCSM_EINVAL = -1
+LCSM_ENOMEM = -2
+LCSM_EDEVICE = -3
+LCSM_EDONE = -4
+LCSM_ESTATE = -5
+
+TILE_NONE, TILE_DIRECT, TILE_FFT, TILE_FFT_HBM = 0, 1, 2, 3
+TILE_KIND_NAMES = {TILE_NONE: "none", TILE_DIRECT: "direct", TILE_FFT: "fft_lds",
+                   TILE_FFT_HBM: "fft_hbm"}
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2410_12982_amd.build`")
+
+# torch brings its own HIP runtime (libamdhip64, soname libamdhip64.so.7).  It
+# must be mapped before liblcsm.so is opened, so that the library binds to the
+# same runtime instance as the tensors it is handed; opened first, liblcsm.so
+# would pull in the system runtime and the process would hold two.
+import torch  # noqa: E402,F401
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+
+def hip_runtimes():
+    """Paths of the HIP runtime libraries mapped into this process."""
+    try:
+        with open("/proc/self/maps") as f:
+            return sorted({ln.split()[-1] for ln in f if "libamdhip64" in ln})
+    except OSError:
+        return []
+
+
+if len(hip_runtimes()) > 1:
+    raise ImportError("two HIP runtimes are loaded in this process (" + ", ".join(hip_runtimes())
+                      + "); import torch before anything that loads libamdhip64")
+
+
+class Options(ctypes.Structure):
+    """``lcsm_options``: 0 selects the library default."""
+    _fields_ = [("direct_max_u", ctypes.c_int), ("lds_fft_max_n", ctypes.c_int),
+                ("reserved", ctypes.c_int * 6)]
+
+
+_c_int_p = ctypes.POINTER(ctypes.c_int)
+_vp = ctypes.c_void_p
+
+_SIGS = {
+    "lcsm_workspace_bytes": (ctypes.c_int, [ctypes.c_int] * 4 + [ctypes.POINTER(Options),
+                                                                  ctypes.POINTER(ctypes.c_size_t)]),
+    "lcsm_init": (ctypes.c_int, [ctypes.POINTER(_vp), _vp] + [ctypes.c_int] * 4
+                  + [_vp, _vp, ctypes.c_size_t, ctypes.POINTER(Options)]),
+    "lcsm_step": (ctypes.c_int, [_vp, _vp, _vp]),
+    "lcsm_step_chain": (ctypes.c_int, [_vp, _vp, _vp]),
+    "lcsm_step_layer": (ctypes.c_int, [_vp, ctypes.c_int, _vp, _vp]),
+    "lcsm_advance": (ctypes.c_int, [_vp]),
+    "lcsm_run": (ctypes.c_int, [_vp, ctypes.c_int, _vp, ctypes.c_size_t, _vp, ctypes.c_size_t]),
+    "lcsm_reset": (ctypes.c_int, [_vp]),
+    "lcsm_position": (ctypes.c_int, [_vp, _c_int_p]),
+    "lcsm_plan_tile": (ctypes.c_int, [ctypes.c_int] * 4 + [ctypes.POINTER(Options), ctypes.c_int]
+                       + [_c_int_p] * 4),
+    "lcsm_destroy": (None, [_vp]),
+    "lcsm_strerror": (ctypes.c_char_p, [ctypes.c_int]),
+    "lcsm_last_error": (ctypes.c_char_p, [_vp]),
+}
+
+for _name, (_res, _args) in _SIGS.items():
+    _fn = getattr(_lib, _name)
+    _fn.restype = _res
+    _fn.argtypes = _args
+
+EXPORTED = tuple(_SIGS)
+
+
+class LcsmError(RuntimeError):
+    def __init__(self, code, where, detail=""):
+        self.code = code
+        msg = f"{where}: {_lib.lcsm_strerror(code).decode()} ({code})"
+        if detail:
+            msg += f": {detail}"
+        super().__init__(msg)
+
+
+def _opts(options):
+    if options is None:
+        return None
+    if isinstance(options, Options):
+        return ctypes.byref(options)
+    o = Options()
+    for k, v in dict(options).items():
+        setattr(o, k, int(v))
+    return ctypes.byref(o)
+
+
+def strerror(code: int) -> str:
+    return _lib.lcsm_strerror(code).decode()
+
+
+def workspace_bytes(M, B, D, L, options=None) -> int:
+    n = ctypes.c_size_t(0)
+    r = _lib.lcsm_workspace_bytes(M, B, D, L, _opts(options), ctypes.byref(n))
+    if r:
+        raise LcsmError(r, "lcsm_workspace_bytes")
+    return n.value
+
+
+def plan_tile(M, B, D, L, t, options=None):
+    """(i, U, dst_len, kind) of the gray tile queued after step t."""
+    i, U, n, k = (ctypes.c_int() for _ in range(4))
+    r = _lib.lcsm_plan_tile(M, B, D, L, _opts(options), t, ctypes.byref(i), ctypes.byref(U),
+                            ctypes.byref(n), ctypes.byref(k))
+    if r:
+        raise LcsmError(r, "lcsm_plan_tile")
+    return i.value, U.value, n.value, k.value
+
+
+def raw():
+    """The ctypes library handle (for tests of the raw ABI)."""
+    return _lib
+
+
+class Lcsm:
+    """One relaxed online convolution context.
+
+    ``filters``: fp32 CUDA tensor [M, D, L] (h[m, d, k]).  ``B``: batch rows.
+    The workspace is a torch uint8 tensor owned by this object; work runs on
+    ``stream`` (a torch.cuda.Stream, default: the current stream).
+    """
+
+    def __init__(self, filters, B: int, options=None, stream=None):
+        import torch
+        if not (filters.is_cuda and filters.dtype == torch.float32 and filters.dim() == 3):
+            raise ValueError("filters must be a CUDA fp32 tensor [M, D, L]")
+        filters = filters.contiguous()
+        self.M, self.D, self.L = (int(v) for v in filters.shape)
+        self.B = int(B)
+        self.device = filters.device
+        self._opts_obj = None
+        if options is not None and not isinstance(options, Options):
+            o = Options()
+            for k, v in dict(options).items():
+                setattr(o, k, int(v))
+            options = o
+        self._opts_obj = options
+        self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
+        nbytes = workspace_bytes(self.M, self.B, self.D, self.L, options)
+        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+        self._ctx = _vp()
+        r = _lib.lcsm_init(ctypes.byref(self._ctx), filters.data_ptr(), self.M, self.B, self.D,
+                           self.L, self.stream.cuda_stream, self.workspace.data_ptr(), nbytes,
+                           _opts(options))
+        if r:
+            raise LcsmError(r, "lcsm_init")
+        self._filters_keepalive = filters
+
+    # -- helpers
+    def _check(self, r, where):
+        if r:
+            detail = _lib.lcsm_last_error(self._ctx).decode() if self._ctx else ""
+            raise LcsmError(r, where, detail)
+
+    def _slab(self, tensor, shape, name):
+        import torch
+        if not (tensor.is_cuda and tensor.dtype == torch.float32 and tensor.is_contiguous()
+                and tuple(tensor.shape) == shape and tensor.device == self.device):
+            raise ValueError(f"{name} must be a contiguous CUDA fp32 tensor of shape {shape}")
+        return tensor.data_ptr()
+
+    # -- ABI calls
+    def step(self, y_t, z_t=None):
+        """Emit z_t for all layers given y_t [M, B, D]; queues the gray tile."""
+        import torch
+        shape = (self.M, self.B, self.D)
+        if z_t is None:
+            z_t = torch.empty(shape, dtype=torch.float32, device=self.device)
+        self._check(_lib.lcsm_step(self._ctx, self._slab(y_t, shape, "y_t"),
+                                   self._slab(z_t, shape, "z_t")), "lcsm_step")
+        return z_t
+
+    def step_chain(self, x_t, z_t=None):
+        """One position with the built-in tanh chain; x_t [M, B, D]."""
+        import torch
+        shape = (self.M, self.B, self.D)
+        if z_t is None:
+            z_t = torch.empty(shape, dtype=torch.float32, device=self.device)
+        self._check(_lib.lcsm_step_chain(self._ctx, self._slab(x_t, shape, "x_t"),
+                                         self._slab(z_t, shape, "z_t")), "lcsm_step_chain")
+        return z_t
+
+    def step_layer(self, layer, y, z=None):
+        import torch
+        shape = (self.B, self.D)
+        if z is None:
+            z = torch.empty(shape, dtype=torch.float32, device=self.device)
+        self._check(_lib.lcsm_step_layer(self._ctx, int(layer), self._slab(y, shape, "y"),
+                                         self._slab(z, shape, "z")), "lcsm_step_layer")
+        return z
+
+    def advance(self):
+        self._check(_lib.lcsm_advance(self._ctx), "lcsm_advance")
+
+    def run(self, y, z, n=None, t0=0):
+        """Steps t0 .. t0+n-1 reading y[k] and writing z[k] ([n, M, B, D] tensors)."""
+        shape = (self.M, self.B, self.D)
+        n = y.shape[0] if n is None else n
+        if y.shape[1:] != shape or z.shape[1:] != shape or y.shape[0] < n or z.shape[0] < n:
+            raise ValueError("y and z must be [n, M, B, D]")
+        if not (y.is_contiguous() and z.is_contiguous() and y.is_cuda and z.is_cuda):
+            raise ValueError("y and z must be contiguous CUDA tensors")
+        slab = self.M * self.B * self.D
+        self._check(_lib.lcsm_run(self._ctx, int(n), y.data_ptr(), slab, z.data_ptr(), slab),
+                    "lcsm_run")
+        return z
+
+    def reset(self):
+        self._check(_lib.lcsm_reset(self._ctx), "lcsm_reset")
+
+    @property
+    def position(self) -> int:
+        t = ctypes.c_int()
+        self._check(_lib.lcsm_position(self._ctx, ctypes.byref(t)), "lcsm_position")
+        return t.value
+
+    def plan(self, t):
+        return plan_tile(self.M, self.B, self.D, self.L, t, self._opts_obj)
+
+    def close(self):
+        if self._ctx:
+            _lib.lcsm_destroy(self._ctx)
+            self._ctx = _vp()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,132 @@
+"""The C ABI loads, exports what include/lcsm.h declares, validates arguments
+on the host and plans the same tiles as the oracle's schedule -- CPU only
+(no call here reaches the device)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from oracle.schedule import tile_after_step
+
+import paper_2410_12982_amd.lcsm as lcsm  # noqa: E402  (built by conftest if missing)
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    text = open(os.path.join(ROOT, "include", "lcsm.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(lcsm_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = _declared()
+    assert len(names) >= 13
+    lib = lcsm.raw()
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(lcsm.EXPORTED) == names
+
+
+@pytest.mark.parametrize("L", [1, 2, 3, 12, 100, 1024, 8192])
+def test_plan_tile_matches_oracle_schedule(L):
+    for t in range(L):
+        i, U, n, kind = lcsm.plan_tile(1, 1, 1, L, t)
+        want = tile_after_step(t, L)
+        if want is None:
+            assert (i, U, n, kind) == (0, 0, 0, lcsm.TILE_NONE)
+        else:
+            wi, wU, s0, s1, d0, d1 = want
+            assert (i, U, n) == (wi, wU, d1 - d0)
+            assert kind != lcsm.TILE_NONE
+
+
+def test_plan_tile_large_L_every_step():
+    L = 1 << 17
+    for t in range(0, L, 97):
+        i, U, n, _ = lcsm.plan_tile(18, 1, 1024, L, t)
+        want = tile_after_step(t, L)
+        assert want is None or (i, U, n) == (want[0], want[1], want[5] - want[4])
+
+
+def test_tile_kind_selection_follows_options():
+    o = {"direct_max_u": 8, "lds_fft_max_n": 64}
+    kinds = {}
+    for t in range(1023):
+        _, U, _, k = lcsm.plan_tile(1, 1, 4, 1024, t, o)
+        kinds[U] = k
+    assert all(kinds[u] == lcsm.TILE_DIRECT for u in (1, 2, 4, 8))
+    assert all(kinds[u] == lcsm.TILE_FFT for u in (16, 32))
+    assert all(kinds[u] == lcsm.TILE_FFT_HBM for u in (64, 128, 256, 512))
+
+
+@pytest.mark.parametrize("shape", [(0, 1, 1, 8), (1, 0, 1, 8), (1, 1, 0, 8), (1, 1, 1, 0),
+                                   (1, 1, 1, -5), (1 << 16, 1 << 8, 1 << 8, 8), (1, 1, 1, 1 << 30)])
+def test_workspace_bytes_rejects_bad_shapes(shape):
+    with pytest.raises(lcsm.LcsmError) as e:
+        lcsm.workspace_bytes(*shape)
+    assert e.value.code == lcsm.LCSM_EINVAL
+
+
+def test_workspace_bytes_covers_state_and_filters():
+    M, B, D, L = 3, 4, 40, 300
+    n = lcsm.workspace_bytes(M, B, D, L)
+    assert n >= 4 * (M * L * B * D + M * L * D)
+    assert n % 256 == 0
+
+
+@pytest.mark.parametrize("opts", [{"direct_max_u": 3}, {"lds_fft_max_n": 100},
+                                  {"direct_max_u": -1}])
+def test_bad_options_rejected(opts):
+    with pytest.raises(lcsm.LcsmError) as e:
+        lcsm.workspace_bytes(1, 1, 1, 16, opts)
+    assert e.value.code == lcsm.LCSM_EINVAL
+
+
+def test_reserved_options_must_be_zero():
+    o = lcsm.Options()
+    o.reserved[2] = 1
+    with pytest.raises(lcsm.LcsmError):
+        lcsm.workspace_bytes(1, 1, 1, 16, o)
+
+
+def test_init_validates_before_touching_the_device():
+    lib = lcsm.raw()
+    ctx = ctypes.c_void_p(123)
+    fake = ctypes.c_void_p(4096)
+    # null out-pointer, null filters, bad shape, too-small or misaligned workspace
+    assert lib.lcsm_init(None, fake, 1, 1, 1, 8, None, None, 0, None) == lcsm.LCSM_EINVAL
+    assert lib.lcsm_init(ctypes.byref(ctx), None, 1, 1, 1, 8, None, None, 0, None) == lcsm.LCSM_EINVAL
+    assert ctx.value is None
+    assert lib.lcsm_init(ctypes.byref(ctx), fake, 1, 0, 1, 8, None, None, 0, None) == lcsm.LCSM_EINVAL
+    need = lcsm.workspace_bytes(1, 1, 1, 8)
+    assert lib.lcsm_init(ctypes.byref(ctx), fake, 1, 1, 1, 8, None, fake, need - 1, None) == lcsm.LCSM_ENOMEM
+    assert lib.lcsm_init(ctypes.byref(ctx), fake, 1, 1, 1, 8, None, ctypes.c_void_p(4096 + 4),
+                         need, None) == lcsm.LCSM_EINVAL
+
+
+def test_null_context_calls():
+    lib = lcsm.raw()
+    fake = ctypes.c_void_p(4096)
+    assert lib.lcsm_step(None, fake, fake) == lcsm.LCSM_EINVAL
+    assert lib.lcsm_step_chain(None, fake, fake) == lcsm.LCSM_EINVAL
+    assert lib.lcsm_step_layer(None, 0, fake, fake) == lcsm.LCSM_EINVAL
+    assert lib.lcsm_advance(None) == lcsm.LCSM_EINVAL
+    assert lib.lcsm_reset(None) == lcsm.LCSM_EINVAL
+    assert lib.lcsm_run(None, 1, fake, 0, fake, 0) == lcsm.LCSM_EINVAL
+    t = ctypes.c_int()
+    assert lib.lcsm_position(None, ctypes.byref(t)) == lcsm.LCSM_EINVAL
+    lib.lcsm_destroy(None)
+    assert lib.lcsm_last_error(None) == b""
+
+
+def test_strerror_covers_codes():
+    seen = {lcsm.strerror(c) for c in (0, -1, -2, -3, -4, -5)}
+    assert len(seen) == 6
+    assert lcsm.strerror(-99) == "unknown error code"
+
+
+def test_single_hip_runtime_in_process():
+    """The binding binds to torch's HIP runtime; a second copy must not load."""
+    assert len(lcsm.hip_runtimes()) <= 1
