@@ -53,9 +53,13 @@ extern "C" {
 /* Tuning options.  A NULL pointer, or a field left at 0, selects the
  * library default. */
 typedef struct lcsm_options {
-  int direct_max_u;  /* tiles with U <= direct_max_u use the direct kernel (power of two, >= 1) */
-  int lds_fft_max_n; /* FFT tiles with 2U <= lds_fft_max_n run in one LDS pass (power of two) */
-  int reserved[6];   /* must be zero */
+  int direct_max_u;  /* tiles with U <= direct_max_u use the direct kernel (power of two, >= 1;
+                        default 32); larger tiles use the FFT */
+  int lds_fft_max_n; /* FFT tiles with 2U <= lds_fft_max_n run in one LDS pass, larger ones in
+                        three passes through scratch (power of two in [16, 4096]; default 2048) */
+  int scratch_mib;   /* cap of the multi-pass FFT scratch in MiB (default 512); the scratch is
+                        never smaller than one chunk of 16 complex columns */
+  int reserved[5];   /* must be zero */
 } lcsm_options;
 
 typedef struct lcsm_ctx lcsm_ctx;
@@ -63,7 +67,7 @@ typedef struct lcsm_ctx lcsm_ctx;
 /* Device bytes of the workspace a context of this shape needs (state
  * M*L*B*D fp32, filters M*L*D fp32, filter spectra of the FFT tile sizes, FFT
  * scratch and a few small buffers).  Host only: touches no device.
- * Errors: LCSM_EINVAL for sizes < 1, M*B*D >= 2^31, L >= 2^30 or bad options. */
+ * Errors: LCSM_EINVAL for sizes < 1, M*B*D >= 2^31, L > 2^19 or bad options. */
 int lcsm_workspace_bytes(int M, int B, int D, int L, const lcsm_options* opt, size_t* bytes);
 
 /* Create a context (Alg. 3's state: all activations zero, position t = 0).

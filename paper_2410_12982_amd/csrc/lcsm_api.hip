@@ -1,9 +1,11 @@
 // C ABI of the relaxed online convolution library: context, workspace,
 // argument checks and the per-step tile scheduler (Alg. 1 / Alg. 3).
+#include <math.h>
 #include <stdio.h>
 #include <string.h>
 
 #include <new>
+#include <vector>
 
 #include "lcsm.h"
 #include "lcsm_internal.h"
@@ -13,8 +15,11 @@ using lcsm::Shape;
 namespace {
 
 constexpr size_t kAlign = 256;
-constexpr int kDefaultDirectMaxU = 1 << 30;  // every tile direct until FFT tiles are selected
-constexpr int kDefaultLdsFftMaxN = 2048;
+constexpr int kDefaultDirectMaxU = 32;     // tiles U <= 32 direct (fused with the red cell)
+constexpr int kDefaultLdsFftMaxN = 2048;   // 2U <= 2048: one LDS pass
+constexpr int kDefaultScratchMib = 512;    // multi-pass FFT scratch cap
+constexpr int kMaxL = 1 << 19;             // FFT lengths up to 2^19 are built
+constexpr int kMaxLevels = 20;
 
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
@@ -25,39 +30,52 @@ int lowbit(int i) { return i & -i; }
 struct Options {
   int direct_max_u;
   int lds_fft_max_n;
+  int scratch_mib;
 };
 
 int resolve_options(const lcsm_options* o, Options* r) {
   r->direct_max_u = kDefaultDirectMaxU;
   r->lds_fft_max_n = kDefaultLdsFftMaxN;
+  r->scratch_mib = kDefaultScratchMib;
   if (!o) return LCSM_OK;
-  for (int k = 0; k < 6; ++k)
+  for (int k = 0; k < 5; ++k)
     if (o->reserved[k] != 0) return LCSM_EINVAL;
-  if (o->direct_max_u < 0 || o->lds_fft_max_n < 0) return LCSM_EINVAL;
+  if (o->direct_max_u < 0 || o->lds_fft_max_n < 0 || o->scratch_mib < 0) return LCSM_EINVAL;
   if (o->direct_max_u) {
     if (!is_pow2(o->direct_max_u)) return LCSM_EINVAL;
     r->direct_max_u = o->direct_max_u;
   }
   if (o->lds_fft_max_n) {
-    if (!is_pow2(o->lds_fft_max_n)) return LCSM_EINVAL;
+    if (!is_pow2(o->lds_fft_max_n) || o->lds_fft_max_n < lcsm::kMinLdsFftN ||
+        o->lds_fft_max_n > lcsm::kMaxLdsFftN)
+      return LCSM_EINVAL;
     r->lds_fft_max_n = o->lds_fft_max_n;
   }
+  if (o->scratch_mib) r->scratch_mib = o->scratch_mib;
   return LCSM_OK;
 }
 
 int check_shape(int M, int B, int D, int L) {
   if (M < 1 || B < 1 || D < 1 || L < 1) return LCSM_EINVAL;
   if ((long long)M * B * D >= (1LL << 31)) return LCSM_EINVAL;
-  if (L >= (1 << 30)) return LCSM_EINVAL;
+  if (L > kMaxL) return LCSM_EINVAL;
   return LCSM_OK;
+}
+
+int tile_kind(const Options& o, int U) {
+  if (U <= 0) return LCSM_TILE_NONE;
+  if (U <= o.direct_max_u) return LCSM_TILE_DIRECT;
+  return (2 * U <= o.lds_fft_max_n) ? LCSM_TILE_FFT : LCSM_TILE_FFT_HBM;
 }
 
 // Offsets of the workspace sections, in bytes.
 struct Layout {
-  size_t S, Hf, prev, total;
+  size_t S, Hf, prev, tw, scratch, scratch_bytes, total;
+  size_t H[kMaxLevels];  // spectra of tile size 2^q (FFT levels only)
+  int nmax;              // largest FFT length, 0 if no tile uses the FFT
 };
 
-Layout layout_for(const Shape& s, const Options&) {
+Layout layout_for(const Shape& s, const Options& o) {
   Layout ly{};
   size_t off = 0;
   ly.S = off;
@@ -66,14 +84,46 @@ Layout layout_for(const Shape& s, const Options&) {
   off = align_up(off + sizeof(float) * (size_t)s.M * s.L * s.D);
   ly.prev = off;
   off = align_up(off + sizeof(float) * (size_t)s.BD);
+  bool multipass = false;
+  for (int q = 0; q < kMaxLevels && (1 << q) <= s.L - 1; ++q) {
+    const int U = 1 << q;
+    const int kind = tile_kind(o, U);
+    if (kind == LCSM_TILE_DIRECT) continue;
+    ly.nmax = 2 * U;
+    if (kind == LCSM_TILE_FFT_HBM) multipass = true;
+    ly.H[q] = off;
+    off = align_up(off + sizeof(float2) * (size_t)s.M * (U + 1) * s.D);
+  }
+  if (ly.nmax) {
+    ly.tw = off;
+    off = align_up(off + sizeof(float2) * 2 * (size_t)ly.nmax);
+  }
+  if (multipass) {
+    // C and E of one chunk: 2 * N complex per complex column
+    const size_t per_col = 2 * sizeof(float2) * (size_t)ly.nmax;
+    const size_t cols = ((size_t)s.M * ((s.BD + 1) / 2) + 15) / 16 * 16;
+    size_t want = (size_t)o.scratch_mib << 20;
+    if (want > per_col * cols) want = per_col * cols;
+    if (want < per_col * 16) want = per_col * 16;
+    ly.scratch = off;
+    ly.scratch_bytes = want;
+    off = align_up(off + want);
+  }
   ly.total = off;
   return ly;
 }
 
-int tile_kind(const Options& o, int U) {
-  if (U <= 0) return LCSM_TILE_NONE;
-  if (U <= o.direct_max_u) return LCSM_TILE_DIRECT;
-  return (2 * U <= o.lds_fft_max_n) ? LCSM_TILE_FFT : LCSM_TILE_FFT_HBM;
+// Twiddle table tw[n + m] = exp(-2 pi i m / n) for n = 1, 2, 4, ..., nmax.
+std::vector<float2> twiddle_table(int nmax) {
+  std::vector<float2> t(2 * (size_t)nmax);
+  t[0] = make_float2(0.f, 0.f);
+  t[1] = make_float2(1.f, 0.f);
+  for (int n = 2; n <= nmax; n *= 2)
+    for (int m = 0; m < n; ++m) {
+      const double a = 2.0 * M_PI * (double)m / (double)n;
+      t[(size_t)n + m] = make_float2((float)cos(a), (float)-sin(a));
+    }
+  return t;
 }
 
 }  // namespace
@@ -90,6 +140,8 @@ struct lcsm_ctx {
   float* S;
   float* Hf;
   float* prev;
+  float2* tw;
+  float2* scratch;
   int t;            // next position to emit
   int layers_done;  // lcsm_step_layer progress at position t
   bool faulted;
@@ -114,7 +166,27 @@ hipError_t launch_tile(lcsm_ctx* c, int i, int U, int dst_len) {
   const int kind = tile_kind(c->opt, U);
   if (kind == LCSM_TILE_DIRECT)
     return lcsm::launch_direct_tile(c->S, c->Hf, c->s, i, U, dst_len, c->stream);
-  return hipErrorNotSupported;
+  const int q = __builtin_ctz((unsigned)U);
+  const float2* H = (const float2*)(c->ws + c->ly.H[q]);
+  return lcsm::launch_fft_tile(c->S, H, c->tw, c->s, i, U, dst_len, c->opt.lds_fft_max_n,
+                               c->scratch, c->ly.scratch_bytes, c->stream);
+}
+
+// Filter spectra of every FFT tile size (the cached kernel DFTs).
+hipError_t init_spectra(lcsm_ctx* c) {
+  if (!c->ly.nmax) return hipSuccess;
+  std::vector<float2> t = twiddle_table(c->ly.nmax);
+  hipError_t e = hipMemcpyAsync(c->tw, t.data(), t.size() * sizeof(float2), hipMemcpyHostToDevice,
+                                c->stream);
+  for (int q = 0; e == hipSuccess && q < kMaxLevels && (1 << q) <= c->s.L - 1; ++q) {
+    const int U = 1 << q;
+    if (tile_kind(c->opt, U) == LCSM_TILE_DIRECT) continue;
+    e = lcsm::launch_spectra(c->Hf, (float2*)(c->ws + c->ly.H[q]), c->tw, c->s, U,
+                             c->opt.lds_fft_max_n, c->scratch, c->ly.scratch_bytes, c->stream);
+  }
+  // the host table must outlive the copy
+  if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+  return e;
 }
 
 int step_common(lcsm_ctx* c, const float* in, float* z, bool chain) {
@@ -202,9 +274,12 @@ int lcsm_init(lcsm_ctx** out, const float* filters, int M, int B, int D, int L, 
   c->S = (float*)(c->ws + ly.S);
   c->Hf = (float*)(c->ws + ly.Hf);
   c->prev = (float*)(c->ws + ly.prev);
+  c->tw = ly.nmax ? (float2*)(c->ws + ly.tw) : nullptr;
+  c->scratch = ly.scratch_bytes ? (float2*)(c->ws + ly.scratch) : nullptr;
   hipError_t e = lcsm::launch_transpose_filters(filters, c->Hf, s, c->stream);
   if (e == hipSuccess) e = lcsm::launch_zero(c->S, (size_t)s.M * s.L * s.BD, c->stream);
   if (e == hipSuccess) e = lcsm::launch_zero(c->prev, (size_t)s.BD, c->stream);
+  if (e == hipSuccess) e = init_spectra(c);
   if (e != hipSuccess) {
     if (c->owns_ws) (void)hipFree(c->ws);
     delete c;

@@ -1,0 +1,485 @@
+// FFT gray tiles and filter spectra of the relaxed online convolution, for
+// gfx950.
+//
+// A gray tile of side U (Eq. taus) adds, for j < U,
+//     z[i+j] += sum_{k<U} y[i-U+k] h[U+j-k]
+// Lemma 1 with the cyclic shortcut of App. B: right-pad the U inputs with U
+// zeros, multiply the N = 2U point DFT with the DFT of the filter prefix
+// h[0, N), and invert; outputs U..N-1 of the cyclic convolution are the
+// wanted ones (the wrap-around only reaches outputs < U-1).  The filter DFTs
+// are computed once per tile size at initialisation (the cached kernel DFTs
+// of Sec. 5 / App. B) and stored pre-scaled by 1/N.
+//
+// Two real columns are carried in one complex signal: real part column c,
+// imaginary part column c+1 (one float2 load per row).  If Z is the DFT of
+// the pair and Ha, Hb the filter spectra of the two columns, the spectrum of
+// (conv(a, ha) + i conv(b, hb)) is
+//     P[k] = Z[k] S[k] + conj(Z[N-k]) D[k],   S = (Ha+Hb)/2,  D = (Ha-Hb)/2,
+// which needs the bins k and N-k together.
+//
+// Data layout: state S[m][t][c] (c = b*D + d, row stride B*D), filters
+// Hf[m][k][d], spectra of tile size U: H[m][k][d] complex, k = 0..U (the
+// other bins follow from conjugate symmetry).
+//
+// Single pass (N <= LDS limit): one workgroup owns WC complex columns and all
+// N points in LDS; it reads the U input rows once and adds into the U output
+// rows once.
+//
+// Multi pass (larger N), a four-step split N = N1 N2 with time index
+// n = n1 + N1 n2 and frequency index k = N2 k1 + k2:
+//   pass R  : for each n1 an N2-point FFT over the rows n1 + N1 n2 of the
+//             block (only n2 < N2/2 are non-zero), times w_N^{n1 k2} -> C
+//   pass M  : for each k2 an N1-point DFT over n1 (giving X[N2 k1 + k2]),
+//             the spectral product (partner bin N-k lies in column N2-k2),
+//             the inverse N1-point DFT and the conjugate twiddle -> E
+//   pass R' : for each n1 the inverse N2-point FFT of E; outputs n2 >= N2/2
+//             are the time indices U..N-1, added into the state.
+// C and E live in a scratch buffer, processed in chunks of columns.
+#include "lcsm_fft_core.h"
+#include "lcsm_internal.h"
+
+namespace lcsm {
+namespace {
+
+using fft::cadd;
+using fft::cmul;
+using fft::cmulc;
+using fft::conjf2;
+using fft::csub;
+
+// Per-size launch shape of the LDS transforms: WC complex columns per
+// workgroup, NT threads.  WC * 8 bytes is the contiguous run read per row.
+template <int N>
+struct Cfg {
+  static constexpr int WC = N <= 512 ? 16 : (N <= 2048 ? 8 : 4);
+  static constexpr int NT = N <= 256 ? 128 : (N <= 1024 ? 256 : 512);
+};
+
+// Pair load / accumulate of real columns c, c+1 of a row.
+__device__ __forceinline__ float2 load_pair(const float* __restrict__ row, int c, int ncols, bool vec) {
+  if (c >= ncols) return make_float2(0.f, 0.f);
+  if (vec) return *reinterpret_cast<const float2*>(row + c);
+  return make_float2(row[c], c + 1 < ncols ? row[c + 1] : 0.f);
+}
+
+__device__ __forceinline__ void add_pair(float* row, int c, int ncols, bool vec, float2 v) {
+  if (c >= ncols) return;
+  if (vec) {
+    float2* p = reinterpret_cast<float2*>(row + c);
+    float2 o = *p;
+    o.x += v.x;
+    o.y += v.y;
+    *p = o;
+  } else {
+    row[c] += v.x;
+    if (c + 1 < ncols) row[c + 1] += v.y;
+  }
+}
+
+// Spectral product of the column pair (a, b) at bin k given Z[k] and
+// Z[N-k]: returns P[k] (see the file header).
+__device__ __forceinline__ float2 pair_product(float2 zk, float2 znk, float2 ha, float2 hb) {
+  const float2 s = make_float2(0.5f * (ha.x + hb.x), 0.5f * (ha.y + hb.y));
+  const float2 d = make_float2(0.5f * (ha.x - hb.x), 0.5f * (ha.y - hb.y));
+  return cadd(cmul(zk, s), cmul(conjf2(znk), d));
+}
+
+// ----------------------------------------------------------- single pass
+
+template <int N>
+__global__ __launch_bounds__(Cfg<N>::NT) void k_fft_tile(float* __restrict__ S,
+                                                         const float2* __restrict__ H,
+                                                         const float2* __restrict__ tw, int L,
+                                                         int BD, int D, int B, int i, int dst_len,
+                                                         int ppl, int hgroup) {
+  constexpr int WC = Cfg<N>::WC, NT = Cfg<N>::NT, U = N / 2;
+  __shared__ float2 buf[N * WC];
+  const int q = fft::xcd_logical((int)blockIdx.x, (int)gridDim.x);
+  const int m = q / ppl;
+  const int r = q - m * ppl;
+  // panels of the same channels (different batch rows) are neighbours, so
+  // they share the filter spectrum through L2
+  const int panel = hgroup > 0 ? (r % B) * hgroup + r / B : r;
+  const int c0 = panel * 2 * WC;
+  const bool vec = (BD & 1) == 0;
+  float* Sm = S + (size_t)m * L * BD;
+  const float* ysrc = Sm + (size_t)(i - U) * BD;
+
+  fft::forward_from_global<N, WC, WC, NT, true>(buf, tw, [&](int row, int col) {
+    return load_pair(ysrc + (size_t)row * BD, c0 + 2 * col, BD, vec);
+  });
+
+  const float2* Hm = H + (size_t)m * (U + 1) * D;
+  for (int u = (int)threadIdx.x; u < (U + 1) * WC; u += NT) {
+    const int kk = u / WC, col = u - kk * WC;
+    const int c = c0 + 2 * col;
+    if (c >= BD) continue;
+    const int da = c % D;
+    const int db = (c + 1 < BD) ? (c + 1) % D : da;
+    const float2 ha = Hm[(size_t)kk * D + da], hb = Hm[(size_t)kk * D + db];
+    const int nk = (N - kk) & (N - 1);
+    const float2 zk = buf[kk * WC + col], znk = buf[nk * WC + col];
+    buf[kk * WC + col] = pair_product(zk, znk, ha, hb);
+    if (nk != kk) buf[nk * WC + col] = pair_product(znk, zk, conjf2(ha), conjf2(hb));
+  }
+  __syncthreads();
+
+  float* zdst = Sm + (size_t)i * BD;
+  fft::inverse_to_global<N, WC, WC, NT, true>(buf, tw, [&](int row, int col, float2 v) {
+    const int oi = row - U;
+    if (oi < dst_len) add_pair(zdst + (size_t)oi * BD, c0 + 2 * col, BD, vec, v);
+  });
+}
+
+// Filter spectra of tile size U = N/2 for all layers: H[m][k][d] =
+// DFT_N(h[m][0..N), d)[k] / N for k <= N/2 (taps at lags >= L are zero).
+template <int N>
+__global__ __launch_bounds__(Cfg<N>::NT) void k_fft_spectra(const float* __restrict__ Hf,
+                                                            float2* __restrict__ Hout,
+                                                            const float2* __restrict__ tw, int L,
+                                                            int D, int ppl) {
+  constexpr int WC = Cfg<N>::WC, NT = Cfg<N>::NT, U = N / 2;
+  __shared__ float2 buf[N * WC];
+  const int m = (int)blockIdx.x / ppl;
+  const int c0 = ((int)blockIdx.x - m * ppl) * 2 * WC;
+  const bool vec = (D & 1) == 0;
+  const float* src = Hf + (size_t)m * L * D;
+  fft::forward_from_global<N, WC, WC, NT, false>(buf, tw, [&](int row, int col) {
+    return row < L ? load_pair(src + (size_t)row * D, c0 + 2 * col, D, vec) : make_float2(0.f, 0.f);
+  });
+  constexpr float inv_n = 1.0f / (float)N;
+  float2* Hm = Hout + (size_t)m * (U + 1) * D;
+  for (int u = (int)threadIdx.x; u < (U + 1) * WC; u += NT) {
+    const int kk = u / WC, col = u - kk * WC;
+    const int c = c0 + 2 * col;
+    if (c >= D) continue;
+    const float2 a = buf[kk * WC + col], b = buf[((N - kk) & (N - 1)) * WC + col];
+    Hm[(size_t)kk * D + c] = make_float2(0.5f * inv_n * (a.x + b.x), 0.5f * inv_n * (a.y - b.y));
+    if (c + 1 < D)
+      Hm[(size_t)kk * D + c + 1] = make_float2(0.5f * inv_n * (a.y + b.y), -0.5f * inv_n * (a.x - b.x));
+  }
+}
+
+// ------------------------------------------------------------ multi pass
+
+// Geometry of a multi-pass launch over one chunk of complex columns.
+// Complex column g (global over layers) is layer g / ncc, real columns
+// 2 (g % ncc) and 2 (g % ncc) + 1 of that layer.  Scratch element (row r,
+// chunk column x) sits at r * cstride + x.
+struct Chunk {
+  int g0;       // first complex column of the chunk
+  int nvalid;   // complex columns in the chunk
+  int cstride;  // scratch row stride (complex columns, >= nvalid)
+  int ncc;      // complex columns per layer = ceil(ncols / 2)
+  int ncols;    // real columns per layer (B*D for the state, D for filters)
+  int N1, N2;
+};
+
+// Pass R: N2-point FFT over rows row0 + n1 + N1 n2 of every layer's matrix
+// (src + m*lstride, row stride ncols), rows >= rows_valid read as zero; HALF:
+// only n2 < N2/2 are read.  Output C[n1*N2 + k2][x] = FFT[k2] * w_N^{n1 k2}.
+template <int N2, bool HALF>
+__global__ __launch_bounds__(Cfg<N2>::NT) void k_fft_rows_fwd(const float* __restrict__ src,
+                                                              size_t lstride, int row0,
+                                                              int rows_valid, Chunk ch,
+                                                              float2* __restrict__ C,
+                                                              const float2* __restrict__ tw) {
+  constexpr int WC = Cfg<N2>::WC, NT = Cfg<N2>::NT;
+  __shared__ float2 buf[N2 * WC];
+  const int npan = (ch.nvalid + WC - 1) / WC;
+  const int q = fft::xcd_logical((int)blockIdx.x, (int)gridDim.x);
+  const int n1 = q / npan;
+  const int x0 = (q - n1 * npan) * WC;
+  const bool vec = (ch.ncols & 1) == 0;
+  fft::forward_from_global<N2, WC, WC, NT, HALF>(buf, tw, [&](int n2, int col) {
+    const int x = x0 + col;
+    const int row = row0 + n1 + ch.N1 * n2;
+    if (x >= ch.nvalid || row >= rows_valid) return make_float2(0.f, 0.f);
+    const int g = ch.g0 + x;
+    const int m = g / ch.ncc;
+    const int c = 2 * (g - m * ch.ncc);
+    return load_pair(src + m * lstride + (size_t)row * ch.ncols, c, ch.ncols, vec);
+  });
+  const int N = ch.N1 * N2;
+  for (int u = (int)threadIdx.x; u < N2 * WC; u += NT) {
+    const int k2 = u / WC, col = u - k2 * WC;
+    const int x = x0 + col;
+    if (x >= ch.nvalid) continue;
+    C[(size_t)(n1 * N2 + k2) * ch.cstride + x] = cmul(buf[k2 * WC + col], fft::twiddle<false>(tw, N, n1 * k2));
+  }
+}
+
+constexpr int kMidG = 8;   // frequency columns k2 per pass-M workgroup
+constexpr int kMidWC = 8;  // complex columns per pass-M workgroup
+constexpr int kMidNT = 256;
+
+// Pass M.  Workgroup (kg, panel) owns the frequency columns k2 = kg*G + s
+// (s < G) of complex columns x0 .. x0+WCM-1, and reads their partner columns
+// N2 - k2 as well.  LDS slot s holds k2, slot G + s its partner.
+//   SPECTRA = false: X = DFT_N1(C), P = pair_product, E = IDFT_N1(P) times
+//                    conj(w_N^{n1 k2}), written to E for the own columns.
+//   SPECTRA = true : C holds the DFT pieces of the filter pairs; the
+//                    separated, 1/N-scaled spectra of bins k <= N/2 are
+//                    written to Hout[m][k][d].
+template <int N1, bool SPECTRA>
+__global__ __launch_bounds__(kMidNT) void k_fft_mid(const float2* __restrict__ C,
+                                                    float2* __restrict__ E,
+                                                    const float2* __restrict__ H,
+                                                    float2* __restrict__ Hout, int D, Chunk ch,
+                                                    const float2* __restrict__ tw) {
+  constexpr int G = kMidG, WCM = kMidWC, NT = kMidNT;
+  constexpr int W = 2 * G * WCM;  // LDS row stride
+  __shared__ float2 buf[N1 * W];
+  const int N2 = ch.N2, N = N1 * N2, U = N / 2;
+  const int npan = (ch.nvalid + WCM - 1) / WCM;
+  const int q = fft::xcd_logical((int)blockIdx.x, (int)gridDim.x);
+  const int kg = q / npan;
+  const int x0 = (q - kg * npan) * WCM;
+  const int kA = kg * G;
+
+  for (int u = (int)threadIdx.x; u < N1 * W; u += NT) {
+    const int n1 = u / W, slot = (u - n1 * W) / WCM, cc = u % WCM;
+    const int s = slot % G;
+    const int k2 = slot < G ? kA + s : (N2 - kA - s) & (N2 - 1);
+    const int x = x0 + cc;
+    buf[u] = x < ch.nvalid ? C[(size_t)(n1 * N2 + k2) * ch.cstride + x] : make_float2(0.f, 0.f);
+  }
+  __syncthreads();
+  fft::lds_passes<N1, 0, fft::Plan<N1>::NP, W, W, NT, false>(buf, tw);
+
+  // spectral step over the own columns (partner slots are only read)
+  for (int u = (int)threadIdx.x; u < N1 * G * WCM; u += NT) {
+    const int k1 = u / (G * WCM), sc = u - k1 * (G * WCM);
+    const int s = sc / WCM, cc = sc - s * WCM;
+    const int x = x0 + cc;
+    if (x >= ch.nvalid) continue;
+    const int k2 = kA + s;
+    const int pk1 = k2 == 0 ? (N1 - k1) & (N1 - 1) : N1 - 1 - k1;
+    const float2 xk = buf[k1 * W + s * WCM + cc];
+    const float2 xp = buf[pk1 * W + (G + s) * WCM + cc];
+    const int g = ch.g0 + x;
+    const int m = g / ch.ncc;
+    const int c = 2 * (g - m * ch.ncc);
+    const int k = N2 * k1 + k2;
+    if constexpr (SPECTRA) {
+      if (k > U) continue;
+      const float inv_n = 1.0f / (float)N;
+      float2* Hm = Hout + (size_t)m * (U + 1) * D;
+      Hm[(size_t)k * D + c] = make_float2(0.5f * inv_n * (xk.x + xp.x), 0.5f * inv_n * (xk.y - xp.y));
+      if (c + 1 < D)
+        Hm[(size_t)k * D + c + 1] =
+            make_float2(0.5f * inv_n * (xk.y + xp.y), -0.5f * inv_n * (xk.x - xp.x));
+    } else {
+      const int BD = ch.ncols;
+      const int da = c % D;
+      const int db = (c + 1 < BD) ? (c + 1) % D : da;
+      const float2* Hm = H + (size_t)m * (U + 1) * D;
+      float2 ha, hb;
+      if (k <= U) {
+        ha = Hm[(size_t)k * D + da];
+        hb = Hm[(size_t)k * D + db];
+      } else {
+        ha = conjf2(Hm[(size_t)(N - k) * D + da]);
+        hb = conjf2(Hm[(size_t)(N - k) * D + db]);
+      }
+      buf[k1 * W + s * WCM + cc] = pair_product(xk, xp, ha, hb);
+    }
+  }
+  if constexpr (!SPECTRA) {
+    __syncthreads();
+    fft::lds_passes<N1, 0, fft::Plan<N1>::NP, G * WCM, W, NT, true>(buf, tw);
+    for (int u = (int)threadIdx.x; u < N1 * G * WCM; u += NT) {
+      const int n1 = u / (G * WCM), sc = u - n1 * (G * WCM);
+      const int s = sc / WCM, cc = sc - s * WCM;
+      const int x = x0 + cc;
+      if (x >= ch.nvalid) continue;
+      const int k2 = kA + s;
+      E[(size_t)(n1 * N2 + k2) * ch.cstride + x] = cmulc(buf[n1 * W + s * WCM + cc], fft::twiddle<false>(tw, N, n1 * k2));
+    }
+  }
+}
+
+// Pass R': inverse N2-point FFT of E[n1][.] for each n1; output n2 >= N2/2 is
+// time index n = n1 + N1 n2 >= U and is added into state row i + n - U when
+// n - U < dst_len.
+template <int N2>
+__global__ __launch_bounds__(Cfg<N2>::NT) void k_fft_rows_inv(const float2* __restrict__ E,
+                                                              float* __restrict__ S, int L, int i,
+                                                              int dst_len, Chunk ch,
+                                                              const float2* __restrict__ tw) {
+  constexpr int WC = Cfg<N2>::WC, NT = Cfg<N2>::NT;
+  __shared__ float2 buf[N2 * WC];
+  const int npan = (ch.nvalid + WC - 1) / WC;
+  const int q = fft::xcd_logical((int)blockIdx.x, (int)gridDim.x);
+  const int n1 = q / npan;
+  const int x0 = (q - n1 * npan) * WC;
+  for (int u = (int)threadIdx.x; u < N2 * WC; u += NT) {
+    const int k2 = u / WC, col = u - k2 * WC;
+    const int x = x0 + col;
+    buf[u] = x < ch.nvalid ? E[(size_t)(n1 * N2 + k2) * ch.cstride + x] : make_float2(0.f, 0.f);
+  }
+  __syncthreads();
+  const int N1 = ch.N1, U = N1 * N2 / 2, BD = ch.ncols;
+  const bool vec = (BD & 1) == 0;
+  fft::inverse_to_global<N2, WC, WC, NT, true>(buf, tw, [&](int n2, int col, float2 v) {
+    const int x = x0 + col;
+    const int oi = n1 + N1 * n2 - U;
+    if (x >= ch.nvalid || oi >= dst_len) return;
+    const int g = ch.g0 + x;
+    const int m = g / ch.ncc;
+    const int c = 2 * (g - m * ch.ncc);
+    add_pair(S + ((size_t)m * L + i + oi) * BD, c, BD, vec, v);
+  });
+}
+
+// ------------------------------------------------------------- dispatch
+
+#define LCSM_POW2_CASES(X) X(4) X(8) X(16) X(32) X(64) X(128) X(256) X(512) X(1024) X(2048) X(4096)
+
+hipError_t tile_single(int N, float* S, const float2* H, const float2* tw, const Shape& s, int i,
+                       int dst_len, hipStream_t st) {
+#define LCSM_CASE(NN)                                                                             \
+  case NN: {                                                                                      \
+    constexpr int WC = Cfg<NN>::WC;                                                               \
+    const int ppl = (s.BD + 2 * WC - 1) / (2 * WC);                                               \
+    const int hgroup = (s.D % (2 * WC) == 0) ? s.D / (2 * WC) : 0;                                \
+    hipLaunchKernelGGL(k_fft_tile<NN>, dim3((unsigned)(ppl * s.M)), dim3(Cfg<NN>::NT), 0, st, S, \
+                       H, tw, s.L, s.BD, s.D, s.B, i, dst_len, ppl, hgroup);                      \
+    return hipGetLastError();                                                                     \
+  }
+  switch (N) { LCSM_POW2_CASES(LCSM_CASE) }
+#undef LCSM_CASE
+  return hipErrorInvalidValue;
+}
+
+hipError_t spectra_single(int N, const float* Hf, float2* Hout, const float2* tw, const Shape& s,
+                          hipStream_t st) {
+#define LCSM_CASE(NN)                                                                            \
+  case NN: {                                                                                     \
+    const int ppl = (s.D + 2 * Cfg<NN>::WC - 1) / (2 * Cfg<NN>::WC);                             \
+    hipLaunchKernelGGL(k_fft_spectra<NN>, dim3((unsigned)(ppl * s.M)), dim3(Cfg<NN>::NT), 0, st, \
+                       Hf, Hout, tw, s.L, s.D, ppl);                                             \
+    return hipGetLastError();                                                                    \
+  }
+  switch (N) { LCSM_POW2_CASES(LCSM_CASE) }
+#undef LCSM_CASE
+  return hipErrorInvalidValue;
+}
+
+#define LCSM_ROW_CASES(X) X(16) X(32) X(64) X(128) X(256) X(512) X(1024) X(2048) X(4096)
+#define LCSM_MID_CASES(X) X(2) X(4) X(8) X(16) X(32) X(64) X(128)
+
+template <bool HALF>
+hipError_t rows_fwd(const float* src, size_t lstride, int row0, int rows_valid, const Chunk& ch,
+                    float2* C, const float2* tw, hipStream_t st) {
+#define LCSM_CASE(NN)                                                                            \
+  case NN: {                                                                                     \
+    const int npan = (ch.nvalid + Cfg<NN>::WC - 1) / Cfg<NN>::WC;                                \
+    hipLaunchKernelGGL((k_fft_rows_fwd<NN, HALF>), dim3((unsigned)(npan * ch.N1)),               \
+                       dim3(Cfg<NN>::NT), 0, st, src, lstride, row0, rows_valid, ch, C, tw);     \
+    return hipGetLastError();                                                                    \
+  }
+  switch (ch.N2) { LCSM_ROW_CASES(LCSM_CASE) }
+#undef LCSM_CASE
+  return hipErrorInvalidValue;
+}
+
+hipError_t rows_inv(const float2* E, float* S, int L, int i, int dst_len, const Chunk& ch,
+                    const float2* tw, hipStream_t st) {
+#define LCSM_CASE(NN)                                                                         \
+  case NN: {                                                                                  \
+    const int npan = (ch.nvalid + Cfg<NN>::WC - 1) / Cfg<NN>::WC;                             \
+    hipLaunchKernelGGL(k_fft_rows_inv<NN>, dim3((unsigned)(npan * ch.N1)), dim3(Cfg<NN>::NT), \
+                       0, st, E, S, L, i, dst_len, ch, tw);                                   \
+    return hipGetLastError();                                                                 \
+  }
+  switch (ch.N2) { LCSM_ROW_CASES(LCSM_CASE) }
+#undef LCSM_CASE
+  return hipErrorInvalidValue;
+}
+
+template <bool SPECTRA>
+hipError_t mid(const float2* C, float2* E, const float2* H, float2* Hout, int D, const Chunk& ch,
+               const float2* tw, hipStream_t st) {
+  const int npan = (ch.nvalid + kMidWC - 1) / kMidWC;
+  const dim3 grid((unsigned)(npan * (ch.N2 / kMidG)));
+#define LCSM_CASE(NN)                                                                            \
+  case NN:                                                                                       \
+    hipLaunchKernelGGL((k_fft_mid<NN, SPECTRA>), grid, dim3(kMidNT), 0, st, C, E, H, Hout, D, ch, \
+                       tw);                                                                      \
+    return hipGetLastError();
+  switch (ch.N1) { LCSM_MID_CASES(LCSM_CASE) }
+#undef LCSM_CASE
+  return hipErrorInvalidValue;
+}
+
+// Row length of the multi-pass split of an N-point transform.
+int split_n2(int N, int lds_max_n) {
+  int n2 = lds_max_n;
+  while (N / n2 > kMaxMidN1) n2 *= 2;
+  return n2;
+}
+
+}  // namespace
+
+int fft_multipass_chunk(int N, int lds_max_n, size_t scratch_bytes, int total_cc) {
+  (void)lds_max_n;
+  // C and E: 2 * N complex values per chunk column
+  long long cap = (long long)(scratch_bytes / (2 * sizeof(float2) * (size_t)N));
+  cap = cap / 16 * 16;
+  const long long need = ((long long)total_cc + 15) / 16 * 16;
+  if (cap > need) cap = need;
+  return (int)cap;
+}
+
+hipError_t launch_spectra(const float* Hf, float2* Hout, const float2* tw, const Shape& s, int U,
+                          int lds_max_n, float2* scratch, size_t scratch_bytes, hipStream_t st) {
+  const int N = 2 * U;
+  if (N <= lds_max_n) return spectra_single(N, Hf, Hout, tw, s, st);
+  Chunk ch{};
+  ch.ncols = s.D;
+  ch.ncc = (s.D + 1) / 2;
+  ch.N2 = split_n2(N, lds_max_n);
+  ch.N1 = N / ch.N2;
+  const int total = s.M * ch.ncc;
+  ch.cstride = fft_multipass_chunk(N, lds_max_n, scratch_bytes, total);
+  if (ch.cstride <= 0) return hipErrorOutOfMemory;
+  float2* C = scratch;
+  for (int g0 = 0; g0 < total; g0 += ch.cstride) {
+    ch.g0 = g0;
+    ch.nvalid = total - g0 < ch.cstride ? total - g0 : ch.cstride;
+    hipError_t e = rows_fwd<false>(Hf, (size_t)s.L * s.D, 0, s.L, ch, C, tw, st);
+    if (e == hipSuccess) e = mid<true>(C, nullptr, nullptr, Hout, s.D, ch, tw, st);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+hipError_t launch_fft_tile(float* S, const float2* H, const float2* tw, const Shape& s, int i,
+                           int U, int dst_len, int lds_max_n, float2* scratch, size_t scratch_bytes,
+                           hipStream_t st) {
+  if (dst_len <= 0) return hipSuccess;
+  const int N = 2 * U;
+  if (N <= lds_max_n) return tile_single(N, S, H, tw, s, i, dst_len, st);
+  Chunk ch{};
+  ch.ncols = s.BD;
+  ch.ncc = (s.BD + 1) / 2;
+  ch.N2 = split_n2(N, lds_max_n);
+  ch.N1 = N / ch.N2;
+  const int total = s.M * ch.ncc;
+  ch.cstride = fft_multipass_chunk(N, lds_max_n, scratch_bytes, total);
+  if (ch.cstride <= 0) return hipErrorOutOfMemory;
+  float2* C = scratch;
+  float2* E = scratch + (size_t)N * ch.cstride;
+  for (int g0 = 0; g0 < total; g0 += ch.cstride) {
+    ch.g0 = g0;
+    ch.nvalid = total - g0 < ch.cstride ? total - g0 : ch.cstride;
+    hipError_t e = rows_fwd<true>(S, (size_t)s.L * s.BD, i - U, i, ch, C, tw, st);
+    if (e == hipSuccess) e = mid<false>(C, E, H, nullptr, s.D, ch, tw, st);
+    if (e == hipSuccess) e = rows_inv(E, S, s.L, i, dst_len, ch, tw, st);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+}  // namespace lcsm

@@ -1,0 +1,258 @@
+// Radix-8/4/2 Stockham FFT over columns held in LDS, for gfx950.
+//
+// A workgroup transforms WC complex columns of N points at once.  The LDS
+// buffer is laid out [n][col] with a row stride of LDSW float2 (LDSW >= WC),
+// so one row of the buffer is a contiguous run of the workgroup's columns and
+// a wavefront touches consecutive 8-byte words.
+//
+// Pass structure (Stockham autosort, no bit reversal).  With p the product of
+// the radices already applied (p = 1 before the first pass), a radix-R pass
+// maps, for every j < N/R with k = j mod p,
+//     u_q = x[j + q N/R] * w_{pR}^{q k}         (q < R)
+//     x'[(j - k) R + k + s p] = sum_q u_q w_R^{q s}   (s < R)
+// where w_n = exp(-2 pi i / n) for the forward and exp(+2 pi i / n) for the
+// inverse transform (no 1/N factor).  After the last pass x' is the DFT in
+// natural order.  Passes are radix 8 except possibly the last (radix 2 or 4).
+//
+// Twiddles come from a table tw[n + m] = exp(-2 pi i m / n) for every power of
+// two n (m < n), built on the host in double precision and rounded once.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+namespace lcsm {
+namespace fft {
+
+__device__ __forceinline__ float2 cadd(float2 a, float2 b) { return make_float2(a.x + b.x, a.y + b.y); }
+__device__ __forceinline__ float2 csub(float2 a, float2 b) { return make_float2(a.x - b.x, a.y - b.y); }
+__device__ __forceinline__ float2 cmul(float2 a, float2 b) {
+  return make_float2(fmaf(a.x, b.x, -a.y * b.y), fmaf(a.x, b.y, a.y * b.x));
+}
+// a * conj(b)
+__device__ __forceinline__ float2 cmulc(float2 a, float2 b) {
+  return make_float2(fmaf(a.x, b.x, a.y * b.y), fmaf(a.y, b.x, -a.x * b.y));
+}
+__device__ __forceinline__ float2 conjf2(float2 a) { return make_float2(a.x, -a.y); }
+
+// Twiddle w_n^e (forward sign) or its conjugate (inverse), 0 <= e < n.
+template <bool INV>
+__device__ __forceinline__ float2 twiddle(const float2* __restrict__ tw, int n, int e) {
+  const float2 w = tw[n + e];
+  return INV ? conjf2(w) : w;
+}
+
+// multiply by w_4 (forward -i, inverse +i)
+template <bool INV>
+__device__ __forceinline__ float2 rot90(float2 a) {
+  return INV ? make_float2(-a.y, a.x) : make_float2(a.y, -a.x);
+}
+// multiply by w_8
+template <bool INV>
+__device__ __forceinline__ float2 rot45(float2 a) {
+  constexpr float c = 0.70710678118654752440f;
+  return INV ? make_float2(c * (a.x - a.y), c * (a.x + a.y)) : make_float2(c * (a.x + a.y), c * (a.y - a.x));
+}
+// multiply by w_8^3
+template <bool INV>
+__device__ __forceinline__ float2 rot135(float2 a) {
+  constexpr float c = 0.70710678118654752440f;
+  return INV ? make_float2(-c * (a.x + a.y), c * (a.x - a.y)) : make_float2(c * (a.y - a.x), -c * (a.x + a.y));
+}
+
+template <bool INV>
+__device__ __forceinline__ void dft2(float2& a, float2& b) {
+  const float2 t = a;
+  a = cadd(t, b);
+  b = csub(t, b);
+}
+
+template <bool INV>
+__device__ __forceinline__ void dft4(float2& a0, float2& a1, float2& a2, float2& a3) {
+  const float2 t0 = cadd(a0, a2), t1 = csub(a0, a2);
+  const float2 t2 = cadd(a1, a3), t3 = rot90<INV>(csub(a1, a3));
+  a0 = cadd(t0, t2);
+  a2 = csub(t0, t2);
+  a1 = cadd(t1, t3);
+  a3 = csub(t1, t3);
+}
+
+template <int R, bool INV>
+__device__ __forceinline__ void dft(float2* v) {
+  if constexpr (R == 2) {
+    dft2<INV>(v[0], v[1]);
+  } else if constexpr (R == 4) {
+    dft4<INV>(v[0], v[1], v[2], v[3]);
+  } else {
+    static_assert(R == 8, "radix 2, 4 or 8");
+    float2 e0 = v[0], e1 = v[2], e2 = v[4], e3 = v[6];
+    float2 o0 = v[1], o1 = v[3], o2 = v[5], o3 = v[7];
+    dft4<INV>(e0, e1, e2, e3);
+    dft4<INV>(o0, o1, o2, o3);
+    o1 = rot45<INV>(o1);
+    o2 = rot90<INV>(o2);
+    o3 = rot135<INV>(o3);
+    v[0] = cadd(e0, o0);
+    v[4] = csub(e0, o0);
+    v[1] = cadd(e1, o1);
+    v[5] = csub(e1, o1);
+    v[2] = cadd(e2, o2);
+    v[6] = csub(e2, o2);
+    v[3] = cadd(e3, o3);
+    v[7] = csub(e3, o3);
+  }
+}
+
+constexpr int ilog2(int n) { return n <= 1 ? 0 : 1 + ilog2(n / 2); }
+
+// Radix plan of an N-point transform.
+template <int N>
+struct Plan {
+  static_assert(N >= 2 && (N & (N - 1)) == 0, "power of two");
+  static constexpr int LOG = ilog2(N);
+  static constexpr int N8 = LOG / 3;               // radix-8 passes
+  static constexpr int REM = LOG - 3 * N8;         // 0, 1 or 2
+  static constexpr int NP = N8 + (REM ? 1 : 0);    // passes
+  static constexpr int radix(int ps) { return ps < N8 ? 8 : (1 << REM); }
+  static constexpr int p_before(int ps) { return ps <= N8 ? (1 << (3 * ps)) : N; }
+};
+
+// One radix-R pass (pass index PS of Plan<N>) in LDS, in place: every thread
+// loads the inputs of all its butterflies, the workgroup synchronises, then
+// every thread writes its outputs.  Callers synchronise before the first pass.
+template <int N, int PS, int WC, int LDSW, int NT, bool INV>
+__device__ __forceinline__ void lds_pass(float2* buf, const float2* __restrict__ tw) {
+  constexpr int R = Plan<N>::radix(PS);
+  constexpr int P = Plan<N>::p_before(PS);
+  constexpr int UNITS = N / R * WC;
+  constexpr int UPT = (UNITS + NT - 1) / NT;
+  float2 v[UPT][R];
+#pragma unroll
+  for (int a = 0; a < UPT; ++a) {
+    const int u = (int)threadIdx.x + a * NT;
+    if (UNITS % NT == 0 || u < UNITS) {
+      const int j = u / WC, col = u % WC;
+#pragma unroll
+      for (int q = 0; q < R; ++q) v[a][q] = buf[(j + q * (N / R)) * LDSW + col];
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int a = 0; a < UPT; ++a) {
+    const int u = (int)threadIdx.x + a * NT;
+    if (UNITS % NT == 0 || u < UNITS) {
+      const int j = u / WC, col = u % WC;
+      const int k = j & (P - 1);
+      if constexpr (P > 1) {
+#pragma unroll
+        for (int q = 1; q < R; ++q) v[a][q] = cmul(v[a][q], twiddle<INV>(tw, P * R, q * k));
+      }
+      dft<R, INV>(v[a]);
+#pragma unroll
+      for (int s = 0; s < R; ++s) buf[((j - k) * R + k + s * P) * LDSW + col] = v[a][s];
+    }
+  }
+  __syncthreads();
+}
+
+template <int N, int PS, int PE, int WC, int LDSW, int NT, bool INV>
+__device__ __forceinline__ void lds_passes(float2* buf, const float2* __restrict__ tw) {
+  if constexpr (PS < PE) {
+    lds_pass<N, PS, WC, LDSW, NT, INV>(buf, tw);
+    lds_passes<N, PS + 1, PE, WC, LDSW, NT, INV>(buf, tw);
+  }
+}
+
+// First pass (index 0, p = 1, no twiddles) with inputs fetched by
+// load(row, col) instead of from LDS; only rows < N*QIN/R are fetched (the
+// rest are zero: QIN = R/2 for a zero-padded upper half, R for full input).
+// Writes its outputs to LDS and synchronises.
+template <int N, int WC, int LDSW, int NT, bool INV, bool HALF, class Load>
+__device__ __forceinline__ void first_pass_global(float2* buf, const Load& load) {
+  constexpr int R = Plan<N>::radix(0);
+  constexpr int QIN = HALF ? R / 2 : R;
+  constexpr int UNITS = N / R * WC;
+  constexpr int UPT = (UNITS + NT - 1) / NT;
+  float2 v[UPT][R];
+#pragma unroll
+  for (int a = 0; a < UPT; ++a) {
+    const int u = (int)threadIdx.x + a * NT;
+    if (UNITS % NT == 0 || u < UNITS) {
+      const int j = u / WC, col = u % WC;
+#pragma unroll
+      for (int q = 0; q < R; ++q) v[a][q] = (q < QIN) ? load(j + q * (N / R), col) : make_float2(0.f, 0.f);
+    }
+  }
+#pragma unroll
+  for (int a = 0; a < UPT; ++a) {
+    const int u = (int)threadIdx.x + a * NT;
+    if (UNITS % NT == 0 || u < UNITS) {
+      const int j = u / WC, col = u % WC;
+      dft<R, INV>(v[a]);
+#pragma unroll
+      for (int s = 0; s < R; ++s) buf[(j * R + s) * LDSW + col] = v[a][s];
+    }
+  }
+  __syncthreads();
+}
+
+// Last pass (index NP-1, p = N/R) reading LDS and handing the outputs of
+// rows >= N/2 (HALF) or of all rows to store(row, col, value) instead of
+// writing LDS.  No synchronisation at the end (LDS is only read).
+template <int N, int WC, int LDSW, int NT, bool INV, bool HALF, class Store>
+__device__ __forceinline__ void last_pass_global(const float2* buf, const float2* __restrict__ tw,
+                                                 const Store& store) {
+  constexpr int PS = Plan<N>::NP - 1;
+  constexpr int R = Plan<N>::radix(PS);
+  constexpr int P = Plan<N>::p_before(PS);
+  static_assert(P * R == N, "last pass");
+  constexpr int UNITS = N / R * WC;
+  constexpr int UPT = (UNITS + NT - 1) / NT;
+  constexpr int S0 = HALF ? R / 2 : 0;
+#pragma unroll
+  for (int a = 0; a < UPT; ++a) {
+    const int u = (int)threadIdx.x + a * NT;
+    if (UNITS % NT == 0 || u < UNITS) {
+      const int j = u / WC, col = u % WC;  // j < P, so k = j
+      float2 v[R];
+#pragma unroll
+      for (int q = 0; q < R; ++q) v[q] = buf[(j + q * (N / R)) * LDSW + col];
+      if constexpr (P > 1) {
+#pragma unroll
+        for (int q = 1; q < R; ++q) v[q] = cmul(v[q], twiddle<INV>(tw, N, q * j));
+      }
+      dft<R, INV>(v);
+#pragma unroll
+      for (int s = S0; s < R; ++s) store(j + s * P, col, v[s]);
+    }
+  }
+}
+
+// Forward transform whose input is fetched by load(): first pass from
+// global, the rest in LDS.  Result in LDS, natural order.
+template <int N, int WC, int LDSW, int NT, bool HALF, class Load>
+__device__ __forceinline__ void forward_from_global(float2* buf, const float2* __restrict__ tw,
+                                                    const Load& load) {
+  first_pass_global<N, WC, LDSW, NT, false, HALF>(buf, load);
+  lds_passes<N, 1, Plan<N>::NP, WC, LDSW, NT, false>(buf, tw);
+}
+
+// Inverse transform of the LDS contents whose outputs go to store() (rows >=
+// N/2 only when HALF).  The caller synchronises before.
+template <int N, int WC, int LDSW, int NT, bool HALF, class Store>
+__device__ __forceinline__ void inverse_to_global(float2* buf, const float2* __restrict__ tw,
+                                                  const Store& store) {
+  lds_passes<N, 0, Plan<N>::NP - 1, WC, LDSW, NT, true>(buf, tw);
+  last_pass_global<N, WC, LDSW, NT, true, HALF>(buf, tw, store);
+}
+
+// Hardware dispatches workgroup b to XCD b mod 8.  Remap so that XCD x runs a
+// contiguous range of logical workgroup ids (neighbours then share that
+// XCD's L2).  A bijection on [0, nb).
+__device__ __forceinline__ int xcd_logical(int b, int nb) {
+  const int per = nb / 8;
+  if (b >= per * 8) return b;
+  return (b % 8) * per + b / 8;
+}
+
+}  // namespace fft
+}  // namespace lcsm

@@ -42,4 +42,29 @@ hipError_t launch_direct_tile(float* S, const float* Hf, const Shape& s, int i, 
 // Fill n floats with zero (a kernel, so it is safe under graph capture).
 hipError_t launch_zero(float* p, size_t n, hipStream_t st);
 
+// ---- FFT tiles (lcsm_fft.hip)
+
+// Largest column-DFT length of the multi-pass split (N = N1 * N2).
+constexpr int kMaxMidN1 = 128;
+// Row-FFT lengths the single-pass and multi-pass kernels are built for.
+constexpr int kMinLdsFftN = 16;
+constexpr int kMaxLdsFftN = 4096;
+
+// Complex columns per multi-pass chunk for an N-point transform over
+// total_cc complex columns when the scratch holds scratch_bytes (a multiple
+// of 16, or 0 if the scratch cannot hold one chunk of 16).
+int fft_multipass_chunk(int N, int lds_max_n, size_t scratch_bytes, int total_cc);
+
+// Filter spectra of tile size U (N = 2U): Hout[m][k][d] = DFT_N(h[m,d,0:N))[k]
+// / N for k = 0..U.  tw: twiddle table (see lcsm_fft_core.h).
+hipError_t launch_spectra(const float* Hf, float2* Hout, const float2* tw, const Shape& s, int U,
+                          int lds_max_n, float2* scratch, size_t scratch_bytes, hipStream_t st);
+
+// FFT gray tile of all layers: y rows [i-U, i) -> z rows [i, i+dst_len),
+// with the spectra H of tile size U.  Single LDS pass when 2U <= lds_max_n,
+// else the chunked multi-pass transform through scratch.
+hipError_t launch_fft_tile(float* S, const float2* H, const float2* tw, const Shape& s, int i,
+                           int U, int dst_len, int lds_max_n, float2* scratch,
+                           size_t scratch_bytes, hipStream_t st);
+
 }  // namespace lcsm

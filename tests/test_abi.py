@@ -77,7 +77,8 @@ def test_workspace_bytes_covers_state_and_filters():
 
 
 @pytest.mark.parametrize("opts", [{"direct_max_u": 3}, {"lds_fft_max_n": 100},
-                                  {"direct_max_u": -1}])
+                                  {"direct_max_u": -1}, {"lds_fft_max_n": 8},
+                                  {"lds_fft_max_n": 8192}, {"scratch_mib": -1}])
 def test_bad_options_rejected(opts):
     with pytest.raises(lcsm.LcsmError) as e:
         lcsm.workspace_bytes(1, 1, 1, 16, opts)
@@ -89,6 +90,41 @@ def test_reserved_options_must_be_zero():
     o.reserved[2] = 1
     with pytest.raises(lcsm.LcsmError):
         lcsm.workspace_bytes(1, 1, 1, 16, o)
+
+
+def test_options_struct_matches_header():
+    text = open(os.path.join(ROOT, "include", "lcsm.h")).read()
+    body = text[text.index("typedef struct lcsm_options"):text.index("} lcsm_options;")]
+    body = re.sub(r"/\*.*?\*/", "", body, flags=re.S)
+    fields = re.findall(r"int\s+([a-z_]+)(?:\[(\d+)\])?;", body)
+    assert [f for f, _ in fields] == [f for f, _ in lcsm.Options._fields_]
+    assert ctypes.sizeof(lcsm.Options) == 32
+
+
+def test_workspace_grows_with_fft_levels():
+    M, B, D, L = 2, 4, 96, 4096
+    direct = lcsm.workspace_bytes(M, B, D, L, {"direct_max_u": 1 << 20})
+    fft = lcsm.workspace_bytes(M, B, D, L)
+    # spectra of U = 64..2048: M * (U+1) * D complex values each
+    spectra = sum(8 * M * (u + 1) * D for u in (64, 128, 256, 512, 1024, 2048))
+    assert fft >= direct + spectra
+    # the multi-pass scratch obeys the cap but never drops below one chunk
+    small = lcsm.workspace_bytes(M, B, D, L, {"lds_fft_max_n": 16, "scratch_mib": 1})
+    big = lcsm.workspace_bytes(M, B, D, L, {"lds_fft_max_n": 16, "scratch_mib": 4096})
+    assert small < big
+    assert small >= direct + spectra + 2 * 8 * 4096 * 16
+
+
+def test_plan_tile_default_kinds_for_workloads():
+    # default: direct up to U = 32, one LDS pass up to 2U = 2048, multi-pass above
+    L = 1 << 17
+    kinds = {}
+    for t in range(L - 1):
+        _, U, _, k = lcsm.plan_tile(18, 1, 1024, L, t)
+        kinds[U] = k
+    assert all(kinds[1 << q] == lcsm.TILE_DIRECT for q in range(6))
+    assert all(kinds[1 << q] == lcsm.TILE_FFT for q in range(6, 11))
+    assert all(kinds[1 << q] == lcsm.TILE_FFT_HBM for q in range(11, 17))
 
 
 def test_init_validates_before_touching_the_device():

@@ -1,0 +1,161 @@
+"""GPU parity of the FFT gray tiles (needs an MI355X).
+
+The tiles with U above the crossover run as 2U-point cyclic FFT
+convolutions with precomputed filter spectra (Lemma 1, App. B): in one LDS
+pass when 2U fits, else in three passes through a chunked scratch buffer.
+The option sets below force each form onto every tile size a short run has,
+including ragged column counts (odd B*D, D not a multiple of the panel
+width) and a scratch cap small enough to need many chunks.
+
+Bars: on small-integer data the exact result is an integer and the fp32
+FFT error stays far below 1/2, so the rounded GPU output must equal the
+exact int64 convolution; on random data max|z_gpu - z_ref| <= 1e-4 *
+max|z_ref| against the fp64 oracle.
+"""
+import numpy as np
+import pytest
+import torch
+
+import datagen
+from oracle import conv, feedback
+from oracle.relaxed import filters_to_columns, relaxed_online
+
+from gpu_harness import TOL, dev, make_ctx, rel_err, say
+
+pytestmark = pytest.mark.gpu
+
+FFT_OPTIONS = {
+    # every tile with U >= 2 is an FFT tile, in one LDS pass up to 2U = 4096
+    "lds_from_2": {"direct_max_u": 1, "lds_fft_max_n": 4096},
+    # every tile with 2U > 16 goes through the three-pass form
+    "multipass_from_16": {"direct_max_u": 1, "lds_fft_max_n": 16},
+    # multi-pass with a 1 MiB scratch: many chunks per tile
+    "tiny_scratch": {"direct_max_u": 4, "lds_fft_max_n": 32, "scratch_mib": 1},
+    "default": None,
+}
+
+
+def _int_case(M, B, D, L, r, seed):
+    w = datagen.Workload("int", M, B, D, L, decay=1.0, seed=seed)
+    return w, datagen.int_filters_np(w, r), datagen.int_y_np(w, r)
+
+
+def _exact(h, y):
+    L, M, B, D = y.shape
+    z = np.zeros((L, M, B, D), dtype=np.int64)
+    for m in range(M):
+        for b in range(B):
+            for d in range(D):
+                z[:, m, b, d] = np.convolve(y[:, m, b, d].astype(np.int64),
+                                            h[m, d].astype(np.int64))[:L]
+    return z
+
+
+def _run_full(ctx, y):
+    z = torch.empty_like(y)
+    ctx.run(y, z)
+    torch.cuda.synchronize()
+    return z.cpu().numpy()
+
+
+@pytest.mark.parametrize("opt", ["lds_from_2", "multipass_from_16", "tiny_scratch"])
+@pytest.mark.parametrize("shape", [(2, 3, 40, 300), (1, 1, 5, 257), (3, 2, 33, 1000),
+                                   (1, 4, 64, 2048)])
+def test_integer_data_rounds_to_exact(opt, shape):
+    M, B, D, L = shape
+    say(f"[int fft] M={M} B={B} D={D} L={L} options={opt}")
+    w, h, y = _int_case(M, B, D, L, 3, seed=3 * sum(shape))
+    ctx, _ = make_ctx(w, torch.from_numpy(h).to(dev()), FFT_OPTIONS[opt])
+    z = _run_full(ctx, torch.from_numpy(y).to(dev()))
+    ex = _exact(h, y)
+    err = np.abs(z.astype(np.float64) - ex).max()
+    say(f"  max abs err {err:.3e}")
+    assert err < 0.25
+    assert np.array_equal(np.rint(z).astype(np.int64), ex)
+
+
+@pytest.mark.parametrize("opt", ["lds_from_2", "multipass_from_16", "tiny_scratch", "default"])
+def test_m1b8d768l8k_teacher_forced_all_columns(opt):
+    w = datagen.WORKLOADS["m1b8d768l8k"]
+    say(f"[fft teacher-forced all columns] {w.name} options={opt}")
+    ctx, _ = make_ctx(w, options=FFT_OPTIONS[opt])
+    y = datagen.y_torch(w, dev())
+    z = _run_full(ctx, y)
+    h = filters_to_columns(datagen.filters_np(w), w.B)
+    zr = conv.causal_conv_fft(y.cpu().numpy().reshape(w.L, -1).astype(np.float64), h[:, 0])
+    err = rel_err(z.reshape(w.L, -1), zr)
+    say(f"  rel err {err:.3e}")
+    assert err <= TOL
+
+
+@pytest.mark.parametrize("opt", ["lds_from_2", "multipass_from_16"])
+def test_small_workload_closed_loop(opt):
+    w = datagen.WORKLOADS["m1b1d16l1k"]
+    say(f"[fft closed loop] {w.name} options={opt}")
+    ctx, _ = make_ctx(w, options=FFT_OPTIONS[opt])
+    x = datagen.x_torch(w, dev())
+    z = torch.empty_like(x)
+    for t in range(w.L):
+        ctx.step_chain(x[t], z[t])
+    torch.cuda.synchronize()
+    h = filters_to_columns(datagen.filters_np(w), w.B)
+    zr, _ = relaxed_online(h, feedback.tanh_chain(datagen.x_np(w).reshape(w.L, w.M, -1), w.M))
+    err = rel_err(z.cpu().numpy().reshape(w.L, w.M, -1), zr)
+    say(f"  closed-loop rel err {err:.3e}")
+    assert err <= TOL
+
+
+@pytest.mark.parametrize("opt", ["default", "multipass_from_16"])
+def test_fft_rerun_bitwise_and_step_layer_path(opt):
+    w = datagen.Workload("fftdet", 3, 2, 70, 1500, decay=400.0, seed=12)
+    say(f"[fft determinism / step_layer] M=3 B=2 D=70 L=1500 options={opt}")
+    ctx, filt = make_ctx(w, options=FFT_OPTIONS[opt])
+    y = datagen.y_torch(w, dev())
+    z1 = _run_full(ctx, y)
+    ctx.reset()
+    z2 = _run_full(ctx, y)
+    assert np.array_equal(z1, z2)
+    ctx.reset()
+    z3 = torch.empty_like(y)
+    for t in range(w.L):
+        for m in range(w.M):
+            ctx.step_layer(m, y[t, m], z3[t, m])
+        ctx.advance()
+    torch.cuda.synchronize()
+    assert np.array_equal(z1, z3.cpu().numpy())
+    h = filters_to_columns(datagen.filters_np(w), w.B)
+    yn = y.cpu().numpy().reshape(w.L, w.M, -1).astype(np.float64)
+    zr = conv.causal_conv_fft(yn, h)
+    assert rel_err(z1.reshape(w.L, w.M, -1), zr) <= TOL
+
+
+@pytest.mark.parametrize("opt", ["default", "multipass_from_16"])
+def test_fft_causality_past_outputs_bit_identical(opt):
+    w = datagen.Workload("causal", 2, 2, 96, 1000, decay=300.0, seed=8)
+    say(f"[fft causality] M=2 B=2 D=96 L=1000 options={opt}")
+    ctx, _ = make_ctx(w, options=FFT_OPTIONS[opt])
+    y1 = datagen.y_torch(w, dev())
+    y2 = y1.clone()
+    t0 = 511
+    y2[t0 + 1:] = -y2[t0 + 1:] * 0.5
+    z1 = _run_full(ctx, y1)
+    ctx.reset()
+    z2 = _run_full(ctx, y2)
+    assert np.array_equal(z1[: t0 + 1], z2[: t0 + 1])
+    assert not np.array_equal(z1[t0 + 1:], z2[t0 + 1:])
+
+
+def test_geometric_filter_multipass():
+    """h = r^k (one-state LTI system): z_t = r z_{t-1} + y_t, through the
+    three-pass tiles at every U >= 16."""
+    M, B, D, L = 1, 1, 32, 8192
+    say(f"[geometric multipass] M={M} B={B} D={D} L={L}")
+    w = datagen.Workload("geo", M, B, D, L, decay=1.0, seed=10)
+    r = (0.9 + 0.0995 * np.linspace(0, 1, M * D).reshape(M, D)).astype(np.float32).astype(np.float64)
+    h = (r[:, :, None] ** np.arange(L)[None, None, :]).astype(np.float32)
+    ctx, _ = make_ctx(w, torch.from_numpy(h).to(dev()), FFT_OPTIONS["multipass_from_16"])
+    y = datagen.y_torch(w, dev())
+    z = _run_full(ctx, y)
+    yn = y.cpu().numpy().astype(np.float64)
+    zr = conv.geometric_recurrence(yn[:, 0], r[0][None, :])
+    assert rel_err(z[:, 0], zr) <= TOL

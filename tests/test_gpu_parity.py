@@ -155,18 +155,28 @@ def test_causality_future_inputs_leave_past_outputs_bit_identical():
     assert not np.array_equal(z1[t0 + 1:], z2[t0 + 1:])
 
 
-def test_nan_poison_stays_in_its_column_and_reaches_all_later_outputs():
+@pytest.mark.parametrize("opt", ["all_direct", "default"])
+def test_nan_poison_stays_in_its_column_and_reaches_all_later_outputs(opt):
+    """A NaN input reaches every later output of its column (coverage >= 1,
+    causality).  Direct tiles keep it in that column; FFT tiles carry the
+    real columns c and c^1 of a layer together in one complex transform, so
+    there it may also reach the partner column, and nothing else."""
     w = datagen.Workload("nan", 2, 3, 50, 512, decay=100.0, seed=9)
-    say("[nan poison] M=2 B=3 D=50 L=512")
-    ctx, _ = make_ctx(w)
+    say(f"[nan poison] M=2 B=3 D=50 L=512 options={opt}")
+    ctx, _ = make_ctx(w, options=OPTION_SETS[opt])
     y = datagen.y_torch(w, dev())
     t0, col = 123, (1, 2, 17)
     y[t0, col[0], col[1], col[2]] = float("nan")
     z = _run_full(ctx, y)
-    assert np.all(np.isnan(z[t0:, col[0], col[1], col[2]]))
-    mask = np.ones(z.shape, dtype=bool)
-    mask[t0:, col[0], col[1], col[2]] = False
-    assert np.all(np.isfinite(z[mask]))
+    zc = z.reshape(w.L, w.M, w.B * w.D)
+    c = col[1] * w.D + col[2]
+    assert np.all(np.isnan(zc[t0:, col[0], c]))
+    mask = np.ones(zc.shape, dtype=bool)
+    mask[t0:, col[0], c] = False
+    if opt != "all_direct":
+        mask[t0:, col[0], c ^ 1] = False
+    assert np.all(np.isfinite(zc[mask]))
+    assert np.all(np.isfinite(zc[:t0]))
 
 
 def test_geometric_filter_matches_recurrence():
