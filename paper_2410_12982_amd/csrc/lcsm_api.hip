@@ -57,6 +57,7 @@ int resolve_options(const lcsm_options* o, Options* r) {
 
 int check_shape(int M, int B, int D, int L) {
   if (M < 1 || B < 1 || D < 1 || L < 1) return LCSM_EINVAL;
+  if (M > 65535 || B > 65535) return LCSM_EINVAL;  // grid y/z extents of the step kernels
   if ((long long)M * B * D >= (1LL << 31)) return LCSM_EINVAL;
   if (L > kMaxL) return LCSM_EINVAL;
   return LCSM_OK;

@@ -25,17 +25,21 @@ constexpr int kThreads = 256;
 // tile's newest input y_t then comes from the register, not from memory).
 // U == 0: no tile.  1 <= U <= kFusedMaxU: the tile i = t+1 is computed
 // whole by the thread (U outputs from U inputs and 2U-1 lags).
+// Every load (inputs, lags, the red cell's accumulator and the tile's
+// destination accumulators) is issued before the first store, so the step
+// costs one memory round trip; the slots read and written are distinct rows.
 template <int U, bool RED>
 __global__ __launch_bounds__(kThreads) void k_step_fused(const float* __restrict__ y,
                                                         float* __restrict__ z,
                                                         float* __restrict__ S,
                                                         const float* __restrict__ Hf, int M, int L,
                                                         int BD, int D, int t, int dst_len) {
-  const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  if (e >= (int64_t)M * BD) return;
-  const int m = (int)(e / BD);
-  const int c = (int)(e - (int64_t)m * BD);
-  const int d = c % D;
+  // grid (channel blocks, B, M): no integer division on the critical path
+  const int d = (int)blockIdx.x * kThreads + (int)threadIdx.x;
+  if (d >= D) return;
+  const int m = (int)blockIdx.z;
+  const int c = (int)blockIdx.y * D + d;
+  const size_t e = (size_t)m * BD + c;
   float* col = S + (size_t)m * L * BD + c;
   const float* hc = Hf + (size_t)m * L * D + d;
   const size_t rs = (size_t)BD;
@@ -44,25 +48,30 @@ __global__ __launch_bounds__(kThreads) void k_step_fused(const float* __restrict
   constexpr int NH = U > 0 ? 2 * U : 1;
   float yb[NY];
   float hh[NH];
+  float zo[NY];
   const bool tile = (U > 0) && (dst_len > 0);
+  float yt, acc = 0.f, h0 = 0.f;
+  if constexpr (RED) {
+    yt = y[e];
+    acc = col[(size_t)t * rs];
+    h0 = hc[0];
+  } else {
+    yt = col[(size_t)t * rs];
+  }
   if constexpr (U > 0) {
     if (tile) {
-      // Operands of the tile are issued before the red cell's store so their
-      // latency overlaps it.  Rows t+1-U .. t-1 already hold inputs.
+      // rows t+1-U .. t-1 already hold inputs; row t is y_t
 #pragma unroll
       for (int k = 0; k < U - 1; ++k) yb[k] = col[(size_t)(t + 1 - U + k) * rs];
 #pragma unroll
       for (int l = 1; l < 2 * U; ++l) hh[l] = (l < L) ? hc[(size_t)l * D] : 0.f;
+#pragma unroll
+      for (int j = 0; j < U; ++j) zo[j] = (j < dst_len) ? col[(size_t)(t + 1 + j) * rs] : 0.f;
     }
   }
-  float yt;
   if constexpr (RED) {
-    yt = y[e];
-    const float acc = col[(size_t)t * rs];
-    z[e] = fmaf(hc[0], yt, acc);
+    z[e] = fmaf(h0, yt, acc);
     col[(size_t)t * rs] = yt;
-  } else {
-    yt = col[(size_t)t * rs];
   }
   if constexpr (U > 0) {
     if (tile) {
@@ -73,7 +82,7 @@ __global__ __launch_bounds__(kThreads) void k_step_fused(const float* __restrict
           float o = 0.f;
 #pragma unroll
           for (int k = 0; k < U; ++k) o = fmaf(yb[k], hh[U + j - k], o);
-          col[(size_t)(t + 1 + j) * rs] += o;
+          col[(size_t)(t + 1 + j) * rs] = zo[j] + o;
         }
       }
     }
@@ -90,9 +99,9 @@ __global__ __launch_bounds__(kThreads) void k_chain_fused(const float* __restric
                                                          const float* __restrict__ Hf,
                                                          float* __restrict__ prev, int M, int L,
                                                          int BD, int D, int t, int dst_len) {
-  const int c = blockIdx.x * kThreads + threadIdx.x;
-  if (c >= BD) return;
-  const int d = c % D;
+  const int d = (int)blockIdx.x * kThreads + (int)threadIdx.x;
+  if (d >= D) return;
+  const int c = (int)blockIdx.y * D + d;
   const size_t rs = (size_t)BD;
   constexpr int NY = U > 0 ? U : 1;
   constexpr int NH = U > 0 ? 2 * U : 1;
@@ -220,7 +229,7 @@ inline unsigned blocks_for(int64_t n) { return (unsigned)((n + kThreads - 1) / k
 template <bool RED>
 hipError_t dispatch_fused(int U, const float* y, float* z, float* S, const float* Hf,
                           const Shape& s, int t, int dst_len, hipStream_t st) {
-  const dim3 grid(blocks_for((int64_t)s.M * s.BD)), block(kThreads);
+  const dim3 grid(blocks_for(s.D), (unsigned)s.B, (unsigned)s.M), block(kThreads);
 #define LCSM_FUSED_CASE(UU)                                                                  \
   case UU:                                                                                   \
     hipLaunchKernelGGL((k_step_fused<UU, RED>), grid, block, 0, st, y, z, S, Hf, s.M, s.L, \
@@ -256,7 +265,7 @@ hipError_t launch_step_fused(const float* y, float* z, float* S, const float* Hf
 
 hipError_t launch_chain_fused(const float* x, float* z, float* S, const float* Hf, float* prev,
                               const Shape& s, int t, int U, int dst_len, hipStream_t st) {
-  const dim3 grid(blocks_for(s.BD)), block(kThreads);
+  const dim3 grid(blocks_for(s.D), (unsigned)s.B), block(kThreads);
 #define LCSM_CHAIN_CASE(UU)                                                                   \
   case UU:                                                                                    \
     hipLaunchKernelGGL((k_chain_fused<UU>), grid, block, 0, st, x, z, S, Hf, prev, s.M, s.L, \
