@@ -53,6 +53,8 @@ def parse():
     p.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work, about")
     p.add_argument("--no-kernel-pass", action="store_true")
     p.add_argument("--closed-loop", action="store_true", help="also time the tanh-chain generation")
+    p.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                   help="only run a plain elementwise copy of MIB MiB 5 times (counter calibration)")
     return p.parse_args()
 
 
@@ -110,6 +112,10 @@ def main():
         sys.exit(2)
 
     import torch
+
+    if args.copy_probe:
+        copy_probe(args.copy_probe, torch)
+        return
 
     import datagen
     import paper_2410_12982_amd.lcsm as lcsm
@@ -205,6 +211,19 @@ def main():
     if closed:
         out["closed_loop"] = closed
     print(json.dumps(out), flush=True)
+
+
+def copy_probe(mib, torch):
+    """A plain elementwise kernel reading and writing mib MiB each (b = -a),
+    five times: the reference for scaling the HBM byte counters."""
+    n = mib * (1 << 20) // 4
+    a = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        torch.neg(a, out=b)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_mib": mib, "bytes_read": 4 * n, "bytes_written": 4 * n}), flush=True)
 
 
 def kernel_pass(w, filters, y, z, opts, lcsm, torch):

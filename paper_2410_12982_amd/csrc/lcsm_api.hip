@@ -16,7 +16,7 @@ namespace {
 
 constexpr size_t kAlign = 256;
 constexpr int kDefaultDirectMaxU = 32;     // tiles U <= 32 direct (fused with the red cell)
-constexpr int kDefaultLdsFftMaxN = 2048;   // 2U <= 2048: one LDS pass
+constexpr int kDefaultLdsFftMaxN = 8192;   // 2U <= 8192: one LDS pass
 constexpr int kDefaultScratchMib = 512;    // multi-pass FFT scratch cap
 constexpr int kMaxL = 1 << 19;             // FFT lengths up to 2^19 are built
 constexpr int kMaxLevels = 20;

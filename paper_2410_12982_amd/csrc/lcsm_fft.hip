@@ -35,6 +35,8 @@
 //   pass R' : for each n1 the inverse N2-point FFT of E; outputs n2 >= N2/2
 //             are the time indices U..N-1, added into the state.
 // C and E live in a scratch buffer, processed in chunks of columns.
+#include <type_traits>
+
 #include "lcsm_fft_core.h"
 #include "lcsm_internal.h"
 
@@ -49,11 +51,31 @@ using fft::csub;
 
 // Per-size launch shape of the LDS transforms: WC complex columns per
 // workgroup, NT threads.  WC * 8 bytes is the contiguous run read per row.
+// Up to 2U = 2048 two workgroups fit in one CU's 160 KB of LDS (data plus the
+// twiddle table w_N^m), so one workgroup's global loads overlap the other's
+// LDS passes.  TWL: the twiddle table fits in LDS beside the data.
 template <int N>
 struct Cfg {
-  static constexpr int WC = N <= 512 ? 16 : (N <= 2048 ? 8 : 4);
-  static constexpr int NT = N <= 256 ? 128 : (N <= 1024 ? 256 : 512);
+  static constexpr int WC = N <= 512 ? 16 : (N <= 1024 ? 8 : (N <= 4096 ? 4 : 2));
+  static constexpr int NT = N <= 256 ? 128 : (N <= 2048 ? 256 : 512);
+  static constexpr bool TWL = (size_t)N * 8 * (WC + 1) <= 163840;
 };
+
+// Twiddle source of an N-point transform: LDS copy when it fits, else the
+// global table.  The LDS copy is written here and read after the caller's
+// next __syncthreads.
+template <int N>
+using TwOf = typename std::conditional<Cfg<N>::TWL, fft::TwLds<N>, fft::TwGlobal>::type;
+
+template <int N>
+__device__ __forceinline__ TwOf<N> make_tw(float2* lds, const float2* __restrict__ tw) {
+  if constexpr (Cfg<N>::TWL) {
+    fft::load_twiddles<N, Cfg<N>::NT>(lds, tw);
+    return fft::TwLds<N>{lds};
+  } else {
+    return fft::TwGlobal{tw};
+  }
+}
 
 // Pair load / accumulate of real columns c, c+1 of a row.
 __device__ __forceinline__ float2 load_pair(const float* __restrict__ row, int c, int ncols, bool vec) {
@@ -86,6 +108,11 @@ __device__ __forceinline__ float2 pair_product(float2 zk, float2 znk, float2 ha,
 
 // ----------------------------------------------------------- single pass
 
+// Every global load of a stage is issued before that stage needs it: the
+// spectrum bins of the spectral product right after the first forward pass
+// (in flight during the other forward passes), and the destination rows of
+// the last inverse pass before the inverse passes start.  Without this the
+// per-unit loads in loops that also store would each cost a full round trip.
 template <int N>
 __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_tile(float* __restrict__ S,
                                                          const float2* __restrict__ H,
@@ -93,7 +120,10 @@ __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_tile(float* __restrict__ S,
                                                          int BD, int D, int B, int i, int dst_len,
                                                          int ppl, int hgroup) {
   constexpr int WC = Cfg<N>::WC, NT = Cfg<N>::NT, U = N / 2;
+  using P = fft::Plan<N>;
   __shared__ float2 buf[N * WC];
+  __shared__ float2 twl[Cfg<N>::TWL ? N : 1];
+  const auto twz = make_tw<N>(twl, tw);
   const int q = fft::xcd_logical((int)blockIdx.x, (int)gridDim.x);
   const int m = q / ppl;
   const int r = q - m * ppl;
@@ -105,30 +135,114 @@ __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_tile(float* __restrict__ S,
   float* Sm = S + (size_t)m * L * BD;
   const float* ysrc = Sm + (size_t)(i - U) * BD;
 
-  fft::forward_from_global<N, WC, WC, NT, true>(buf, tw, [&](int row, int col) {
-    return load_pair(ysrc + (size_t)row * BD, c0 + 2 * col, BD, vec);
-  });
+  // forward: first pass straight from the input rows
+  fft::first_pass_global<N, WC, WC, NT, false, true>(
+      buf, [&](int row, int col) { return load_pair(ysrc + (size_t)row * BD, c0 + 2 * col, BD, vec); });
 
+  // spectrum bins kk = 0..U of this thread's product units, loaded before
+  // the remaining forward passes when the registers allow it (2U <= 4096)
+  constexpr int PUN = (U + 1) * WC;
+  constexpr int PU = (PUN + NT - 1) / NT;
+  constexpr bool PREH = N <= 4096;
+  constexpr int PH = PREH ? PU : 1;
   const float2* Hm = H + (size_t)m * (U + 1) * D;
-  for (int u = (int)threadIdx.x; u < (U + 1) * WC; u += NT) {
-    const int kk = u / WC, col = u - kk * WC;
-    const int c = c0 + 2 * col;
-    if (c >= BD) continue;
-    const int da = c % D;
-    const int db = (c + 1 < BD) ? (c + 1) % D : da;
-    const float2 ha = Hm[(size_t)kk * D + da], hb = Hm[(size_t)kk * D + db];
-    const int nk = (N - kk) & (N - 1);
-    const float2 zk = buf[kk * WC + col], znk = buf[nk * WC + col];
-    buf[kk * WC + col] = pair_product(zk, znk, ha, hb);
-    if (nk != kk) buf[nk * WC + col] = pair_product(znk, zk, conjf2(ha), conjf2(hb));
+  float2 ha[PH], hb[PH];
+  if constexpr (PREH) {
+#pragma unroll
+    for (int a = 0; a < PU; ++a) {
+      const int u = (int)threadIdx.x + a * NT;
+      const int kk = u / WC, col = u - kk * WC;
+      const int c = c0 + 2 * col;
+      ha[a] = hb[a] = make_float2(0.f, 0.f);
+      if (u < PUN && c < BD) {
+        const int da = c % D;
+        const int db = (c + 1 < BD) ? (c + 1) % D : da;
+        ha[a] = Hm[(size_t)kk * D + da];
+        hb[a] = Hm[(size_t)kk * D + db];
+      }
+    }
+  }
+  fft::lds_passes<N, 1, P::NP, WC, WC, NT, false>(buf, twz);
+
+#pragma unroll
+  for (int a = 0; a < PU; ++a) {
+    const int u = (int)threadIdx.x + a * NT;
+    if (u < PUN) {
+      const int kk = u / WC, col = u - kk * WC;
+      const int c = c0 + 2 * col;
+      float2 xa = make_float2(0.f, 0.f), xb = xa;
+      if constexpr (PREH) {
+        xa = ha[a];
+        xb = hb[a];
+      } else if (c < BD) {
+        const int da = c % D;
+        const int db = (c + 1 < BD) ? (c + 1) % D : da;
+        xa = Hm[(size_t)kk * D + da];
+        xb = Hm[(size_t)kk * D + db];
+      }
+      const int nk = (N - kk) & (N - 1);
+      const float2 zk = buf[kk * WC + col], znk = buf[nk * WC + col];
+      buf[kk * WC + col] = pair_product(zk, znk, xa, xb);
+      if (nk != kk) buf[nk * WC + col] = pair_product(znk, zk, conjf2(xa), conjf2(xb));
+    }
+  }
+
+  // destination rows of the last inverse pass (radix RL, p = N/RL): unit j
+  // writes rows j + s N/RL for s >= RL/2, i.e. outputs oi = j + (s - RL/2) N/RL
+  constexpr int RL = P::radix(P::NP - 1);
+  constexpr int PL = N / RL;
+  constexpr int LUN = PL * WC;
+  constexpr int LU = (LUN + NT - 1) / NT;
+  float* zdst = Sm + (size_t)i * BD;
+  constexpr bool PREZ = N <= 4096;  // registers allow the prefetch
+  float2 zo[PREZ ? LU : 1][RL / 2];
+  if constexpr (PREZ) {
+#pragma unroll
+    for (int a = 0; a < LU; ++a) {
+      const int u = (int)threadIdx.x + a * NT;
+      const int j = u / WC, col = u - j * WC;
+#pragma unroll
+      for (int s = 0; s < RL / 2; ++s) {
+        const int oi = j + s * PL;
+        zo[a][s] = (u < LUN && oi < dst_len) ? load_pair(zdst + (size_t)oi * BD, c0 + 2 * col, BD, vec)
+                                             : make_float2(0.f, 0.f);
+      }
+    }
   }
   __syncthreads();
+  fft::lds_passes<N, 0, P::NP - 1, WC, WC, NT, true>(buf, twz);
 
-  float* zdst = Sm + (size_t)i * BD;
-  fft::inverse_to_global<N, WC, WC, NT, true>(buf, tw, [&](int row, int col, float2 v) {
-    const int oi = row - U;
-    if (oi < dst_len) add_pair(zdst + (size_t)oi * BD, c0 + 2 * col, BD, vec, v);
-  });
+#pragma unroll
+  for (int a = 0; a < LU; ++a) {
+    const int u = (int)threadIdx.x + a * NT;
+    if (u < LUN) {
+      const int j = u / WC, col = u - j * WC;  // j < PL, so k = j
+      float2 v[RL];
+#pragma unroll
+      for (int t = 0; t < RL; ++t) v[t] = buf[(j + t * PL) * WC + col];
+      if constexpr (PL > 1) {
+#pragma unroll
+        for (int t = 1; t < RL; ++t) v[t] = cmul(v[t], twz.template get<true, N>(t * j));
+      }
+      fft::dft<RL, true>(v);
+      const int c = c0 + 2 * col;
+#pragma unroll
+      for (int s = 0; s < RL / 2; ++s) {
+        const int oi = j + s * PL;
+        if (oi < dst_len && c < BD) {
+          const float2 zz = PREZ ? zo[PREZ ? a : 0][s] : load_pair(zdst + (size_t)oi * BD, c, BD, vec);
+          const float2 o = make_float2(zz.x + v[RL / 2 + s].x, zz.y + v[RL / 2 + s].y);
+          float* row = zdst + (size_t)oi * BD;
+          if (vec) {
+            *reinterpret_cast<float2*>(row + c) = o;
+          } else {
+            row[c] = o.x;
+            if (c + 1 < BD) row[c + 1] = o.y;
+          }
+        }
+      }
+    }
+  }
 }
 
 // Filter spectra of tile size U = N/2 for all layers: H[m][k][d] =
@@ -140,11 +254,13 @@ __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_spectra(const float* __restr
                                                             int D, int ppl) {
   constexpr int WC = Cfg<N>::WC, NT = Cfg<N>::NT, U = N / 2;
   __shared__ float2 buf[N * WC];
+  __shared__ float2 twl[Cfg<N>::TWL ? N : 1];
+  const auto twz = make_tw<N>(twl, tw);
   const int m = (int)blockIdx.x / ppl;
   const int c0 = ((int)blockIdx.x - m * ppl) * 2 * WC;
   const bool vec = (D & 1) == 0;
   const float* src = Hf + (size_t)m * L * D;
-  fft::forward_from_global<N, WC, WC, NT, false>(buf, tw, [&](int row, int col) {
+  fft::forward_from_global<N, WC, WC, NT, false>(buf, twz, [&](int row, int col) {
     return row < L ? load_pair(src + (size_t)row * D, c0 + 2 * col, D, vec) : make_float2(0.f, 0.f);
   });
   constexpr float inv_n = 1.0f / (float)N;
@@ -186,12 +302,14 @@ __global__ __launch_bounds__(Cfg<N2>::NT) void k_fft_rows_fwd(const float* __res
                                                               const float2* __restrict__ tw) {
   constexpr int WC = Cfg<N2>::WC, NT = Cfg<N2>::NT;
   __shared__ float2 buf[N2 * WC];
+  __shared__ float2 twl[Cfg<N2>::TWL ? N2 : 1];
+  const auto twz = make_tw<N2>(twl, tw);
   const int npan = (ch.nvalid + WC - 1) / WC;
   const int q = fft::xcd_logical((int)blockIdx.x, (int)gridDim.x);
   const int n1 = q / npan;
   const int x0 = (q - n1 * npan) * WC;
   const bool vec = (ch.ncols & 1) == 0;
-  fft::forward_from_global<N2, WC, WC, NT, HALF>(buf, tw, [&](int n2, int col) {
+  fft::forward_from_global<N2, WC, WC, NT, HALF>(buf, twz, [&](int n2, int col) {
     const int x = x0 + col;
     const int row = row0 + n1 + ch.N1 * n2;
     if (x >= ch.nvalid || row >= rows_valid) return make_float2(0.f, 0.f);
@@ -230,6 +348,9 @@ __global__ __launch_bounds__(kMidNT) void k_fft_mid(const float2* __restrict__ C
   constexpr int G = kMidG, WCM = kMidWC, NT = kMidNT;
   constexpr int W = 2 * G * WCM;  // LDS row stride
   __shared__ float2 buf[N1 * W];
+  __shared__ float2 twl[N1];
+  const fft::TwLds<N1> twz{twl};
+  fft::load_twiddles<N1, NT>(twl, tw);
   const int N2 = ch.N2, N = N1 * N2, U = N / 2;
   const int npan = (ch.nvalid + WCM - 1) / WCM;
   const int q = fft::xcd_logical((int)blockIdx.x, (int)gridDim.x);
@@ -245,7 +366,7 @@ __global__ __launch_bounds__(kMidNT) void k_fft_mid(const float2* __restrict__ C
     buf[u] = x < ch.nvalid ? C[(size_t)(n1 * N2 + k2) * ch.cstride + x] : make_float2(0.f, 0.f);
   }
   __syncthreads();
-  fft::lds_passes<N1, 0, fft::Plan<N1>::NP, W, W, NT, false>(buf, tw);
+  fft::lds_passes<N1, 0, fft::Plan<N1>::NP, W, W, NT, false>(buf, twz);
 
   // spectral step over the own columns (partner slots are only read)
   for (int u = (int)threadIdx.x; u < N1 * G * WCM; u += NT) {
@@ -287,7 +408,7 @@ __global__ __launch_bounds__(kMidNT) void k_fft_mid(const float2* __restrict__ C
   }
   if constexpr (!SPECTRA) {
     __syncthreads();
-    fft::lds_passes<N1, 0, fft::Plan<N1>::NP, G * WCM, W, NT, true>(buf, tw);
+    fft::lds_passes<N1, 0, fft::Plan<N1>::NP, G * WCM, W, NT, true>(buf, twz);
     for (int u = (int)threadIdx.x; u < N1 * G * WCM; u += NT) {
       const int n1 = u / (G * WCM), sc = u - n1 * (G * WCM);
       const int s = sc / WCM, cc = sc - s * WCM;
@@ -309,6 +430,8 @@ __global__ __launch_bounds__(Cfg<N2>::NT) void k_fft_rows_inv(const float2* __re
                                                               const float2* __restrict__ tw) {
   constexpr int WC = Cfg<N2>::WC, NT = Cfg<N2>::NT;
   __shared__ float2 buf[N2 * WC];
+  __shared__ float2 twl[Cfg<N2>::TWL ? N2 : 1];
+  const auto twz = make_tw<N2>(twl, tw);
   const int npan = (ch.nvalid + WC - 1) / WC;
   const int q = fft::xcd_logical((int)blockIdx.x, (int)gridDim.x);
   const int n1 = q / npan;
@@ -321,7 +444,7 @@ __global__ __launch_bounds__(Cfg<N2>::NT) void k_fft_rows_inv(const float2* __re
   __syncthreads();
   const int N1 = ch.N1, U = N1 * N2 / 2, BD = ch.ncols;
   const bool vec = (BD & 1) == 0;
-  fft::inverse_to_global<N2, WC, WC, NT, true>(buf, tw, [&](int n2, int col, float2 v) {
+  fft::inverse_to_global<N2, WC, WC, NT, true>(buf, twz, [&](int n2, int col, float2 v) {
     const int x = x0 + col;
     const int oi = n1 + N1 * n2 - U;
     if (x >= ch.nvalid || oi >= dst_len) return;
@@ -334,7 +457,8 @@ __global__ __launch_bounds__(Cfg<N2>::NT) void k_fft_rows_inv(const float2* __re
 
 // ------------------------------------------------------------- dispatch
 
-#define LCSM_POW2_CASES(X) X(4) X(8) X(16) X(32) X(64) X(128) X(256) X(512) X(1024) X(2048) X(4096)
+#define LCSM_POW2_CASES(X) \
+  X(4) X(8) X(16) X(32) X(64) X(128) X(256) X(512) X(1024) X(2048) X(4096) X(8192)
 
 hipError_t tile_single(int N, float* S, const float2* H, const float2* tw, const Shape& s, int i,
                        int dst_len, hipStream_t st) {
@@ -415,7 +539,7 @@ hipError_t mid(const float2* C, float2* E, const float2* H, float2* Hout, int D,
 
 // Row length of the multi-pass split of an N-point transform.
 int split_n2(int N, int lds_max_n) {
-  int n2 = lds_max_n;
+  int n2 = lds_max_n < kMaxRowN2 ? lds_max_n : kMaxRowN2;
   while (N / n2 > kMaxMidN1) n2 *= 2;
   return n2;
 }

@@ -12,7 +12,7 @@
 //     x'[(j - k) R + k + s p] = sum_q u_q w_R^{q s}   (s < R)
 // where w_n = exp(-2 pi i / n) for the forward and exp(+2 pi i / n) for the
 // inverse transform (no 1/N factor).  After the last pass x' is the DFT in
-// natural order.  Passes are radix 8 except possibly the last (radix 2 or 4).
+// natural order.  Passes are radix 8 except possibly the first (radix 2 or 4).
 //
 // Twiddles come from a table tw[n + m] = exp(-2 pi i m / n) for every power of
 // two n (m < n), built on the host in double precision and rounded once.
@@ -34,11 +34,38 @@ __device__ __forceinline__ float2 cmulc(float2 a, float2 b) {
 }
 __device__ __forceinline__ float2 conjf2(float2 a) { return make_float2(a.x, -a.y); }
 
-// Twiddle w_n^e (forward sign) or its conjugate (inverse), 0 <= e < n.
+// Twiddle w_n^e (forward sign) or its conjugate (inverse), 0 <= e < n, from
+// the global table.
 template <bool INV>
 __device__ __forceinline__ float2 twiddle(const float2* __restrict__ tw, int n, int e) {
   const float2 w = tw[n + e];
   return INV ? conjf2(w) : w;
+}
+
+// Twiddle sources of the passes: the global table, or a copy of
+// w_N^m (m < N) in LDS for an N-point transform (w_n^e = w_N^{e N/n}).
+struct TwGlobal {
+  const float2* __restrict__ t;
+  template <bool INV, int NN>
+  __device__ __forceinline__ float2 get(int e) const {
+    return twiddle<INV>(t, NN, e);
+  }
+};
+
+template <int N>
+struct TwLds {
+  const float2* t;
+  template <bool INV, int NN>
+  __device__ __forceinline__ float2 get(int e) const {
+    const float2 w = t[e * (N / NN)];
+    return INV ? conjf2(w) : w;
+  }
+};
+
+// Copy w_N^m, m < N, from the global table into LDS (no synchronisation).
+template <int N, int NT>
+__device__ __forceinline__ void load_twiddles(float2* lds, const float2* __restrict__ tw) {
+  for (int m = (int)threadIdx.x; m < N; m += NT) lds[m] = tw[N + m];
 }
 
 // multiply by w_4 (forward -i, inverse +i)
@@ -104,7 +131,9 @@ __device__ __forceinline__ void dft(float2* v) {
 
 constexpr int ilog2(int n) { return n <= 1 ? 0 : 1 + ilog2(n / 2); }
 
-// Radix plan of an N-point transform.
+// Radix plan of an N-point transform: one radix-2 or radix-4 pass first when
+// log2 N is not a multiple of 3, radix 8 for all others (so the last pass,
+// which may write to global memory, always has few butterflies per thread).
 template <int N>
 struct Plan {
   static_assert(N >= 2 && (N & (N - 1)) == 0, "power of two");
@@ -112,15 +141,18 @@ struct Plan {
   static constexpr int N8 = LOG / 3;               // radix-8 passes
   static constexpr int REM = LOG - 3 * N8;         // 0, 1 or 2
   static constexpr int NP = N8 + (REM ? 1 : 0);    // passes
-  static constexpr int radix(int ps) { return ps < N8 ? 8 : (1 << REM); }
-  static constexpr int p_before(int ps) { return ps <= N8 ? (1 << (3 * ps)) : N; }
+  static constexpr int radix(int ps) { return (REM && ps == 0) ? (1 << REM) : 8; }
+  // product of the radices of passes 0 .. ps-1
+  static constexpr int p_before(int ps) {
+    return ps == 0 ? 1 : (REM ? (1 << REM) * (1 << (3 * (ps - 1))) : (1 << (3 * ps)));
+  }
 };
 
 // One radix-R pass (pass index PS of Plan<N>) in LDS, in place: every thread
 // loads the inputs of all its butterflies, the workgroup synchronises, then
 // every thread writes its outputs.  Callers synchronise before the first pass.
-template <int N, int PS, int WC, int LDSW, int NT, bool INV>
-__device__ __forceinline__ void lds_pass(float2* buf, const float2* __restrict__ tw) {
+template <int N, int PS, int WC, int LDSW, int NT, bool INV, class TW>
+__device__ __forceinline__ void lds_pass(float2* buf, const TW& tw) {
   constexpr int R = Plan<N>::radix(PS);
   constexpr int P = Plan<N>::p_before(PS);
   constexpr int UNITS = N / R * WC;
@@ -144,7 +176,7 @@ __device__ __forceinline__ void lds_pass(float2* buf, const float2* __restrict__
       const int k = j & (P - 1);
       if constexpr (P > 1) {
 #pragma unroll
-        for (int q = 1; q < R; ++q) v[a][q] = cmul(v[a][q], twiddle<INV>(tw, P * R, q * k));
+        for (int q = 1; q < R; ++q) v[a][q] = cmul(v[a][q], tw.template get<INV, P * R>(q * k));
       }
       dft<R, INV>(v[a]);
 #pragma unroll
@@ -154,8 +186,8 @@ __device__ __forceinline__ void lds_pass(float2* buf, const float2* __restrict__
   __syncthreads();
 }
 
-template <int N, int PS, int PE, int WC, int LDSW, int NT, bool INV>
-__device__ __forceinline__ void lds_passes(float2* buf, const float2* __restrict__ tw) {
+template <int N, int PS, int PE, int WC, int LDSW, int NT, bool INV, class TW>
+__device__ __forceinline__ void lds_passes(float2* buf, const TW& tw) {
   if constexpr (PS < PE) {
     lds_pass<N, PS, WC, LDSW, NT, INV>(buf, tw);
     lds_passes<N, PS + 1, PE, WC, LDSW, NT, INV>(buf, tw);
@@ -198,8 +230,8 @@ __device__ __forceinline__ void first_pass_global(float2* buf, const Load& load)
 // Last pass (index NP-1, p = N/R) reading LDS and handing the outputs of
 // rows >= N/2 (HALF) or of all rows to store(row, col, value) instead of
 // writing LDS.  No synchronisation at the end (LDS is only read).
-template <int N, int WC, int LDSW, int NT, bool INV, bool HALF, class Store>
-__device__ __forceinline__ void last_pass_global(const float2* buf, const float2* __restrict__ tw,
+template <int N, int WC, int LDSW, int NT, bool INV, bool HALF, class TW, class Store>
+__device__ __forceinline__ void last_pass_global(const float2* buf, const TW& tw,
                                                  const Store& store) {
   constexpr int PS = Plan<N>::NP - 1;
   constexpr int R = Plan<N>::radix(PS);
@@ -218,7 +250,7 @@ __device__ __forceinline__ void last_pass_global(const float2* buf, const float2
       for (int q = 0; q < R; ++q) v[q] = buf[(j + q * (N / R)) * LDSW + col];
       if constexpr (P > 1) {
 #pragma unroll
-        for (int q = 1; q < R; ++q) v[q] = cmul(v[q], twiddle<INV>(tw, N, q * j));
+        for (int q = 1; q < R; ++q) v[q] = cmul(v[q], tw.template get<INV, N>(q * j));
       }
       dft<R, INV>(v);
 #pragma unroll
@@ -229,18 +261,16 @@ __device__ __forceinline__ void last_pass_global(const float2* buf, const float2
 
 // Forward transform whose input is fetched by load(): first pass from
 // global, the rest in LDS.  Result in LDS, natural order.
-template <int N, int WC, int LDSW, int NT, bool HALF, class Load>
-__device__ __forceinline__ void forward_from_global(float2* buf, const float2* __restrict__ tw,
-                                                    const Load& load) {
+template <int N, int WC, int LDSW, int NT, bool HALF, class TW, class Load>
+__device__ __forceinline__ void forward_from_global(float2* buf, const TW& tw, const Load& load) {
   first_pass_global<N, WC, LDSW, NT, false, HALF>(buf, load);
   lds_passes<N, 1, Plan<N>::NP, WC, LDSW, NT, false>(buf, tw);
 }
 
 // Inverse transform of the LDS contents whose outputs go to store() (rows >=
 // N/2 only when HALF).  The caller synchronises before.
-template <int N, int WC, int LDSW, int NT, bool HALF, class Store>
-__device__ __forceinline__ void inverse_to_global(float2* buf, const float2* __restrict__ tw,
-                                                  const Store& store) {
+template <int N, int WC, int LDSW, int NT, bool HALF, class TW, class Store>
+__device__ __forceinline__ void inverse_to_global(float2* buf, const TW& tw, const Store& store) {
   lds_passes<N, 0, Plan<N>::NP - 1, WC, LDSW, NT, true>(buf, tw);
   last_pass_global<N, WC, LDSW, NT, true, HALF>(buf, tw, store);
 }

@@ -46,9 +46,11 @@ hipError_t launch_zero(float* p, size_t n, hipStream_t st);
 
 // Largest column-DFT length of the multi-pass split (N = N1 * N2).
 constexpr int kMaxMidN1 = 128;
-// Row-FFT lengths the single-pass and multi-pass kernels are built for.
+// Largest row-FFT length of the multi-pass split.
+constexpr int kMaxRowN2 = 4096;
+// Range of the single-pass limit lds_fft_max_n.
 constexpr int kMinLdsFftN = 16;
-constexpr int kMaxLdsFftN = 4096;
+constexpr int kMaxLdsFftN = 8192;
 
 // Complex columns per multi-pass chunk for an N-point transform over
 // total_cc complex columns when the scratch holds scratch_bytes (a multiple

@@ -78,7 +78,7 @@ def test_workspace_bytes_covers_state_and_filters():
 
 @pytest.mark.parametrize("opts", [{"direct_max_u": 3}, {"lds_fft_max_n": 100},
                                   {"direct_max_u": -1}, {"lds_fft_max_n": 8},
-                                  {"lds_fft_max_n": 8192}, {"scratch_mib": -1}])
+                                  {"lds_fft_max_n": 16384}, {"scratch_mib": -1}])
 def test_bad_options_rejected(opts):
     with pytest.raises(lcsm.LcsmError) as e:
         lcsm.workspace_bytes(1, 1, 1, 16, opts)
@@ -116,15 +116,15 @@ def test_workspace_grows_with_fft_levels():
 
 
 def test_plan_tile_default_kinds_for_workloads():
-    # default: direct up to U = 32, one LDS pass up to 2U = 2048, multi-pass above
+    # default: direct up to U = 32, one LDS pass up to 2U = 8192, multi-pass above
     L = 1 << 17
     kinds = {}
     for t in range(L - 1):
         _, U, _, k = lcsm.plan_tile(18, 1, 1024, L, t)
         kinds[U] = k
     assert all(kinds[1 << q] == lcsm.TILE_DIRECT for q in range(6))
-    assert all(kinds[1 << q] == lcsm.TILE_FFT for q in range(6, 11))
-    assert all(kinds[1 << q] == lcsm.TILE_FFT_HBM for q in range(11, 17))
+    assert all(kinds[1 << q] == lcsm.TILE_FFT for q in range(6, 13))
+    assert all(kinds[1 << q] == lcsm.TILE_FFT_HBM for q in range(13, 17))
 
 
 def test_init_validates_before_touching_the_device():
