@@ -100,8 +100,8 @@ Layout layout_for(const Shape& s, const Options& o) {
     off = align_up(off + sizeof(float2) * 2 * (size_t)ly.nmax);
   }
   if (multipass) {
-    // C and E of one chunk: 2 * N complex per complex column
-    const size_t per_col = 2 * sizeof(float2) * (size_t)ly.nmax;
+    // one chunk: N complex values per complex column
+    const size_t per_col = sizeof(float2) * (size_t)ly.nmax;
     const size_t cols = ((size_t)s.M * ((s.BD + 1) / 2) + 15) / 16 * 16;
     size_t want = (size_t)o.scratch_mib << 20;
     if (want > per_col * cols) want = per_col * cols;

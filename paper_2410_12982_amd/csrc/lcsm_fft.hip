@@ -31,10 +31,10 @@
 //             block (only n2 < N2/2 are non-zero), times w_N^{n1 k2} -> C
 //   pass M  : for each k2 an N1-point DFT over n1 (giving X[N2 k1 + k2]),
 //             the spectral product (partner bin N-k lies in column N2-k2),
-//             the inverse N1-point DFT and the conjugate twiddle -> E
-//   pass R' : for each n1 the inverse N2-point FFT of E; outputs n2 >= N2/2
+//             the inverse N1-point DFT and the conjugate twiddle, in place
+//   pass R' : for each n1 the inverse N2-point FFT of C; outputs n2 >= N2/2
 //             are the time indices U..N-1, added into the state.
-// C and E live in a scratch buffer, processed in chunks of columns.
+// C lives in a scratch buffer; columns are processed in chunks.
 #include <type_traits>
 
 #include "lcsm_fft_core.h"
@@ -51,12 +51,13 @@ using fft::csub;
 
 // Per-size launch shape of the LDS transforms: WC complex columns per
 // workgroup, NT threads.  WC * 8 bytes is the contiguous run read per row.
-// Up to 2U = 2048 two workgroups fit in one CU's 160 KB of LDS (data plus the
-// twiddle table w_N^m), so one workgroup's global loads overlap the other's
-// LDS passes.  TWL: the twiddle table fits in LDS beside the data.
+// The kernels are bound by latency at the occupancy that registers and LDS
+// allow, so up to 2U = 2048 the panel is as narrow as the measured optimum
+// (several workgroups per CU overlap each other's global loads and LDS
+// passes).  TWL: the twiddle table w_N^m fits in LDS beside the data.
 template <int N>
 struct Cfg {
-  static constexpr int WC = N <= 512 ? 16 : (N <= 1024 ? 8 : (N <= 4096 ? 4 : 2));
+  static constexpr int WC = N <= 256 ? 16 : (N <= 512 ? 8 : (N <= 4096 ? 4 : 2));
   static constexpr int NT = N <= 256 ? 128 : (N <= 2048 ? 256 : 512);
   static constexpr bool TWL = (size_t)N * 8 * (WC + 1) <= 163840;
 };
@@ -331,20 +332,17 @@ constexpr int kMidG = 8;   // frequency columns k2 per pass-M workgroup
 constexpr int kMidWC = 8;  // complex columns per pass-M workgroup
 constexpr int kMidNT = 256;
 
-// Pass M.  Workgroup (kg, panel) owns the frequency columns k2 = kg*G + s
-// (s < G) of complex columns x0 .. x0+WCM-1, and reads their partner columns
-// N2 - k2 as well.  LDS slot s holds k2, slot G + s its partner.
-//   SPECTRA = false: X = DFT_N1(C), P = pair_product, E = IDFT_N1(P) times
-//                    conj(w_N^{n1 k2}), written to E for the own columns.
-//   SPECTRA = true : C holds the DFT pieces of the filter pairs; the
-//                    separated, 1/N-scaled spectra of bins k <= N/2 are
-//                    written to Hout[m][k][d].
-template <int N1, bool SPECTRA>
-__global__ __launch_bounds__(kMidNT) void k_fft_mid(const float2* __restrict__ C,
-                                                    float2* __restrict__ E,
-                                                    const float2* __restrict__ H,
-                                                    float2* __restrict__ Hout, int D, Chunk ch,
-                                                    const float2* __restrict__ tw) {
+// Pass M of the filter spectra: C holds, per filter column pair, the
+// pass-R pieces of DFT_N(h[0, N)).  Workgroup (kg, panel) owns the frequency
+// columns k2 = kg*G + s (s < G) of complex columns x0 .. x0+WCM-1 and reads
+// their partner columns N2 - k2 as well (LDS slot s holds k2, slot G + s its
+// partner).  X = DFT_N1(C); the two real filters of each pair are separated
+// and their 1/N-scaled spectra at bins k <= N/2 are written to Hout[m][k][d].
+template <int N1>
+__global__ __launch_bounds__(kMidNT) void k_fft_mid_spectra(const float2* __restrict__ C,
+                                                            float2* __restrict__ Hout, int D,
+                                                            Chunk ch,
+                                                            const float2* __restrict__ tw) {
   constexpr int G = kMidG, WCM = kMidWC, NT = kMidNT;
   constexpr int W = 2 * G * WCM;  // LDS row stride
   __shared__ float2 buf[N1 * W];
@@ -368,55 +366,121 @@ __global__ __launch_bounds__(kMidNT) void k_fft_mid(const float2* __restrict__ C
   __syncthreads();
   fft::lds_passes<N1, 0, fft::Plan<N1>::NP, W, W, NT, false>(buf, twz);
 
-  // spectral step over the own columns (partner slots are only read)
+  const float inv_n = 1.0f / (float)N;
   for (int u = (int)threadIdx.x; u < N1 * G * WCM; u += NT) {
     const int k1 = u / (G * WCM), sc = u - k1 * (G * WCM);
     const int s = sc / WCM, cc = sc - s * WCM;
     const int x = x0 + cc;
     if (x >= ch.nvalid) continue;
     const int k2 = kA + s;
+    const int k = N2 * k1 + k2;
+    if (k > U) continue;
     const int pk1 = k2 == 0 ? (N1 - k1) & (N1 - 1) : N1 - 1 - k1;
     const float2 xk = buf[k1 * W + s * WCM + cc];
     const float2 xp = buf[pk1 * W + (G + s) * WCM + cc];
     const int g = ch.g0 + x;
     const int m = g / ch.ncc;
     const int c = 2 * (g - m * ch.ncc);
-    const int k = N2 * k1 + k2;
-    if constexpr (SPECTRA) {
-      if (k > U) continue;
-      const float inv_n = 1.0f / (float)N;
-      float2* Hm = Hout + (size_t)m * (U + 1) * D;
-      Hm[(size_t)k * D + c] = make_float2(0.5f * inv_n * (xk.x + xp.x), 0.5f * inv_n * (xk.y - xp.y));
-      if (c + 1 < D)
-        Hm[(size_t)k * D + c + 1] =
-            make_float2(0.5f * inv_n * (xk.y + xp.y), -0.5f * inv_n * (xk.x - xp.x));
-    } else {
-      const int BD = ch.ncols;
-      const int da = c % D;
-      const int db = (c + 1 < BD) ? (c + 1) % D : da;
-      const float2* Hm = H + (size_t)m * (U + 1) * D;
-      float2 ha, hb;
-      if (k <= U) {
-        ha = Hm[(size_t)k * D + da];
-        hb = Hm[(size_t)k * D + db];
-      } else {
-        ha = conjf2(Hm[(size_t)(N - k) * D + da]);
-        hb = conjf2(Hm[(size_t)(N - k) * D + db]);
+    float2* Hm = Hout + (size_t)m * (U + 1) * D;
+    Hm[(size_t)k * D + c] = make_float2(0.5f * inv_n * (xk.x + xp.x), 0.5f * inv_n * (xk.y - xp.y));
+    if (c + 1 < D)
+      Hm[(size_t)k * D + c + 1] = make_float2(0.5f * inv_n * (xk.y + xp.y), -0.5f * inv_n * (xk.x - xp.x));
+  }
+}
+
+// Pass M of a tile, in place in C.  Workgroup group 0 owns the two
+// self-paired frequency columns k2 = 0 and N2/2; group g >= 1 owns
+// k2 = 1 + (g-1) G + s (s < G, k2 < N2/2) and their partners N2 - k2, so each
+// column and each spectrum bin is read once.  LDS slot s < G holds k2_s,
+// slot G + s its partner; the partner of bin (k1, slot s) is (N1-1-k1, slot
+// G+s).  Per column: X = DFT_N1(C), spectral product, E = IDFT_N1(P) times
+// conj(w_N^{n1 k2}), written back over C.
+__device__ __forceinline__ int mid_slot_k2(int gi, int slot, int N2) {
+  constexpr int G = kMidG;
+  if (gi == 0) return slot == 0 ? 0 : (slot == 1 ? N2 / 2 : -1);
+  const int s = slot < G ? slot : slot - G;
+  const int k = 1 + (gi - 1) * G + s;
+  if (k >= N2 / 2) return -1;
+  return slot < G ? k : N2 - k;
+}
+
+template <int N1>
+__global__ __launch_bounds__(kMidNT) void k_fft_mid_tile(float2* __restrict__ C,
+                                                         const float2* __restrict__ H, int D,
+                                                         Chunk ch, const float2* __restrict__ tw) {
+  constexpr int G = kMidG, WCM = kMidWC, NT = kMidNT;
+  constexpr int W = 2 * G * WCM;  // LDS row stride
+  __shared__ float2 buf[N1 * W];
+  __shared__ float2 twl[N1];
+  const fft::TwLds<N1> twz{twl};
+  fft::load_twiddles<N1, NT>(twl, tw);
+  const int N2 = ch.N2, N = N1 * N2, U = N / 2;
+  const int npan = (ch.nvalid + WCM - 1) / WCM;
+  const int q = fft::xcd_logical((int)blockIdx.x, (int)gridDim.x);
+  const int gi = q / npan;
+  const int x0 = (q - gi * npan) * WCM;
+
+  for (int u = (int)threadIdx.x; u < N1 * W; u += NT) {
+    const int n1 = u / W, slot = (u - n1 * W) / WCM, cc = u % WCM;
+    const int k2 = mid_slot_k2(gi, slot, N2);
+    const int x = x0 + cc;
+    buf[u] = (k2 >= 0 && x < ch.nvalid) ? C[(size_t)(n1 * N2 + k2) * ch.cstride + x] : make_float2(0.f, 0.f);
+  }
+  __syncthreads();
+  fft::lds_passes<N1, 0, fft::Plan<N1>::NP, W, W, NT, false>(buf, twz);
+
+  // spectral product over disjoint bin pairs (k, N-k)
+  const int BD = ch.ncols;
+  auto spectrum = [&](int m, int c, int k, float2& ha, float2& hb) {
+    const int da = c % D;
+    const int db = (c + 1 < BD) ? (c + 1) % D : da;
+    const float2* Hm = H + (size_t)m * (U + 1) * D;
+    const int kb = k <= U ? k : N - k;
+    ha = Hm[(size_t)kb * D + da];
+    hb = Hm[(size_t)kb * D + db];
+    if (k > U) {
+      ha = conjf2(ha);
+      hb = conjf2(hb);
+    }
+  };
+  auto pair = [&](int ia, int ib, int k, int m, int c) {
+    float2 ha, hb;
+    spectrum(m, c, k, ha, hb);
+    const float2 xa = buf[ia], xb = buf[ib];
+    buf[ia] = pair_product(xa, xb, ha, hb);
+    if (ib != ia) buf[ib] = pair_product(xb, xa, conjf2(ha), conjf2(hb));
+  };
+  const int npairs = gi == 0 ? (N1 / 2 + 1 + N1 / 2) * WCM : N1 * G * WCM;
+  for (int u = (int)threadIdx.x; u < npairs; u += NT) {
+    const int cc = u % WCM, r = u / WCM;
+    const int x = x0 + cc;
+    if (x >= ch.nvalid) continue;
+    const int g = ch.g0 + x;
+    const int m = g / ch.ncc;
+    const int c = 2 * (g - m * ch.ncc);
+    if (gi == 0) {
+      if (r <= N1 / 2) {  // k2 = 0: bins N2 k1 and N2 ((N1 - k1) mod N1)
+        const int k1 = r, pk1 = (N1 - k1) & (N1 - 1);
+        pair(k1 * W + cc, pk1 * W + cc, N2 * k1, m, c);
+      } else {            // k2 = N2/2: bins N2 k1 + N2/2 and its mirror at N1-1-k1
+        const int k1 = r - (N1 / 2 + 1), pk1 = N1 - 1 - k1;
+        pair(k1 * W + WCM + cc, pk1 * W + WCM + cc, N2 * k1 + N2 / 2, m, c);
       }
-      buf[k1 * W + s * WCM + cc] = pair_product(xk, xp, ha, hb);
+    } else {
+      const int s = r % G, k1 = r / G;
+      const int k2 = mid_slot_k2(gi, s, N2);
+      if (k2 < 0) continue;
+      pair(k1 * W + s * WCM + cc, (N1 - 1 - k1) * W + (G + s) * WCM + cc, N2 * k1 + k2, m, c);
     }
   }
-  if constexpr (!SPECTRA) {
-    __syncthreads();
-    fft::lds_passes<N1, 0, fft::Plan<N1>::NP, G * WCM, W, NT, true>(buf, twz);
-    for (int u = (int)threadIdx.x; u < N1 * G * WCM; u += NT) {
-      const int n1 = u / (G * WCM), sc = u - n1 * (G * WCM);
-      const int s = sc / WCM, cc = sc - s * WCM;
-      const int x = x0 + cc;
-      if (x >= ch.nvalid) continue;
-      const int k2 = kA + s;
-      E[(size_t)(n1 * N2 + k2) * ch.cstride + x] = cmulc(buf[n1 * W + s * WCM + cc], fft::twiddle<false>(tw, N, n1 * k2));
-    }
+  __syncthreads();
+  fft::lds_passes<N1, 0, fft::Plan<N1>::NP, W, W, NT, true>(buf, twz);
+  for (int u = (int)threadIdx.x; u < N1 * W; u += NT) {
+    const int n1 = u / W, slot = (u - n1 * W) / WCM, cc = u % WCM;
+    const int k2 = mid_slot_k2(gi, slot, N2);
+    const int x = x0 + cc;
+    if (k2 < 0 || x >= ch.nvalid) continue;
+    C[(size_t)(n1 * N2 + k2) * ch.cstride + x] = cmulc(buf[u], fft::twiddle<false>(tw, N, n1 * k2));
   }
 }
 
@@ -429,6 +493,7 @@ __global__ __launch_bounds__(Cfg<N2>::NT) void k_fft_rows_inv(const float2* __re
                                                               int dst_len, Chunk ch,
                                                               const float2* __restrict__ tw) {
   constexpr int WC = Cfg<N2>::WC, NT = Cfg<N2>::NT;
+  using P = fft::Plan<N2>;
   __shared__ float2 buf[N2 * WC];
   __shared__ float2 twl[Cfg<N2>::TWL ? N2 : 1];
   const auto twz = make_tw<N2>(twl, tw);
@@ -436,23 +501,75 @@ __global__ __launch_bounds__(Cfg<N2>::NT) void k_fft_rows_inv(const float2* __re
   const int q = fft::xcd_logical((int)blockIdx.x, (int)gridDim.x);
   const int n1 = q / npan;
   const int x0 = (q - n1 * npan) * WC;
+  const int N1 = ch.N1, U = N1 * N2 / 2, BD = ch.ncols;
+  const bool vec = (BD & 1) == 0;
   for (int u = (int)threadIdx.x; u < N2 * WC; u += NT) {
     const int k2 = u / WC, col = u - k2 * WC;
     const int x = x0 + col;
     buf[u] = x < ch.nvalid ? E[(size_t)(n1 * N2 + k2) * ch.cstride + x] : make_float2(0.f, 0.f);
   }
-  __syncthreads();
-  const int N1 = ch.N1, U = N1 * N2 / 2, BD = ch.ncols;
-  const bool vec = (BD & 1) == 0;
-  fft::inverse_to_global<N2, WC, WC, NT, true>(buf, twz, [&](int n2, int col, float2 v) {
+  // destination rows of the last pass (radix RL, p = N2/RL): unit j writes
+  // n2 = j + s N2/RL for s >= RL/2, time index n1 + N1 n2 = U + n1 + N1 (j + (s - RL/2) PL)
+  constexpr int RL = P::radix(P::NP - 1);
+  constexpr int PL = N2 / RL;
+  constexpr int LUN = PL * WC;
+  constexpr int LU = (LUN + NT - 1) / NT;
+  float* rowp[LU];  // row i of the column's layer, nullptr for no column
+  int cpos[LU];     // real column index of the pair
+  float2 zo[LU][RL / 2];
+#pragma unroll
+  for (int a = 0; a < LU; ++a) {
+    const int u = (int)threadIdx.x + a * NT;
+    const int j = u / WC, col = u - j * WC;
     const int x = x0 + col;
-    const int oi = n1 + N1 * n2 - U;
-    if (x >= ch.nvalid || oi >= dst_len) return;
-    const int g = ch.g0 + x;
-    const int m = g / ch.ncc;
-    const int c = 2 * (g - m * ch.ncc);
-    add_pair(S + ((size_t)m * L + i + oi) * BD, c, BD, vec, v);
-  });
+    rowp[a] = nullptr;
+    cpos[a] = 0;
+    if (u < LUN && x < ch.nvalid) {
+      const int g = ch.g0 + x;
+      const int m = g / ch.ncc;
+      rowp[a] = S + ((size_t)m * L + i) * BD;
+      cpos[a] = 2 * (g - m * ch.ncc);
+    }
+#pragma unroll
+    for (int s = 0; s < RL / 2; ++s) {
+      const int oi = n1 + N1 * (j + s * PL);
+      zo[a][s] = (rowp[a] && oi < dst_len) ? load_pair(rowp[a] + (size_t)oi * BD, cpos[a], BD, vec)
+                                           : make_float2(0.f, 0.f);
+    }
+  }
+  __syncthreads();
+  fft::lds_passes<N2, 0, P::NP - 1, WC, WC, NT, true>(buf, twz);
+#pragma unroll
+  for (int a = 0; a < LU; ++a) {
+    const int u = (int)threadIdx.x + a * NT;
+    if (u < LUN && rowp[a]) {
+      const int j = u / WC, col = u - j * WC;  // j < PL, so k = j
+      float2 v[RL];
+#pragma unroll
+      for (int t = 0; t < RL; ++t) v[t] = buf[(j + t * PL) * WC + col];
+      if constexpr (PL > 1) {
+#pragma unroll
+        for (int t = 1; t < RL; ++t) v[t] = cmul(v[t], twz.template get<true, N2>(t * j));
+      }
+      fft::dft<RL, true>(v);
+      const int c = cpos[a];
+      (void)col;
+#pragma unroll
+      for (int s = 0; s < RL / 2; ++s) {
+        const int oi = n1 + N1 * (j + s * PL);
+        if (oi < dst_len) {
+          float* row = rowp[a] + (size_t)oi * BD;
+          const float2 o = make_float2(zo[a][s].x + v[RL / 2 + s].x, zo[a][s].y + v[RL / 2 + s].y);
+          if (vec) {
+            *reinterpret_cast<float2*>(row + c) = o;
+          } else {
+            row[c] = o.x;
+            if (c + 1 < BD) row[c + 1] = o.y;
+          }
+        }
+      }
+    }
+  }
 }
 
 // ------------------------------------------------------------- dispatch
@@ -522,15 +639,27 @@ hipError_t rows_inv(const float2* E, float* S, int L, int i, int dst_len, const 
   return hipErrorInvalidValue;
 }
 
-template <bool SPECTRA>
-hipError_t mid(const float2* C, float2* E, const float2* H, float2* Hout, int D, const Chunk& ch,
-               const float2* tw, hipStream_t st) {
+hipError_t mid_tile(float2* C, const float2* H, int D, const Chunk& ch, const float2* tw,
+                    hipStream_t st) {
+  const int npan = (ch.nvalid + kMidWC - 1) / kMidWC;
+  const int groups = 1 + (ch.N2 / 2 - 1 + kMidG - 1) / kMidG;
+  const dim3 grid((unsigned)(npan * groups));
+#define LCSM_CASE(NN)                                                                           \
+  case NN:                                                                                      \
+    hipLaunchKernelGGL(k_fft_mid_tile<NN>, grid, dim3(kMidNT), 0, st, C, H, D, ch, tw);         \
+    return hipGetLastError();
+  switch (ch.N1) { LCSM_MID_CASES(LCSM_CASE) }
+#undef LCSM_CASE
+  return hipErrorInvalidValue;
+}
+
+hipError_t mid_spectra(const float2* C, float2* Hout, int D, const Chunk& ch, const float2* tw,
+                       hipStream_t st) {
   const int npan = (ch.nvalid + kMidWC - 1) / kMidWC;
   const dim3 grid((unsigned)(npan * (ch.N2 / kMidG)));
-#define LCSM_CASE(NN)                                                                            \
-  case NN:                                                                                       \
-    hipLaunchKernelGGL((k_fft_mid<NN, SPECTRA>), grid, dim3(kMidNT), 0, st, C, E, H, Hout, D, ch, \
-                       tw);                                                                      \
+#define LCSM_CASE(NN)                                                                             \
+  case NN:                                                                                        \
+    hipLaunchKernelGGL(k_fft_mid_spectra<NN>, grid, dim3(kMidNT), 0, st, C, Hout, D, ch, tw);     \
     return hipGetLastError();
   switch (ch.N1) { LCSM_MID_CASES(LCSM_CASE) }
 #undef LCSM_CASE
@@ -548,8 +677,8 @@ int split_n2(int N, int lds_max_n) {
 
 int fft_multipass_chunk(int N, int lds_max_n, size_t scratch_bytes, int total_cc) {
   (void)lds_max_n;
-  // C and E: 2 * N complex values per chunk column
-  long long cap = (long long)(scratch_bytes / (2 * sizeof(float2) * (size_t)N));
+  // one N-point complex column of C per chunk column (pass M works in place)
+  long long cap = (long long)(scratch_bytes / (sizeof(float2) * (size_t)N));
   cap = cap / 16 * 16;
   const long long need = ((long long)total_cc + 15) / 16 * 16;
   if (cap > need) cap = need;
@@ -573,7 +702,7 @@ hipError_t launch_spectra(const float* Hf, float2* Hout, const float2* tw, const
     ch.g0 = g0;
     ch.nvalid = total - g0 < ch.cstride ? total - g0 : ch.cstride;
     hipError_t e = rows_fwd<false>(Hf, (size_t)s.L * s.D, 0, s.L, ch, C, tw, st);
-    if (e == hipSuccess) e = mid<true>(C, nullptr, nullptr, Hout, s.D, ch, tw, st);
+    if (e == hipSuccess) e = mid_spectra(C, Hout, s.D, ch, tw, st);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
@@ -594,13 +723,12 @@ hipError_t launch_fft_tile(float* S, const float2* H, const float2* tw, const Sh
   ch.cstride = fft_multipass_chunk(N, lds_max_n, scratch_bytes, total);
   if (ch.cstride <= 0) return hipErrorOutOfMemory;
   float2* C = scratch;
-  float2* E = scratch + (size_t)N * ch.cstride;
   for (int g0 = 0; g0 < total; g0 += ch.cstride) {
     ch.g0 = g0;
     ch.nvalid = total - g0 < ch.cstride ? total - g0 : ch.cstride;
     hipError_t e = rows_fwd<true>(S, (size_t)s.L * s.BD, i - U, i, ch, C, tw, st);
-    if (e == hipSuccess) e = mid<false>(C, E, H, nullptr, s.D, ch, tw, st);
-    if (e == hipSuccess) e = rows_inv(E, S, s.L, i, dst_len, ch, tw, st);
+    if (e == hipSuccess) e = mid_tile(C, H, s.D, ch, tw, st);
+    if (e == hipSuccess) e = rows_inv(C, S, s.L, i, dst_len, ch, tw, st);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
