@@ -55,28 +55,32 @@ def parse():
     p.add_argument("--closed-loop", action="store_true", help="also time the tanh-chain generation")
     p.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                    help="only run a plain elementwise copy of MIB MiB 5 times (counter calibration)")
+    p.add_argument("--traffic-from", metavar="DIR", default=None,
+                   help="only convert rocprofv3 FETCH_SIZE/WRITE_SIZE runs under DIR (pmc_copy_*, "
+                        "pmc_bench_*) into profiles/traffic.json and a text summary")
+    p.add_argument("--copy-mib", type=int, default=1024, help="size the copy probe ran with")
     return p.parse_args()
 
 
 # ----------------------------------------------------------------- algorithmic bytes
 def launch_bytes(name, U, w):
-    """Algorithmic HBM bytes of one launch covering all M layers.
+    """Algorithmic HBM bytes of one position's launch(es) for all M layers.
 
     Per column (m, b, d): the red cell reads y_t and acc_t and writes z_t and
-    the slot (16 B); a gray tile of side U reads the U inputs (4U, or 4(U-1)
-    when fused with the red cell, whose y_t is in a register) and reads and
-    writes the U destination accumulators (8U).  Per (m, d): the lags
-    1..2U-1 of a direct tile (4(2U-1)) or the U+1 complex bins of the
-    cached spectrum of an FFT tile (8(U+1))."""
+    the slot (16 B); a gray tile of side U reads the U inputs (4(U-1) more:
+    y_t is the red cell's) and reads and writes the U destination
+    accumulators (8U).  Per (m, d): the lags 1..2U-1 of a direct tile
+    (4(2U-1)) or the U+1 complex bins of the cached spectrum of an FFT tile
+    (8(U+1)).  "fused": red cell + direct tile (U = 0: red cell only);
+    "fft_lds"/"fft_hbm": red cell + FFT tile."""
     cols = w.M * w.B * w.D
     md = w.M * w.D
-    if name == "red":
+    if U == 0:
         return 16 * cols
+    tile_cols = (16 + 4 * (U - 1) + 8 * U) * cols
     if name == "fused":
-        return 16 * cols + (4 * (U - 1) + 8 * U) * cols + 4 * (2 * U - 1) * md
-    if name == "direct":
-        return 12 * U * cols + 4 * (2 * U - 1) * md
-    return 12 * U * cols + 8 * (U + 1) * md
+        return tile_cols + 4 * (2 * U - 1) * md
+    return tile_cols + 8 * (U + 1) * md
 
 
 def source_digest():
@@ -104,8 +108,92 @@ def committed_traffic(kernel, U, w):
     return None if entry is None else entry.get("bytes_per_launch")
 
 
+def kernel_key(name):
+    """(kernel, U) of a library kernel name as the per-launch pass names it,
+    or None for other kernels."""
+    import re
+    m = re.search(r"k_step_fused<(\d+), (true|false)>", name)
+    if m:
+        u = int(m.group(1))
+        if m.group(2) == "false":
+            return ("direct", u)
+        return ("fused", u) if u else ("red", 0)
+    m = re.search(r"k_fft_tile<(\d+), (true|false)>", name)
+    if m:
+        return ("fft_lds", int(m.group(1)) // 2)
+    return None
+
+
+def traffic_from(args):
+    """Convert counter runs into profiles/traffic.json: HBM bytes per launch
+    per (workload, kernel, U), each counter scaled by what it reads for the
+    copy probe (which reads and writes copy_mib MiB), stamped with the digest
+    of the kernel sources they were taken on."""
+    import csv
+    import collections
+
+    def rows(sub):
+        with open(os.path.join(args.traffic_from, sub, "run_counter_collection.csv")) as f:
+            return list(csv.DictReader(f))
+
+    known = args.copy_mib * (1 << 20)
+    scale = {}
+    for c in ("FETCH_SIZE", "WRITE_SIZE"):
+        vals = [1024.0 * float(r["Counter_Value"]) for r in rows(f"pmc_copy_{c}") if "neg" in r["Kernel_Name"]]
+        scale[c] = known / (sum(vals) / len(vals))
+    per = collections.defaultdict(lambda: {"FETCH_SIZE": [], "WRITE_SIZE": []})
+    for c in ("FETCH_SIZE", "WRITE_SIZE"):
+        for r in rows(f"pmc_bench_{c}"):
+            key = kernel_key(r["Kernel_Name"])
+            if key:
+                per[key][c].append(1024.0 * float(r["Counter_Value"]) * scale[c])
+    kernels = {}
+    for (name, U), v in sorted(per.items(), key=lambda kv: (kv[0][1], kv[0][0])):
+        if not v["FETCH_SIZE"] or not v["WRITE_SIZE"]:
+            continue
+        fb = sum(v["FETCH_SIZE"]) / len(v["FETCH_SIZE"])
+        wb = sum(v["WRITE_SIZE"]) / len(v["WRITE_SIZE"])
+        kernels[f"{args.workload}:{name}:U={U}"] = {"bytes_per_launch": round(fb + wb),
+                                                    "read_bytes": round(fb), "write_bytes": round(wb),
+                                                    "dispatches": len(v["FETCH_SIZE"])}
+    out = {"source_digest": source_digest(), "workload": args.workload,
+           "fetch_scale": round(scale["FETCH_SIZE"], 4), "write_scale": round(scale["WRITE_SIZE"], 4),
+           "commands": ["cd /tmp && export TMPDIR=/tmp && rocprofv3 --pmc {C} --output-format csv "
+                        "-d <dir>/pmc_copy_{C} -o run -- python3 bench.py --copy-probe 1024",
+                        "cd /tmp && export TMPDIR=/tmp && rocprofv3 --pmc {C} --output-format csv "
+                        f"-d <dir>/pmc_bench_{{C}} -o run -- python3 bench.py --workload {args.workload} "
+                        "--no-graph --steps 1 --warmup 0 --no-kernel-pass --no-cpu-baseline",
+                        "  for C in FETCH_SIZE, WRITE_SIZE; then: python3 bench.py --traffic-from <dir> "
+                        f"--workload {args.workload}"],
+           "kernels": kernels}
+    prof = os.path.join(ROOT, "profiles")
+    os.makedirs(prof, exist_ok=True)
+    with open(os.path.join(prof, "traffic.json"), "w") as f:
+        json.dump(out, f, indent=1)
+    import datagen
+    w = datagen.WORKLOADS[args.workload]
+    lines = [f"# HBM traffic per launch, workload {args.workload} (M={w.M} B={w.B} D={w.D} L={w.L})",
+             "# rocprofv3 FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each scaled by what it reads "
+             f"for a plain copy kernel of {args.copy_mib} MiB read + written "
+             f"(FETCH_SIZE x {scale['FETCH_SIZE']:.4f}, WRITE_SIZE x {scale['WRITE_SIZE']:.4f})",
+             *("# " + c for c in out["commands"]),
+             f"# kernel sources digest {out['source_digest']}",
+             "# kernel        U   dispatches   read_MB  write_MB  algorithmic_MB"]
+    for key, v in kernels.items():
+        _, name, u = key.split(":")
+        U = int(u[2:])
+        lines.append(f"{name:12s} {U:5d} {v['dispatches']:10d} {v['read_bytes'] / 1e6:9.3f} "
+                     f"{v['write_bytes'] / 1e6:9.3f} {launch_bytes(name, U, w) / 1e6:12.3f}")
+    with open(os.path.join(prof, f"traffic_{args.workload}.txt"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
     args = parse()
+    if args.traffic_from:
+        traffic_from(args)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
               "(this build has no multi-GPU path).", file=sys.stderr)
@@ -227,13 +315,13 @@ def copy_probe(mib, torch):
 
 
 def kernel_pass(w, filters, y, z, opts, lcsm, torch):
-    """Average launch duration per (kernel, U) over one generation, with HIP
-    events on the library's stream (torch's current stream).  Steps whose
-    tile is fused into the red-cell kernel are one launch; for the other
-    steps the red cells run per layer (lcsm_step_layer) and only the tile
-    launch(es) of lcsm_advance are bracketed.  Empty event pairs, recorded
-    as often as bracketed ones, measure the event overhead, which is
-    subtracted."""
+    """Average duration of one position's launch(es) per tile kind and side U
+    over one generation, with HIP events on the library's stream (torch's
+    current stream), bracketing each lcsm_step exactly as the timed region
+    issues it: one launch for the red cell fused with a direct tile (U <= 32)
+    or with a single-pass FFT tile (2U <= 4096), red cell + tile launches
+    otherwise.  Empty event pairs, recorded as often as bracketed ones,
+    measure the event overhead, which is subtracted."""
     stream = torch.cuda.current_stream()
     ctx = lcsm.Lcsm(filters, w.B, options=opts, stream=stream)
     R = y.shape[0]
@@ -244,22 +332,13 @@ def kernel_pass(w, filters, y, z, opts, lcsm, torch):
     recs, empty, k = [], [], 0
     for t in range(w.L):
         i, U, n, kind = plans[t]
-        fused = kind == lcsm.TILE_NONE or (kind == lcsm.TILE_DIRECT and U <= 32)
         a, b, c, d = pool[k % len(pool)]
         c.record(stream)
         d.record(stream)
-        if fused:
-            a.record(stream)
-            ctx.step(y[t % R], z[t % R])
-            b.record(stream)
-            name = "fused" if U else "red"
-        else:
-            for m in range(w.M):
-                ctx.step_layer(m, y[t % R, m], z[t % R, m])
-            a.record(stream)
-            ctx.advance()
-            b.record(stream)
-            name = lcsm.TILE_KIND_NAMES[kind]
+        a.record(stream)
+        ctx.step(y[t % R], z[t % R])
+        b.record(stream)
+        name = {lcsm.TILE_NONE: "fused", lcsm.TILE_DIRECT: "fused"}.get(kind, lcsm.TILE_KIND_NAMES[kind])
         recs.append((name, U, a, b))
         empty.append((c, d))
         k += 1
@@ -293,6 +372,16 @@ def kernel_pass(w, filters, y, z, opts, lcsm, torch):
                 "avg_launch_us": round(avg_s * 1e6, 3), "launches": n,
                 "event_overhead_us": round(1e3 * overhead_ms, 3),
                 "share_of_gpu_time": round(tot / total, 4)}
+    # the largest tile kernel, for the bandwidth of the FFT path
+    big = [(key, v) for key, v in agg.items() if key[0] != "fused"]
+    if big:
+        (bname, bU), (btot, bn) = max(big, key=lambda kv: kv[0][1])
+        bavg = btot / bn / 1e3
+        bbytes = launch_bytes(bname, bU, w)
+        roofline["largest_tile"] = {"kernel": f"{bname} U={bU}", "bytes_per_launch": bbytes,
+                                    "avg_launch_us": round(bavg * 1e6, 3),
+                                    "achieved": round(bbytes / bavg / 1e9, 2),
+                                    "frac": round(bbytes / bavg / 1e9 / HBM_PEAK_GBS, 5)}
     return roofline, levels
 
 

@@ -67,8 +67,8 @@ typedef struct lcsm_ctx lcsm_ctx;
 /* Device bytes of the workspace a context of this shape needs (state
  * M*L*B*D fp32, filters M*L*D fp32, filter spectra of the FFT tile sizes, FFT
  * scratch and a few small buffers).  Host only: touches no device.
- * Errors: LCSM_EINVAL for sizes < 1, M or B > 65535, M*B*D >= 2^31, L > 2^19 or bad
- * options. */
+ * Errors: LCSM_EINVAL for sizes < 1, M > 16384, B > 65535, M*B*D >= 2^31, L > 2^19 or
+ * bad options. */
 int lcsm_workspace_bytes(int M, int B, int D, int L, const lcsm_options* opt, size_t* bytes);
 
 /* Create a context (Alg. 3's state: all activations zero, position t = 0).

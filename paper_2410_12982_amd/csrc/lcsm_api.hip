@@ -57,7 +57,8 @@ int resolve_options(const lcsm_options* o, Options* r) {
 
 int check_shape(int M, int B, int D, int L) {
   if (M < 1 || B < 1 || D < 1 || L < 1) return LCSM_EINVAL;
-  if (M > 65535 || B > 65535) return LCSM_EINVAL;  // grid y/z extents of the step kernels
+  // grid y/z extents of the step kernels (z = M times the tile's thread split, <= 4)
+  if (M > 16384 || B > 65535) return LCSM_EINVAL;
   if ((long long)M * B * D >= (1LL << 31)) return LCSM_EINVAL;
   if (L > kMaxL) return LCSM_EINVAL;
   return LCSM_OK;
@@ -202,6 +203,14 @@ int step_common(lcsm_ctx* c, const float* in, float* z, bool chain) {
   const int kind = tile_kind(c->opt, U);
   const bool fuse = (kind == LCSM_TILE_DIRECT && U <= lcsm::kFusedMaxU);
   hipError_t e;
+  if (!chain && kind == LCSM_TILE_FFT && dst_len > 0 && 2 * U <= lcsm::kMaxRedFftN) {
+    // red cells fused into the single-pass FFT tile: one launch
+    const float2* H = (const float2*)(c->ws + c->ly.H[__builtin_ctz((unsigned)U)]);
+    e = lcsm::launch_red_fft_tile(in, z, c->S, c->Hf, H, c->tw, c->s, i, U, dst_len, c->stream);
+    if (e != hipSuccess) return fail(c, LCSM_EDEVICE, "red-cell + FFT tile launch", e);
+    c->t = t + 1;
+    return LCSM_OK;
+  }
   if (chain)
     e = lcsm::launch_chain_fused(in, z, c->S, c->Hf, c->prev, c->s, t, fuse ? U : 0, dst_len,
                                  c->stream);

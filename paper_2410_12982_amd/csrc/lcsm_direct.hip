@@ -21,23 +21,37 @@ namespace {
 
 constexpr int kThreads = 256;
 
-// One column per thread.  RED: do the red cell at position t first (the
-// tile's newest input y_t then comes from the register, not from memory).
-// U == 0: no tile.  1 <= U <= kFusedMaxU: the tile i = t+1 is computed
-// whole by the thread (U outputs from U inputs and 2U-1 lags).
+// Output split of the fused tile: SPLIT threads share one column, each
+// computing U/SPLIT of the U outputs (bounds the per-thread work and
+// registers at the larger fused sides).
+template <int U>
+struct Split {
+  static constexpr int value = U >= 32 ? 4 : (U >= 16 ? 2 : 1);
+};
+
+// RED: do the red cell at position t first (the tile's newest input y_t then
+// comes from the register, not from memory).  U == 0: no tile.
+// 1 <= U <= kFusedMaxU: the tile i = t+1 (U outputs from U inputs and 2U-1
+// lags) is computed by SPLIT threads per column, thread part p taking the
+// outputs j in [p U/SPLIT, (p+1) U/SPLIT); part 0 also does the red cell.
 // Every load (inputs, lags, the red cell's accumulator and the tile's
 // destination accumulators) is issued before the first store, so the step
 // costs one memory round trip; the slots read and written are distinct rows.
+// Grid (channel blocks, B, M * SPLIT): no integer division on the critical
+// path, consecutive lanes take consecutive channels.
 template <int U, bool RED>
 __global__ __launch_bounds__(kThreads) void k_step_fused(const float* __restrict__ y,
                                                         float* __restrict__ z,
                                                         float* __restrict__ S,
                                                         const float* __restrict__ Hf, int M, int L,
                                                         int BD, int D, int t, int dst_len) {
-  // grid (channel blocks, B, M): no integer division on the critical path
+  constexpr int SP = U > 0 ? Split<U>::value : 1;
+  constexpr int UJ = U > 0 ? U / SP : 1;  // outputs per thread
   const int d = (int)blockIdx.x * kThreads + (int)threadIdx.x;
   if (d >= D) return;
-  const int m = (int)blockIdx.z;
+  const int m = (int)blockIdx.z / SP;
+  const int part = (int)blockIdx.z - m * SP;
+  const int j0 = part * UJ;
   const int c = (int)blockIdx.y * D + d;
   const size_t e = (size_t)m * BD + c;
   float* col = S + (size_t)m * L * BD + c;
@@ -45,16 +59,19 @@ __global__ __launch_bounds__(kThreads) void k_step_fused(const float* __restrict
   const size_t rs = (size_t)BD;
 
   constexpr int NY = U > 0 ? U : 1;
-  constexpr int NH = U > 0 ? 2 * U : 1;
+  constexpr int NH = U > 0 ? UJ + U : 1;  // lags j0+1 .. j0+UJ+U-1 at hh[1..]
   float yb[NY];
   float hh[NH];
-  float zo[NY];
-  const bool tile = (U > 0) && (dst_len > 0);
+  float zo[UJ];
+  const bool tile = (U > 0) && (j0 < dst_len);
+  const bool red = RED && part == 0;
   float yt, acc = 0.f, h0 = 0.f;
   if constexpr (RED) {
     yt = y[e];
-    acc = col[(size_t)t * rs];
-    h0 = hc[0];
+    if (red) {
+      acc = col[(size_t)t * rs];
+      h0 = hc[0];
+    }
   } else {
     yt = col[(size_t)t * rs];
   }
@@ -63,13 +80,15 @@ __global__ __launch_bounds__(kThreads) void k_step_fused(const float* __restrict
       // rows t+1-U .. t-1 already hold inputs; row t is y_t
 #pragma unroll
       for (int k = 0; k < U - 1; ++k) yb[k] = col[(size_t)(t + 1 - U + k) * rs];
+      // output j uses lags U+j-k, k < U: for j in [j0, j0+UJ) that is j0+1 .. j0+UJ+U-1
 #pragma unroll
-      for (int l = 1; l < 2 * U; ++l) hh[l] = (l < L) ? hc[(size_t)l * D] : 0.f;
+      for (int l = 1; l < UJ + U; ++l) hh[l] = (j0 + l < L) ? hc[(size_t)(j0 + l) * D] : 0.f;
 #pragma unroll
-      for (int j = 0; j < U; ++j) zo[j] = (j < dst_len) ? col[(size_t)(t + 1 + j) * rs] : 0.f;
+      for (int jj = 0; jj < UJ; ++jj)
+        zo[jj] = (j0 + jj < dst_len) ? col[(size_t)(t + 1 + j0 + jj) * rs] : 0.f;
     }
   }
-  if constexpr (RED) {
+  if (red) {
     z[e] = fmaf(h0, yt, acc);
     col[(size_t)t * rs] = yt;
   }
@@ -77,12 +96,12 @@ __global__ __launch_bounds__(kThreads) void k_step_fused(const float* __restrict
     if (tile) {
       yb[U - 1] = yt;
 #pragma unroll
-      for (int j = 0; j < U; ++j) {
-        if (j < dst_len) {
+      for (int jj = 0; jj < UJ; ++jj) {
+        if (j0 + jj < dst_len) {
           float o = 0.f;
 #pragma unroll
-          for (int k = 0; k < U; ++k) o = fmaf(yb[k], hh[U + j - k], o);
-          col[(size_t)(t + 1 + j) * rs] = zo[j] + o;
+          for (int k = 0; k < U; ++k) o = fmaf(yb[k], hh[U + jj - k], o);
+          col[(size_t)(t + 1 + j0 + jj) * rs] = zo[jj] + o;
         }
       }
     }
@@ -229,11 +248,13 @@ inline unsigned blocks_for(int64_t n) { return (unsigned)((n + kThreads - 1) / k
 template <bool RED>
 hipError_t dispatch_fused(int U, const float* y, float* z, float* S, const float* Hf,
                           const Shape& s, int t, int dst_len, hipStream_t st) {
-  const dim3 grid(blocks_for(s.D), (unsigned)s.B, (unsigned)s.M), block(kThreads);
-#define LCSM_FUSED_CASE(UU)                                                                  \
-  case UU:                                                                                   \
-    hipLaunchKernelGGL((k_step_fused<UU, RED>), grid, block, 0, st, y, z, S, Hf, s.M, s.L, \
-                       s.BD, s.D, t, dst_len);                                               \
+  const dim3 block(kThreads);
+#define LCSM_FUSED_CASE(UU)                                                                      \
+  case UU:                                                                                       \
+    hipLaunchKernelGGL((k_step_fused<UU, RED>),                                                  \
+                       dim3(blocks_for(s.D), (unsigned)s.B,                                      \
+                            (unsigned)(s.M * (UU > 0 ? Split<UU>::value : 1))),                  \
+                       block, 0, st, y, z, S, Hf, s.M, s.L, s.BD, s.D, t, dst_len);              \
     break;
   switch (U) {
     LCSM_FUSED_CASE(0)

@@ -114,12 +114,21 @@ __device__ __forceinline__ float2 pair_product(float2 zk, float2 znk, float2 ha,
 // (in flight during the other forward passes), and the destination rows of
 // the last inverse pass before the inverse passes start.  Without this the
 // per-unit loads in loops that also store would each cost a full round trip.
-template <int N>
+//
+// RED: the red cell of position t = i-1 is fused in.  Each workgroup first
+// finalises z_t = fmaf(h_0, y_t, acc_t) for its own columns and stores y_t
+// into state row t; its first forward pass takes block row U-1 (= row t)
+// from the caller's y_t instead of the state, so no thread reads a value
+// another thread of the launch has just written.
+template <int N, bool RED>
 __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_tile(float* __restrict__ S,
                                                          const float2* __restrict__ H,
-                                                         const float2* __restrict__ tw, int L,
-                                                         int BD, int D, int B, int i, int dst_len,
-                                                         int ppl, int hgroup) {
+                                                         const float2* __restrict__ tw,
+                                                         const float* __restrict__ Hf,
+                                                         const float* __restrict__ yt,
+                                                         float* __restrict__ zt, int L, int BD,
+                                                         int D, int B, int i, int dst_len, int ppl,
+                                                         int hgroup) {
   constexpr int WC = Cfg<N>::WC, NT = Cfg<N>::NT, U = N / 2;
   using P = fft::Plan<N>;
   __shared__ float2 buf[N * WC];
@@ -135,10 +144,26 @@ __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_tile(float* __restrict__ S,
   const bool vec = (BD & 1) == 0;
   float* Sm = S + (size_t)m * L * BD;
   const float* ysrc = Sm + (size_t)(i - U) * BD;
+  const float* ym = RED ? yt + (size_t)m * BD : nullptr;
+
+  if constexpr (RED) {
+    const int t = i - 1;
+    for (int k = (int)threadIdx.x; k < 2 * WC; k += NT) {
+      const int c = c0 + k;
+      if (c < BD) {
+        const float y = ym[c];
+        float* slot = Sm + (size_t)t * BD + c;
+        zt[(size_t)m * BD + c] = fmaf(Hf[(size_t)m * L * D + c % D], y, *slot);
+        *slot = y;
+      }
+    }
+  }
 
   // forward: first pass straight from the input rows
-  fft::first_pass_global<N, WC, WC, NT, false, true>(
-      buf, [&](int row, int col) { return load_pair(ysrc + (size_t)row * BD, c0 + 2 * col, BD, vec); });
+  fft::first_pass_global<N, WC, WC, NT, false, true>(buf, [&](int row, int col) {
+    if (RED && row == U - 1) return load_pair(ym, c0 + 2 * col, BD, vec);
+    return load_pair(ysrc + (size_t)row * BD, c0 + 2 * col, BD, vec);
+  });
 
   // spectrum bins kk = 0..U of this thread's product units, loaded before
   // the remaining forward passes when the registers allow it (2U <= 4096)
@@ -577,16 +602,25 @@ __global__ __launch_bounds__(Cfg<N2>::NT) void k_fft_rows_inv(const float2* __re
 #define LCSM_POW2_CASES(X) \
   X(4) X(8) X(16) X(32) X(64) X(128) X(256) X(512) X(1024) X(2048) X(4096) X(8192)
 
-hipError_t tile_single(int N, float* S, const float2* H, const float2* tw, const Shape& s, int i,
-                       int dst_len, hipStream_t st) {
-#define LCSM_CASE(NN)                                                                             \
-  case NN: {                                                                                      \
-    constexpr int WC = Cfg<NN>::WC;                                                               \
-    const int ppl = (s.BD + 2 * WC - 1) / (2 * WC);                                               \
-    const int hgroup = (s.D % (2 * WC) == 0) ? s.D / (2 * WC) : 0;                                \
-    hipLaunchKernelGGL(k_fft_tile<NN>, dim3((unsigned)(ppl * s.M)), dim3(Cfg<NN>::NT), 0, st, S, \
-                       H, tw, s.L, s.BD, s.D, s.B, i, dst_len, ppl, hgroup);                      \
-    return hipGetLastError();                                                                     \
+hipError_t tile_single(int N, float* S, const float2* H, const float2* tw, const float* Hf,
+                       const float* yt, float* zt, const Shape& s, int i, int dst_len,
+                       hipStream_t st) {
+#define LCSM_CASE(NN)                                                                              \
+  case NN: {                                                                                       \
+    constexpr int WC = Cfg<NN>::WC;                                                                \
+    const int ppl = (s.BD + 2 * WC - 1) / (2 * WC);                                                \
+    const int hgroup = (s.D % (2 * WC) == 0) ? s.D / (2 * WC) : 0;                                 \
+    const dim3 grid((unsigned)(ppl * s.M)), block(Cfg<NN>::NT);                                    \
+    if (yt) {                                                                                      \
+      if constexpr (NN <= kMaxRedFftN)                                                             \
+        hipLaunchKernelGGL((k_fft_tile<NN, true>), grid, block, 0, st, S, H, tw, Hf, yt, zt, s.L,  \
+                           s.BD, s.D, s.B, i, dst_len, ppl, hgroup);                               \
+      else                                                                                         \
+        return hipErrorInvalidValue;                                                               \
+    } else                                                                                         \
+      hipLaunchKernelGGL((k_fft_tile<NN, false>), grid, block, 0, st, S, H, tw, Hf, yt, zt, s.L,   \
+                         s.BD, s.D, s.B, i, dst_len, ppl, hgroup);                                 \
+    return hipGetLastError();                                                                      \
   }
   switch (N) { LCSM_POW2_CASES(LCSM_CASE) }
 #undef LCSM_CASE
@@ -713,7 +747,7 @@ hipError_t launch_fft_tile(float* S, const float2* H, const float2* tw, const Sh
                            hipStream_t st) {
   if (dst_len <= 0) return hipSuccess;
   const int N = 2 * U;
-  if (N <= lds_max_n) return tile_single(N, S, H, tw, s, i, dst_len, st);
+  if (N <= lds_max_n) return tile_single(N, S, H, tw, nullptr, nullptr, nullptr, s, i, dst_len, st);
   Chunk ch{};
   ch.ncols = s.BD;
   ch.ncc = (s.BD + 1) / 2;
@@ -732,6 +766,12 @@ hipError_t launch_fft_tile(float* S, const float2* H, const float2* tw, const Sh
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
+}
+
+hipError_t launch_red_fft_tile(const float* yt, float* zt, float* S, const float* Hf,
+                               const float2* H, const float2* tw, const Shape& s, int i, int U,
+                               int dst_len, hipStream_t st) {
+  return tile_single(2 * U, S, H, tw, Hf, yt, zt, s, i, dst_len, st);
 }
 
 }  // namespace lcsm

@@ -69,4 +69,14 @@ hipError_t launch_fft_tile(float* S, const float2* H, const float2* tw, const Sh
                            int U, int dst_len, int lds_max_n, float2* scratch,
                            size_t scratch_bytes, hipStream_t st);
 
+// Largest FFT length with the red cell fused into the tile kernel.
+constexpr int kMaxRedFftN = 4096;
+
+// Red cells of all layers at position t = i-1 (inputs yt, outputs zt, both
+// [M][B][D]) fused with the single-pass FFT tile of side U (2U <= the LDS
+// limit and <= kMaxRedFftN, dst_len >= 1).
+hipError_t launch_red_fft_tile(const float* yt, float* zt, float* S, const float* Hf,
+                               const float2* H, const float2* tw, const Shape& s, int i, int U,
+                               int dst_len, hipStream_t st);
+
 }  // namespace lcsm

@@ -62,7 +62,8 @@ def test_tile_kind_selection_follows_options():
 
 
 @pytest.mark.parametrize("shape", [(0, 1, 1, 8), (1, 0, 1, 8), (1, 1, 0, 8), (1, 1, 1, 0),
-                                   (1, 1, 1, -5), (1 << 16, 1 << 8, 1 << 8, 8), (1, 1, 1, 1 << 30)])
+                                   (1, 1, 1, -5), (1 << 16, 1 << 8, 1 << 8, 8), (1, 1, 1, 1 << 30),
+                                   (16385, 1, 1, 8), (1, 65536, 1, 8), (1, 1, 1, (1 << 19) + 1)])
 def test_workspace_bytes_rejects_bad_shapes(shape):
     with pytest.raises(lcsm.LcsmError) as e:
         lcsm.workspace_bytes(*shape)
