@@ -318,7 +318,7 @@ def kernel_pass(w, filters, y, z, opts, lcsm, torch):
     """Average duration of one position's launch(es) per tile kind and side U
     over one generation, with HIP events on the library's stream (torch's
     current stream), bracketing each lcsm_step exactly as the timed region
-    issues it: one launch for the red cell fused with a direct tile (U <= 32)
+    issues it: one launch for the red cell fused with a direct tile (U <= 64)
     or with a single-pass FFT tile (2U <= 4096), red cell + tile launches
     otherwise.  Empty event pairs, recorded as often as bracketed ones,
     measure the event overhead, which is subtracted."""

@@ -15,7 +15,7 @@ using lcsm::Shape;
 namespace {
 
 constexpr size_t kAlign = 256;
-constexpr int kDefaultDirectMaxU = 32;     // tiles U <= 32 direct (fused with the red cell)
+constexpr int kDefaultDirectMaxU = 64;     // tiles U <= 64 direct (fused with the red cell)
 constexpr int kDefaultLdsFftMaxN = 8192;   // 2U <= 8192: one LDS pass
 constexpr int kDefaultScratchMib = 512;    // multi-pass FFT scratch cap
 constexpr int kMaxL = 1 << 19;             // FFT lengths up to 2^19 are built
@@ -201,7 +201,8 @@ int step_common(lcsm_ctx* c, const float* in, float* z, bool chain) {
   const int U = (i < c->s.L) ? lowbit(i) : 0;
   const int dst_len = U ? (U < c->s.L - i ? U : c->s.L - i) : 0;
   const int kind = tile_kind(c->opt, U);
-  const bool fuse = (kind == LCSM_TILE_DIRECT && U <= lcsm::kFusedMaxU);
+  const bool fuse =
+      kind == LCSM_TILE_DIRECT && U <= (chain ? lcsm::kChainFusedMaxU : lcsm::kFusedMaxU);
   hipError_t e;
   if (!chain && kind == LCSM_TILE_FFT && dst_len > 0 && 2 * U <= lcsm::kMaxRedFftN) {
     // red cells fused into the single-pass FFT tile: one launch

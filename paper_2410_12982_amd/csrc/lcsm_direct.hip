@@ -26,7 +26,7 @@ constexpr int kThreads = 256;
 // registers at the larger fused sides).
 template <int U>
 struct Split {
-  static constexpr int value = U >= 32 ? 4 : (U >= 16 ? 2 : 1);
+  static constexpr int value = U >= 64 ? 8 : (U >= 32 ? 4 : (U >= 16 ? 2 : 1));
 };
 
 // RED: do the red cell at position t first (the tile's newest input y_t then
@@ -109,7 +109,7 @@ __global__ __launch_bounds__(kThreads) void k_step_fused(const float* __restrict
 }
 
 // The chained input rule (lcsm_step_chain) fused with red cells and, for
-// 1 <= U <= kFusedMaxU, the gray tiles.  One thread per (b, d) column walks
+// 1 <= U <= kChainFusedMaxU, the gray tiles.  One thread per (b, d) column walks
 // the layers in order, since y^m_t depends on z^{m-1}_t.
 template <int U>
 __global__ __launch_bounds__(kThreads) void k_chain_fused(const float* __restrict__ x,
@@ -264,6 +264,7 @@ hipError_t dispatch_fused(int U, const float* y, float* z, float* S, const float
     LCSM_FUSED_CASE(8)
     LCSM_FUSED_CASE(16)
     LCSM_FUSED_CASE(32)
+    LCSM_FUSED_CASE(64)
     default:
       return hipErrorInvalidValue;
   }

@@ -14,8 +14,10 @@ struct Shape {
   int BD;  // B * D
 };
 
-// Largest tile side handled by the fused red+direct kernels.
-constexpr int kFusedMaxU = 32;
+// Largest tile side handled by the fused red+direct kernels, and by the
+// fused kernel of the built-in chain (one thread walks all layers there).
+constexpr int kFusedMaxU = 64;
+constexpr int kChainFusedMaxU = 32;
 // Output chunk of the generic direct tile kernel (U >= kDirectJ).
 constexpr int kDirectJ = 16;
 

@@ -106,8 +106,8 @@ def test_workspace_grows_with_fft_levels():
     M, B, D, L = 2, 4, 96, 4096
     direct = lcsm.workspace_bytes(M, B, D, L, {"direct_max_u": 1 << 20})
     fft = lcsm.workspace_bytes(M, B, D, L)
-    # spectra of U = 64..2048: M * (U+1) * D complex values each
-    spectra = sum(8 * M * (u + 1) * D for u in (64, 128, 256, 512, 1024, 2048))
+    # spectra of U = 128..2048: M * (U+1) * D complex values each
+    spectra = sum(8 * M * (u + 1) * D for u in (128, 256, 512, 1024, 2048))
     assert fft >= direct + spectra
     # the multi-pass scratch obeys the cap but never drops below one chunk
     small = lcsm.workspace_bytes(M, B, D, L, {"lds_fft_max_n": 16, "scratch_mib": 1})
@@ -117,14 +117,14 @@ def test_workspace_grows_with_fft_levels():
 
 
 def test_plan_tile_default_kinds_for_workloads():
-    # default: direct up to U = 32, one LDS pass up to 2U = 8192, multi-pass above
+    # default: direct up to U = 64, one LDS pass up to 2U = 8192, multi-pass above
     L = 1 << 17
     kinds = {}
     for t in range(L - 1):
         _, U, _, k = lcsm.plan_tile(18, 1, 1024, L, t)
         kinds[U] = k
-    assert all(kinds[1 << q] == lcsm.TILE_DIRECT for q in range(6))
-    assert all(kinds[1 << q] == lcsm.TILE_FFT for q in range(6, 13))
+    assert all(kinds[1 << q] == lcsm.TILE_DIRECT for q in range(7))
+    assert all(kinds[1 << q] == lcsm.TILE_FFT for q in range(7, 13))
     assert all(kinds[1 << q] == lcsm.TILE_FFT_HBM for q in range(13, 17))
 
 
