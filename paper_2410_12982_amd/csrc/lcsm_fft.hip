@@ -57,8 +57,8 @@ using fft::csub;
 // passes).  TWL: the twiddle table w_N^m fits in LDS beside the data.
 template <int N>
 struct Cfg {
-  static constexpr int WC = N <= 256 ? 16 : (N <= 512 ? 8 : (N <= 4096 ? 4 : 2));
-  static constexpr int NT = N <= 256 ? 128 : (N <= 2048 ? 256 : 512);
+  static constexpr int WC = N <= 256 ? 4 : (N <= 512 ? 8 : (N <= 4096 ? 4 : 2));
+  static constexpr int NT = N <= 128 ? 64 : (N <= 256 ? 128 : (N <= 2048 ? 256 : 512));
   static constexpr bool TWL = (size_t)N * 8 * (WC + 1) <= 163840;
 };
 
