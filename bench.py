@@ -36,6 +36,10 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 DEFAULT_WORKLOAD = "m1b8d768l8k"
 RING = 256  # input slabs kept resident
+# Longest generation replayed from one HIP graph.  A single graph of the
+# 131072-position workload (about 131k kernel nodes) crashed the process
+# during capture/instantiation; runs up to 32768 positions are known good.
+GRAPH_MAX_L = 32768
 
 
 def parse():
@@ -209,6 +213,10 @@ def main():
     import paper_2410_12982_amd.lcsm as lcsm
 
     w = datagen.WORKLOADS[args.workload]
+    if args.graph and w.L > GRAPH_MAX_L:
+        print(f"# L={w.L} > {GRAPH_MAX_L}: launching from the host (no whole-generation graph)",
+              file=sys.stderr, flush=True)
+        args.graph = False
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     opts = {k: v for k, v in (("direct_max_u", args.direct_max_u),
