@@ -700,17 +700,18 @@ hipError_t mid_spectra(const float2* C, float2* Hout, int D, const Chunk& ch, co
   return hipErrorInvalidValue;
 }
 
-// Row length of the multi-pass split of an N-point transform.
+// Row length of the multi-pass split of an N-point transform: 1024-point
+// rows (four row workgroups per CU) measured fastest; longer rows only when
+// the column DFT would exceed kMaxMidN1 points.
 int split_n2(int N, int lds_max_n) {
-  int n2 = lds_max_n < kMaxRowN2 ? lds_max_n : kMaxRowN2;
+  int n2 = lds_max_n < kPreferredRowN2 ? lds_max_n : kPreferredRowN2;
   while (N / n2 > kMaxMidN1) n2 *= 2;
   return n2;
 }
 
 }  // namespace
 
-int fft_multipass_chunk(int N, int lds_max_n, size_t scratch_bytes, int total_cc) {
-  (void)lds_max_n;
+int fft_multipass_chunk(int N, size_t scratch_bytes, int total_cc) {
   // one N-point complex column of C per chunk column (pass M works in place)
   long long cap = (long long)(scratch_bytes / (sizeof(float2) * (size_t)N));
   cap = cap / 16 * 16;
@@ -729,7 +730,7 @@ hipError_t launch_spectra(const float* Hf, float2* Hout, const float2* tw, const
   ch.N2 = split_n2(N, lds_max_n);
   ch.N1 = N / ch.N2;
   const int total = s.M * ch.ncc;
-  ch.cstride = fft_multipass_chunk(N, lds_max_n, scratch_bytes, total);
+  ch.cstride = fft_multipass_chunk(N, scratch_bytes, total);
   if (ch.cstride <= 0) return hipErrorOutOfMemory;
   float2* C = scratch;
   for (int g0 = 0; g0 < total; g0 += ch.cstride) {
@@ -754,7 +755,7 @@ hipError_t launch_fft_tile(float* S, const float2* H, const float2* tw, const Sh
   ch.N2 = split_n2(N, lds_max_n);
   ch.N1 = N / ch.N2;
   const int total = s.M * ch.ncc;
-  ch.cstride = fft_multipass_chunk(N, lds_max_n, scratch_bytes, total);
+  ch.cstride = fft_multipass_chunk(N, scratch_bytes, total);
   if (ch.cstride <= 0) return hipErrorOutOfMemory;
   float2* C = scratch;
   for (int g0 = 0; g0 < total; g0 += ch.cstride) {

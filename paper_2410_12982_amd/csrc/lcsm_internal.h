@@ -48,7 +48,8 @@ hipError_t launch_zero(float* p, size_t n, hipStream_t st);
 
 // Largest column-DFT length of the multi-pass split (N = N1 * N2).
 constexpr int kMaxMidN1 = 128;
-// Largest row-FFT length of the multi-pass split.
+// Preferred and largest row-FFT length of the multi-pass split.
+constexpr int kPreferredRowN2 = 1024;
 constexpr int kMaxRowN2 = 4096;
 // Range of the single-pass limit lds_fft_max_n.
 constexpr int kMinLdsFftN = 16;
@@ -57,7 +58,7 @@ constexpr int kMaxLdsFftN = 8192;
 // Complex columns per multi-pass chunk for an N-point transform over
 // total_cc complex columns when the scratch holds scratch_bytes (a multiple
 // of 16, or 0 if the scratch cannot hold one chunk of 16).
-int fft_multipass_chunk(int N, int lds_max_n, size_t scratch_bytes, int total_cc);
+int fft_multipass_chunk(int N, size_t scratch_bytes, int total_cc);
 
 // Filter spectra of tile size U (N = 2U): Hout[m][k][d] = DFT_N(h[m,d,0:N))[k]
 // / N for k = 0..U.  tw: twiddle table (see lcsm_fft_core.h).
