@@ -15,7 +15,12 @@ using lcsm::Shape;
 namespace {
 
 constexpr size_t kAlign = 256;
-constexpr int kDefaultDirectMaxU = 64;     // tiles U <= 64 direct (fused with the red cell)
+// Default tile-kind choice (the paper's per-shape "Hybrid" choice of tau, from
+// MI355X measurements): direct tiles (fused with the red cell) up to U = 32,
+// and at U = 64 while the launch is small enough to be bound by its latency
+// (M*B*D <= 2^17 columns; above that the FFT tile moves the bytes faster).
+constexpr int kAutoDirectMaxU = 32;
+constexpr int kAutoDirectU64MaxCols = 1 << 17;
 constexpr int kDefaultLdsFftMaxN = 8192;   // 2U <= 8192: one LDS pass
 constexpr int kDefaultScratchMib = 512;    // multi-pass FFT scratch cap
 constexpr int kMaxL = 1 << 19;             // FFT lengths up to 2^19 are built
@@ -28,13 +33,13 @@ bool is_pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
 int lowbit(int i) { return i & -i; }
 
 struct Options {
-  int direct_max_u;
+  int direct_max_u;  // 0: the shape-dependent default
   int lds_fft_max_n;
   int scratch_mib;
 };
 
 int resolve_options(const lcsm_options* o, Options* r) {
-  r->direct_max_u = kDefaultDirectMaxU;
+  r->direct_max_u = 0;
   r->lds_fft_max_n = kDefaultLdsFftMaxN;
   r->scratch_mib = kDefaultScratchMib;
   if (!o) return LCSM_OK;
@@ -64,9 +69,12 @@ int check_shape(int M, int B, int D, int L) {
   return LCSM_OK;
 }
 
-int tile_kind(const Options& o, int U) {
+int tile_kind(const Options& o, const Shape& s, int U) {
   if (U <= 0) return LCSM_TILE_NONE;
-  if (U <= o.direct_max_u) return LCSM_TILE_DIRECT;
+  int dmax = o.direct_max_u;
+  if (dmax == 0)
+    dmax = ((long long)s.M * s.BD <= kAutoDirectU64MaxCols) ? 2 * kAutoDirectMaxU : kAutoDirectMaxU;
+  if (U <= dmax) return LCSM_TILE_DIRECT;
   return (2 * U <= o.lds_fft_max_n) ? LCSM_TILE_FFT : LCSM_TILE_FFT_HBM;
 }
 
@@ -89,7 +97,7 @@ Layout layout_for(const Shape& s, const Options& o) {
   bool multipass = false;
   for (int q = 0; q < kMaxLevels && (1 << q) <= s.L - 1; ++q) {
     const int U = 1 << q;
-    const int kind = tile_kind(o, U);
+    const int kind = tile_kind(o, s, U);
     if (kind == LCSM_TILE_DIRECT) continue;
     ly.nmax = 2 * U;
     if (kind == LCSM_TILE_FFT_HBM) multipass = true;
@@ -165,7 +173,7 @@ int fail(lcsm_ctx* c, int code, const char* what, hipError_t e) {
 // Gray tile of i = t+1 for all layers, when it was not fused into the red
 // launch.
 hipError_t launch_tile(lcsm_ctx* c, int i, int U, int dst_len) {
-  const int kind = tile_kind(c->opt, U);
+  const int kind = tile_kind(c->opt, c->s, U);
   if (kind == LCSM_TILE_DIRECT)
     return lcsm::launch_direct_tile(c->S, c->Hf, c->s, i, U, dst_len, c->stream);
   const int q = __builtin_ctz((unsigned)U);
@@ -182,7 +190,7 @@ hipError_t init_spectra(lcsm_ctx* c) {
                                 c->stream);
   for (int q = 0; e == hipSuccess && q < kMaxLevels && (1 << q) <= c->s.L - 1; ++q) {
     const int U = 1 << q;
-    if (tile_kind(c->opt, U) == LCSM_TILE_DIRECT) continue;
+    if (tile_kind(c->opt, c->s, U) == LCSM_TILE_DIRECT) continue;
     e = lcsm::launch_spectra(c->Hf, (float2*)(c->ws + c->ly.H[q]), c->tw, c->s, U,
                              c->opt.lds_fft_max_n, c->scratch, c->ly.scratch_bytes, c->stream);
   }
@@ -200,7 +208,7 @@ int step_common(lcsm_ctx* c, const float* in, float* z, bool chain) {
   const int t = c->t, i = t + 1;
   const int U = (i < c->s.L) ? lowbit(i) : 0;
   const int dst_len = U ? (U < c->s.L - i ? U : c->s.L - i) : 0;
-  const int kind = tile_kind(c->opt, U);
+  const int kind = tile_kind(c->opt, c->s, U);
   const bool fuse =
       kind == LCSM_TILE_DIRECT && U <= (chain ? lcsm::kChainFusedMaxU : lcsm::kFusedMaxU);
   hipError_t e;
@@ -388,7 +396,7 @@ int lcsm_plan_tile(int M, int B, int D, int L, const lcsm_options* opt, int t, i
   *i = ii;
   *U = u;
   *dst_len = u < L - ii ? u : L - ii;
-  *kind = tile_kind(o, u);
+  *kind = tile_kind(o, Shape{M, B, D, L, B * D}, u);
   return LCSM_OK;
 }
 

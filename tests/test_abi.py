@@ -167,3 +167,20 @@ def test_strerror_covers_codes():
 def test_single_hip_runtime_in_process():
     """The binding binds to torch's HIP runtime; a second copy must not load."""
     assert len(lcsm.hip_runtimes()) <= 1
+
+
+def test_default_crossover_depends_on_shape():
+    """Direct tiles up to U = 32 always; U = 64 direct only while M*B*D <= 2^17
+    (small launches are latency-bound), FFT above."""
+    def kind_at_u(M, B, D, L, u):
+        # the tile after step t = u - 1 has i = u, side lowbit(u) = u
+        return lcsm.plan_tile(M, B, D, L, u - 1)[3]
+    for shape in [(1, 8, 768, 8192), (18, 4, 768, 32768), (18, 1, 1024, 1 << 17)]:
+        assert kind_at_u(*shape, 32) == lcsm.TILE_DIRECT
+        assert kind_at_u(*shape, 64) == lcsm.TILE_DIRECT
+        assert kind_at_u(*shape, 128) == lcsm.TILE_FFT
+    wide = (32, 16, 2048, 16384)
+    assert kind_at_u(*wide, 32) == lcsm.TILE_DIRECT
+    assert kind_at_u(*wide, 64) == lcsm.TILE_FFT
+    # an explicit option overrides the shape rule
+    assert lcsm.plan_tile(*wide, 63, {"direct_max_u": 64})[3] == lcsm.TILE_DIRECT
