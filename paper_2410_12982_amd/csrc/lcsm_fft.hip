@@ -54,25 +54,33 @@ using fft::csub;
 // The kernels are bound by latency at the occupancy that registers and LDS
 // allow, so up to 2U = 2048 the panel is as narrow as the measured optimum
 // (several workgroups per CU overlap each other's global loads and LDS
-// passes).  TWL: the twiddle table w_N^m fits in LDS beside the data.
+// passes).  TWL: the twiddle table w_N^m fits in LDS beside the data; TWH:
+// only its first half does (the rest follows from w_N^{m+N/2} = -w_N^m).
 template <int N>
 struct Cfg {
   static constexpr int WC = N <= 256 ? 4 : (N <= 512 ? 8 : (N <= 4096 ? 4 : 2));
-  static constexpr int NT = N <= 128 ? 64 : (N <= 256 ? 128 : (N <= 2048 ? 256 : 512));
+  static constexpr int NT = N <= 128 ? 64 : (N <= 256 ? 128 : (N <= 2048 ? 256 : (N <= 4096 ? 512 : 1024)));
   static constexpr bool TWL = (size_t)N * 8 * (WC + 1) <= 163840;
+  static constexpr bool TWH = !TWL && (size_t)N * 8 * WC + (size_t)N * 4 <= 163840;
+  static constexpr int TWN = TWL ? N : (TWH ? N / 2 : 1);  // LDS twiddle entries
 };
 
-// Twiddle source of an N-point transform: LDS copy when it fits, else the
-// global table.  The LDS copy is written here and read after the caller's
-// next __syncthreads.
+// Twiddle source of an N-point transform: LDS copy (whole or half) when it
+// fits, else the global table.  The LDS copy is written here and read after
+// the caller's next __syncthreads.
 template <int N>
-using TwOf = typename std::conditional<Cfg<N>::TWL, fft::TwLds<N>, fft::TwGlobal>::type;
+using TwOf = typename std::conditional<
+    Cfg<N>::TWL, fft::TwLds<N>,
+    typename std::conditional<Cfg<N>::TWH, fft::TwLdsHalf<N>, fft::TwGlobal>::type>::type;
 
 template <int N>
 __device__ __forceinline__ TwOf<N> make_tw(float2* lds, const float2* __restrict__ tw) {
   if constexpr (Cfg<N>::TWL) {
     fft::load_twiddles<N, Cfg<N>::NT>(lds, tw);
     return fft::TwLds<N>{lds};
+  } else if constexpr (Cfg<N>::TWH) {
+    fft::load_twiddles<N, Cfg<N>::NT, N / 2>(lds, tw);
+    return fft::TwLdsHalf<N>{lds};
   } else {
     return fft::TwGlobal{tw};
   }
@@ -120,7 +128,13 @@ __device__ __forceinline__ float2 pair_product(float2 zk, float2 znk, float2 ha,
 // into state row t; its first forward pass takes block row U-1 (= row t)
 // from the caller's y_t instead of the state, so no thread reads a value
 // another thread of the launch has just written.
-template <int N, bool RED>
+//
+// FAST: every panel is whole and lies inside one batch row (D a multiple of
+// 2 WC) and the destination is not clipped (dst_len = U).  Then no access
+// needs a bounds check, the channel of a panel column is d0 + 2 col with d0
+// computed once, and the two filter spectra of a column pair are adjacent
+// (one 16-byte load).
+template <int N, bool RED, bool FAST>
 __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_tile(float* __restrict__ S,
                                                          const float2* __restrict__ H,
                                                          const float2* __restrict__ tw,
@@ -132,7 +146,7 @@ __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_tile(float* __restrict__ S,
   constexpr int WC = Cfg<N>::WC, NT = Cfg<N>::NT, U = N / 2;
   using P = fft::Plan<N>;
   __shared__ float2 buf[N * WC];
-  __shared__ float2 twl[Cfg<N>::TWL ? N : 1];
+  __shared__ float2 twl[Cfg<N>::TWN];
   const auto twz = make_tw<N>(twl, tw);
   const int q = fft::xcd_logical((int)blockIdx.x, (int)gridDim.x);
   const int m = q / ppl;
@@ -141,19 +155,21 @@ __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_tile(float* __restrict__ S,
   // they share the filter spectrum through L2
   const int panel = hgroup > 0 ? (r % B) * hgroup + r / B : r;
   const int c0 = panel * 2 * WC;
-  const bool vec = (BD & 1) == 0;
+  const int d0 = FAST ? c0 % D : 0;
+  const bool vec = FAST || (BD & 1) == 0;
   float* Sm = S + (size_t)m * L * BD;
   const float* ysrc = Sm + (size_t)(i - U) * BD;
   const float* ym = RED ? yt + (size_t)m * BD : nullptr;
+  const int dlen = FAST ? U : dst_len;
 
   if constexpr (RED) {
     const int t = i - 1;
     for (int k = (int)threadIdx.x; k < 2 * WC; k += NT) {
       const int c = c0 + k;
-      if (c < BD) {
+      if (FAST || c < BD) {
         const float y = ym[c];
         float* slot = Sm + (size_t)t * BD + c;
-        zt[(size_t)m * BD + c] = fmaf(Hf[(size_t)m * L * D + c % D], y, *slot);
+        zt[(size_t)m * BD + c] = fmaf(Hf[(size_t)m * L * D + (FAST ? d0 + k : c % D)], y, *slot);
         *slot = y;
       }
     }
@@ -161,8 +177,9 @@ __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_tile(float* __restrict__ S,
 
   // forward: first pass straight from the input rows
   fft::first_pass_global<N, WC, WC, NT, false, true>(buf, [&](int row, int col) {
-    if (RED && row == U - 1) return load_pair(ym, c0 + 2 * col, BD, vec);
-    return load_pair(ysrc + (size_t)row * BD, c0 + 2 * col, BD, vec);
+    const float* src = (RED && row == U - 1) ? ym : ysrc + (size_t)row * BD;
+    if constexpr (FAST) return *reinterpret_cast<const float2*>(src + c0 + 2 * col);
+    return load_pair(src, c0 + 2 * col, BD, vec);
   });
 
   // spectrum bins kk = 0..U of this thread's product units, loaded before
@@ -172,20 +189,31 @@ __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_tile(float* __restrict__ S,
   constexpr bool PREH = N <= 4096;
   constexpr int PH = PREH ? PU : 1;
   const float2* Hm = H + (size_t)m * (U + 1) * D;
+  // spectra of the column pair (c, c+1) at bin kk
+  auto load_h = [&](int kk, int col, float2& xa, float2& xb) {
+    if constexpr (FAST) {
+      const float4 v = *reinterpret_cast<const float4*>(Hm + (size_t)kk * D + d0 + 2 * col);
+      xa = make_float2(v.x, v.y);
+      xb = make_float2(v.z, v.w);
+    } else {
+      const int c = c0 + 2 * col;
+      xa = xb = make_float2(0.f, 0.f);
+      if (c < BD) {
+        const int da = c % D;
+        const int db = (c + 1 < BD) ? (c + 1) % D : da;
+        xa = Hm[(size_t)kk * D + da];
+        xb = Hm[(size_t)kk * D + db];
+      }
+    }
+  };
   float2 ha[PH], hb[PH];
   if constexpr (PREH) {
 #pragma unroll
     for (int a = 0; a < PU; ++a) {
       const int u = (int)threadIdx.x + a * NT;
       const int kk = u / WC, col = u - kk * WC;
-      const int c = c0 + 2 * col;
       ha[a] = hb[a] = make_float2(0.f, 0.f);
-      if (u < PUN && c < BD) {
-        const int da = c % D;
-        const int db = (c + 1 < BD) ? (c + 1) % D : da;
-        ha[a] = Hm[(size_t)kk * D + da];
-        hb[a] = Hm[(size_t)kk * D + db];
-      }
+      if (PUN % NT == 0 || u < PUN) load_h(kk, col, ha[a], hb[a]);
     }
   }
   fft::lds_passes<N, 1, P::NP, WC, WC, NT, false>(buf, twz);
@@ -193,18 +221,14 @@ __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_tile(float* __restrict__ S,
 #pragma unroll
   for (int a = 0; a < PU; ++a) {
     const int u = (int)threadIdx.x + a * NT;
-    if (u < PUN) {
+    if (PUN % NT == 0 || u < PUN) {
       const int kk = u / WC, col = u - kk * WC;
-      const int c = c0 + 2 * col;
-      float2 xa = make_float2(0.f, 0.f), xb = xa;
+      float2 xa, xb;
       if constexpr (PREH) {
         xa = ha[a];
         xb = hb[a];
-      } else if (c < BD) {
-        const int da = c % D;
-        const int db = (c + 1 < BD) ? (c + 1) % D : da;
-        xa = Hm[(size_t)kk * D + da];
-        xb = Hm[(size_t)kk * D + db];
+      } else {
+        load_h(kk, col, xa, xb);
       }
       const int nk = (N - kk) & (N - 1);
       const float2 zk = buf[kk * WC + col], znk = buf[nk * WC + col];
@@ -221,6 +245,10 @@ __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_tile(float* __restrict__ S,
   constexpr int LU = (LUN + NT - 1) / NT;
   float* zdst = Sm + (size_t)i * BD;
   constexpr bool PREZ = N <= 4096;  // registers allow the prefetch
+  auto load_z = [&](int oi, int c) -> float2 {
+    if constexpr (FAST) return *reinterpret_cast<const float2*>(zdst + (size_t)oi * BD + c);
+    return load_pair(zdst + (size_t)oi * BD, c, BD, vec);
+  };
   float2 zo[PREZ ? LU : 1][RL / 2];
   if constexpr (PREZ) {
 #pragma unroll
@@ -230,8 +258,8 @@ __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_tile(float* __restrict__ S,
 #pragma unroll
       for (int s = 0; s < RL / 2; ++s) {
         const int oi = j + s * PL;
-        zo[a][s] = (u < LUN && oi < dst_len) ? load_pair(zdst + (size_t)oi * BD, c0 + 2 * col, BD, vec)
-                                             : make_float2(0.f, 0.f);
+        zo[a][s] = ((LUN % NT == 0 || u < LUN) && (FAST || oi < dlen)) ? load_z(oi, c0 + 2 * col)
+                                                                       : make_float2(0.f, 0.f);
       }
     }
   }
@@ -241,7 +269,7 @@ __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_tile(float* __restrict__ S,
 #pragma unroll
   for (int a = 0; a < LU; ++a) {
     const int u = (int)threadIdx.x + a * NT;
-    if (u < LUN) {
+    if (LUN % NT == 0 || u < LUN) {
       const int j = u / WC, col = u - j * WC;  // j < PL, so k = j
       float2 v[RL];
 #pragma unroll
@@ -255,8 +283,8 @@ __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_tile(float* __restrict__ S,
 #pragma unroll
       for (int s = 0; s < RL / 2; ++s) {
         const int oi = j + s * PL;
-        if (oi < dst_len && c < BD) {
-          const float2 zz = PREZ ? zo[PREZ ? a : 0][s] : load_pair(zdst + (size_t)oi * BD, c, BD, vec);
+        if (FAST || (oi < dlen && c < BD)) {
+          const float2 zz = PREZ ? zo[PREZ ? a : 0][s] : load_z(oi, c);
           const float2 o = make_float2(zz.x + v[RL / 2 + s].x, zz.y + v[RL / 2 + s].y);
           float* row = zdst + (size_t)oi * BD;
           if (vec) {
@@ -280,7 +308,7 @@ __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_spectra(const float* __restr
                                                             int D, int ppl) {
   constexpr int WC = Cfg<N>::WC, NT = Cfg<N>::NT, U = N / 2;
   __shared__ float2 buf[N * WC];
-  __shared__ float2 twl[Cfg<N>::TWL ? N : 1];
+  __shared__ float2 twl[Cfg<N>::TWN];
   const auto twz = make_tw<N>(twl, tw);
   const int m = (int)blockIdx.x / ppl;
   const int c0 = ((int)blockIdx.x - m * ppl) * 2 * WC;
@@ -328,7 +356,7 @@ __global__ __launch_bounds__(Cfg<N2>::NT) void k_fft_rows_fwd(const float* __res
                                                               const float2* __restrict__ tw) {
   constexpr int WC = Cfg<N2>::WC, NT = Cfg<N2>::NT;
   __shared__ float2 buf[N2 * WC];
-  __shared__ float2 twl[Cfg<N2>::TWL ? N2 : 1];
+  __shared__ float2 twl[Cfg<N2>::TWN];
   const auto twz = make_tw<N2>(twl, tw);
   const int npan = (ch.nvalid + WC - 1) / WC;
   const int q = fft::xcd_logical((int)blockIdx.x, (int)gridDim.x);
@@ -520,7 +548,7 @@ __global__ __launch_bounds__(Cfg<N2>::NT) void k_fft_rows_inv(const float2* __re
   constexpr int WC = Cfg<N2>::WC, NT = Cfg<N2>::NT;
   using P = fft::Plan<N2>;
   __shared__ float2 buf[N2 * WC];
-  __shared__ float2 twl[Cfg<N2>::TWL ? N2 : 1];
+  __shared__ float2 twl[Cfg<N2>::TWN];
   const auto twz = make_tw<N2>(twl, tw);
   const int npan = (ch.nvalid + WC - 1) / WC;
   const int q = fft::xcd_logical((int)blockIdx.x, (int)gridDim.x);
@@ -611,15 +639,25 @@ hipError_t tile_single(int N, float* S, const float2* H, const float2* tw, const
     const int ppl = (s.BD + 2 * WC - 1) / (2 * WC);                                                \
     const int hgroup = (s.D % (2 * WC) == 0) ? s.D / (2 * WC) : 0;                                 \
     const dim3 grid((unsigned)(ppl * s.M)), block(Cfg<NN>::NT);                                    \
+    const bool fast = hgroup > 0 && dst_len == NN / 2;                                             \
     if (yt) {                                                                                      \
-      if constexpr (NN <= kMaxRedFftN)                                                             \
-        hipLaunchKernelGGL((k_fft_tile<NN, true>), grid, block, 0, st, S, H, tw, Hf, yt, zt, s.L,  \
-                           s.BD, s.D, s.B, i, dst_len, ppl, hgroup);                               \
-      else                                                                                         \
+      if constexpr (NN <= kMaxRedFftN) {                                                           \
+        if (fast)                                                                                  \
+          hipLaunchKernelGGL((k_fft_tile<NN, true, true>), grid, block, 0, st, S, H, tw, Hf, yt,   \
+                             zt, s.L, s.BD, s.D, s.B, i, dst_len, ppl, hgroup);                    \
+        else                                                                                       \
+          hipLaunchKernelGGL((k_fft_tile<NN, true, false>), grid, block, 0, st, S, H, tw, Hf, yt,  \
+                             zt, s.L, s.BD, s.D, s.B, i, dst_len, ppl, hgroup);                    \
+      } else {                                                                                     \
         return hipErrorInvalidValue;                                                               \
-    } else                                                                                         \
-      hipLaunchKernelGGL((k_fft_tile<NN, false>), grid, block, 0, st, S, H, tw, Hf, yt, zt, s.L,   \
-                         s.BD, s.D, s.B, i, dst_len, ppl, hgroup);                                 \
+      }                                                                                            \
+    } else if (fast) {                                                                             \
+      hipLaunchKernelGGL((k_fft_tile<NN, false, true>), grid, block, 0, st, S, H, tw, Hf, yt, zt,  \
+                         s.L, s.BD, s.D, s.B, i, dst_len, ppl, hgroup);                            \
+    } else {                                                                                       \
+      hipLaunchKernelGGL((k_fft_tile<NN, false, false>), grid, block, 0, st, S, H, tw, Hf, yt, zt, \
+                         s.L, s.BD, s.D, s.B, i, dst_len, ppl, hgroup);                            \
+    }                                                                                              \
     return hipGetLastError();                                                                      \
   }
   switch (N) { LCSM_POW2_CASES(LCSM_CASE) }
@@ -701,11 +739,15 @@ hipError_t mid_spectra(const float2* C, float2* Hout, int D, const Chunk& ch, co
 }
 
 // Row length of the multi-pass split of an N-point transform: 1024-point
-// rows (four row workgroups per CU) measured fastest; longer rows only when
-// the column DFT would exceed kMaxMidN1 points.
+// rows (four row workgroups per CU) measured fastest while the columns stay
+// short; 4096-point rows when the columns would be longer than
+// kPreferredMidN1 points (a 128-point column pass runs at one wave per SIMD).
 int split_n2(int N, int lds_max_n) {
   int n2 = lds_max_n < kPreferredRowN2 ? lds_max_n : kPreferredRowN2;
   while (N / n2 > kMaxMidN1) n2 *= 2;
+  // past the preferred column length, straight to the longest rows (2048-point
+  // rows measured slower than both 1024- and 4096-point ones)
+  if (N / n2 > kPreferredMidN1 && N / kMaxRowN2 >= 2 && n2 < kMaxRowN2) n2 = kMaxRowN2;
   return n2;
 }
 

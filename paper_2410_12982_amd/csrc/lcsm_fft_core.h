@@ -1,4 +1,4 @@
-// Radix-8/4/2 Stockham FFT over columns held in LDS, for gfx950.
+// Radix-16/8/4/2 Stockham FFT over columns held in LDS, for gfx950.
 //
 // A workgroup transforms WC complex columns of N points at once.  The LDS
 // buffer is laid out [n][col] with a row stride of LDSW float2 (LDSW >= WC),
@@ -12,7 +12,7 @@
 //     x'[(j - k) R + k + s p] = sum_q u_q w_R^{q s}   (s < R)
 // where w_n = exp(-2 pi i / n) for the forward and exp(+2 pi i / n) for the
 // inverse transform (no 1/N factor).  After the last pass x' is the DFT in
-// natural order.  Passes are radix 8 except possibly the first (radix 2 or 4).
+// natural order.  The radices of an N-point transform are given by Plan<N>.
 //
 // Twiddles come from a table tw[n + m] = exp(-2 pi i m / n) for every power of
 // two n (m < n), built on the host in double precision and rounded once.
@@ -62,10 +62,25 @@ struct TwLds {
   }
 };
 
-// Copy w_N^m, m < N, from the global table into LDS (no synchronisation).
-template <int N, int NT>
+// Half table: w_N^m for m < N/2 only, using w_N^{m + N/2} = -w_N^m (for an
+// N-point transform whose data leaves no room for the full table).
+template <int N>
+struct TwLdsHalf {
+  const float2* t;
+  template <bool INV, int NN>
+  __device__ __forceinline__ float2 get(int e) const {
+    const int f = e * (N / NN);
+    const float2 w = t[f & (N / 2 - 1)];
+    const float s = (f & (N / 2)) ? -1.f : 1.f;
+    return INV ? make_float2(s * w.x, -s * w.y) : make_float2(s * w.x, s * w.y);
+  }
+};
+
+// Copy w_N^m, m < NM, from the global table of the N-point twiddles into LDS
+// (no synchronisation).
+template <int N, int NT, int NM = N>
 __device__ __forceinline__ void load_twiddles(float2* lds, const float2* __restrict__ tw) {
-  for (int m = (int)threadIdx.x; m < N; m += NT) lds[m] = tw[N + m];
+  for (int m = (int)threadIdx.x; m < NM; m += NT) lds[m] = tw[N + m];
 }
 
 // multiply by w_4 (forward -i, inverse +i)
@@ -103,14 +118,29 @@ __device__ __forceinline__ void dft4(float2& a0, float2& a1, float2& a2, float2&
   a3 = csub(t1, t3);
 }
 
+// multiply by the constant w_16^e (e = 1 or 3; forward sign, conjugated for
+// the inverse)
+template <bool INV, int E>
+__device__ __forceinline__ float2 rot16(float2 a) {
+  constexpr float c1 = 0.92387953251128675613f;  // cos(pi/8)
+  constexpr float s1 = 0.38268343236508977173f;  // sin(pi/8)
+  constexpr float c = E == 1 ? c1 : s1;           // cos(E pi/8)
+  constexpr float s = E == 1 ? s1 : c1;           // sin(E pi/8)
+  // w = c - i s (forward), c + i s (inverse)
+  return INV ? make_float2(c * a.x - s * a.y, c * a.y + s * a.x)
+             : make_float2(c * a.x + s * a.y, c * a.y - s * a.x);
+}
+
+// In-place DFT of R points held in registers, natural order in and out.
+// Radix 16 is four radix-4 DFTs over the stride-4 subsequences, the twiddles
+// w_16^{n2 k1}, and four radix-4 DFTs across them.
 template <int R, bool INV>
 __device__ __forceinline__ void dft(float2* v) {
   if constexpr (R == 2) {
     dft2<INV>(v[0], v[1]);
   } else if constexpr (R == 4) {
     dft4<INV>(v[0], v[1], v[2], v[3]);
-  } else {
-    static_assert(R == 8, "radix 2, 4 or 8");
+  } else if constexpr (R == 8) {
     float2 e0 = v[0], e1 = v[2], e2 = v[4], e3 = v[6];
     float2 o0 = v[1], o1 = v[3], o2 = v[5], o3 = v[7];
     dft4<INV>(e0, e1, e2, e3);
@@ -126,25 +156,95 @@ __device__ __forceinline__ void dft(float2* v) {
     v[6] = csub(e2, o2);
     v[3] = cadd(e3, o3);
     v[7] = csub(e3, o3);
+  } else {
+    static_assert(R == 16, "radix 2, 4, 8 or 16");
+    // y[n2][k1] = sum_{n1} x[4 n1 + n2] w_4^{n1 k1}
+    float2 y[4][4];
+#pragma unroll
+    for (int n2 = 0; n2 < 4; ++n2) {
+      y[n2][0] = v[n2];
+      y[n2][1] = v[4 + n2];
+      y[n2][2] = v[8 + n2];
+      y[n2][3] = v[12 + n2];
+      dft4<INV>(y[n2][0], y[n2][1], y[n2][2], y[n2][3]);
+    }
+    // twiddles w_16^{n2 k1}: exponents 1 2 3 / 2 4 6 / 3 6 9
+    y[1][1] = rot16<INV, 1>(y[1][1]);
+    y[1][2] = rot45<INV>(y[1][2]);
+    y[1][3] = rot16<INV, 3>(y[1][3]);
+    y[2][1] = rot45<INV>(y[2][1]);
+    y[2][2] = rot90<INV>(y[2][2]);
+    y[2][3] = rot135<INV>(y[2][3]);
+    y[3][1] = rot16<INV, 3>(y[3][1]);
+    y[3][2] = rot135<INV>(y[3][2]);
+    {
+      const float2 w = rot16<INV, 1>(y[3][3]);  // w_16^9 = -w_16^1
+      y[3][3] = make_float2(-w.x, -w.y);
+    }
+    // X[k1 + 4 k2] = sum_{n2} y[n2][k1] w_4^{n2 k2}
+#pragma unroll
+    for (int k1 = 0; k1 < 4; ++k1) {
+      float2 a0 = y[0][k1], a1 = y[1][k1], a2 = y[2][k1], a3 = y[3][k1];
+      dft4<INV>(a0, a1, a2, a3);
+      v[k1] = a0;
+      v[k1 + 4] = a1;
+      v[k1 + 8] = a2;
+      v[k1 + 12] = a3;
+    }
   }
 }
 
 constexpr int ilog2(int n) { return n <= 1 ? 0 : 1 + ilog2(n / 2); }
 
-// Radix plan of an N-point transform: one radix-2 or radix-4 pass first when
-// log2 N is not a multiple of 3, radix 8 for all others (so the last pass,
-// which may write to global memory, always has few butterflies per thread).
+// Radix plan of an N-point transform, as few passes as radices 16 and 8
+// allow: radix-16 passes first (the very first may be radix 2 or 4 when
+// neither fits exactly), then radix 8.  log2 N -> radices:
+//   1..4: N;  5: 2 16;  6: 8 8;  7: 16 8;  8: 16 16;  9: 8 8 8;  10: 16 8 8;
+//   11: 16 16 8;  12: 16 16 16;  13: 16 8 8 8;  and so on.
+// With LCSM_RADIX8_ONLY defined: radix 8 throughout, radix 2 or 4 first.
 template <int N>
 struct Plan {
   static_assert(N >= 2 && (N & (N - 1)) == 0, "power of two");
   static constexpr int LOG = ilog2(N);
-  static constexpr int N8 = LOG / 3;               // radix-8 passes
-  static constexpr int REM = LOG - 3 * N8;         // 0, 1 or 2
-  static constexpr int NP = N8 + (REM ? 1 : 0);    // passes
-  static constexpr int radix(int ps) { return (REM && ps == 0) ? (1 << REM) : 8; }
+#ifdef LCSM_RADIX8_ONLY
+  static constexpr int N16 = 0;
+  static constexpr int N8 = LOG / 3;
+  static constexpr int REM = LOG - 3 * N8;  // 0, 1 or 2
+#else
+  // number of radix-16 passes n16 and radix-8 passes n8 with 4 n16 + 3 n8 =
+  // LOG - rem, minimising the pass count, rem in {0, 1, 2} only if needed
+  static constexpr int pick(int what) {
+    int best_np = 1 << 30, b16 = 0, b8 = 0, brem = 0;
+    for (int rem = 0; rem <= 2; ++rem)
+      for (int n16 = 0; 4 * n16 <= LOG - rem; ++n16) {
+        const int left = LOG - rem - 4 * n16;
+        if (left % 3) continue;
+        const int n8 = left / 3;
+        const int np = n16 + n8 + (rem ? 1 : 0);
+        // fewer passes first, then no remainder pass, then fewer radix-16
+        if (np < best_np || (np == best_np && rem < brem) ||
+            (np == best_np && rem == brem && n16 < b16)) {
+          best_np = np;
+          b16 = n16;
+          b8 = n8;
+          brem = rem;
+        }
+      }
+    return what == 0 ? b16 : (what == 1 ? b8 : brem);
+  }
+  static constexpr int N16 = LOG <= 4 ? 0 : pick(0);
+  static constexpr int N8 = LOG <= 4 ? 0 : pick(1);
+  static constexpr int REM = LOG <= 4 ? LOG : pick(2);  // LOG <= 4: one pass of radix N
+#endif
+  static constexpr int NP = N16 + N8 + (REM ? 1 : 0);
+  static constexpr int radix(int ps) {
+    return REM ? (ps == 0 ? (1 << REM) : (ps <= N16 ? 16 : 8)) : (ps < N16 ? 16 : 8);
+  }
   // product of the radices of passes 0 .. ps-1
   static constexpr int p_before(int ps) {
-    return ps == 0 ? 1 : (REM ? (1 << REM) * (1 << (3 * (ps - 1))) : (1 << (3 * ps)));
+    int p = 1;
+    for (int k = 0; k < ps; ++k) p *= radix(k);
+    return p;
   }
 };
 

@@ -46,8 +46,11 @@ hipError_t launch_zero(float* p, size_t n, hipStream_t st);
 
 // ---- FFT tiles (lcsm_fft.hip)
 
-// Largest column-DFT length of the multi-pass split (N = N1 * N2).
+// Largest and preferred column-DFT length of the multi-pass split
+// (N = N1 * N2): when preferred-length rows would leave columns longer than
+// kPreferredMidN1, the rows take their largest length kMaxRowN2 instead.
 constexpr int kMaxMidN1 = 128;
+constexpr int kPreferredMidN1 = 32;
 // Preferred and largest row-FFT length of the multi-pass split.
 constexpr int kPreferredRowN2 = 1024;
 constexpr int kMaxRowN2 = 4096;
