@@ -50,16 +50,17 @@ using fft::conjf2;
 using fft::csub;
 
 // Per-size launch shape of the LDS transforms: WC complex columns per
-// workgroup, NT threads.  WC * 8 bytes is the contiguous run read per row.
-// The kernels are bound by latency at the occupancy that registers and LDS
-// allow, so up to 2U = 2048 the panel is as narrow as the measured optimum
-// (several workgroups per CU overlap each other's global loads and LDS
-// passes).  TWL: the twiddle table w_N^m fits in LDS beside the data; TWH:
-// only its first half does (the rest follows from w_N^{m+N/2} = -w_N^m).
+// workgroup, NT threads.  WC * 8 bytes is the contiguous run read and written
+// per state row.  For 2U >= 1024 the tile kernels are bound by these strided
+// row accesses far more than by the transforms (without any LDS pass they
+// run barely faster), and narrow runs are expensive, so panels are as wide as
+// LDS allows: 64-byte runs up to 2U = 2048, 32 at 4096, 16 at 8192.  TWL:
+// the twiddle table w_N^m fits in LDS beside the data; TWH: only its first
+// half does (the rest follows from w_N^{m+N/2} = -w_N^m).
 template <int N>
 struct Cfg {
-  static constexpr int WC = N <= 256 ? 4 : (N <= 512 ? 8 : (N <= 4096 ? 4 : 2));
-  static constexpr int NT = N <= 128 ? 64 : (N <= 256 ? 128 : (N <= 2048 ? 256 : (N <= 4096 ? 512 : 1024)));
+  static constexpr int WC = N <= 256 ? 4 : (N <= 2048 ? 8 : (N <= 4096 ? 4 : 2));
+  static constexpr int NT = N <= 128 ? 64 : (N <= 256 ? 128 : (N <= 512 ? 256 : (N <= 1024 ? 512 : (N <= 2048 ? 1024 : (N <= 4096 ? 512 : 1024)))));
   static constexpr bool TWL = (size_t)N * 8 * (WC + 1) <= 163840;
   static constexpr bool TWH = !TWL && (size_t)N * 8 * WC + (size_t)N * 4 <= 163840;
   static constexpr int TWN = TWL ? N : (TWH ? N / 2 : 1);  // LDS twiddle entries
