@@ -152,9 +152,18 @@ __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_tile(float* __restrict__ S,
   const int q = fft::xcd_logical((int)blockIdx.x, (int)gridDim.x);
   const int m = q / ppl;
   const int r = q - m * ppl;
-  // panels of the same channels (different batch rows) are neighbours, so
-  // they share the filter spectrum through L2
-  const int panel = hgroup > 0 ? (r % B) * hgroup + r / B : r;
+  // Panel order: the LG panels that share 128-byte lines of a state row are
+  // consecutive (adjacent workgroups run together on one XCD, so each line is
+  // fetched and written back whole), and these line groups cycle through the
+  // batch rows of the same channels (which share the filter spectrum in L2).
+  constexpr int LG = WC >= 16 ? 1 : 16 / WC;
+  int panel = r;
+  if (hgroup > 0 && hgroup % LG == 0) {
+    const int g = r / LG;
+    panel = (g % B) * hgroup + (g / B) * LG + (r - g * LG);
+  } else if (hgroup > 0) {
+    panel = (r % B) * hgroup + r / B;
+  }
   const int c0 = panel * 2 * WC;
   const int d0 = FAST ? c0 % D : 0;
   const bool vec = FAST || (BD & 1) == 0;
