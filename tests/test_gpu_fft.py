@@ -74,6 +74,25 @@ def test_integer_data_rounds_to_exact(opt, shape):
     assert np.array_equal(np.rint(z).astype(np.int64), ex)
 
 
+@pytest.mark.parametrize("opt", ["default", "lds_from_2"])
+@pytest.mark.parametrize("shape", [(1, 2, 48, 4500), (1, 3, 24, 4200), (2, 1, 10, 6000)])
+def test_integer_data_panel_orders_and_clipped_large_tiles(opt, shape):
+    """Shapes whose channel count is not a whole number of 128-byte line
+    groups of panels (48 and 24 channels: the batch-row panel order), or not
+    a whole number of panels (10 channels), and lengths that clip the 2U =
+    8192 tile's destination window (the general, bounds-checked kernel)."""
+    M, B, D, L = shape
+    say(f"[int fft panels/clipped] M={M} B={B} D={D} L={L} options={opt}")
+    w, h, y = _int_case(M, B, D, L, 3, seed=5 * sum(shape))
+    ctx, _ = make_ctx(w, torch.from_numpy(h).to(dev()), FFT_OPTIONS[opt])
+    z = _run_full(ctx, torch.from_numpy(y).to(dev()))
+    ex = _exact(h, y)
+    err = np.abs(z.astype(np.float64) - ex).max()
+    say(f"  max abs err {err:.3e}")
+    assert err < 0.25
+    assert np.array_equal(np.rint(z).astype(np.int64), ex)
+
+
 @pytest.mark.parametrize("opt", ["lds_from_2", "multipass_from_16", "tiny_scratch", "default"])
 def test_m1b8d768l8k_teacher_forced_all_columns(opt):
     w = datagen.WORKLOADS["m1b8d768l8k"]
