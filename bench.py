@@ -63,6 +63,12 @@ def parse():
                    help="only convert rocprofv3 FETCH_SIZE/WRITE_SIZE runs under DIR (pmc_copy_*, "
                         "pmc_bench_*) into profiles/traffic.json and a text summary")
     p.add_argument("--copy-mib", type=int, default=1024, help="size the copy probe ran with")
+    p.add_argument("--copy-scalar", action="store_true",
+                   help="copy probe with 4-byte accesses per lane (a one-element offset keeps torch "
+                        "from vectorising) instead of 16-byte vector accesses")
+    p.add_argument("--positions", type=int, default=0, metavar="P",
+                   help="only run the first P positions of one generation from the host, printing "
+                        "progress (for counter runs: few dispatches); prints no metric")
     return p.parse_args()
 
 
@@ -166,7 +172,7 @@ def traffic_from(args):
                         "-d <dir>/pmc_copy_{C} -o run -- python3 bench.py --copy-probe 1024",
                         "cd /tmp && export TMPDIR=/tmp && rocprofv3 --pmc {C} --output-format csv "
                         f"-d <dir>/pmc_bench_{{C}} -o run -- python3 bench.py --workload {args.workload} "
-                        "--no-graph --steps 1 --warmup 0 --no-kernel-pass --no-cpu-baseline",
+                        f"--positions {args.positions or '<P>'}",
                         "  for C in FETCH_SIZE, WRITE_SIZE; then: python3 bench.py --traffic-from <dir> "
                         f"--workload {args.workload}"],
            "kernels": kernels}
@@ -206,13 +212,16 @@ def main():
     import torch
 
     if args.copy_probe:
-        copy_probe(args.copy_probe, torch)
+        copy_probe(args.copy_probe, torch, args.copy_scalar)
         return
 
     import datagen
     import paper_2410_12982_amd.lcsm as lcsm
 
     w = datagen.WORKLOADS[args.workload]
+    if args.positions:
+        counter_run(args, w, torch, datagen, lcsm)
+        return
     if args.graph and w.L > GRAPH_MAX_L:
         print(f"# L={w.L} > {GRAPH_MAX_L}: launching from the host (no whole-generation graph)",
               file=sys.stderr, flush=True)
@@ -309,17 +318,46 @@ def main():
     print(json.dumps(out), flush=True)
 
 
-def copy_probe(mib, torch):
+def counter_run(args, w, torch, datagen, lcsm):
+    """The first P positions of one generation, launched from the host (the
+    dispatches a counter run should see), with a progress line every 256
+    positions.  No timing and no metric."""
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    opts = {k: v for k, v in (("direct_max_u", args.direct_max_u),
+                              ("lds_fft_max_n", args.lds_fft_max_n),
+                              ("scratch_mib", args.scratch_mib)) if v} or None
+    P = min(args.positions, w.L)
+    filters = datagen.filters_torch(w, dev)
+    R = min(RING, w.L)
+    y = datagen.y_torch(w, dev, 0, R)
+    z = torch.empty_like(y)
+    ctx = lcsm.Lcsm(filters, w.B, options=opts)
+    torch.cuda.synchronize()
+    for t in range(P):
+        ctx.step(y[t % R], z[t % R])
+        if (t + 1) % 256 == 0 or t + 1 == P:
+            torch.cuda.synchronize()
+            print(f"# position {t + 1} of {P}", file=sys.stderr, flush=True)
+    ctx.close()
+    print(json.dumps({"counter_run": True, "workload": w.name, "positions": P}), flush=True)
+
+
+def copy_probe(mib, torch, scalar=False):
     """A plain elementwise kernel reading and writing mib MiB each (b = -a),
-    five times: the reference for scaling the HBM byte counters."""
+    five times: the reference for scaling the HBM byte counters.  scalar: the
+    views start one element into their buffers, so torch cannot use vector
+    accesses and every lane moves 4 bytes."""
     n = mib * (1 << 20) // 4
-    a = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    a = torch.ones(n + 1, dtype=torch.float32, device="cuda:0")
     b = torch.empty_like(a)
+    src, dst = (a[1:], b[1:]) if scalar else (a[:n], b[:n])
     torch.cuda.synchronize()
     for _ in range(5):
-        torch.neg(a, out=b)
+        torch.neg(src, out=dst)
     torch.cuda.synchronize()
-    print(json.dumps({"copy_probe_mib": mib, "bytes_read": 4 * n, "bytes_written": 4 * n}), flush=True)
+    print(json.dumps({"copy_probe_mib": mib, "scalar": scalar, "bytes_read": 4 * n,
+                      "bytes_written": 4 * n}), flush=True)
 
 
 def kernel_pass(w, filters, y, z, opts, lcsm, torch):
@@ -389,7 +427,8 @@ def kernel_pass(w, filters, y, z, opts, lcsm, torch):
         roofline["largest_tile"] = {"kernel": f"{bname} U={bU}", "bytes_per_launch": bbytes,
                                     "avg_launch_us": round(bavg * 1e6, 3),
                                     "achieved": round(bbytes / bavg / 1e9, 2),
-                                    "frac": round(bbytes / bavg / 1e9 / HBM_PEAK_GBS, 5)}
+                                    "frac": round(bbytes / bavg / 1e9 / HBM_PEAK_GBS, 5),
+                                    "traffic": committed_traffic(bname, bU, w)}
     return roofline, levels
 
 

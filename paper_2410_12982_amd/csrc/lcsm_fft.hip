@@ -116,6 +116,24 @@ __device__ __forceinline__ float2 pair_product(float2 zk, float2 znk, float2 ha,
   return cadd(cmul(zk, s), cmul(conjf2(znk), d));
 }
 
+// Panel of the r-th workgroup of a layer (panels of WC complex columns).  The
+// LG panels that share 128-byte lines of a state row are consecutive
+// (adjacent workgroups run together on one XCD, so each line is fetched and
+// written back whole), and these line groups cycle through the batch rows of
+// the same channels (which share the filter spectrum in L2).  hgroup = panels
+// per batch row when D is a multiple of the panel width, else 0.  A bijection
+// on [0, panels per layer).
+template <int WC>
+__device__ __forceinline__ int panel_of(int r, int B, int hgroup) {
+  constexpr int LG = WC >= 16 ? 1 : 16 / WC;
+  if (hgroup > 0 && hgroup % LG == 0) {
+    const int g = r / LG;
+    return (g % B) * hgroup + (g / B) * LG + (r - g * LG);
+  }
+  if (hgroup > 0) return (r % B) * hgroup + r / B;
+  return r;
+}
+
 // ----------------------------------------------------------- single pass
 
 // Every global load of a stage is issued before that stage needs it: the
@@ -151,20 +169,7 @@ __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_tile(float* __restrict__ S,
   const auto twz = make_tw<N>(twl, tw);
   const int q = fft::xcd_logical((int)blockIdx.x, (int)gridDim.x);
   const int m = q / ppl;
-  const int r = q - m * ppl;
-  // Panel order: the LG panels that share 128-byte lines of a state row are
-  // consecutive (adjacent workgroups run together on one XCD, so each line is
-  // fetched and written back whole), and these line groups cycle through the
-  // batch rows of the same channels (which share the filter spectrum in L2).
-  constexpr int LG = WC >= 16 ? 1 : 16 / WC;
-  int panel = r;
-  if (hgroup > 0 && hgroup % LG == 0) {
-    const int g = r / LG;
-    panel = (g % B) * hgroup + (g / B) * LG + (r - g * LG);
-  } else if (hgroup > 0) {
-    panel = (r % B) * hgroup + r / B;
-  }
-  const int c0 = panel * 2 * WC;
+  const int c0 = panel_of<WC>(q - m * ppl, B, hgroup) * 2 * WC;
   const int d0 = FAST ? c0 % D : 0;
   const bool vec = FAST || (BD & 1) == 0;
   float* Sm = S + (size_t)m * L * BD;
