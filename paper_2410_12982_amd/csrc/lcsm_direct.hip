@@ -43,14 +43,14 @@ template <int U, bool RED>
 __global__ __launch_bounds__(kThreads) void k_step_fused(const float* __restrict__ y,
                                                         float* __restrict__ z,
                                                         float* __restrict__ S,
-                                                        const float* __restrict__ Hf, int M, int L,
+                                                        const float* __restrict__ Hf, int m0, int L,
                                                         int BD, int D, int t, int dst_len) {
   constexpr int SP = U > 0 ? Split<U>::value : 1;
   constexpr int UJ = U > 0 ? U / SP : 1;  // outputs per thread
   const int d = (int)blockIdx.x * kThreads + (int)threadIdx.x;
   if (d >= D) return;
-  const int m = (int)blockIdx.z / SP;
-  const int part = (int)blockIdx.z - m * SP;
+  const int m = m0 + (int)blockIdx.z / SP;
+  const int part = (int)blockIdx.z - (m - m0) * SP;
   const int j0 = part * UJ;
   const int c = (int)blockIdx.y * D + d;
   const size_t e = (size_t)m * BD + c;
@@ -222,10 +222,12 @@ __global__ __launch_bounds__(kThreads) void k_direct_tile(float* __restrict__ S,
 
 __global__ __launch_bounds__(kThreads) void k_transpose(const float* __restrict__ src,
                                                        float* __restrict__ dst, int D, int L) {
-  // src [D][L] -> dst [L][D] for layer blockIdx.z; 32x32 tiles, padded LDS
+  // src [D][L] -> dst [L][D] for layer blockIdx.z; 32x32 tiles, padded LDS.
+  // Channel tiles on x (up to 2^31 blocks), lag tiles on y (L <= 2^19 gives
+  // at most 16384, inside the 65536-block limit of y and z).
   __shared__ float tile[32][33];
   const size_t off = (size_t)blockIdx.z * D * L;
-  const int l0 = blockIdx.x * 32, d0 = blockIdx.y * 32;
+  const int d0 = blockIdx.x * 32, l0 = blockIdx.y * 32;
   const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 32 x 8
   for (int r = ty; r < 32; r += 8) {
     const int d = d0 + r, l = l0 + tx;
@@ -245,17 +247,24 @@ __global__ __launch_bounds__(kThreads) void k_zero(float* __restrict__ p, size_t
 
 inline unsigned blocks_for(int64_t n) { return (unsigned)((n + kThreads - 1) / kThreads); }
 
+// Layers go on grid z (times the output split); launches are chunked over
+// layers so that z stays within the 65536-block limit of y and z.
 template <bool RED>
 hipError_t dispatch_fused(int U, const float* y, float* z, float* S, const float* Hf,
                           const Shape& s, int t, int dst_len, hipStream_t st) {
   const dim3 block(kThreads);
 #define LCSM_FUSED_CASE(UU)                                                                      \
-  case UU:                                                                                       \
-    hipLaunchKernelGGL((k_step_fused<UU, RED>),                                                  \
-                       dim3(blocks_for(s.D), (unsigned)s.B,                                      \
-                            (unsigned)(s.M * (UU > 0 ? Split<UU>::value : 1))),                  \
-                       block, 0, st, y, z, S, Hf, s.M, s.L, s.BD, s.D, t, dst_len);              \
-    break;
+  case UU: {                                                                                     \
+    constexpr int SP = UU > 0 ? Split<UU>::value : 1;                                            \
+    constexpr int MC = 65535 / SP;                                                               \
+    for (int m0 = 0; m0 < s.M; m0 += MC) {                                                       \
+      const int mc = s.M - m0 < MC ? s.M - m0 : MC;                                              \
+      hipLaunchKernelGGL((k_step_fused<UU, RED>),                                                \
+                         dim3(blocks_for(s.D), (unsigned)s.B, (unsigned)(mc * SP)), block, 0,    \
+                         st, y, z, S, Hf, m0, s.L, s.BD, s.D, t, dst_len);                      \
+    }                                                                                            \
+    break;                                                                                       \
+  }
   switch (U) {
     LCSM_FUSED_CASE(0)
     LCSM_FUSED_CASE(1)
@@ -275,7 +284,7 @@ hipError_t dispatch_fused(int U, const float* y, float* z, float* S, const float
 }  // namespace
 
 hipError_t launch_transpose_filters(const float* src, float* dst, const Shape& s, hipStream_t st) {
-  const dim3 grid((s.L + 31) / 32, (s.D + 31) / 32, s.M);
+  const dim3 grid((s.D + 31) / 32, (s.L + 31) / 32, s.M);
   hipLaunchKernelGGL(k_transpose, grid, dim3(kThreads), 0, st, src, dst, s.D, s.L);
   return hipGetLastError();
 }

@@ -220,3 +220,36 @@ def test_sequencing_errors():
     assert ctx.position == 1
     with pytest.raises(ValueError):
         ctx.step(torch.zeros((w.M, w.B, w.D + 1), device=dev()))
+
+
+def _exact_by_lag(h, y):
+    """Exact integer reference like _exact, vectorised over columns: one
+    shifted multiply-add per lag (z[t] += y[t-k] h[k])."""
+    L, M, B, D = y.shape
+    hi = h.astype(np.int64)            # [M, D, L]
+    yi = y.astype(np.int64)            # [L, M, B, D]
+    z = np.zeros_like(yi)
+    for k in range(L):
+        z[k:] += yi[: L - k] * hi[None, :, None, :, k]
+    return z
+
+
+@pytest.mark.parametrize("opt", ["default", "fft_from_2"])
+@pytest.mark.parametrize("shape", [(16384, 1, 1, 64), (1, 65535, 1, 64)])
+def test_integer_data_at_the_layer_and_batch_limits(opt, shape):
+    """The largest layer count (16384: the step launches are split over layers
+    to keep grid z within 65536 blocks) and batch-row count (65535: grid y)
+    the library accepts, on small-integer data: bit-exact with direct tiles,
+    rounding to the exact integers with FFT tiles (error far below 1/2)."""
+    M, B, D, L = shape
+    say(f"[limits] M={M} B={B} D={D} L={L} options={opt}")
+    w, h, y = _int_case(M, B, D, L, 3, seed=sum(shape))
+    ctx, _ = make_ctx(w, torch.from_numpy(h).to(dev()), OPTION_SETS[opt])
+    z = _run_full(ctx, torch.from_numpy(y).to(dev()))
+    ctx.close()
+    ex = _exact_by_lag(h, y)
+    if opt == "default":  # every tile of a 64-long run is direct
+        assert np.array_equal(z, ex.astype(np.float32))
+    else:
+        assert np.abs(z.astype(np.float64) - ex).max() < 0.25
+        assert np.array_equal(np.rint(z).astype(np.int64), ex)
