@@ -65,28 +65,49 @@ __global__ __launch_bounds__(kThreads) void k_step_fused(const float* __restrict
   float zo[UJ];
   const bool tile = (U > 0) && (j0 < dst_len);
   const bool red = RED && part == 0;
+  // Every load is unconditional, with its row or lag clamped into range
+  // (values past the end are never used): loads under a condition are issued
+  // only after the earlier ones have returned, a second round trip per step.
   float yt, acc = 0.f, h0 = 0.f;
   if constexpr (RED) {
     yt = y[e];
-    if (red) {
-      acc = col[(size_t)t * rs];
-      h0 = hc[0];
-    }
+    acc = col[(size_t)t * rs];
+    h0 = hc[0];
   } else {
     yt = col[(size_t)t * rs];
   }
   if constexpr (U > 0) {
-    if (tile) {
-      // rows t+1-U .. t-1 already hold inputs; row t is y_t
+    // rows t+1-U .. t-1 already hold inputs (U divides t+1); row t is y_t
 #pragma unroll
-      for (int k = 0; k < U - 1; ++k) yb[k] = col[(size_t)(t + 1 - U + k) * rs];
-      // output j uses lags U+j-k, k < U: for j in [j0, j0+UJ) that is j0+1 .. j0+UJ+U-1
+    for (int k = 0; k < U - 1; ++k) yb[k] = col[(size_t)(t + 1 - U + k) * rs];
+    // output j uses lags U+j-k, k < U: for j in [j0, j0+UJ) that is j0+1 .. j0+UJ+U-1
 #pragma unroll
-      for (int l = 1; l < UJ + U; ++l) hh[l] = (j0 + l < L) ? hc[(size_t)(j0 + l) * D] : 0.f;
-#pragma unroll
-      for (int jj = 0; jj < UJ; ++jj)
-        zo[jj] = (j0 + jj < dst_len) ? col[(size_t)(t + 1 + j0 + jj) * rs] : 0.f;
+    for (int l = 1; l < UJ + U; ++l) {
+      const int lag = j0 + l;
+      const float v = hc[(size_t)(lag < L ? lag : L - 1) * D];
+      hh[l] = lag < L ? v : 0.f;
     }
+#pragma unroll
+    for (int jj = 0; jj < UJ; ++jj) {
+      const int row = t + 1 + j0 + jj;
+      zo[jj] = col[(size_t)(row < L ? row : L - 1) * rs];
+    }
+  }
+  // Pin every loaded value here, after the last load (an empty statement
+  // that reads and writes each register): no load is sunk into the
+  // conditional red-cell or tile blocks below, and all of them are in flight
+  // together.  The tile's values only up to U = 16: with the 80 and more
+  // values of the larger tiles held at once the compiler issues the loads in
+  // small groups instead.
+  constexpr bool PIN = U <= 16;
+  if constexpr (RED) asm volatile("" : "+v"(acc), "+v"(h0));
+  if constexpr (U > 0 && PIN) {
+#pragma unroll
+    for (int l = 1; l < UJ + U; ++l) asm volatile("" : "+v"(hh[l]));
+#pragma unroll
+    for (int jj = 0; jj < UJ; ++jj) asm volatile("" : "+v"(zo[jj]));
+#pragma unroll
+    for (int k = 0; k < U - 1; ++k) asm volatile("" : "+v"(yb[k]));
   }
   if (red) {
     z[e] = fmaf(h0, yt, acc);
