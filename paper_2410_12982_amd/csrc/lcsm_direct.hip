@@ -131,52 +131,86 @@ __global__ __launch_bounds__(kThreads) void k_step_fused(const float* __restrict
 
 // The chained input rule (lcsm_step_chain) fused with red cells and, for
 // 1 <= U <= kChainFusedMaxU, the gray tiles.  One thread per (b, d) column walks
-// the layers in order, since y^m_t depends on z^{m-1}_t.
+// the layers in order, since y^m_t depends on z^{m-1}_t.  Only the arithmetic
+// is sequential: the layers' loads (x, accumulator, h_0 and the tile's inputs,
+// lags and destination rows) do not depend on the chain, so they are issued
+// K layers at a time ahead of that chunk's stores, and a step costs about
+// M/K memory round trips instead of M.
+// Largest chunk for a tile side U (bounds the registers the chunk's loads
+// take); the launch uses the largest power of two not above it or M.
 template <int U>
+struct ChainChunk {
+  static constexpr int value = U <= 2 ? 8 : (U <= 8 ? 4 : (U <= 16 ? 2 : 1));
+};
+
+template <int U, int K>
 __global__ __launch_bounds__(kThreads) void k_chain_fused(const float* __restrict__ x,
                                                          float* __restrict__ z,
                                                          float* __restrict__ S,
                                                          const float* __restrict__ Hf,
                                                          float* __restrict__ prev, int M, int L,
                                                          int BD, int D, int t, int dst_len) {
+  constexpr int NY = U > 0 ? U : 1;
+  constexpr int NH = U > 0 ? 2 * U : 1;
+  constexpr int NZ = U > 0 ? U : 1;
   const int d = (int)blockIdx.x * kThreads + (int)threadIdx.x;
   if (d >= D) return;
   const int c = (int)blockIdx.y * D + d;
   const size_t rs = (size_t)BD;
-  constexpr int NY = U > 0 ? U : 1;
-  constexpr int NH = U > 0 ? 2 * U : 1;
   const bool tile = (U > 0) && (dst_len > 0);
-  float zl = (t > 0) ? prev[c] : 0.f;  // z^{M-1}_{t-1}, then z^{m-1}_t
-  for (int m = 0; m < M; ++m) {
-    float* col = S + (size_t)m * L * BD + c;
-    const float* hc = Hf + (size_t)m * L * D + d;
-    float yb[NY];
-    float hh[NH];
-    if constexpr (U > 0) {
-      if (tile) {
+  float zl = 0.f;  // z^{M-1}_{t-1} (loaded with the first chunk), then z^{m-1}_t
+  for (int m0 = 0; m0 < M; m0 += K) {
+    float xv[K], acc[K], h0[K];
+    float yb[K][NY], hh[K][NH], zo[K][NZ];
+    // loads of the chunk's layers (past the last layer: layer M-1 again,
+    // unused; rows and lags clamped into range)
 #pragma unroll
-        for (int k = 0; k < U - 1; ++k) yb[k] = col[(size_t)(t + 1 - U + k) * rs];
+    for (int kk = 0; kk < K; ++kk) {
+      const int m = m0 + kk < M ? m0 + kk : M - 1;
+      const float* col = S + (size_t)m * L * BD + c;
+      const float* hc = Hf + (size_t)m * L * D + d;
+      xv[kk] = x[(size_t)m * BD + c];
+      acc[kk] = col[(size_t)t * rs];
+      h0[kk] = hc[0];
+      if constexpr (U > 0) {
 #pragma unroll
-        for (int l = 1; l < 2 * U; ++l) hh[l] = (l < L) ? hc[(size_t)l * D] : 0.f;
-      }
-    }
-    const float xv = x[(size_t)m * BD + c];
-    const float yv = (m == 0 && t == 0) ? xv : fmaf(0.5f, tanhf(zl), xv);
-    const float acc = col[(size_t)t * rs];
-    const float zv = fmaf(hc[0], yv, acc);
-    z[(size_t)m * BD + c] = zv;
-    col[(size_t)t * rs] = yv;
-    zl = zv;
-    if constexpr (U > 0) {
-      if (tile) {
-        yb[U - 1] = yv;
+        for (int k = 0; k < U - 1; ++k) yb[kk][k] = col[(size_t)(t + 1 - U + k) * rs];
+#pragma unroll
+        for (int l = 1; l < 2 * U; ++l) {
+          const float v = hc[(size_t)(l < L ? l : L - 1) * D];
+          hh[kk][l] = l < L ? v : 0.f;
+        }
 #pragma unroll
         for (int j = 0; j < U; ++j) {
-          if (j < dst_len) {
-            float o = 0.f;
+          const int row = t + 1 + j;
+          zo[kk][j] = col[(size_t)(row < L ? row : L - 1) * rs];
+        }
+      }
+    }
+    if (m0 == 0) zl = prev[c];  // unused at t = 0
+    // the chain through the chunk, then its stores
 #pragma unroll
-            for (int k = 0; k < U; ++k) o = fmaf(yb[k], hh[U + j - k], o);
-            col[(size_t)(t + 1 + j) * rs] += o;
+    for (int kk = 0; kk < K; ++kk) {
+      const int m = m0 + kk;
+      if (m < M) {
+        float* col = S + (size_t)m * L * BD + c;
+        const float yv = (m == 0 && t == 0) ? xv[kk] : fmaf(0.5f, tanhf(zl), xv[kk]);
+        const float zv = fmaf(h0[kk], yv, acc[kk]);
+        z[(size_t)m * BD + c] = zv;
+        col[(size_t)t * rs] = yv;
+        zl = zv;
+        if constexpr (U > 0) {
+          if (tile) {
+            yb[kk][U - 1] = yv;
+#pragma unroll
+            for (int j = 0; j < U; ++j) {
+              if (j < dst_len) {
+                float o = 0.f;
+#pragma unroll
+                for (int k = 0; k < U; ++k) o = fmaf(yb[kk][k], hh[kk][U + j - k], o);
+                col[(size_t)(t + 1 + j) * rs] = zo[kk][j] + o;
+              }
+            }
           }
         }
       }
@@ -318,11 +352,23 @@ hipError_t launch_step_fused(const float* y, float* z, float* S, const float* Hf
 hipError_t launch_chain_fused(const float* x, float* z, float* S, const float* Hf, float* prev,
                               const Shape& s, int t, int U, int dst_len, hipStream_t st) {
   const dim3 grid(blocks_for(s.D), (unsigned)s.B), block(kThreads);
-#define LCSM_CHAIN_CASE(UU)                                                                   \
-  case UU:                                                                                    \
-    hipLaunchKernelGGL((k_chain_fused<UU>), grid, block, 0, st, x, z, S, Hf, prev, s.M, s.L, \
-                       s.BD, s.D, t, dst_len);                                                \
-    break;
+#define LCSM_CHAIN_K(UU, KK)                                                                      \
+  hipLaunchKernelGGL((k_chain_fused<UU, KK>), grid, block, 0, st, x, z, S, Hf, prev, s.M, s.L,   \
+                     s.BD, s.D, t, dst_len)
+#define LCSM_CHAIN_CASE(UU)                                                                       \
+  case UU: {                                                                                      \
+    constexpr int KM = ChainChunk<UU>::value;                                                     \
+    if (KM >= 8 && s.M >= 8) {                                                                    \
+      LCSM_CHAIN_K(UU, (KM >= 8 ? 8 : 1));                                                        \
+    } else if (KM >= 4 && s.M >= 4) {                                                             \
+      LCSM_CHAIN_K(UU, (KM >= 4 ? 4 : 1));                                                        \
+    } else if (KM >= 2 && s.M >= 2) {                                                             \
+      LCSM_CHAIN_K(UU, (KM >= 2 ? 2 : 1));                                                        \
+    } else {                                                                                      \
+      LCSM_CHAIN_K(UU, 1);                                                                        \
+    }                                                                                             \
+    break;                                                                                        \
+  }
   switch (U) {
     LCSM_CHAIN_CASE(0)
     LCSM_CHAIN_CASE(1)
@@ -335,6 +381,7 @@ hipError_t launch_chain_fused(const float* x, float* z, float* S, const float* H
       return hipErrorInvalidValue;
   }
 #undef LCSM_CHAIN_CASE
+#undef LCSM_CHAIN_K
   return hipGetLastError();
 }
 
