@@ -19,7 +19,10 @@ Printed: one JSON line, with
                 subtracted);
   cpu_baseline  the CPU oracle (relaxed tiling, fp64 numpy, as it stands) on
                 a bounded sample of columns of the same workload, spread over
-                worker processes.
+                worker processes;
+  closed_loop   the same generation with the workload's own feedback (the
+                built-in tanh chain, lcsm_step_chain) instead of
+                teacher-forced inputs, dispatched the same way.
 """
 from __future__ import annotations
 
@@ -56,7 +59,9 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work, about")
     p.add_argument("--no-kernel-pass", action="store_true")
-    p.add_argument("--closed-loop", action="store_true", help="also time the tanh-chain generation")
+    p.add_argument("--no-closed-loop", dest="closed_loop", action="store_false", default=True,
+                   help="skip timing the closed-loop generation (the built-in tanh chain feeding each "
+                        "layer's output into the next input)")
     p.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                    help="only run a plain elementwise copy of MIB MiB 5 times (counter calibration)")
     p.add_argument("--traffic-from", metavar="DIR", default=None,
@@ -286,7 +291,7 @@ def main():
 
     closed = None
     if args.closed_loop:
-        closed = closed_loop(w, filters, opts, lcsm, torch, dev)
+        closed = closed_loop(w, filters, opts, lcsm, torch, dev, args)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -432,23 +437,48 @@ def kernel_pass(w, filters, y, z, opts, lcsm, torch):
     return roofline, levels
 
 
-def closed_loop(w, filters, opts, lcsm, torch, dev):
-    """Time one closed-loop generation with the built-in tanh chain."""
+def closed_loop(w, filters, opts, lcsm, torch, dev, args):
+    """Closed-loop generations (lcsm_step_chain: y^0_t = 0.5 tanh(z^{M-1}_{t-1})
+    + x^0_t, y^m_t = 0.5 tanh(z^{m-1}_t) + x^m_t), dispatched like the timed
+    region (one HIP graph per generation up to GRAPH_MAX_L positions, host
+    launches above): warmup untimed, then steps timed with events."""
     import datagen
     R = min(RING, w.L)
     x = datagen.x_torch(w, dev, 0, R)
     z = torch.empty_like(x)
-    ctx = lcsm.Lcsm(filters, w.B, options=opts)
+    graph_ok = args.graph and w.L <= GRAPH_MAX_L
+    stream = torch.cuda.Stream(dev) if graph_ok else torch.cuda.current_stream(dev)
+    ctx = lcsm.Lcsm(filters, w.B, options=opts, stream=stream)
+    torch.cuda.synchronize()
+
+    def generation():
+        ctx.reset()
+        for t in range(w.L):
+            ctx.step_chain(x[t % R], z[t % R])
+
+    if graph_ok:
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=stream):
+            generation()
+        torch.cuda.synchronize()
+        one = graph.replay
+    else:
+        one = generation
+    for _ in range(args.warmup):
+        one()
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
-    for t in range(w.L):
-        ctx.step_chain(x[t % R], z[t % R])
+    for _ in range(args.steps):
+        one()
     e1.record()
     torch.cuda.synchronize()
-    cms = e0.elapsed_time(e1)
+    cms = e0.elapsed_time(e1) / args.steps
+    if graph_ok:
+        del graph
     ctx.close()
-    return {"ms": round(cms, 3), "tokens_per_s": round(w.B * w.L / (cms / 1e3), 1)}
+    return {"ms_per_step": round(cms, 4), "tokens_per_s": round(w.B * w.L / (cms / 1e3), 1),
+            "graph": graph_ok}
 
 
 def _oracle_shard(arg):
