@@ -209,8 +209,12 @@ int step_common(lcsm_ctx* c, const float* in, float* z, bool chain) {
   const int U = (i < c->s.L) ? lowbit(i) : 0;
   const int dst_len = U ? (U < c->s.L - i ? U : c->s.L - i) : 0;
   const int kind = tile_kind(c->opt, c->s, U);
-  const bool fuse =
-      kind == LCSM_TILE_DIRECT && U <= (chain ? lcsm::kChainFusedMaxU : lcsm::kFusedMaxU);
+  // The chained step fuses its tiles only for a single layer: with several,
+  // the red cells run one thread per column through all layers, and the
+  // tiles go to the ordinary all-layer tile launch (parallel over layers).
+  const bool fuse = kind == LCSM_TILE_DIRECT &&
+                    (chain ? (U <= lcsm::kChainFusedMaxU && c->s.M <= lcsm::kChainFusedMaxM)
+                           : U <= lcsm::kFusedMaxU);
   hipError_t e;
   if (!chain && kind == LCSM_TILE_FFT && dst_len > 0 && 2 * U <= lcsm::kMaxRedFftN) {
     // red cells fused into the single-pass FFT tile: one launch

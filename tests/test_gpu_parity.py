@@ -110,6 +110,30 @@ def test_small_workload_closed_loop():
     assert err <= TOL
 
 
+@pytest.mark.parametrize("opt", ["default", "fft_from_2", "all_direct"])
+@pytest.mark.parametrize("shape", [(4, 2, 24, 300), (11, 1, 8, 130)])
+def test_multilayer_closed_loop(opt, shape):
+    """The chain across layers (y^m_t from z^{m-1}_t, layer 0 from the last
+    layer's z_{t-1}): with several layers the red cells walk the layers in
+    chunks of loads and the tiles run in the separate all-layer launch.
+    Filters decay fast (as in the 1024-position workload), so the fp32 closed
+    loop stays close to the fp64 one over these lengths."""
+    M, B, D, L = shape
+    w = datagen.Workload("chain", M, B, D, L, decay=200.0, seed=21 + M)
+    say(f"[multi-layer closed loop] M={M} B={B} D={D} L={L} options={opt}")
+    ctx, _ = make_ctx(w, options=OPTION_SETS[opt])
+    x = datagen.x_torch(w, dev())
+    z = torch.empty_like(x)
+    for t in range(w.L):
+        ctx.step_chain(x[t], z[t])
+    torch.cuda.synchronize()
+    h = filters_to_columns(datagen.filters_np(w), w.B)
+    zr, _ = relaxed_online(h, feedback.tanh_chain(datagen.x_np(w).reshape(w.L, w.M, -1), w.M))
+    err = rel_err(z.cpu().numpy().reshape(w.L, w.M, -1), zr)
+    say(f"  closed-loop rel err {err:.3e}")
+    assert err <= TOL
+
+
 @pytest.mark.parametrize("opt", ["all_direct"])
 def test_m1b8d768l8k_teacher_forced_all_columns(opt):
     w = datagen.WORKLOADS["m1b8d768l8k"]
