@@ -288,6 +288,12 @@ def main():
     roofline, levels = None, {}
     if not args.no_kernel_pass:
         roofline, levels = kernel_pass(w, filters, y, z, opts, lcsm, torch)
+        # the per-launch floor this launch-bound path sits on, measured live
+        floor_us = launch_floor(w, torch, dev)
+        roofline["launch_floor"] = {
+            "us_per_launch": round(floor_us, 3),
+            "how": "graph-replayed elementwise kernels on a tensor of one position's M*B*D floats",
+            "generation_us_per_position": round(1e3 * ms / w.L, 3)}
 
     closed = None
     if args.closed_loop:
@@ -363,6 +369,32 @@ def copy_probe(mib, torch, scalar=False):
     torch.cuda.synchronize()
     print(json.dumps({"copy_probe_mib": mib, "scalar": scalar, "bytes_read": 4 * n,
                       "bytes_written": 4 * n}), flush=True)
+
+
+def launch_floor(w, torch, dev, n=2048):
+    """Microseconds per launch of n back-to-back elementwise kernels (x += 1
+    on M*B*D floats, one position's slab) replayed from one HIP graph: the
+    cost of a launch that does one read and one write per element."""
+    x = torch.zeros(w.M * w.B * w.D, dtype=torch.float32, device=dev)
+    s = torch.cuda.Stream(dev)
+    g = torch.cuda.CUDAGraph()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g, stream=s):
+        for _ in range(n):
+            x.add_(1.0)
+    torch.cuda.synchronize()
+    g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    best = float("inf")
+    for _ in range(3):
+        e0.record()
+        g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        best = min(best, e0.elapsed_time(e1))
+    del g
+    return 1e3 * best / n
 
 
 def kernel_pass(w, filters, y, z, opts, lcsm, torch):
