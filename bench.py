@@ -59,6 +59,8 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work, about")
     p.add_argument("--no-kernel-pass", action="store_true")
+    p.add_argument("--no-prefill", dest="prefill", action="store_false", default=True,
+                   help="skip timing the prompt prefill against the same positions stepped online")
     p.add_argument("--no-closed-loop", dest="closed_loop", action="store_false", default=True,
                    help="skip timing the closed-loop generation (the built-in tanh chain feeding each "
                         "layer's output into the next input)")
@@ -299,6 +301,10 @@ def main():
     if args.closed_loop:
         closed = closed_loop(w, filters, opts, lcsm, torch, dev, args)
 
+    prefill = None
+    if args.prefill:
+        prefill = prefill_timing(w, filters, opts, lcsm, torch, dev)
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(w, args.cpu_budget)
@@ -326,6 +332,8 @@ def main():
         out["per_level_us"] = levels
     if closed:
         out["closed_loop"] = closed
+    if prefill:
+        out["prefill"] = prefill
     print(json.dumps(out), flush=True)
 
 
@@ -511,6 +519,47 @@ def closed_loop(w, filters, opts, lcsm, torch, dev, args):
     ctx.close()
     return {"ms_per_step": round(cms, 4), "tokens_per_s": round(w.B * w.L / (cms / 1e3), 1),
             "graph": graph_ok}
+
+
+def prefill_timing(w, filters, opts, lcsm, torch, dev, max_bytes=2 << 30):
+    """A prompt of P positions (the largest power of two with 2P <= L whose
+    inputs fit in max_bytes) through lcsm_prefill against the same P
+    positions through lcsm_run, each captured in a HIP graph (reset
+    included) and replayed: prompt tokens/s of both."""
+    import datagen
+    slab = w.M * w.B * w.D * 4
+    P = 1
+    while 4 * P <= w.L and 2 * P * slab <= max_bytes:
+        P *= 2
+    y = datagen.y_torch(w, dev, 0, P)
+    z = torch.empty_like(y)
+    stream = torch.cuda.Stream(dev)
+    ctx = lcsm.Lcsm(filters, w.B, options=opts, stream=stream)
+    torch.cuda.synchronize()
+    res = {}
+    for mode in ("prefill", "steps"):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            ctx.reset()
+            if mode == "prefill":
+                ctx.prefill(y, z, P)
+            else:
+                ctx.run(y, z, n=P)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(3):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        res[mode] = e0.elapsed_time(e1) / 3
+        del g
+    ctx.close()
+    return {"P": P, "ms": round(res["prefill"], 4), "steps_ms": round(res["steps"], 4),
+            "prompt_tokens_per_s": round(w.B * P / (res["prefill"] / 1e3), 1),
+            "speedup_vs_steps": round(res["steps"] / res["prefill"], 2)}
 
 
 def _oracle_shard(arg):

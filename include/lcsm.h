@@ -121,6 +121,26 @@ int lcsm_advance(lcsm_ctx* ctx);
  * steps, with one host call.  Errors as lcsm_step; stops at the first. */
 int lcsm_run(lcsm_ctx* ctx, int n, const float* y, size_t y_stride, float* z, size_t z_stride);
 
+/* Prompt prefill (Sec. 2.2.1 "The Inference Problem"; the appendix on the
+ * prefilling and autoregressive stages): with all P prompt inputs known, the
+ * prompt's own outputs come from one transform instead of P online steps.
+ *   y  device [P][M][B][D] prompt inputs y^m_t, position k at y + k*y_stride;
+ *   z  device [P][M][B][D] receives z^m_t for t < P, at z + k*z_stride
+ *      (strides in floats, as for lcsm_run).
+ * P must be a power of two with 2P <= L, and the context at position 0 (after
+ * lcsm_init or lcsm_reset).  Afterwards the context is at position P in
+ * exactly the state P calls of lcsm_step would leave (state rows < P hold the
+ * prompt, rows >= P its contributions from the gray tile of i = P), so
+ * lcsm_step / lcsm_run continue the generation.  When P is an FFT tile size
+ * (above the direct crossover) the work is: copy the prompt into the state,
+ * one 2P-point tile with the filter spectrum delayed by P rows (its outputs
+ * are the causal convolution of the prompt), the same tile with the cached
+ * spectrum; the spectra of tile size P are recomputed twice in place.  For a
+ * direct tile size it runs the P ordinary steps.  Errors: LCSM_EINVAL (null
+ * pointers, P not a power of two or 2P > L), LCSM_ESTATE (not at position 0,
+ * or faulted), LCSM_EDEVICE. */
+int lcsm_prefill(lcsm_ctx* ctx, int P, const float* y, size_t y_stride, float* z, size_t z_stride);
+
 /* Restart at position 0 with all activations zero; keeps filters and
  * spectra and clears a fault.  Errors: LCSM_EDEVICE. */
 int lcsm_reset(lcsm_ctx* ctx);

@@ -191,7 +191,7 @@ hipError_t init_spectra(lcsm_ctx* c) {
   for (int q = 0; e == hipSuccess && q < kMaxLevels && (1 << q) <= c->s.L - 1; ++q) {
     const int U = 1 << q;
     if (tile_kind(c->opt, c->s, U) == LCSM_TILE_DIRECT) continue;
-    e = lcsm::launch_spectra(c->Hf, (float2*)(c->ws + c->ly.H[q]), c->tw, c->s, U,
+    e = lcsm::launch_spectra(c->Hf, (float2*)(c->ws + c->ly.H[q]), c->tw, c->s, U, 0,
                              c->opt.lds_fft_max_n, c->scratch, c->ly.scratch_bytes, c->stream);
   }
   // the host table must outlive the copy
@@ -361,6 +361,40 @@ int lcsm_run(lcsm_ctx* c, int n, const float* y, size_t y_stride, float* z, size
     const int r = step_common(c, y + (size_t)k * y_stride, z + (size_t)k * z_stride, false);
     if (r) return r;
   }
+  return LCSM_OK;
+}
+
+int lcsm_prefill(lcsm_ctx* c, int P, const float* y, size_t y_stride, float* z, size_t z_stride) {
+  if (!c) return LCSM_EINVAL;
+  if (!y || !z) return fail(c, LCSM_EINVAL, "null input or output pointer", hipSuccess);
+  if (c->faulted) return LCSM_ESTATE;
+  if (c->t != 0 || c->layers_done != 0)
+    return fail(c, LCSM_ESTATE, "prefill only at position 0 (after init or reset)", hipSuccess);
+  if (!is_pow2(P) || 2 * P > c->s.L)
+    return fail(c, LCSM_EINVAL, "prompt length must be a power of two with 2P <= L", hipSuccess);
+  const Shape& s = c->s;
+  // a prompt of a direct tile size: P ordinary steps
+  if (tile_kind(c->opt, s, P) == LCSM_TILE_DIRECT) return lcsm_run(c, P, y, y_stride, z, z_stride);
+  // P is an FFT tile size, so its cached spectra and the twiddles for 2P exist
+  float2* H = (float2*)(c->ws + c->ly.H[__builtin_ctz((unsigned)P)]);
+  // the prompt into state rows [0, P)
+  hipError_t e = lcsm::launch_rows_in(y, y_stride, c->S, s, P, c->stream);
+  // the tile i = P with the filter delayed by P rows puts, in rows [P, 2P),
+  // sum_{k<P} y[k] h[j - k] = z_j for j < P: the prompt's own outputs
+  if (e == hipSuccess)
+    e = lcsm::launch_spectra(c->Hf, H, c->tw, s, P, P, c->opt.lds_fft_max_n, c->scratch,
+                             c->ly.scratch_bytes, c->stream);
+  if (e == hipSuccess)
+    e = lcsm::launch_fft_tile(c->S, H, c->tw, s, P, P, P, c->opt.lds_fft_max_n, c->scratch,
+                              c->ly.scratch_bytes, c->stream);
+  if (e == hipSuccess) e = lcsm::launch_rows_out_clear(c->S, s, P, P, z, z_stride, c->stream);
+  // the tile spectra back, then the gray tile of i = P that P steps would end with
+  if (e == hipSuccess)
+    e = lcsm::launch_spectra(c->Hf, H, c->tw, s, P, 0, c->opt.lds_fft_max_n, c->scratch,
+                             c->ly.scratch_bytes, c->stream);
+  if (e == hipSuccess) e = launch_tile(c, P, P, P);
+  if (e != hipSuccess) return fail(c, LCSM_EDEVICE, "prefill", e);
+  c->t = P;
   return LCSM_OK;
 }
 

@@ -295,6 +295,36 @@ __global__ __launch_bounds__(kThreads) void k_transpose(const float* __restrict_
   }
 }
 
+// Prompt rows in: S[m][t][c] = y[t * ys + m * BD + c] for t < P (grid-stride
+// over P * M * BD, consecutive threads on consecutive c).
+__global__ __launch_bounds__(kThreads) void k_rows_in(const float* __restrict__ y, size_t ys,
+                                                     float* __restrict__ S, int M, int L, int BD,
+                                                     int P) {
+  const size_t n = (size_t)P * M * BD, stride = (size_t)gridDim.x * kThreads;
+  for (size_t e = (size_t)blockIdx.x * kThreads + threadIdx.x; e < n; e += stride) {
+    const size_t tm = e / BD;
+    const int c = (int)(e - tm * BD);
+    const int m = (int)(tm % M), t = (int)(tm / M);
+    S[((size_t)m * L + t) * BD + c] = y[t * ys + (size_t)m * BD + c];
+  }
+}
+
+// State rows out: z[t * zs + m * BD + c] = S[m][row0 + t][c], then the state
+// entry is cleared, for t < P.
+__global__ __launch_bounds__(kThreads) void k_rows_out_clear(float* __restrict__ S, int M, int L,
+                                                            int BD, int row0, int P,
+                                                            float* __restrict__ z, size_t zs) {
+  const size_t n = (size_t)P * M * BD, stride = (size_t)gridDim.x * kThreads;
+  for (size_t e = (size_t)blockIdx.x * kThreads + threadIdx.x; e < n; e += stride) {
+    const size_t tm = e / BD;
+    const int c = (int)(e - tm * BD);
+    const int m = (int)(tm % M), t = (int)(tm / M);
+    float* p = S + ((size_t)m * L + row0 + t) * BD + c;
+    z[t * zs + (size_t)m * BD + c] = *p;
+    *p = 0.f;
+  }
+}
+
 __global__ __launch_bounds__(kThreads) void k_zero(float* __restrict__ p, size_t n) {
   const size_t stride = (size_t)gridDim.x * kThreads;
   for (size_t k = (size_t)blockIdx.x * kThreads + threadIdx.x; k < n; k += stride) p[k] = 0.f;
@@ -404,6 +434,28 @@ hipError_t launch_direct_tile(float* S, const float* Hf, const Shape& s, int i, 
   const dim3 grid(blocks_for(s.BD), (dst_len + kDirectJ - 1) / kDirectJ, s.M);
   hipLaunchKernelGGL(k_direct_tile<kDirectJ>, grid, dim3(kThreads), 0, st, S, Hf, s.L, s.BD, s.D,
                      i, U, dst_len);
+  return hipGetLastError();
+}
+
+hipError_t launch_rows_in(const float* y, size_t y_stride, float* S, const Shape& s, int P,
+                          hipStream_t st) {
+  const size_t n = (size_t)P * s.M * s.BD;
+  if (n == 0) return hipSuccess;
+  size_t blocks = (n + kThreads - 1) / kThreads;
+  if (blocks > 8192) blocks = 8192;
+  hipLaunchKernelGGL(k_rows_in, dim3((unsigned)blocks), dim3(kThreads), 0, st, y, y_stride, S, s.M,
+                     s.L, s.BD, P);
+  return hipGetLastError();
+}
+
+hipError_t launch_rows_out_clear(float* S, const Shape& s, int row0, int P, float* z,
+                                 size_t z_stride, hipStream_t st) {
+  const size_t n = (size_t)P * s.M * s.BD;
+  if (n == 0) return hipSuccess;
+  size_t blocks = (n + kThreads - 1) / kThreads;
+  if (blocks > 8192) blocks = 8192;
+  hipLaunchKernelGGL(k_rows_out_clear, dim3((unsigned)blocks), dim3(kThreads), 0, st, S, s.M, s.L,
+                     s.BD, row0, P, z, z_stride);
   return hipGetLastError();
 }
 

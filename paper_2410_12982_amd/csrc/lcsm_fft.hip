@@ -315,12 +315,14 @@ __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_tile(float* __restrict__ S,
 }
 
 // Filter spectra of tile size U = N/2 for all layers: H[m][k][d] =
-// DFT_N(h[m][0..N), d)[k] / N for k <= N/2 (taps at lags >= L are zero).
+// DFT_N(g[m][0..N), d)[k] / N for k <= N/2, where g is the filter delayed by
+// shift rows (g[r] = h[r - shift], zero before; taps at lags >= L are zero).
+// shift = 0 for the tile spectra; shift = U for the prompt's own outputs.
 template <int N>
 __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_spectra(const float* __restrict__ Hf,
                                                             float2* __restrict__ Hout,
                                                             const float2* __restrict__ tw, int L,
-                                                            int D, int ppl) {
+                                                            int D, int ppl, int shift) {
   constexpr int WC = Cfg<N>::WC, NT = Cfg<N>::NT, U = N / 2;
   __shared__ float2 buf[N * WC];
   __shared__ float2 twl[Cfg<N>::TWN];
@@ -330,7 +332,9 @@ __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_spectra(const float* __restr
   const bool vec = (D & 1) == 0;
   const float* src = Hf + (size_t)m * L * D;
   fft::forward_from_global<N, WC, WC, NT, false>(buf, twz, [&](int row, int col) {
-    return row < L ? load_pair(src + (size_t)row * D, c0 + 2 * col, D, vec) : make_float2(0.f, 0.f);
+    const int hr = row - shift;  // the filter delayed by shift rows
+    return (hr >= 0 && hr < L) ? load_pair(src + (size_t)hr * D, c0 + 2 * col, D, vec)
+                               : make_float2(0.f, 0.f);
   });
   constexpr float inv_n = 1.0f / (float)N;
   float2* Hm = Hout + (size_t)m * (U + 1) * D;
@@ -361,7 +365,7 @@ struct Chunk {
 };
 
 // Pass R: N2-point FFT over rows row0 + n1 + N1 n2 of every layer's matrix
-// (src + m*lstride, row stride ncols), rows >= rows_valid read as zero; HALF:
+// (src + m*lstride, row stride ncols), rows < 0 or >= rows_valid read as zero; HALF:
 // only n2 < N2/2 are read.  Output C[n1*N2 + k2][x] = FFT[k2] * w_N^{n1 k2}.
 template <int N2, bool HALF>
 __global__ __launch_bounds__(Cfg<N2>::NT) void k_fft_rows_fwd(const float* __restrict__ src,
@@ -381,7 +385,7 @@ __global__ __launch_bounds__(Cfg<N2>::NT) void k_fft_rows_fwd(const float* __res
   fft::forward_from_global<N2, WC, WC, NT, HALF>(buf, twz, [&](int n2, int col) {
     const int x = x0 + col;
     const int row = row0 + n1 + ch.N1 * n2;
-    if (x >= ch.nvalid || row >= rows_valid) return make_float2(0.f, 0.f);
+    if (x >= ch.nvalid || row < 0 || row >= rows_valid) return make_float2(0.f, 0.f);
     const int g = ch.g0 + x;
     const int m = g / ch.ncc;
     const int c = 2 * (g - m * ch.ncc);
@@ -681,12 +685,12 @@ hipError_t tile_single(int N, float* S, const float2* H, const float2* tw, const
 }
 
 hipError_t spectra_single(int N, const float* Hf, float2* Hout, const float2* tw, const Shape& s,
-                          hipStream_t st) {
+                          int shift, hipStream_t st) {
 #define LCSM_CASE(NN)                                                                            \
   case NN: {                                                                                     \
     const int ppl = (s.D + 2 * Cfg<NN>::WC - 1) / (2 * Cfg<NN>::WC);                             \
     hipLaunchKernelGGL(k_fft_spectra<NN>, dim3((unsigned)(ppl * s.M)), dim3(Cfg<NN>::NT), 0, st, \
-                       Hf, Hout, tw, s.L, s.D, ppl);                                             \
+                       Hf, Hout, tw, s.L, s.D, ppl, shift);                                      \
     return hipGetLastError();                                                                    \
   }
   switch (N) { LCSM_POW2_CASES(LCSM_CASE) }
@@ -778,9 +782,10 @@ int fft_multipass_chunk(int N, size_t scratch_bytes, int total_cc) {
 }
 
 hipError_t launch_spectra(const float* Hf, float2* Hout, const float2* tw, const Shape& s, int U,
-                          int lds_max_n, float2* scratch, size_t scratch_bytes, hipStream_t st) {
+                          int shift, int lds_max_n, float2* scratch, size_t scratch_bytes,
+                          hipStream_t st) {
   const int N = 2 * U;
-  if (N <= lds_max_n) return spectra_single(N, Hf, Hout, tw, s, st);
+  if (N <= lds_max_n) return spectra_single(N, Hf, Hout, tw, s, shift, st);
   Chunk ch{};
   ch.ncols = s.D;
   ch.ncc = (s.D + 1) / 2;
@@ -793,7 +798,7 @@ hipError_t launch_spectra(const float* Hf, float2* Hout, const float2* tw, const
   for (int g0 = 0; g0 < total; g0 += ch.cstride) {
     ch.g0 = g0;
     ch.nvalid = total - g0 < ch.cstride ? total - g0 : ch.cstride;
-    hipError_t e = rows_fwd<false>(Hf, (size_t)s.L * s.D, 0, s.L, ch, C, tw, st);
+    hipError_t e = rows_fwd<false>(Hf, (size_t)s.L * s.D, -shift, s.L, ch, C, tw, st);
     if (e == hipSuccess) e = mid_spectra(C, Hout, s.D, ch, tw, st);
     if (e != hipSuccess) return e;
   }

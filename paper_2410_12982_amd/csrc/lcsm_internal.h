@@ -47,6 +47,16 @@ hipError_t launch_direct_tile(float* S, const float* Hf, const Shape& s, int i, 
 // Fill n floats with zero (a kernel, so it is safe under graph capture).
 hipError_t launch_zero(float* p, size_t n, hipStream_t st);
 
+// Prompt rows: copy y[t][m][:] (position stride y_stride floats) into state
+// rows t < P of every layer.
+hipError_t launch_rows_in(const float* y, size_t y_stride, float* S, const Shape& s, int P,
+                          hipStream_t st);
+
+// Copy state rows row0 + t (t < P) of every layer out to z[t][m][:]
+// (position stride z_stride floats) and clear them.
+hipError_t launch_rows_out_clear(float* S, const Shape& s, int row0, int P, float* z,
+                                 size_t z_stride, hipStream_t st);
+
 // ---- FFT tiles (lcsm_fft.hip)
 
 // Largest and preferred column-DFT length of the multi-pass split
@@ -66,10 +76,12 @@ constexpr int kMaxLdsFftN = 8192;
 // of 16, or 0 if the scratch cannot hold one chunk of 16).
 int fft_multipass_chunk(int N, size_t scratch_bytes, int total_cc);
 
-// Filter spectra of tile size U (N = 2U): Hout[m][k][d] = DFT_N(h[m,d,0:N))[k]
-// / N for k = 0..U.  tw: twiddle table (see lcsm_fft_core.h).
+// Filter spectra of tile size U (N = 2U): Hout[m][k][d] = DFT_N(g[m,d,0:N))[k]
+// / N for k = 0..U, with g the filter delayed by shift rows (g[r] = h[r -
+// shift], zero for r < shift).  tw: twiddle table (see lcsm_fft_core.h).
 hipError_t launch_spectra(const float* Hf, float2* Hout, const float2* tw, const Shape& s, int U,
-                          int lds_max_n, float2* scratch, size_t scratch_bytes, hipStream_t st);
+                          int shift, int lds_max_n, float2* scratch, size_t scratch_bytes,
+                          hipStream_t st);
 
 // FFT gray tile of all layers: y rows [i-U, i) -> z rows [i, i+dst_len),
 // with the spectra H of tile size U.  Single LDS pass when 2U <= lds_max_n,

@@ -69,6 +69,7 @@ _SIGS = {
     "lcsm_step_layer": (ctypes.c_int, [_vp, ctypes.c_int, _vp, _vp]),
     "lcsm_advance": (ctypes.c_int, [_vp]),
     "lcsm_run": (ctypes.c_int, [_vp, ctypes.c_int, _vp, ctypes.c_size_t, _vp, ctypes.c_size_t]),
+    "lcsm_prefill": (ctypes.c_int, [_vp, ctypes.c_int, _vp, ctypes.c_size_t, _vp, ctypes.c_size_t]),
     "lcsm_reset": (ctypes.c_int, [_vp]),
     "lcsm_position": (ctypes.c_int, [_vp, _c_int_p]),
     "lcsm_plan_tile": (ctypes.c_int, [ctypes.c_int] * 4 + [ctypes.POINTER(Options), ctypes.c_int]
@@ -224,6 +225,21 @@ class Lcsm:
         slab = self.M * self.B * self.D
         self._check(_lib.lcsm_run(self._ctx, int(n), y.data_ptr(), slab, z.data_ptr(), slab),
                     "lcsm_run")
+        return z
+
+    def prefill(self, y, z, P=None):
+        """Prompt prefill at position 0: y, z are [P, M, B, D] tensors (P a power
+        of two, 2P <= L); z receives the prompt's outputs and the context moves
+        to position P."""
+        shape = (self.M, self.B, self.D)
+        P = y.shape[0] if P is None else P
+        if y.shape[1:] != shape or z.shape[1:] != shape or y.shape[0] < P or z.shape[0] < P:
+            raise ValueError("y and z must be [P, M, B, D]")
+        if not (y.is_contiguous() and z.is_contiguous() and y.is_cuda and z.is_cuda):
+            raise ValueError("y and z must be contiguous CUDA tensors")
+        slab = self.M * self.B * self.D
+        self._check(_lib.lcsm_prefill(self._ctx, int(P), y.data_ptr(), slab, z.data_ptr(), slab),
+                    "lcsm_prefill")
         return z
 
     def reset(self):
