@@ -22,7 +22,11 @@ Printed: one JSON line, with
                 worker processes;
   closed_loop   the same generation with the workload's own feedback (the
                 built-in tanh chain, lcsm_step_chain) instead of
-                teacher-forced inputs, dispatched the same way.
+                teacher-forced inputs, dispatched the same way;
+  prefill       a prompt through lcsm_prefill against the same positions
+                stepped;
+  half_state    the timed generations again with half-state storage (T of
+                the L state rows per layer), and the bytes it saves.
 """
 from __future__ import annotations
 
@@ -61,6 +65,8 @@ def parse():
     p.add_argument("--no-kernel-pass", action="store_true")
     p.add_argument("--no-prefill", dest="prefill", action="store_false", default=True,
                    help="skip timing the prompt prefill against the same positions stepped online")
+    p.add_argument("--no-half-state", dest="half_state", action="store_false", default=True,
+                   help="skip the generations with half-state storage")
     p.add_argument("--no-closed-loop", dest="closed_loop", action="store_false", default=True,
                    help="skip timing the closed-loop generation (the built-in tanh chain feeding each "
                         "layer's output into the next input)")
@@ -135,7 +141,7 @@ def kernel_key(name):
         if m.group(2) == "false":
             return ("direct", u)
         return ("fused", u) if u else ("red", 0)
-    m = re.search(r"k_fft_tile<(\d+), (true|false)(, (true|false))?>", name)
+    m = re.search(r"k_fft_tile<(\d+), (true|false)(, (true|false))*>", name)
     if m:
         return ("fft_lds", int(m.group(1)) // 2)
     return None
@@ -245,46 +251,8 @@ def main():
     R = min(RING, w.L)
     y = datagen.y_torch(w, dev, 0, R)                 # [R, M, B, D] resident in HBM
     z = torch.empty_like(y)
-    stream = torch.cuda.Stream(dev) if args.graph else torch.cuda.current_stream(dev)
-    ctx = lcsm.Lcsm(filters, w.B, options=opts, stream=stream)
-    torch.cuda.synchronize()
-
-    def generation():
-        ctx.reset()
-        for t0 in range(0, w.L, R):
-            ctx.run(y, z, n=min(R, w.L - t0))
-
-    if args.graph:
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph, stream=stream):
-            generation()
-        torch.cuda.synchronize()
-        one_step = graph.replay
-    else:
-        one_step = generation
-
-    for _ in range(args.warmup):
-        one_step()
-    torch.cuda.synchronize()
-    print(f"# warmup done ({args.warmup})", file=sys.stderr, flush=True)
-
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter()
-    ev0.record()
-    for _ in range(args.steps):
-        one_step()
-    ev1.record()
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter() - t_wall
-    ms = ev0.elapsed_time(ev1) / args.steps
+    ms = timed_generations(w, filters, y, z, opts, lcsm, torch, dev, args, verbose=True)
     value = w.B * w.L / (ms / 1e3)
-    print(f"# timed {args.steps} steps: {ms:.3f} ms/step (wall {1e3 * t_wall / args.steps:.3f})",
-          file=sys.stderr, flush=True)
-    if args.graph:
-        del graph
-    ctx.close()
-    del ctx
     torch.cuda.synchronize()
 
     roofline, levels = None, {}
@@ -304,6 +272,10 @@ def main():
     prefill = None
     if args.prefill:
         prefill = prefill_timing(w, filters, opts, lcsm, torch, dev)
+
+    half = None
+    if args.half_state:
+        half = half_state_timing(w, filters, y, z, opts, ms, lcsm, torch, dev, args)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -334,6 +306,8 @@ def main():
         out["closed_loop"] = closed
     if prefill:
         out["prefill"] = prefill
+    if half:
+        out["half_state"] = half
     print(json.dumps(out), flush=True)
 
 
@@ -475,6 +449,78 @@ def kernel_pass(w, filters, y, z, opts, lcsm, torch):
                                     "frac": round(bbytes / bavg / 1e9 / HBM_PEAK_GBS, 5),
                                     "traffic": committed_traffic(bname, bU, w)}
     return roofline, levels
+
+
+def timed_generations(w, filters, y, z, opts, lcsm, torch, dev, args, verbose=False):
+    """Teacher-forced generations of all L positions (inputs from the ring y
+    resident in HBM), one HIP graph per generation up to GRAPH_MAX_L positions
+    (host launches above): warmup untimed, then args.steps timed with events.
+    Returns ms per generation."""
+    R = y.shape[0]
+    stream = torch.cuda.Stream(dev) if args.graph else torch.cuda.current_stream(dev)
+    ctx = lcsm.Lcsm(filters, w.B, options=opts, stream=stream)
+    torch.cuda.synchronize()
+
+    def generation():
+        ctx.reset()
+        for t0 in range(0, w.L, R):
+            ctx.run(y, z, n=min(R, w.L - t0))
+
+    if args.graph:
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=stream):
+            generation()
+        torch.cuda.synchronize()
+        one_step = graph.replay
+    else:
+        one_step = generation
+
+    for _ in range(args.warmup):
+        one_step()
+    torch.cuda.synchronize()
+    if verbose:
+        print(f"# warmup done ({args.warmup})", file=sys.stderr, flush=True)
+
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    ev0.record()
+    for _ in range(args.steps):
+        one_step()
+    ev1.record()
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    ms = ev0.elapsed_time(ev1) / args.steps
+    if verbose:
+        print(f"# timed {args.steps} steps: {ms:.3f} ms/step (wall {1e3 * t_wall / args.steps:.3f})",
+              file=sys.stderr, flush=True)
+    if args.graph:
+        del graph
+    ctx.close()
+    del ctx
+    torch.cuda.synchronize()
+    return ms
+
+
+def half_state_timing(w, filters, y, z, opts, ms_full, lcsm, torch, dev, args):
+    """The same generations with half-state storage (App. C: T state rows per
+    layer instead of L, the tile of i = T storing over its own inputs), timed
+    the same way; with the state bytes of both forms."""
+    hopts = dict(opts or {}, half_state=1)
+    try:
+        full_b = lcsm.workspace_bytes(w.M, w.B, w.D, w.L, opts)
+        half_b = lcsm.workspace_bytes(w.M, w.B, w.D, w.L, hopts)
+    except lcsm.LcsmError as e:  # the tile of side T is a direct tile here
+        return {"skipped": str(e)}
+    print("# half-state generations", file=sys.stderr, flush=True)
+    ms = timed_generations(w, filters, y, z, hopts, lcsm, torch, dev, args)
+    T = 1
+    while 2 * T < w.L:
+        T *= 2
+    return {"T": T, "ms_per_step": round(ms, 4), "tokens_per_s": round(w.B * w.L / (ms / 1e3), 1),
+            "time_vs_full_state": round(ms / ms_full, 4),
+            "state_bytes": 4 * w.M * T * w.B * w.D, "state_bytes_full": 4 * w.M * w.L * w.B * w.D,
+            "workspace_bytes": half_b, "workspace_bytes_full": full_b}
 
 
 def closed_loop(w, filters, opts, lcsm, torch, dev, args):

@@ -60,16 +60,33 @@ typedef struct lcsm_options {
                         three passes through scratch (power of two in [16, 8192]; default 8192) */
   int scratch_mib;   /* cap of the multi-pass FFT scratch in MiB (default 512); the scratch is
                         never smaller than one chunk of 16 complex columns */
-  int reserved[5];   /* must be zero */
+  int half_state;    /* 1: keep only T state rows per layer instead of L, T the largest power
+                        of two below L (App. C, "Storing Only Half of the Activations"); see
+                        the note below.  0 (default): L rows */
+  int reserved[4];   /* must be zero */
 } lcsm_options;
+
+/* Half-state storage (lcsm_options.half_state = 1).  After position T-1 no
+ * input y_s with s < T is read again, and before it no contribution lands at
+ * a position >= T.  So the state keeps rows for positions [0, T) only, and
+ * the gray tile of i = T (side T, the largest one) writes its outputs for
+ * positions [T, L) over the rows of its own inputs, which it has already
+ * read: workgroup by workgroup (one LDS pass) or chunk by chunk of columns
+ * (multi-pass), each reading its columns' inputs before it stores any of
+ * their outputs.  From then on state row r stands for position T + r.  Needs
+ * no memory beyond the ordinary tile's; every output is bit-for-bit that of
+ * the full-state context (a zero's sign aside).  Requirements: the tile of
+ * side T is an FFT tile (L > 2 * the direct limit), and a prefill prompt P
+ * satisfies 2P <= T.  State memory: M*T*B*D floats instead of M*L*B*D. */
 
 typedef struct lcsm_ctx lcsm_ctx;
 
 /* Device bytes of the workspace a context of this shape needs (state
- * M*L*B*D fp32, filters M*L*D fp32, filter spectra of the FFT tile sizes, FFT
+ * M*L*B*D fp32 -- M*T*B*D with half_state --, filters M*L*D fp32, filter spectra of the FFT tile sizes, FFT
  * scratch and a few small buffers).  Host only: touches no device.
  * Errors: LCSM_EINVAL for sizes < 1, M > 16384, B > 65535, M*B*D >= 2^31, L > 2^19 or
- * bad options. */
+ * bad options (half_state not 0 or 1, or 1 where the tile of side T would be
+ * a direct tile). */
 int lcsm_workspace_bytes(int M, int B, int D, int L, const lcsm_options* opt, size_t* bytes);
 
 /* Create a context (Alg. 3's state: all activations zero, position t = 0).
@@ -127,7 +144,8 @@ int lcsm_run(lcsm_ctx* ctx, int n, const float* y, size_t y_stride, float* z, si
  *   y  device [P][M][B][D] prompt inputs y^m_t, position k at y + k*y_stride;
  *   z  device [P][M][B][D] receives z^m_t for t < P, at z + k*z_stride
  *      (strides in floats, as for lcsm_run).
- * P must be a power of two with 2P <= L, and the context at position 0 (after
+ * P must be a power of two with 2P <= L (2P <= T with half_state), and the
+ * context at position 0 (after
  * lcsm_init or lcsm_reset).  Afterwards the context is at position P in
  * exactly the state P calls of lcsm_step would leave (state rows < P hold the
  * prompt, rows >= P its contributions from the gray tile of i = P), so
@@ -137,8 +155,8 @@ int lcsm_run(lcsm_ctx* ctx, int n, const float* y, size_t y_stride, float* z, si
  * are the causal convolution of the prompt), the same tile with the cached
  * spectrum; the spectra of tile size P are recomputed twice in place.  For a
  * direct tile size it runs the P ordinary steps.  Errors: LCSM_EINVAL (null
- * pointers, P not a power of two or 2P > L), LCSM_ESTATE (not at position 0,
- * or faulted), LCSM_EDEVICE. */
+ * pointers, P not a power of two, 2P > L, or 2P > T with half_state),
+ * LCSM_ESTATE (not at position 0, or faulted), LCSM_EDEVICE. */
 int lcsm_prefill(lcsm_ctx* ctx, int P, const float* y, size_t y_stride, float* z, size_t z_stride);
 
 /* Restart at position 0 with all activations zero; keeps filters and

@@ -36,16 +36,20 @@ struct Options {
   int direct_max_u;  // 0: the shape-dependent default
   int lds_fft_max_n;
   int scratch_mib;
+  int half_state;
 };
 
 int resolve_options(const lcsm_options* o, Options* r) {
   r->direct_max_u = 0;
   r->lds_fft_max_n = kDefaultLdsFftMaxN;
   r->scratch_mib = kDefaultScratchMib;
+  r->half_state = 0;
   if (!o) return LCSM_OK;
-  for (int k = 0; k < 5; ++k)
+  for (int k = 0; k < 4; ++k)
     if (o->reserved[k] != 0) return LCSM_EINVAL;
   if (o->direct_max_u < 0 || o->lds_fft_max_n < 0 || o->scratch_mib < 0) return LCSM_EINVAL;
+  if (o->half_state != 0 && o->half_state != 1) return LCSM_EINVAL;
+  r->half_state = o->half_state;
   if (o->direct_max_u) {
     if (!is_pow2(o->direct_max_u)) return LCSM_EINVAL;
     r->direct_max_u = o->direct_max_u;
@@ -78,6 +82,23 @@ int tile_kind(const Options& o, const Shape& s, int U) {
   return (2 * U <= o.lds_fft_max_n) ? LCSM_TILE_FFT : LCSM_TILE_FFT_HBM;
 }
 
+// Shape with its state rows per layer: L, or with half-state storage (App. C)
+// T = the largest power of two below L, the side of the largest tile (i = T).
+// Half-state needs that tile to be an FFT tile: only those can store their
+// outputs over their own inputs (-1 otherwise).
+int make_shape(int M, int B, int D, int L, const Options& o, Shape* out) {
+  Shape s{M, B, D, L, B * D, L};
+  if (o.half_state) {
+    if (L < 2) return LCSM_EINVAL;
+    int T = 1;
+    while (2 * T < L) T *= 2;
+    s.SL = T;
+    if (tile_kind(o, s, T) == LCSM_TILE_DIRECT) return LCSM_EINVAL;
+  }
+  *out = s;
+  return LCSM_OK;
+}
+
 // Offsets of the workspace sections, in bytes.
 struct Layout {
   size_t S, Hf, prev, tw, scratch, scratch_bytes, total;
@@ -89,7 +110,7 @@ Layout layout_for(const Shape& s, const Options& o) {
   Layout ly{};
   size_t off = 0;
   ly.S = off;
-  off = align_up(off + sizeof(float) * (size_t)s.M * s.L * s.BD);
+  off = align_up(off + sizeof(float) * (size_t)s.M * s.SL * s.BD);
   ly.Hf = off;
   off = align_up(off + sizeof(float) * (size_t)s.M * s.L * s.D);
   ly.prev = off;
@@ -152,6 +173,7 @@ struct lcsm_ctx {
   float* prev;
   float2* tw;
   float2* scratch;
+  int T;            // half-state swap position (the state's rows per layer), 0 without
   int t;            // next position to emit
   int layers_done;  // lcsm_step_layer progress at position t
   bool faulted;
@@ -170,16 +192,28 @@ int fail(lcsm_ctx* c, int code, const char* what, hipError_t e) {
   return code;
 }
 
+// State pointer of the phase that position p belongs to: the array itself
+// before the half-state swap, the array moved back by T rows from position T
+// on (position p at row p - T; every row touched then is >= T).  Integer
+// arithmetic: the moved pointer lies outside the allocation.
+float* state_base(const lcsm_ctx* c, int p) {
+  if (!c->T || p < c->T) return c->S;
+  return (float*)((uintptr_t)c->S - sizeof(float) * (size_t)c->T * c->s.BD);
+}
+
 // Gray tile of i = t+1 for all layers, when it was not fused into the red
-// launch.
+// launch.  With half-state storage the tile of i = T (an FFT tile) stores
+// its outputs for positions [T, L) over its inputs, rows [0, L - T).
 hipError_t launch_tile(lcsm_ctx* c, int i, int U, int dst_len) {
   const int kind = tile_kind(c->opt, c->s, U);
+  const bool swap = c->T && i == c->T;
   if (kind == LCSM_TILE_DIRECT)
-    return lcsm::launch_direct_tile(c->S, c->Hf, c->s, i, U, dst_len, c->stream);
+    return lcsm::launch_direct_tile(state_base(c, i), c->Hf, c->s, i, U, dst_len, c->stream);
   const int q = __builtin_ctz((unsigned)U);
   const float2* H = (const float2*)(c->ws + c->ly.H[q]);
-  return lcsm::launch_fft_tile(c->S, H, c->tw, c->s, i, U, dst_len, c->opt.lds_fft_max_n,
-                               c->scratch, c->ly.scratch_bytes, c->stream);
+  return lcsm::launch_fft_tile(swap ? c->S : state_base(c, i), H, c->tw, c->s, i, U, dst_len,
+                               c->opt.lds_fft_max_n, c->scratch, c->ly.scratch_bytes, c->stream,
+                               swap);
 }
 
 // Filter spectra of every FFT tile size (the cached kernel DFTs).
@@ -209,26 +243,29 @@ int step_common(lcsm_ctx* c, const float* in, float* z, bool chain) {
   const int U = (i < c->s.L) ? lowbit(i) : 0;
   const int dst_len = U ? (U < c->s.L - i ? U : c->s.L - i) : 0;
   const int kind = tile_kind(c->opt, c->s, U);
+  // the half-state swap tile runs on its own, after the red cells
+  const bool swap = c->T && i == c->T;
   // The chained step fuses its tiles only for a single layer: with several,
   // the red cells run one thread per column through all layers, and the
   // tiles go to the ordinary all-layer tile launch (parallel over layers).
-  const bool fuse = kind == LCSM_TILE_DIRECT &&
+  const bool fuse = kind == LCSM_TILE_DIRECT && !swap &&
                     (chain ? (U <= lcsm::kChainFusedMaxU && c->s.M <= lcsm::kChainFusedMaxM)
                            : U <= lcsm::kFusedMaxU);
+  float* S = state_base(c, t);
   hipError_t e;
-  if (!chain && kind == LCSM_TILE_FFT && dst_len > 0 && 2 * U <= lcsm::kMaxRedFftN) {
+  if (!chain && !swap && kind == LCSM_TILE_FFT && dst_len > 0 && 2 * U <= lcsm::kMaxRedFftN) {
     // red cells fused into the single-pass FFT tile: one launch
     const float2* H = (const float2*)(c->ws + c->ly.H[__builtin_ctz((unsigned)U)]);
-    e = lcsm::launch_red_fft_tile(in, z, c->S, c->Hf, H, c->tw, c->s, i, U, dst_len, c->stream);
+    e = lcsm::launch_red_fft_tile(in, z, S, c->Hf, H, c->tw, c->s, i, U, dst_len, c->stream);
     if (e != hipSuccess) return fail(c, LCSM_EDEVICE, "red-cell + FFT tile launch", e);
     c->t = t + 1;
     return LCSM_OK;
   }
   if (chain)
-    e = lcsm::launch_chain_fused(in, z, c->S, c->Hf, c->prev, c->s, t, fuse ? U : 0, dst_len,
+    e = lcsm::launch_chain_fused(in, z, S, c->Hf, c->prev, c->s, t, fuse ? U : 0, dst_len,
                                  c->stream);
   else
-    e = lcsm::launch_step_fused(in, z, c->S, c->Hf, c->s, t, fuse ? U : 0, dst_len, c->stream);
+    e = lcsm::launch_step_fused(in, z, S, c->Hf, c->s, t, fuse ? U : 0, dst_len, c->stream);
   if (e != hipSuccess) return fail(c, LCSM_EDEVICE, "red-cell launch", e);
   if (!fuse && kind != LCSM_TILE_NONE) {
     e = launch_tile(c, i, U, dst_len);
@@ -248,7 +285,8 @@ int lcsm_workspace_bytes(int M, int B, int D, int L, const lcsm_options* opt, si
   if (r) return r;
   Options o;
   if ((r = resolve_options(opt, &o))) return r;
-  const Shape s{M, B, D, L, B * D};
+  Shape s;
+  if ((r = make_shape(M, B, D, L, o, &s))) return r;
   *bytes = layout_for(s, o).total;
   return LCSM_OK;
 }
@@ -262,7 +300,8 @@ int lcsm_init(lcsm_ctx** out, const float* filters, int M, int B, int D, int L, 
   if (r) return r;
   Options o;
   if ((r = resolve_options(opt, &o))) return r;
-  const Shape s{M, B, D, L, B * D};
+  Shape s;
+  if ((r = make_shape(M, B, D, L, o, &s))) return r;
   const Layout ly = layout_for(s, o);
   if (workspace) {
     if (workspace_bytes < ly.total) return LCSM_ENOMEM;
@@ -299,8 +338,9 @@ int lcsm_init(lcsm_ctx** out, const float* filters, int M, int B, int D, int L, 
   c->prev = (float*)(c->ws + ly.prev);
   c->tw = ly.nmax ? (float2*)(c->ws + ly.tw) : nullptr;
   c->scratch = ly.scratch_bytes ? (float2*)(c->ws + ly.scratch) : nullptr;
+  c->T = o.half_state ? s.SL : 0;
   hipError_t e = lcsm::launch_transpose_filters(filters, c->Hf, s, c->stream);
-  if (e == hipSuccess) e = lcsm::launch_zero(c->S, (size_t)s.M * s.L * s.BD, c->stream);
+  if (e == hipSuccess) e = lcsm::launch_zero(c->S, (size_t)s.M * s.SL * s.BD, c->stream);
   if (e == hipSuccess) e = lcsm::launch_zero(c->prev, (size_t)s.BD, c->stream);
   if (e == hipSuccess) e = init_spectra(c);
   if (e != hipSuccess) {
@@ -330,7 +370,8 @@ int lcsm_step_layer(lcsm_ctx* c, int layer, const float* y, float* z) {
   if (c->t >= c->s.L) return LCSM_EDONE;
   if (layer != c->layers_done)
     return fail(c, LCSM_ESTATE, "layers must be stepped in order 0..M-1", hipSuccess);
-  hipError_t e = lcsm::launch_red_layer(y, z, c->S, c->Hf, c->s, layer, c->t, c->stream);
+  hipError_t e =
+      lcsm::launch_red_layer(y, z, state_base(c, c->t), c->Hf, c->s, layer, c->t, c->stream);
   if (e != hipSuccess) return fail(c, LCSM_EDEVICE, "red-cell launch", e);
   c->layers_done = layer + 1;
   return LCSM_OK;
@@ -372,6 +413,9 @@ int lcsm_prefill(lcsm_ctx* c, int P, const float* y, size_t y_stride, float* z, 
     return fail(c, LCSM_ESTATE, "prefill only at position 0 (after init or reset)", hipSuccess);
   if (!is_pow2(P) || 2 * P > c->s.L)
     return fail(c, LCSM_EINVAL, "prompt length must be a power of two with 2P <= L", hipSuccess);
+  // with half-state storage the prompt's outputs need state rows [P, 2P)
+  if (2 * P > c->s.SL)
+    return fail(c, LCSM_EINVAL, "half-state storage: the prompt needs 2P <= T", hipSuccess);
   const Shape& s = c->s;
   // a prompt of a direct tile size: P ordinary steps
   if (tile_kind(c->opt, s, P) == LCSM_TILE_DIRECT) return lcsm_run(c, P, y, y_stride, z, z_stride);
@@ -400,7 +444,7 @@ int lcsm_prefill(lcsm_ctx* c, int P, const float* y, size_t y_stride, float* z, 
 
 int lcsm_reset(lcsm_ctx* c) {
   if (!c) return LCSM_EINVAL;
-  hipError_t e = lcsm::launch_zero(c->S, (size_t)c->s.M * c->s.L * c->s.BD, c->stream);
+  hipError_t e = lcsm::launch_zero(c->S, (size_t)c->s.M * c->s.SL * c->s.BD, c->stream);
   if (e == hipSuccess) e = lcsm::launch_zero(c->prev, (size_t)c->s.BD, c->stream);
   if (e != hipSuccess) return fail(c, LCSM_EDEVICE, "reset", e);
   c->t = 0;
@@ -434,7 +478,9 @@ int lcsm_plan_tile(int M, int B, int D, int L, const lcsm_options* opt, int t, i
   *i = ii;
   *U = u;
   *dst_len = u < L - ii ? u : L - ii;
-  *kind = tile_kind(o, Shape{M, B, D, L, B * D}, u);
+  Shape s;
+  if ((r = make_shape(M, B, D, L, o, &s))) return r;
+  *kind = tile_kind(o, s, u);
   return LCSM_OK;
 }
 

@@ -44,7 +44,7 @@ __global__ __launch_bounds__(kThreads) void k_step_fused(const float* __restrict
                                                         float* __restrict__ z,
                                                         float* __restrict__ S,
                                                         const float* __restrict__ Hf, int m0, int L,
-                                                        int BD, int D, int t, int dst_len) {
+                                                        int SL, int BD, int D, int t, int dst_len) {
   constexpr int SP = U > 0 ? Split<U>::value : 1;
   constexpr int UJ = U > 0 ? U / SP : 1;  // outputs per thread
   const int d = (int)blockIdx.x * kThreads + (int)threadIdx.x;
@@ -54,7 +54,7 @@ __global__ __launch_bounds__(kThreads) void k_step_fused(const float* __restrict
   const int j0 = part * UJ;
   const int c = (int)blockIdx.y * D + d;
   const size_t e = (size_t)m * BD + c;
-  float* col = S + (size_t)m * L * BD + c;
+  float* col = S + (size_t)m * SL * BD + c;
   const float* hc = Hf + (size_t)m * L * D + d;
   const size_t rs = (size_t)BD;
 
@@ -149,7 +149,8 @@ __global__ __launch_bounds__(kThreads) void k_chain_fused(const float* __restric
                                                          float* __restrict__ S,
                                                          const float* __restrict__ Hf,
                                                          float* __restrict__ prev, int M, int L,
-                                                         int BD, int D, int t, int dst_len) {
+                                                         int SL, int BD, int D, int t,
+                                                         int dst_len) {
   constexpr int NY = U > 0 ? U : 1;
   constexpr int NH = U > 0 ? 2 * U : 1;
   constexpr int NZ = U > 0 ? U : 1;
@@ -167,7 +168,7 @@ __global__ __launch_bounds__(kThreads) void k_chain_fused(const float* __restric
 #pragma unroll
     for (int kk = 0; kk < K; ++kk) {
       const int m = m0 + kk < M ? m0 + kk : M - 1;
-      const float* col = S + (size_t)m * L * BD + c;
+      const float* col = S + (size_t)m * SL * BD + c;
       const float* hc = Hf + (size_t)m * L * D + d;
       xv[kk] = x[(size_t)m * BD + c];
       acc[kk] = col[(size_t)t * rs];
@@ -193,7 +194,7 @@ __global__ __launch_bounds__(kThreads) void k_chain_fused(const float* __restric
     for (int kk = 0; kk < K; ++kk) {
       const int m = m0 + kk;
       if (m < M) {
-        float* col = S + (size_t)m * L * BD + c;
+        float* col = S + (size_t)m * SL * BD + c;
         const float yv = (m == 0 && t == 0) ? xv[kk] : fmaf(0.5f, tanhf(zl), xv[kk]);
         const float zv = fmaf(h0[kk], yv, acc[kk]);
         z[(size_t)m * BD + c] = zv;
@@ -240,7 +241,7 @@ __global__ __launch_bounds__(kThreads) void k_red_layer(const float* __restrict_
 template <int J>
 __global__ __launch_bounds__(kThreads) void k_direct_tile(float* __restrict__ S,
                                                          const float* __restrict__ Hf, int L,
-                                                         int BD, int D, int i, int U,
+                                                         int SL, int BD, int D, int i, int U,
                                                          int dst_len) {
   const int c = blockIdx.x * kThreads + threadIdx.x;
   const int j0 = blockIdx.y * J;
@@ -248,7 +249,7 @@ __global__ __launch_bounds__(kThreads) void k_direct_tile(float* __restrict__ S,
   if (c >= BD || j0 >= dst_len) return;
   const int d = c % D;
   const size_t rs = (size_t)BD;
-  float* col = S + (size_t)m * L * BD + c;
+  float* col = S + (size_t)m * SL * BD + c;
   const float* hc = Hf + (size_t)m * L * D + d;
 
   float acc[J];
@@ -298,20 +299,20 @@ __global__ __launch_bounds__(kThreads) void k_transpose(const float* __restrict_
 // Prompt rows in: S[m][t][c] = y[t * ys + m * BD + c] for t < P (grid-stride
 // over P * M * BD, consecutive threads on consecutive c).
 __global__ __launch_bounds__(kThreads) void k_rows_in(const float* __restrict__ y, size_t ys,
-                                                     float* __restrict__ S, int M, int L, int BD,
+                                                     float* __restrict__ S, int M, int SL, int BD,
                                                      int P) {
   const size_t n = (size_t)P * M * BD, stride = (size_t)gridDim.x * kThreads;
   for (size_t e = (size_t)blockIdx.x * kThreads + threadIdx.x; e < n; e += stride) {
     const size_t tm = e / BD;
     const int c = (int)(e - tm * BD);
     const int m = (int)(tm % M), t = (int)(tm / M);
-    S[((size_t)m * L + t) * BD + c] = y[t * ys + (size_t)m * BD + c];
+    S[((size_t)m * SL + t) * BD + c] = y[t * ys + (size_t)m * BD + c];
   }
 }
 
 // State rows out: z[t * zs + m * BD + c] = S[m][row0 + t][c], then the state
 // entry is cleared, for t < P.
-__global__ __launch_bounds__(kThreads) void k_rows_out_clear(float* __restrict__ S, int M, int L,
+__global__ __launch_bounds__(kThreads) void k_rows_out_clear(float* __restrict__ S, int M, int SL,
                                                             int BD, int row0, int P,
                                                             float* __restrict__ z, size_t zs) {
   const size_t n = (size_t)P * M * BD, stride = (size_t)gridDim.x * kThreads;
@@ -319,7 +320,7 @@ __global__ __launch_bounds__(kThreads) void k_rows_out_clear(float* __restrict__
     const size_t tm = e / BD;
     const int c = (int)(e - tm * BD);
     const int m = (int)(tm % M), t = (int)(tm / M);
-    float* p = S + ((size_t)m * L + row0 + t) * BD + c;
+    float* p = S + ((size_t)m * SL + row0 + t) * BD + c;
     z[t * zs + (size_t)m * BD + c] = *p;
     *p = 0.f;
   }
@@ -346,7 +347,7 @@ hipError_t dispatch_fused(int U, const float* y, float* z, float* S, const float
       const int mc = s.M - m0 < MC ? s.M - m0 : MC;                                              \
       hipLaunchKernelGGL((k_step_fused<UU, RED>),                                                \
                          dim3(blocks_for(s.D), (unsigned)s.B, (unsigned)(mc * SP)), block, 0,    \
-                         st, y, z, S, Hf, m0, s.L, s.BD, s.D, t, dst_len);                      \
+                         st, y, z, S, Hf, m0, s.L, s.SL, s.BD, s.D, t, dst_len);                \
     }                                                                                            \
     break;                                                                                       \
   }
@@ -384,7 +385,7 @@ hipError_t launch_chain_fused(const float* x, float* z, float* S, const float* H
   const dim3 grid(blocks_for(s.D), (unsigned)s.B), block(kThreads);
 #define LCSM_CHAIN_K(UU, KK)                                                                      \
   hipLaunchKernelGGL((k_chain_fused<UU, KK>), grid, block, 0, st, x, z, S, Hf, prev, s.M, s.L,   \
-                     s.BD, s.D, t, dst_len)
+                     s.SL, s.BD, s.D, t, dst_len)
 #define LCSM_CHAIN_CASE(UU)                                                                       \
   case UU: {                                                                                      \
     constexpr int KM = ChainChunk<UU>::value;                                                     \
@@ -417,7 +418,7 @@ hipError_t launch_chain_fused(const float* x, float* z, float* S, const float* H
 
 hipError_t launch_red_layer(const float* y, float* z, float* S, const float* Hf, const Shape& s,
                             int layer, int t, hipStream_t st) {
-  float* Sm = S + (size_t)layer * s.L * s.BD;
+  float* Sm = S + (size_t)layer * s.SL * s.BD;
   const float* Hm = Hf + (size_t)layer * s.L * s.D;
   hipLaunchKernelGGL(k_red_layer, dim3(blocks_for(s.BD)), dim3(kThreads), 0, st, y, z, Sm, Hm,
                      s.BD, s.D, t);
@@ -432,8 +433,8 @@ hipError_t launch_direct_tile(float* S, const float* Hf, const Shape& s, int i, 
     return dispatch_fused<false>(U, nullptr, nullptr, S, Hf, s, i - 1, dst_len, st);
   }
   const dim3 grid(blocks_for(s.BD), (dst_len + kDirectJ - 1) / kDirectJ, s.M);
-  hipLaunchKernelGGL(k_direct_tile<kDirectJ>, grid, dim3(kThreads), 0, st, S, Hf, s.L, s.BD, s.D,
-                     i, U, dst_len);
+  hipLaunchKernelGGL(k_direct_tile<kDirectJ>, grid, dim3(kThreads), 0, st, S, Hf, s.L, s.SL, s.BD,
+                     s.D, i, U, dst_len);
   return hipGetLastError();
 }
 
@@ -444,7 +445,7 @@ hipError_t launch_rows_in(const float* y, size_t y_stride, float* S, const Shape
   size_t blocks = (n + kThreads - 1) / kThreads;
   if (blocks > 8192) blocks = 8192;
   hipLaunchKernelGGL(k_rows_in, dim3((unsigned)blocks), dim3(kThreads), 0, st, y, y_stride, S, s.M,
-                     s.L, s.BD, P);
+                     s.SL, s.BD, P);
   return hipGetLastError();
 }
 
@@ -454,7 +455,7 @@ hipError_t launch_rows_out_clear(float* S, const Shape& s, int row0, int P, floa
   if (n == 0) return hipSuccess;
   size_t blocks = (n + kThreads - 1) / kThreads;
   if (blocks > 8192) blocks = 8192;
-  hipLaunchKernelGGL(k_rows_out_clear, dim3((unsigned)blocks), dim3(kThreads), 0, st, S, s.M, s.L,
+  hipLaunchKernelGGL(k_rows_out_clear, dim3((unsigned)blocks), dim3(kThreads), 0, st, S, s.M, s.SL,
                      s.BD, row0, P, z, z_stride);
   return hipGetLastError();
 }

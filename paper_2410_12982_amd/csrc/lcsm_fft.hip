@@ -153,15 +153,20 @@ __device__ __forceinline__ int panel_of(int r, int B, int hgroup) {
 // needs a bounds check, the channel of a panel column is d0 + 2 col with d0
 // computed once, and the two filter spectra of a column pair are adjacent
 // (one 16-byte load).
-template <int N, bool RED, bool FAST>
+// STORE (not with RED): the outputs are stored over the input rows [i-U,
+// i-U+dst_len) instead of added into rows [i, i+dst_len).  The workgroup has
+// read all inputs of its columns (the first pass, before the barriers of the
+// LDS passes) before it stores, and no other workgroup touches its columns.
+template <int N, bool RED, bool FAST, bool STORE = false>
 __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_tile(float* __restrict__ S,
                                                          const float2* __restrict__ H,
                                                          const float2* __restrict__ tw,
                                                          const float* __restrict__ Hf,
                                                          const float* __restrict__ yt,
-                                                         float* __restrict__ zt, int L, int BD,
-                                                         int D, int B, int i, int dst_len, int ppl,
-                                                         int hgroup) {
+                                                         float* __restrict__ zt, int L, int SL,
+                                                         int BD, int D, int B, int i, int dst_len,
+                                                         int ppl, int hgroup) {
+  static_assert(!(RED && STORE), "the in-place store has no red cell");
   constexpr int WC = Cfg<N>::WC, NT = Cfg<N>::NT, U = N / 2;
   using P = fft::Plan<N>;
   __shared__ float2 buf[N * WC];
@@ -172,7 +177,7 @@ __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_tile(float* __restrict__ S,
   const int c0 = panel_of<WC>(q - m * ppl, B, hgroup) * 2 * WC;
   const int d0 = FAST ? c0 % D : 0;
   const bool vec = FAST || (BD & 1) == 0;
-  float* Sm = S + (size_t)m * L * BD;
+  float* Sm = S + (size_t)m * SL * BD;
   const float* ysrc = Sm + (size_t)(i - U) * BD;
   const float* ym = RED ? yt + (size_t)m * BD : nullptr;
   const int dlen = FAST ? U : dst_len;
@@ -258,8 +263,8 @@ __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_tile(float* __restrict__ S,
   constexpr int PL = N / RL;
   constexpr int LUN = PL * WC;
   constexpr int LU = (LUN + NT - 1) / NT;
-  float* zdst = Sm + (size_t)i * BD;
-  constexpr bool PREZ = N <= 4096;  // registers allow the prefetch
+  float* zdst = Sm + (size_t)(STORE ? i - U : i) * BD;
+  constexpr bool PREZ = N <= 4096 && !STORE;  // registers allow the prefetch
   auto load_z = [&](int oi, int c) -> float2 {
     if constexpr (FAST) return *reinterpret_cast<const float2*>(zdst + (size_t)oi * BD + c);
     return load_pair(zdst + (size_t)oi * BD, c, BD, vec);
@@ -299,8 +304,11 @@ __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_tile(float* __restrict__ S,
       for (int s = 0; s < RL / 2; ++s) {
         const int oi = j + s * PL;
         if (FAST || (oi < dlen && c < BD)) {
-          const float2 zz = PREZ ? zo[PREZ ? a : 0][s] : load_z(oi, c);
-          const float2 o = make_float2(zz.x + v[RL / 2 + s].x, zz.y + v[RL / 2 + s].y);
+          float2 o = v[RL / 2 + s];
+          if constexpr (!STORE) {
+            const float2 zz = PREZ ? zo[PREZ ? a : 0][s] : load_z(oi, c);
+            o = make_float2(zz.x + o.x, zz.y + o.y);
+          }
           float* row = zdst + (size_t)oi * BD;
           if (vec) {
             *reinterpret_cast<float2*>(row + c) = o;
@@ -558,10 +566,11 @@ __global__ __launch_bounds__(kMidNT) void k_fft_mid_tile(float2* __restrict__ C,
 
 // Pass R': inverse N2-point FFT of E[n1][.] for each n1; output n2 >= N2/2 is
 // time index n = n1 + N1 n2 >= U and is added into state row i + n - U when
-// n - U < dst_len.
-template <int N2>
+// n - U < dst_len.  STORE: stored into row i - U + n - U instead (over the
+// inputs, which the chunk's first pass has read).
+template <int N2, bool STORE>
 __global__ __launch_bounds__(Cfg<N2>::NT) void k_fft_rows_inv(const float2* __restrict__ E,
-                                                              float* __restrict__ S, int L, int i,
+                                                              float* __restrict__ S, int SL, int i,
                                                               int dst_len, Chunk ch,
                                                               const float2* __restrict__ tw) {
   constexpr int WC = Cfg<N2>::WC, NT = Cfg<N2>::NT;
@@ -586,7 +595,7 @@ __global__ __launch_bounds__(Cfg<N2>::NT) void k_fft_rows_inv(const float2* __re
   constexpr int PL = N2 / RL;
   constexpr int LUN = PL * WC;
   constexpr int LU = (LUN + NT - 1) / NT;
-  float* rowp[LU];  // row i of the column's layer, nullptr for no column
+  float* rowp[LU];  // row of output 0 in the column's layer, nullptr for no column
   int cpos[LU];     // real column index of the pair
   float2 zo[LU][RL / 2];
 #pragma unroll
@@ -599,14 +608,15 @@ __global__ __launch_bounds__(Cfg<N2>::NT) void k_fft_rows_inv(const float2* __re
     if (u < LUN && x < ch.nvalid) {
       const int g = ch.g0 + x;
       const int m = g / ch.ncc;
-      rowp[a] = S + ((size_t)m * L + i) * BD;
+      rowp[a] = S + ((size_t)m * SL + (STORE ? i - U : i)) * BD;
       cpos[a] = 2 * (g - m * ch.ncc);
     }
 #pragma unroll
     for (int s = 0; s < RL / 2; ++s) {
       const int oi = n1 + N1 * (j + s * PL);
-      zo[a][s] = (rowp[a] && oi < dst_len) ? load_pair(rowp[a] + (size_t)oi * BD, cpos[a], BD, vec)
-                                           : make_float2(0.f, 0.f);
+      zo[a][s] = (!STORE && rowp[a] && oi < dst_len)
+                     ? load_pair(rowp[a] + (size_t)oi * BD, cpos[a], BD, vec)
+                     : make_float2(0.f, 0.f);
     }
   }
   __syncthreads();
@@ -631,7 +641,9 @@ __global__ __launch_bounds__(Cfg<N2>::NT) void k_fft_rows_inv(const float2* __re
         const int oi = n1 + N1 * (j + s * PL);
         if (oi < dst_len) {
           float* row = rowp[a] + (size_t)oi * BD;
-          const float2 o = make_float2(zo[a][s].x + v[RL / 2 + s].x, zo[a][s].y + v[RL / 2 + s].y);
+          const float2 o = STORE ? v[RL / 2 + s]
+                                 : make_float2(zo[a][s].x + v[RL / 2 + s].x,
+                                               zo[a][s].y + v[RL / 2 + s].y);
           if (vec) {
             *reinterpret_cast<float2*>(row + c) = o;
           } else {
@@ -651,36 +663,41 @@ __global__ __launch_bounds__(Cfg<N2>::NT) void k_fft_rows_inv(const float2* __re
 
 hipError_t tile_single(int N, float* S, const float2* H, const float2* tw, const float* Hf,
                        const float* yt, float* zt, const Shape& s, int i, int dst_len,
-                       hipStream_t st) {
-#define LCSM_CASE(NN)                                                                              \
-  case NN: {                                                                                       \
-    constexpr int WC = Cfg<NN>::WC;                                                                \
-    const int ppl = (s.BD + 2 * WC - 1) / (2 * WC);                                                \
-    const int hgroup = (s.D % (2 * WC) == 0) ? s.D / (2 * WC) : 0;                                 \
-    const dim3 grid((unsigned)(ppl * s.M)), block(Cfg<NN>::NT);                                    \
-    const bool fast = hgroup > 0 && dst_len == NN / 2;                                             \
-    if (yt) {                                                                                      \
-      if constexpr (NN <= kMaxRedFftN) {                                                           \
-        if (fast)                                                                                  \
-          hipLaunchKernelGGL((k_fft_tile<NN, true, true>), grid, block, 0, st, S, H, tw, Hf, yt,   \
-                             zt, s.L, s.BD, s.D, s.B, i, dst_len, ppl, hgroup);                    \
-        else                                                                                       \
-          hipLaunchKernelGGL((k_fft_tile<NN, true, false>), grid, block, 0, st, S, H, tw, Hf, yt,  \
-                             zt, s.L, s.BD, s.D, s.B, i, dst_len, ppl, hgroup);                    \
-      } else {                                                                                     \
-        return hipErrorInvalidValue;                                                               \
-      }                                                                                            \
-    } else if (fast) {                                                                             \
-      hipLaunchKernelGGL((k_fft_tile<NN, false, true>), grid, block, 0, st, S, H, tw, Hf, yt, zt,  \
-                         s.L, s.BD, s.D, s.B, i, dst_len, ppl, hgroup);                            \
-    } else {                                                                                       \
-      hipLaunchKernelGGL((k_fft_tile<NN, false, false>), grid, block, 0, st, S, H, tw, Hf, yt, zt, \
-                         s.L, s.BD, s.D, s.B, i, dst_len, ppl, hgroup);                            \
-    }                                                                                              \
-    return hipGetLastError();                                                                      \
+                       bool in_place, hipStream_t st) {
+#define LCSM_TILE_ARGS S, H, tw, Hf, yt, zt, s.L, s.SL, s.BD, s.D, s.B, i, dst_len, ppl, hgroup
+#define LCSM_CASE(NN)                                                                             \
+  case NN: {                                                                                      \
+    constexpr int WC = Cfg<NN>::WC;                                                               \
+    const int ppl = (s.BD + 2 * WC - 1) / (2 * WC);                                               \
+    const int hgroup = (s.D % (2 * WC) == 0) ? s.D / (2 * WC) : 0;                                \
+    const dim3 grid((unsigned)(ppl * s.M)), block(Cfg<NN>::NT);                                   \
+    const bool fast = hgroup > 0 && dst_len == NN / 2;                                            \
+    if (yt) {                                                                                     \
+      if constexpr (NN <= kMaxRedFftN) {                                                          \
+        if (fast)                                                                                 \
+          hipLaunchKernelGGL((k_fft_tile<NN, true, true>), grid, block, 0, st, LCSM_TILE_ARGS);   \
+        else                                                                                      \
+          hipLaunchKernelGGL((k_fft_tile<NN, true, false>), grid, block, 0, st, LCSM_TILE_ARGS);  \
+      } else {                                                                                    \
+        return hipErrorInvalidValue;                                                              \
+      }                                                                                           \
+    } else if (in_place) {                                                                        \
+      if (fast)                                                                                   \
+        hipLaunchKernelGGL((k_fft_tile<NN, false, true, true>), grid, block, 0, st,               \
+                           LCSM_TILE_ARGS);                                                       \
+      else                                                                                        \
+        hipLaunchKernelGGL((k_fft_tile<NN, false, false, true>), grid, block, 0, st,              \
+                           LCSM_TILE_ARGS);                                                       \
+    } else if (fast) {                                                                            \
+      hipLaunchKernelGGL((k_fft_tile<NN, false, true>), grid, block, 0, st, LCSM_TILE_ARGS);      \
+    } else {                                                                                      \
+      hipLaunchKernelGGL((k_fft_tile<NN, false, false>), grid, block, 0, st, LCSM_TILE_ARGS);     \
+    }                                                                                             \
+    return hipGetLastError();                                                                     \
   }
   switch (N) { LCSM_POW2_CASES(LCSM_CASE) }
 #undef LCSM_CASE
+#undef LCSM_TILE_ARGS
   return hipErrorInvalidValue;
 }
 
@@ -716,14 +733,15 @@ hipError_t rows_fwd(const float* src, size_t lstride, int row0, int rows_valid, 
   return hipErrorInvalidValue;
 }
 
-hipError_t rows_inv(const float2* E, float* S, int L, int i, int dst_len, const Chunk& ch,
+template <bool STORE>
+hipError_t rows_inv(const float2* E, float* S, int SL, int i, int dst_len, const Chunk& ch,
                     const float2* tw, hipStream_t st) {
-#define LCSM_CASE(NN)                                                                         \
-  case NN: {                                                                                  \
-    const int npan = (ch.nvalid + Cfg<NN>::WC - 1) / Cfg<NN>::WC;                             \
-    hipLaunchKernelGGL(k_fft_rows_inv<NN>, dim3((unsigned)(npan * ch.N1)), dim3(Cfg<NN>::NT), \
-                       0, st, E, S, L, i, dst_len, ch, tw);                                   \
-    return hipGetLastError();                                                                 \
+#define LCSM_CASE(NN)                                                                           \
+  case NN: {                                                                                    \
+    const int npan = (ch.nvalid + Cfg<NN>::WC - 1) / Cfg<NN>::WC;                               \
+    hipLaunchKernelGGL((k_fft_rows_inv<NN, STORE>), dim3((unsigned)(npan * ch.N1)),             \
+                       dim3(Cfg<NN>::NT), 0, st, E, S, SL, i, dst_len, ch, tw);                 \
+    return hipGetLastError();                                                                   \
   }
   switch (ch.N2) { LCSM_ROW_CASES(LCSM_CASE) }
 #undef LCSM_CASE
@@ -807,10 +825,11 @@ hipError_t launch_spectra(const float* Hf, float2* Hout, const float2* tw, const
 
 hipError_t launch_fft_tile(float* S, const float2* H, const float2* tw, const Shape& s, int i,
                            int U, int dst_len, int lds_max_n, float2* scratch, size_t scratch_bytes,
-                           hipStream_t st) {
+                           hipStream_t st, bool in_place) {
   if (dst_len <= 0) return hipSuccess;
   const int N = 2 * U;
-  if (N <= lds_max_n) return tile_single(N, S, H, tw, nullptr, nullptr, nullptr, s, i, dst_len, st);
+  if (N <= lds_max_n)
+    return tile_single(N, S, H, tw, nullptr, nullptr, nullptr, s, i, dst_len, in_place, st);
   Chunk ch{};
   ch.ncols = s.BD;
   ch.ncc = (s.BD + 1) / 2;
@@ -823,9 +842,12 @@ hipError_t launch_fft_tile(float* S, const float2* H, const float2* tw, const Sh
   for (int g0 = 0; g0 < total; g0 += ch.cstride) {
     ch.g0 = g0;
     ch.nvalid = total - g0 < ch.cstride ? total - g0 : ch.cstride;
-    hipError_t e = rows_fwd<true>(S, (size_t)s.L * s.BD, i - U, i, ch, C, tw, st);
+    // the chunk's columns: all inputs into C, then (stream order) the outputs
+    hipError_t e = rows_fwd<true>(S, (size_t)s.SL * s.BD, i - U, i, ch, C, tw, st);
     if (e == hipSuccess) e = mid_tile(C, H, s.D, ch, tw, st);
-    if (e == hipSuccess) e = rows_inv(C, S, s.L, i, dst_len, ch, tw, st);
+    if (e == hipSuccess)
+      e = in_place ? rows_inv<true>(C, S, s.SL, i, dst_len, ch, tw, st)
+                   : rows_inv<false>(C, S, s.SL, i, dst_len, ch, tw, st);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
@@ -834,7 +856,7 @@ hipError_t launch_fft_tile(float* S, const float2* H, const float2* tw, const Sh
 hipError_t launch_red_fft_tile(const float* yt, float* zt, float* S, const float* Hf,
                                const float2* H, const float2* tw, const Shape& s, int i, int U,
                                int dst_len, hipStream_t st) {
-  return tile_single(2 * U, S, H, tw, Hf, yt, zt, s, i, dst_len, st);
+  return tile_single(2 * U, S, H, tw, Hf, yt, zt, s, i, dst_len, false, st);
 }
 
 }  // namespace lcsm

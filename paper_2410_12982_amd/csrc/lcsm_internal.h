@@ -9,9 +9,15 @@ namespace lcsm {
 
 // Shape of one context.  State rows are indexed [m][t][b*D + d] (time-major:
 // one position of one layer is a contiguous B*D slab), filters [m][k][d].
+// A layer's state holds SL rows: L, or with half-state storage the largest
+// power of two T below L.  The kernels take the state pointer of the
+// current phase: the array itself while positions are below T, the array
+// moved back by T rows after the swap (position p at row p - T), so they
+// index rows by position in both phases.
 struct Shape {
   int M, B, D, L;
   int BD;  // B * D
+  int SL;  // state rows per layer
 };
 
 // Largest tile side handled by the fused red+direct kernels, and by the
@@ -85,10 +91,14 @@ hipError_t launch_spectra(const float* Hf, float2* Hout, const float2* tw, const
 
 // FFT gray tile of all layers: y rows [i-U, i) -> z rows [i, i+dst_len),
 // with the spectra H of tile size U.  Single LDS pass when 2U <= lds_max_n,
-// else the chunked multi-pass transform through scratch.
+// else the chunked multi-pass transform through scratch.  in_place: the
+// outputs are stored (not added) over the input rows [i-U, i-U+dst_len)
+// instead -- the swap of half-state storage; every workgroup (single pass) or
+// chunk of columns (multi-pass) reads all of its columns' inputs before it
+// stores any of their outputs.
 hipError_t launch_fft_tile(float* S, const float2* H, const float2* tw, const Shape& s, int i,
                            int U, int dst_len, int lds_max_n, float2* scratch,
-                           size_t scratch_bytes, hipStream_t st);
+                           size_t scratch_bytes, hipStream_t st, bool in_place = false);
 
 // Largest FFT length with the red cell fused into the tile kernel.
 constexpr int kMaxRedFftN = 4096;

@@ -53,7 +53,8 @@ if len(hip_runtimes()) > 1:
 class Options(ctypes.Structure):
     """``lcsm_options``: 0 selects the library default."""
     _fields_ = [("direct_max_u", ctypes.c_int), ("lds_fft_max_n", ctypes.c_int),
-                ("scratch_mib", ctypes.c_int), ("reserved", ctypes.c_int * 5)]
+                ("scratch_mib", ctypes.c_int), ("half_state", ctypes.c_int),
+                ("reserved", ctypes.c_int * 4)]
 
 
 _c_int_p = ctypes.POINTER(ctypes.c_int)

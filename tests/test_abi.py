@@ -102,6 +102,44 @@ def test_options_struct_matches_header():
     assert ctypes.sizeof(lcsm.Options) == 32
 
 
+@pytest.mark.parametrize("L,T", [(4096, 2048), (1000, 512), (513, 512), (8192, 4096)])
+def test_half_state_saves_the_rows_past_T(L, T):
+    """Half-state storage (App. C): T = the largest power of two below L
+    state rows per layer instead of L; everything else is unchanged."""
+    M, B, D = 3, 4, 40
+    full = lcsm.workspace_bytes(M, B, D, L)
+    half = lcsm.workspace_bytes(M, B, D, L, {"half_state": 1})
+    saved = 4 * M * (L - T) * B * D
+    assert abs((full - half) - saved) < 256
+    # the schedule does not change
+    for t in (0, T - 2, T - 1, T, L - 2, L - 1):
+        assert lcsm.plan_tile(M, B, D, L, t, {"half_state": 1}) == lcsm.plan_tile(M, B, D, L, t)
+
+
+@pytest.mark.parametrize("L,opts", [(128, {}), (64, {}), (1, {}), (2, {}),
+                                    (4096, {"direct_max_u": 2048}),
+                                    (4096, {"direct_max_u": 1 << 20})])
+def test_half_state_needs_an_fft_swap_tile(L, opts):
+    """The tile of side T overwrites its own inputs, which only the FFT
+    tiles can do: a direct tile of side T is rejected, as is L < 2."""
+    o = dict(opts, half_state=1)
+    with pytest.raises(lcsm.LcsmError) as e:
+        lcsm.workspace_bytes(1, 1, 16, L, o)
+    assert e.value.code == lcsm.LCSM_EINVAL
+    with pytest.raises(lcsm.LcsmError):
+        lcsm.plan_tile(1, 1, 16, max(L, 2), 0, o)
+
+
+def test_half_state_flag_is_0_or_1():
+    for v in (2, -1, 7):
+        with pytest.raises(lcsm.LcsmError) as e:
+            lcsm.workspace_bytes(1, 1, 16, 4096, {"half_state": v})
+        assert e.value.code == lcsm.LCSM_EINVAL
+    # the smallest lengths it takes with the default crossover (T = 128 > 64)
+    lcsm.workspace_bytes(1, 1, 16, 129, {"half_state": 1})
+    lcsm.workspace_bytes(1, 1, 16, 256, {"half_state": 1})
+
+
 def test_workspace_grows_with_fft_levels():
     M, B, D, L = 2, 4, 96, 4096
     direct = lcsm.workspace_bytes(M, B, D, L, {"direct_max_u": 1 << 20})

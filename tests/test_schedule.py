@@ -129,3 +129,28 @@ def test_non_power_of_two_clips_destination():
     tiles = all_tiles(L)
     assert tiles[7] == (8, 8, 0, 8, 8, 12)        # i = 8, U = 8 clipped at L
     assert tile_after_step(L - 1, L) is None
+
+
+@pytest.mark.parametrize("L", [3, 5, 8, 12, 100, 129, 256, 1000, 4500, 8192])
+def test_half_state_premise(L):
+    """App. C's premise, on the schedule: with T the largest power of two
+    below L, no tile before the one of i = T writes at a position >= T, that
+    tile reads exactly y[0, T) and writes z[T, L), and every later tile reads
+    and writes only positions >= T; the red cell of step t touches position t
+    alone.  So T rows per layer suffice when the tile of i = T writes its
+    outputs over its own inputs, and position p >= T is kept at row p - T."""
+    T = 1
+    while 2 * T < L:
+        T *= 2
+    seen_swap = False
+    for (i, U, s0, s1, d0, d1) in all_tiles(L):
+        if i < T:
+            assert d1 <= T
+        elif i == T:
+            assert (U, s0, s1, d0, d1) == (T, 0, T, T, L)
+            assert d1 - d0 <= s1 - s0      # the outputs fit in the inputs' rows
+            seen_swap = True
+        else:
+            assert s0 >= T and d0 >= T and d1 <= L
+            assert d1 - T <= T             # rows p - T stay below T
+    assert seen_swap
