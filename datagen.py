@@ -36,6 +36,16 @@ Tensors and their flat index order:
 * additive chain inputs ``x[t, m, b, d]``: same index, stream 2,
   ``x = fp32(sigma * g)``.
 * small-integer data (bit-exact tests): ``v = (w mod (2r+1)) - r``.
+* weights of the synthetic model's MLP blocks (the [out][in] layout):
+  ``w_up[m, n, k]`` (n < 2D, k < D, index ``(m*2D + n)*D + k``, stream 3),
+  ``b_up[m, n]`` (``m*2D + n``, stream 4), ``w_down[m, n, k]`` (n < D,
+  k < 2D, ``(m*D + n)*2D + k``, stream 5), ``b_down[m, n]`` (``m*D + n``,
+  stream 6).  ``w_up = fp32(g / sqrt(D))``, ``w_down = fp32(g * s / sqrt(2D))``
+  with ``s = 1 / (2 * sqrt(sum_k exp(-2k/decay)))`` (the inverse of twice a
+  filter's expected L2 norm, so that a layer -- mixer then block -- does not
+  amplify and the closed loop stays bounded), biases ``fp32(0.1 g)``.
+* sampler noise ``eps[t, b, d]``: ``n = (t*B + b)*D + d``, stream 7,
+  ``eps = fp32(sigma * g)``.
 """
 from __future__ import annotations
 
@@ -48,6 +58,7 @@ M32 = 0xFFFFFFFF
 
 # stream ids
 FILTERS, YIN, XIN = 0, 1, 2
+W_UP, B_UP, W_DOWN, B_DOWN, NOISE = 3, 4, 5, 6, 7
 
 
 @dataclass(frozen=True)
@@ -226,7 +237,71 @@ def int_y_np(w: Workload, r: int = 3) -> np.ndarray:
     return small_int(n, w.seed, YIN, r).reshape(w.L, w.M, w.B, w.D).astype(np.float32)
 
 
+def mlp_scales(w: Workload):
+    """(scale of w_up, scale of w_down, scale of the biases), fp64."""
+    norm = math.sqrt(float(np.sum(decay_table(w.L, w.decay) ** 2)))
+    return 1.0 / math.sqrt(w.D), 1.0 / (2.0 * norm * math.sqrt(2 * w.D)), 0.1
+
+
+def _mlp_index_shapes(w: Workload):
+    D2 = 2 * w.D
+    return ((W_UP, (w.M, D2, w.D), 0), (B_UP, (w.M, D2), 2), (W_DOWN, (w.M, w.D, D2), 1),
+            (B_DOWN, (w.M, w.D), 2))
+
+
+def mlp_weights_np(w: Workload):
+    """(w_up [M,2D,D], b_up [M,2D], w_down [M,D,2D], b_down [M,D]) fp32 numpy."""
+    sc = mlp_scales(w)
+    out = []
+    for stream, shape, which in _mlp_index_shapes(w):
+        n = np.arange(int(np.prod(shape)), dtype=np.uint64)
+        out.append((sc[which] * normal(n, w.seed, stream)).astype(np.float32).reshape(shape))
+    return tuple(out)
+
+
+def noise_np(w: Workload, t0: int = 0, t1: int | None = None) -> np.ndarray:
+    """Sampler noise eps[t0:t1, b, d] (fp32)."""
+    t1 = w.L if t1 is None else t1
+    slab = w.B * w.D
+    n = (np.arange(t0, t1, dtype=np.uint64)[:, None] * np.uint64(slab)
+         + np.arange(slab, dtype=np.uint64)[None, :])
+    return (w.x_sigma * normal(n, w.seed, NOISE)).astype(np.float32).reshape(t1 - t0, w.B, w.D)
+
+
 # ---------------------------------------------------------------- torch views
+
+def mlp_weights_torch(w: Workload, device):
+    """The weights of :func:`mlp_weights_np` as fp32 torch tensors (bit-identical)."""
+    import torch
+    sc = mlp_scales(w)
+    out = []
+    for stream, shape, which in _mlp_index_shapes(w):
+        total = int(np.prod(shape))
+        t = torch.empty(total, dtype=torch.float32, device=device)
+        step = 1 << 24
+        for a in range(0, total, step):
+            n = torch.arange(a, min(total, a + step), device=device, dtype=torch.int64)
+            t[a:a + len(n)] = (sc[which] * normal(n, w.seed, stream)).to(torch.float32)
+        out.append(t.view(shape))
+    return tuple(out)
+
+
+def noise_torch(w: Workload, device, t0: int = 0, t1: int | None = None):
+    """Sampler noise eps[t0:t1, b, d] as an fp32 torch tensor on ``device``."""
+    import torch
+    t1 = w.L if t1 is None else t1
+    slab = w.B * w.D
+    out = torch.empty((t1 - t0, w.B, w.D), dtype=torch.float32, device=device)
+    flat = out.view(t1 - t0, slab)
+    j = torch.arange(slab, device=device, dtype=torch.int64)
+    step = max(1, (1 << 22) // slab)
+    for a in range(t0, t1, step):
+        b = min(t1, a + step)
+        ts = torch.arange(a, b, device=device, dtype=torch.int64)
+        n = ts[:, None] * slab + j[None, :]
+        flat[a - t0:b - t0] = (w.x_sigma * normal(n, w.seed, NOISE)).to(torch.float32)
+    return out
+
 
 def filters_torch(w: Workload, device, m_chunk: int = 1):
     """Filters h[m, d, k] as an fp32 torch tensor [M, D, L] on ``device``.
