@@ -26,7 +26,10 @@ Printed: one JSON line, with
   prefill       a prompt through lcsm_prefill against the same positions
                 stepped;
   half_state    the timed generations again with half-state storage (T of
-                the L state rows per layer), and the bytes it saves.
+                the L state rows per layer), and the bytes it saves;
+  synthetic_model  generations of the synthetic end-to-end model (per layer
+                the mixer and an MLP block of hidden 2D with GELU, the next
+                token = last layer's output + noise), with the mixer's share.
 """
 from __future__ import annotations
 
@@ -65,6 +68,8 @@ def parse():
     p.add_argument("--no-kernel-pass", action="store_true")
     p.add_argument("--no-prefill", dest="prefill", action="store_false", default=True,
                    help="skip timing the prompt prefill against the same positions stepped online")
+    p.add_argument("--no-synth", dest="synth", action="store_false", default=True,
+                   help="skip the synthetic end-to-end model (MLP blocks + noise sampler)")
     p.add_argument("--no-half-state", dest="half_state", action="store_false", default=True,
                    help="skip the generations with half-state storage")
     p.add_argument("--no-closed-loop", dest="closed_loop", action="store_false", default=True,
@@ -277,6 +282,10 @@ def main():
     if args.half_state:
         half = half_state_timing(w, filters, y, z, opts, ms, lcsm, torch, dev, args)
 
+    synth = None
+    if args.synth:
+        synth = synth_timing(w, filters, opts, ms, lcsm, torch, dev, args)
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(w, args.cpu_budget)
@@ -308,6 +317,8 @@ def main():
         out["prefill"] = prefill
     if half:
         out["half_state"] = half
+    if synth:
+        out["synthetic_model"] = synth
     print(json.dumps(out), flush=True)
 
 
@@ -521,6 +532,58 @@ def half_state_timing(w, filters, y, z, opts, ms_full, lcsm, torch, dev, args):
             "time_vs_full_state": round(ms / ms_full, 4),
             "state_bytes": 4 * w.M * T * w.B * w.D, "state_bytes_full": 4 * w.M * w.L * w.B * w.D,
             "workspace_bytes": half_b, "workspace_bytes_full": full_b}
+
+
+def synth_timing(w, filters, opts, ms_mixer, lcsm, torch, dev, args):
+    """Generations of the synthetic end-to-end model (lcsm_synth_step: per
+    layer the mixer and an MLP block of hidden 2D with GELU; the next token
+    = last layer's output + noise), dispatched like the timed region: warmup
+    untimed, then args.steps timed with events.  ms_mixer: the teacher-forced
+    mixer generation time, for the mixer's share of the model's time."""
+    import datagen
+    R = min(RING, w.L)
+    weights = datagen.mlp_weights_torch(w, dev)
+    eps = datagen.noise_torch(w, dev, 0, R)
+    act = torch.empty((R, w.M, w.B, w.D), dtype=torch.float32, device=dev)
+    graph_ok = args.graph and w.L <= GRAPH_MAX_L
+    stream = torch.cuda.Stream(dev) if graph_ok else torch.cuda.current_stream(dev)
+    model = lcsm.Synth(filters, *weights, w.B, options=opts, stream=stream)
+    torch.cuda.synchronize()
+
+    def generation():
+        model.reset()
+        for t in range(w.L):
+            model.step(eps[t % R], act[t % R])
+
+    if graph_ok:
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=stream):
+            generation()
+        torch.cuda.synchronize()
+        one = graph.replay
+    else:
+        one = generation
+    print("# synthetic-model generations", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        one()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        one()
+    e1.record()
+    torch.cuda.synchronize()
+    sms = e0.elapsed_time(e1) / args.steps
+    if graph_ok:
+        del graph
+    model.close()
+    wbytes = 4 * w.M * (4 * w.D * w.D + 3 * w.D)
+    return {"ms_per_step": round(sms, 4), "tokens_per_s": round(w.B * w.L / (sms / 1e3), 1),
+            "us_per_position": round(1e3 * sms / w.L, 3),
+            "mixer_share": round(ms_mixer / sms, 4),
+            "weight_bytes_per_position": wbytes,
+            "launches_per_position": 2 * w.M + 2,
+            "graph": graph_ok}
 
 
 def closed_loop(w, filters, opts, lcsm, torch, dev, args):

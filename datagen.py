@@ -183,18 +183,20 @@ def decay_table(L: int, decay: float) -> np.ndarray:
 
 # ---------------------------------------------------------------- numpy views
 
-def filters_np(w: Workload, m_idx=None, d_idx=None) -> np.ndarray:
-    """Filters h[m, d, k] as fp32 numpy, for the selected layers/channels.
+def filters_np(w: Workload, m_idx=None, d_idx=None, lags=None) -> np.ndarray:
+    """Filters h[m, d, k] as fp32 numpy, for the selected layers/channels and
+    the first ``lags`` lags (default all L).
 
-    Returns shape [len(m_idx), len(d_idx), L].
+    Returns shape [len(m_idx), len(d_idx), lags].
     """
     m_idx = np.arange(w.M) if m_idx is None else np.asarray(m_idx)
     d_idx = np.arange(w.D) if d_idx is None else np.asarray(d_idx)
-    k = np.arange(w.L, dtype=np.uint64)
+    lags = w.L if lags is None else lags
+    k = np.arange(lags, dtype=np.uint64)
     n = ((m_idx[:, None, None].astype(np.uint64) * np.uint64(w.D)
           + d_idx[None, :, None].astype(np.uint64)) * np.uint64(w.L) + k[None, None, :])
     g = normal(n, w.seed, FILTERS)
-    return (g * decay_table(w.L, w.decay)[None, None, :]).astype(np.float32)
+    return (g * decay_table(w.L, w.decay)[None, None, :lags]).astype(np.float32)
 
 
 def _tmbd_index(w: Workload, t_idx, m_idx, b_idx, d_idx):

@@ -277,6 +277,29 @@ int step_common(lcsm_ctx* c, const float* in, float* z, bool chain) {
 
 }  // namespace
 
+namespace lcsm {
+
+int begin_external_step(lcsm_ctx* c, StepView* v) {
+  if (!c || !v) return LCSM_EINVAL;
+  if (c->faulted) return LCSM_ESTATE;
+  if (c->layers_done != 0) return fail(c, LCSM_ESTATE, "step during a per-layer position", hipSuccess);
+  if (c->t >= c->s.L) return LCSM_EDONE;
+  v->S = state_base(c, c->t);
+  v->Hf = c->Hf;
+  v->s = c->s;
+  v->t = c->t;
+  v->stream = c->stream;
+  return LCSM_OK;
+}
+
+int end_external_step(lcsm_ctx* c) {
+  if (!c) return LCSM_EINVAL;
+  c->layers_done = c->s.M;
+  return lcsm_advance(c);
+}
+
+}  // namespace lcsm
+
 extern "C" {
 
 int lcsm_workspace_bytes(int M, int B, int D, int L, const lcsm_options* opt, size_t* bytes) {

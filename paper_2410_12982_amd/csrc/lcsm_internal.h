@@ -5,6 +5,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "lcsm.h"
+
 namespace lcsm {
 
 // Shape of one context.  State rows are indexed [m][t][b*D + d] (time-major:
@@ -99,6 +101,23 @@ hipError_t launch_spectra(const float* Hf, float2* Hout, const float2* tw, const
 hipError_t launch_fft_tile(float* S, const float2* H, const float2* tw, const Shape& s, int i,
                            int U, int dst_len, int lds_max_n, float2* scratch,
                            size_t scratch_bytes, hipStream_t st, bool in_place = false);
+
+// ---- hooks for a caller that runs the red cells in its own kernels (the
+// synthetic model, lcsm_synth.hip): between two steps of a context,
+// begin_external_step reports the position t and the state of its phase;
+// after the caller has done the red cells of every layer at t (state slot
+// of position t: S + (m*SL + t)*BD + c, z = fmaf(Hf[m*L*D + d], y, slot),
+// slot = y), end_external_step queues the gray tiles of i = t+1 for all
+// layers and advances t.  Return codes as lcsm_step.
+struct StepView {
+  float* S;         // state pointer of the phase of position t
+  const float* Hf;  // filters [M][L][D]
+  Shape s;
+  int t;
+  hipStream_t stream;
+};
+int begin_external_step(lcsm_ctx* c, StepView* v);
+int end_external_step(lcsm_ctx* c);
 
 // Largest FFT length with the red cell fused into the tile kernel.
 constexpr int kMaxRedFftN = 4096;

@@ -1,0 +1,326 @@
+// The synthetic end-to-end model of the experiments (Sec. 5): per layer a
+// long-convolution mixer and an MLP block of hidden width 2D with the exact
+// GELU; the next token's input is the last layer's output plus noise (the
+// sampler of Alg. 3).
+//
+// Per position t the work is (all on the mixer context's stream):
+//   k_synth_red0            y^0_t = eps_t (+ a^M_{t-1}); layer 0's red cell
+//   for each layer m:
+//     k_gemv<UP>            hid = gelu(W_up[m] z^m_t + b_up[m])        [B][2D]
+//     k_gemv<DOWN>          a^{m+1}_t = W_down[m] hid + b_down[m] -> act[m];
+//                           its epilogue is layer m+1's red cell (y^{m+1}_t =
+//                           a^{m+1}_t), or keeps a^M_t for the sampler
+//   the gray tiles of i = t+1 for all layers (the mixer's batched launch).
+//
+// The products are matrix-vector products over B <= 16 rows at a time: their
+// time is the weight read (4 bytes per weight, 2B flops), so they run on the
+// vector ALUs with coalesced weight rows, not on the matrix cores.  A wave
+// takes one output unit: its 64 lanes stride the unit's weight row in
+// 16-byte pieces (1 KB contiguous per load), multiply them with the same
+// pieces of the B input rows (shared through L1 by the block's 4 waves) and
+// reduce over the wave with butterfly shuffles, after which lane r stores
+// row r.  The K loop is unrolled so that one memory round trip covers several
+// pieces per lane.
+#include <math.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <new>
+
+#include "lcsm_internal.h"
+#include "lcsm_synth.h"
+
+namespace lcsm {
+namespace {
+
+constexpr int kGemvWaves = 4;    // output units per block, one per wave
+constexpr int kGemvThreads = 64 * kGemvWaves;
+constexpr int kMaxRows = 16;     // batch rows per product launch
+
+enum { kUp = 0, kDown = 1 };
+
+// Arguments of the DOWN epilogue: the next layer's red cell, or the copy of
+// a^M_t for the sampler (S == nullptr).
+struct RedNext {
+  float* S;          // state slot row of position t, layer m+1: S + (m+1)*SL*BD + t*BD
+  const float* h0;   // filter taps h[m+1, d, 0] (lag-0 row of layer m+1)
+  float* z;          // [B][D] the next layer's mixer output
+  float* last;       // [B][D] a^M_t (last layer only)
+};
+
+__device__ __forceinline__ float gelu(float v) {
+  return 0.5f * v * (1.0f + erff(v * 0.70710678118654752f));
+}
+
+// out rows r < nrows of the product W [N][K] x^T with x [nrows][K] (row
+// stride K): MODE kUp -> out[r][n] = gelu(sum + bias[n]) (row stride N);
+// MODE kDown -> a = sum + bias[n], out[r][n] = a (row stride N = D), then the
+// red cell of the next layer or the sampler copy.  NR >= nrows, a power of
+// two <= kMaxRows; rows nrows..NR-1 are computed from row nrows-1 and not
+// stored.  K must be a multiple of 4 and the rows 16-byte aligned.
+template <int NR, int MODE>
+__global__ __launch_bounds__(kGemvThreads) void k_gemv(const float* __restrict__ x,
+                                                       const float* __restrict__ W,
+                                                       const float* __restrict__ bias,
+                                                       float* __restrict__ out, int N, int K,
+                                                       int nrows, RedNext rn) {
+  constexpr int UNR = NR <= 8 ? 4 : 2;  // pieces per lane and round trip
+  const int lane = (int)threadIdx.x & 63;
+  const int n = (int)blockIdx.x * kGemvWaves + ((int)threadIdx.x >> 6);
+  const bool live = n < N;
+  const float* wr = W + (size_t)(live ? n : N - 1) * K;
+  const float* xr[NR];
+#pragma unroll
+  for (int r = 0; r < NR; ++r) xr[r] = x + (size_t)(r < nrows ? r : nrows - 1) * K;
+  float acc[NR];
+#pragma unroll
+  for (int r = 0; r < NR; ++r) acc[r] = 0.f;
+  for (int k0 = lane * 4; k0 < K; k0 += 256 * UNR) {
+    float4 w[UNR];
+    float4 v[UNR][NR];
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      const int k = k0 + 256 * u;
+      const bool in = k < K;
+      w[u] = in ? *reinterpret_cast<const float4*>(wr + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+      for (int r = 0; r < NR; ++r)
+        v[u][r] = in ? *reinterpret_cast<const float4*>(xr[r] + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+#pragma unroll
+      for (int r = 0; r < NR; ++r) {
+        acc[r] = fmaf(w[u].x, v[u][r].x, acc[r]);
+        acc[r] = fmaf(w[u].y, v[u][r].y, acc[r]);
+        acc[r] = fmaf(w[u].z, v[u][r].z, acc[r]);
+        acc[r] = fmaf(w[u].w, v[u][r].w, acc[r]);
+      }
+    }
+  }
+  // sum over the wave: every lane ends with the totals
+#pragma unroll
+  for (int r = 0; r < NR; ++r) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) acc[r] += __shfl_xor(acc[r], off, 64);
+  }
+  if (!live) return;
+  const float bn = bias[n];
+#pragma unroll
+  for (int r = 0; r < NR; ++r) {
+    if (r != lane || r >= nrows) continue;
+    const float s = acc[r] + bn;
+    const size_t e = (size_t)r * N + n;
+    if constexpr (MODE == kUp) {
+      out[e] = gelu(s);
+    } else {
+      out[e] = s;
+      if (rn.S) {
+        float* slot = rn.S + e;
+        rn.z[e] = fmaf(rn.h0[n], s, *slot);
+        *slot = s;
+      } else {
+        rn.last[e] = s;
+      }
+    }
+  }
+}
+
+// Sampler and layer 0's red cell at position t: y = eps (+ last for t > 0),
+// z = fmaf(h0[d], y, slot), slot = y.
+__global__ __launch_bounds__(256) void k_synth_red0(const float* __restrict__ eps,
+                                                    const float* __restrict__ last,
+                                                    float* __restrict__ slot_row,
+                                                    const float* __restrict__ h0,
+                                                    float* __restrict__ z, int BD, int D, int t) {
+  const int c = (int)blockIdx.x * 256 + (int)threadIdx.x;
+  if (c >= BD) return;
+  const float y = t > 0 ? last[c] + eps[c] : eps[c];
+  z[c] = fmaf(h0[c % D], y, slot_row[c]);
+  slot_row[c] = y;
+}
+
+template <int MODE>
+hipError_t gemv(const float* x, const float* W, const float* bias, float* out, int N, int K,
+                int nrows, const RedNext& rn, hipStream_t st) {
+  const dim3 grid((unsigned)((N + kGemvWaves - 1) / kGemvWaves)), block(kGemvThreads);
+#define LCSM_GEMV(NR) \
+  hipLaunchKernelGGL((k_gemv<NR, MODE>), grid, block, 0, st, x, W, bias, out, N, K, nrows, rn)
+  if (nrows <= 1)
+    LCSM_GEMV(1);
+  else if (nrows <= 2)
+    LCSM_GEMV(2);
+  else if (nrows <= 4)
+    LCSM_GEMV(4);
+  else if (nrows <= 8)
+    LCSM_GEMV(8);
+  else
+    LCSM_GEMV(16);
+#undef LCSM_GEMV
+  return hipGetLastError();
+}
+
+}  // namespace
+}  // namespace lcsm
+
+struct lcsm_synth {
+  lcsm_ctx* mixer;
+  int M, B, D, L;
+  hipStream_t stream;
+  char* mem;
+  float *w_up, *b_up, *w_down, *b_down;
+  float *z, *hid, *last;
+  bool faulted;
+  char msg[256];
+};
+
+namespace {
+
+int synth_fail(lcsm_synth* s, int code, const char* what, hipError_t e) {
+  if (e != hipSuccess) {
+    snprintf(s->msg, sizeof(s->msg), "%s: %s", what, hipGetErrorString(e));
+    s->faulted = true;
+    return LCSM_EDEVICE;
+  }
+  snprintf(s->msg, sizeof(s->msg), "%s", what);
+  return code;
+}
+
+size_t align256(size_t v) { return (v + 255) / 256 * 256; }
+
+}  // namespace
+
+extern "C" {
+
+int lcsm_synth_init(lcsm_synth** out, const float* filters, const float* w_up, const float* b_up,
+                    const float* w_down, const float* b_down, int M, int B, int D, int L,
+                    void* stream, const lcsm_options* opt) {
+  if (!out) return LCSM_EINVAL;
+  *out = nullptr;
+  if (!filters || !w_up || !b_up || !w_down || !b_down) return LCSM_EINVAL;
+  if (D < 4 || D % 4 != 0) return LCSM_EINVAL;
+  size_t need = 0;
+  int r = lcsm_workspace_bytes(M, B, D, L, opt, &need);  // validates shape and options
+  if (r) return r;
+  lcsm_synth* s = new (std::nothrow) lcsm_synth();
+  if (!s) return LCSM_ENOMEM;
+  s->M = M;
+  s->B = B;
+  s->D = D;
+  s->L = L;
+  s->stream = (hipStream_t)stream;
+  s->msg[0] = 0;
+  const size_t D2 = 2 * (size_t)D, BD = (size_t)B * D;
+  const size_t n_wup = (size_t)M * D2 * D, n_bup = (size_t)M * D2, n_wdn = (size_t)M * D * D2,
+               n_bdn = (size_t)M * D;
+  size_t off[7], total = 0;
+  const size_t sizes[7] = {n_wup, n_bup, n_wdn, n_bdn, BD, (size_t)B * D2, BD};
+  for (int k = 0; k < 7; ++k) {
+    off[k] = total;
+    total = align256(total + sizeof(float) * sizes[k]);
+  }
+  void* p = nullptr;
+  if (hipMalloc(&p, total) != hipSuccess) {
+    (void)hipGetLastError();
+    delete s;
+    return LCSM_ENOMEM;
+  }
+  s->mem = (char*)p;
+  float* f[7];
+  for (int k = 0; k < 7; ++k) f[k] = (float*)(s->mem + off[k]);
+  s->w_up = f[0];
+  s->b_up = f[1];
+  s->w_down = f[2];
+  s->b_down = f[3];
+  s->z = f[4];
+  s->hid = f[5];
+  s->last = f[6];
+  r = lcsm_init(&s->mixer, filters, M, B, D, L, stream, nullptr, 0, opt);
+  if (r) {
+    (void)hipFree(s->mem);
+    delete s;
+    return r;
+  }
+  const float* src[4] = {w_up, b_up, w_down, b_down};
+  hipError_t e = hipSuccess;
+  for (int k = 0; k < 4 && e == hipSuccess; ++k)
+    e = hipMemcpyAsync(f[k], src[k], sizeof(float) * sizes[k], hipMemcpyDeviceToDevice, s->stream);
+  if (e == hipSuccess) e = lcsm::launch_zero(s->last, BD, s->stream);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    lcsm_destroy(s->mixer);
+    (void)hipFree(s->mem);
+    delete s;
+    return LCSM_EDEVICE;
+  }
+  s->faulted = false;
+  *out = s;
+  return LCSM_OK;
+}
+
+int lcsm_synth_step(lcsm_synth* s, const float* eps_t, float* act_t) {
+  if (!s) return LCSM_EINVAL;
+  if (!eps_t || !act_t) return synth_fail(s, LCSM_EINVAL, "null input or output pointer", hipSuccess);
+  if (s->faulted) return LCSM_ESTATE;
+  lcsm::StepView v;
+  int r = lcsm::begin_external_step(s->mixer, &v);
+  if (r) return r == LCSM_EDONE ? r : synth_fail(s, r, lcsm_last_error(s->mixer), hipSuccess);
+  const int M = s->M, B = s->B, D = s->D, D2 = 2 * D, BD = B * D;
+  const size_t lstride = (size_t)v.s.SL * BD;  // state floats per layer
+  const size_t hstride = (size_t)v.s.L * D;    // filter floats per layer
+  hipStream_t st = v.stream;
+  // sampler + layer 0's red cell (state slot row of position t, layer 0)
+  hipLaunchKernelGGL(lcsm::k_synth_red0, dim3((unsigned)((BD + 255) / 256)), dim3(256), 0, st,
+                     eps_t, s->last, v.S + (size_t)v.t * BD, v.Hf, s->z, BD, D, v.t);
+  hipError_t e = hipGetLastError();
+  for (int m = 0; m < M && e == hipSuccess; ++m) {
+    for (int r0 = 0; r0 < B && e == hipSuccess; r0 += lcsm::kMaxRows) {
+      const int nr = B - r0 < lcsm::kMaxRows ? B - r0 : lcsm::kMaxRows;
+      lcsm::RedNext none{nullptr, nullptr, nullptr, nullptr};
+      e = lcsm::gemv<lcsm::kUp>(s->z + (size_t)r0 * D, s->w_up + (size_t)m * D2 * D,
+                                s->b_up + (size_t)m * D2, s->hid + (size_t)r0 * D2, D2, D, nr,
+                                none, st);
+      lcsm::RedNext rn{nullptr, nullptr, nullptr, nullptr};
+      if (m + 1 < M) {
+        rn.S = v.S + (size_t)(m + 1) * lstride + (size_t)v.t * BD + (size_t)r0 * D;
+        rn.h0 = v.Hf + (size_t)(m + 1) * hstride;
+        rn.z = s->z + (size_t)r0 * D;
+      } else {
+        rn.last = s->last + (size_t)r0 * D;
+      }
+      if (e == hipSuccess)
+        e = lcsm::gemv<lcsm::kDown>(s->hid + (size_t)r0 * D2, s->w_down + (size_t)m * D * D2,
+                                    s->b_down + (size_t)m * D,
+                                    act_t + (size_t)m * BD + (size_t)r0 * D, D, D2, nr, rn, st);
+    }
+  }
+  if (e != hipSuccess) return synth_fail(s, LCSM_EDEVICE, "model kernel launch", e);
+  r = lcsm::end_external_step(s->mixer);
+  if (r) return synth_fail(s, r, lcsm_last_error(s->mixer), hipSuccess);
+  return LCSM_OK;
+}
+
+int lcsm_synth_reset(lcsm_synth* s) {
+  if (!s) return LCSM_EINVAL;
+  int r = lcsm_reset(s->mixer);
+  if (r) return synth_fail(s, r, lcsm_last_error(s->mixer), hipSuccess);
+  s->faulted = false;
+  s->msg[0] = 0;
+  return LCSM_OK;
+}
+
+int lcsm_synth_position(const lcsm_synth* s, int* t) {
+  if (!s || !t) return LCSM_EINVAL;
+  return lcsm_position(s->mixer, t);
+}
+
+void lcsm_synth_destroy(lcsm_synth* s) {
+  if (!s) return;
+  lcsm_destroy(s->mixer);  // waits for the stream
+  (void)hipFree(s->mem);
+  delete s;
+}
+
+const char* lcsm_synth_last_error(const lcsm_synth* s) { return s ? s->msg : ""; }
+
+}  // extern "C"

@@ -1,4 +1,4 @@
-"""Python binding of the C ABI in ``include/lcsm.h`` (ctypes).
+"""Python binding of the C ABI in ``include/lcsm.h`` and ``include/lcsm_synth.h`` (ctypes).
 
 Argument marshalling only: every step of the computation runs in the HIP
 kernels of ``liblcsm.so``.  PyTorch supplies device memory (the workspace and
@@ -78,6 +78,14 @@ _SIGS = {
     "lcsm_destroy": (None, [_vp]),
     "lcsm_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "lcsm_last_error": (ctypes.c_char_p, [_vp]),
+    # include/lcsm_synth.h
+    "lcsm_synth_init": (ctypes.c_int, [ctypes.POINTER(_vp)] + [_vp] * 5 + [ctypes.c_int] * 4
+                        + [_vp, ctypes.POINTER(Options)]),
+    "lcsm_synth_step": (ctypes.c_int, [_vp, _vp, _vp]),
+    "lcsm_synth_reset": (ctypes.c_int, [_vp]),
+    "lcsm_synth_position": (ctypes.c_int, [_vp, _c_int_p]),
+    "lcsm_synth_destroy": (None, [_vp]),
+    "lcsm_synth_last_error": (ctypes.c_char_p, [_vp]),
 }
 
 for _name, (_res, _args) in _SIGS.items():
@@ -258,6 +266,86 @@ class Lcsm:
     def close(self):
         if self._ctx:
             _lib.lcsm_destroy(self._ctx)
+            self._ctx = _vp()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class Synth:
+    """The synthetic end-to-end model (``include/lcsm_synth.h``): per layer the
+    long-convolution mixer and an MLP block (hidden 2D, GELU); the next
+    token's input is the last layer's output plus the noise handed to step.
+
+    ``filters`` [M, D, L]; ``w_up`` [M, 2D, D], ``b_up`` [M, 2D], ``w_down``
+    [M, D, 2D], ``b_down`` [M, D] (fp32 CUDA tensors, copied at init).
+    """
+
+    def __init__(self, filters, w_up, b_up, w_down, b_down, B: int, options=None, stream=None):
+        import torch
+        ts = (filters, w_up, b_up, w_down, b_down)
+        if not all(t.is_cuda and t.dtype == torch.float32 for t in ts):
+            raise ValueError("filters and weights must be CUDA fp32 tensors")
+        filters, w_up, b_up, w_down, b_down = (t.contiguous() for t in ts)
+        self.M, self.D, self.L = (int(v) for v in filters.shape)
+        self.B = int(B)
+        M, D = self.M, self.D
+        shapes = {"w_up": (M, 2 * D, D), "b_up": (M, 2 * D), "w_down": (M, D, 2 * D),
+                  "b_down": (M, D)}
+        for name, t in zip(shapes, (w_up, b_up, w_down, b_down)):
+            if tuple(t.shape) != shapes[name]:
+                raise ValueError(f"{name} must have shape {shapes[name]}")
+        self.device = filters.device
+        if options is not None and not isinstance(options, Options):
+            o = Options()
+            for k, v in dict(options).items():
+                setattr(o, k, int(v))
+            options = o
+        self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
+        self._ctx = _vp()
+        r = _lib.lcsm_synth_init(ctypes.byref(self._ctx), filters.data_ptr(), w_up.data_ptr(),
+                                 b_up.data_ptr(), w_down.data_ptr(), b_down.data_ptr(), M, self.B,
+                                 D, self.L, self.stream.cuda_stream, _opts(options))
+        if r:
+            raise LcsmError(r, "lcsm_synth_init")
+        # the copies are queued on the stream: keep the sources until it passes them
+        self._keepalive = (filters, w_up, b_up, w_down, b_down)
+
+    def _check(self, r, where):
+        if r:
+            detail = _lib.lcsm_synth_last_error(self._ctx).decode() if self._ctx else ""
+            raise LcsmError(r, where, detail)
+
+    def step(self, eps_t, act_t=None):
+        """Position t: noise eps_t [B, D] in, block outputs of every layer
+        act_t [M, B, D] out (act_t[M-1] is the model's output)."""
+        import torch
+        if act_t is None:
+            act_t = torch.empty((self.M, self.B, self.D), dtype=torch.float32, device=self.device)
+        for t, shape, name in ((eps_t, (self.B, self.D), "eps_t"),
+                               (act_t, (self.M, self.B, self.D), "act_t")):
+            if not (t.is_cuda and t.dtype == torch.float32 and t.is_contiguous()
+                    and tuple(t.shape) == shape):
+                raise ValueError(f"{name} must be a contiguous CUDA fp32 tensor of shape {shape}")
+        self._check(_lib.lcsm_synth_step(self._ctx, eps_t.data_ptr(), act_t.data_ptr()),
+                    "lcsm_synth_step")
+        return act_t
+
+    def reset(self):
+        self._check(_lib.lcsm_synth_reset(self._ctx), "lcsm_synth_reset")
+
+    @property
+    def position(self) -> int:
+        t = ctypes.c_int()
+        self._check(_lib.lcsm_synth_position(self._ctx, ctypes.byref(t)), "lcsm_synth_position")
+        return t.value
+
+    def close(self):
+        if self._ctx:
+            _lib.lcsm_synth_destroy(self._ctx)
             self._ctx = _vp()
 
     def __del__(self):

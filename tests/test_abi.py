@@ -1,4 +1,4 @@
-"""The C ABI loads, exports what include/lcsm.h declares, validates arguments
+"""The C ABI loads, exports what include/*.h declare, validates arguments
 on the host and plans the same tiles as the oracle's schedule -- CPU only
 (no call here reaches the device)."""
 import ctypes
@@ -15,14 +15,17 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
 def _declared():
-    text = open(os.path.join(ROOT, "include", "lcsm.h")).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(lcsm_[a-z_]+)\s*\(", text)))
+    import glob
+    names = set()
+    for path in glob.glob(os.path.join(ROOT, "include", "*.h")):
+        text = re.sub(r"/\*.*?\*/", "", open(path).read(), flags=re.S)
+        names |= set(re.findall(r"\b(lcsm_[a-z_]+)\s*\(", text))
+    return sorted(names)
 
 
 def test_every_declared_symbol_is_exported():
     names = _declared()
-    assert len(names) >= 13
+    assert len(names) >= 19
     lib = lcsm.raw()
     for n in names:
         assert hasattr(lib, n), n
@@ -222,3 +225,32 @@ def test_default_crossover_depends_on_shape():
     assert kind_at_u(*wide, 64) == lcsm.TILE_FFT
     # an explicit option overrides the shape rule
     assert lcsm.plan_tile(*wide, 63, {"direct_max_u": 64})[3] == lcsm.TILE_DIRECT
+
+
+def test_synth_init_validates_before_touching_the_device():
+    """lcsm_synth_init rejects null pointers, D not a multiple of 4 and what
+    lcsm_init rejects, without any device work."""
+    lib = lcsm.raw()
+    out = ctypes.c_void_p()
+    p = ctypes.c_void_p(256)  # never dereferenced: validation fails first
+    assert lib.lcsm_synth_init(None, p, p, p, p, p, 1, 1, 16, 64, None, None) == lcsm.LCSM_EINVAL
+    assert lib.lcsm_synth_init(ctypes.byref(out), None, p, p, p, p, 1, 1, 16, 64, None,
+                               None) == lcsm.LCSM_EINVAL
+    assert lib.lcsm_synth_init(ctypes.byref(out), p, p, p, None, p, 1, 1, 16, 64, None,
+                               None) == lcsm.LCSM_EINVAL
+    for D in (1, 2, 6, 18):
+        assert lib.lcsm_synth_init(ctypes.byref(out), p, p, p, p, p, 1, 1, D, 64, None,
+                                   None) == lcsm.LCSM_EINVAL
+    assert lib.lcsm_synth_init(ctypes.byref(out), p, p, p, p, p, 0, 1, 16, 64, None,
+                               None) == lcsm.LCSM_EINVAL
+    o = lcsm.Options()
+    o.half_state = 1
+    assert lib.lcsm_synth_init(ctypes.byref(out), p, p, p, p, p, 1, 1, 16, 64, None,
+                               ctypes.byref(o)) == lcsm.LCSM_EINVAL
+    assert not out.value
+    for f in (lib.lcsm_synth_step, ):
+        assert f(None, p, p) == lcsm.LCSM_EINVAL
+    assert lib.lcsm_synth_reset(None) == lcsm.LCSM_EINVAL
+    assert lib.lcsm_synth_position(None, ctypes.byref(ctypes.c_int())) == lcsm.LCSM_EINVAL
+    lib.lcsm_synth_destroy(None)
+    assert lib.lcsm_synth_last_error(None) == b""

@@ -24,6 +24,27 @@ def test_numpy_and_torch_agree():
     assert np.array_equal(sub, full[[5, 299]][:, [1]][:, :, [2]][..., [0, 39]])
 
 
+def test_model_weights_and_noise():
+    """The synthetic model's weights and noise: numpy and torch views agree bit
+    for bit, the streams are distinct, the scales are the stated ones, and the
+    lag-limited filter view is a prefix of the full one."""
+    w = g.Workload("m", 2, 3, 16, 300, decay=50.0, seed=4)
+    a, b = g.mlp_weights_np(w), g.mlp_weights_torch(w, "cpu")
+    assert [x.shape for x in a] == [(2, 32, 16), (2, 32), (2, 16, 32), (2, 16)]
+    assert all(np.array_equal(x, y.numpy()) for x, y in zip(a, b))
+    assert np.array_equal(g.noise_np(w), g.noise_torch(w, "cpu").numpy())
+    assert np.array_equal(g.noise_np(w, 7, 20), g.noise_np(w)[7:20])
+    s_up, s_down, s_b = g.mlp_scales(w)
+    assert s_up == 1 / 4.0
+    norm = np.sqrt(np.sum(np.exp(-2 * np.arange(300) / 50.0)))
+    assert abs(s_down - 1 / (2 * norm * np.sqrt(32))) < 1e-15
+    big = g.Workload("mb", 1, 1, 256, 16, decay=5.0, seed=1)
+    wu = g.mlp_weights_np(big)[0]
+    assert abs(wu.std() * np.sqrt(256) - 1) < 0.01
+    assert not np.array_equal(a[1][0, :16], a[3][0])          # distinct streams
+    assert np.array_equal(g.filters_np(w, lags=37), g.filters_np(w)[:, :, :37])
+
+
 def test_moments_and_ranges():
     n = np.arange(1 << 20, dtype=np.uint64)
     u = g.uniform(n, 1, 1)
