@@ -19,6 +19,9 @@ Contents (all indices 0-based: positions 0..L-1, z_t = sum_{s<=t} y_s h_{t-s}):
 * ``feedback``  -- the elementwise chained block used by the synthetic
   workloads (y^{l+1}_t = 0.5 tanh(z^l_t) + x^l_t, layer 0 fed from the last
   layer at t-1).
+* ``dd``        -- the relaxed online product with data-dependent filters
+  (Alg. 5): rho_t revealed with y_t, parallelogram tiles of untruncated
+  convolutions of two length-U blocks, every power of two U dividing t+1.
 * ``block``     -- the blocks and sampler of the paper's synthetic model
   (Sec. 5): an MLP of hidden width 2D with GELU per layer, and the next
   token's input = the last layer's output plus noise.
