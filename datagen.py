@@ -46,6 +46,9 @@ Tensors and their flat index order:
   amplify and the closed loop stays bounded), biases ``fp32(0.1 g)``.
 * sampler noise ``eps[t, b, d]``: ``n = (t*B + b)*D + d``, stream 7,
   ``eps = fp32(sigma * g)``.
+* data-dependent filter inputs ``rho[t, m, b, d]`` (revealed with y_t):
+  index as y, stream 8, ``rho = fp32(g * exp(-t/decay))`` (a filter's
+  decaying profile, drawn per batch row as well).
 """
 from __future__ import annotations
 
@@ -59,6 +62,7 @@ M32 = 0xFFFFFFFF
 # stream ids
 FILTERS, YIN, XIN = 0, 1, 2
 W_UP, B_UP, W_DOWN, B_DOWN, NOISE = 3, 4, 5, 6, 7
+RHO = 8
 
 
 @dataclass(frozen=True)
@@ -227,6 +231,20 @@ def x_np(w: Workload, t_idx=None, m_idx=None, b_idx=None, d_idx=None) -> np.ndar
     return (w.x_sigma * normal(n, w.seed, XIN)).astype(np.float32)
 
 
+def rho_np(w: Workload, t_idx=None, m_idx=None, b_idx=None, d_idx=None) -> np.ndarray:
+    """Data-dependent filter inputs rho[t, m, b, d] (fp32), N(0,1) * exp(-t/decay)."""
+    sel = _sel(w, t_idx, m_idx, b_idx, d_idx)
+    n = _tmbd_index(w, *sel)
+    dec = decay_table(w.L, w.decay)[np.asarray(sel[0])][:, None, None, None]
+    return (normal(n, w.seed, RHO) * dec).astype(np.float32)
+
+
+def int_rho_np(w: Workload, r: int = 3) -> np.ndarray:
+    """Small-integer data-dependent filter inputs rho[t, m, b, d] in [-r, r] (fp32)."""
+    n = np.arange(w.L * w.M * w.B * w.D, dtype=np.uint64)
+    return small_int(n, w.seed, RHO, r).reshape(w.L, w.M, w.B, w.D).astype(np.float32)
+
+
 def int_filters_np(w: Workload, r: int = 3) -> np.ndarray:
     """Small-integer filters h[m, d, k] in [-r, r] (fp32)."""
     n = np.arange(w.M * w.D * w.L, dtype=np.uint64)
@@ -354,6 +372,24 @@ def x_torch(w: Workload, device, t0: int = 0, t1: int | None = None):
         ts = torch.arange(a, b, device=device, dtype=torch.int64)
         n = ts[:, None] * slab + j[None, :]
         flat[a - t0:b - t0] = (w.x_sigma * normal(n, w.seed, XIN)).to(torch.float32)
+    return out
+
+
+def rho_torch(w: Workload, device, t0: int = 0, t1: int | None = None):
+    """Data-dependent filter inputs rho[t0:t1, m, b, d] as an fp32 torch tensor."""
+    import torch
+    t1 = w.L if t1 is None else t1
+    slab = w.M * w.B * w.D
+    out = torch.empty((t1 - t0, w.M, w.B, w.D), dtype=torch.float32, device=device)
+    flat = out.view(t1 - t0, slab)
+    dec = torch.from_numpy(decay_table(w.L, w.decay)).to(device)
+    j = torch.arange(slab, device=device, dtype=torch.int64)
+    step = max(1, (1 << 22) // slab)
+    for a in range(t0, t1, step):
+        b = min(t1, a + step)
+        ts = torch.arange(a, b, device=device, dtype=torch.int64)
+        n = ts[:, None] * slab + j[None, :]
+        flat[a - t0:b - t0] = (normal(n, w.seed, RHO) * dec[a:b, None]).to(torch.float32)
     return out
 
 

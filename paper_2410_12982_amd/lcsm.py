@@ -1,4 +1,4 @@
-"""Python binding of the C ABI in ``include/lcsm.h`` and ``include/lcsm_synth.h`` (ctypes).
+"""Python binding of the C ABI in ``include/lcsm.h``, ``lcsm_dd.h`` and ``lcsm_synth.h`` (ctypes).
 
 Argument marshalling only: every step of the computation runs in the HIP
 kernels of ``liblcsm.so``.  PyTorch supplies device memory (the workspace and
@@ -78,6 +78,16 @@ _SIGS = {
     "lcsm_destroy": (None, [_vp]),
     "lcsm_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "lcsm_last_error": (ctypes.c_char_p, [_vp]),
+    # include/lcsm_dd.h
+    "lcsm_dd_workspace_bytes": (ctypes.c_int, [ctypes.c_int] * 4
+                                + [ctypes.POINTER(Options), ctypes.POINTER(ctypes.c_size_t)]),
+    "lcsm_dd_init": (ctypes.c_int, [ctypes.POINTER(_vp)] + [ctypes.c_int] * 4
+                     + [_vp, _vp, ctypes.c_size_t, ctypes.POINTER(Options)]),
+    "lcsm_dd_step": (ctypes.c_int, [_vp, _vp, _vp, _vp]),
+    "lcsm_dd_reset": (ctypes.c_int, [_vp]),
+    "lcsm_dd_position": (ctypes.c_int, [_vp, _c_int_p]),
+    "lcsm_dd_destroy": (None, [_vp]),
+    "lcsm_dd_last_error": (ctypes.c_char_p, [_vp]),
     # include/lcsm_synth.h
     "lcsm_synth_init": (ctypes.c_int, [ctypes.POINTER(_vp)] + [_vp] * 5 + [ctypes.c_int] * 4
                         + [_vp, ctypes.POINTER(Options)]),
@@ -266,6 +276,78 @@ class Lcsm:
     def close(self):
         if self._ctx:
             _lib.lcsm_destroy(self._ctx)
+            self._ctx = _vp()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def dd_workspace_bytes(M, B, D, L, options=None) -> int:
+    n = ctypes.c_size_t(0)
+    r = _lib.lcsm_dd_workspace_bytes(M, B, D, L, _opts(options), ctypes.byref(n))
+    if r:
+        raise LcsmError(r, "lcsm_dd_workspace_bytes")
+    return n.value
+
+
+class Dd:
+    """Relaxed online convolution with data-dependent filters
+    (``include/lcsm_dd.h``): at step t both y_t and rho_t [M, B, D] arrive and
+    z_t = sum_{j+k=t} y_j rho_k is returned.  The workspace is a torch uint8
+    tensor owned by this object."""
+
+    def __init__(self, M, B, D, L, options=None, stream=None, device="cuda:0"):
+        import torch
+        self.M, self.B, self.D, self.L = int(M), int(B), int(D), int(L)
+        self.device = torch.device(device)
+        if options is not None and not isinstance(options, Options):
+            o = Options()
+            for k, v in dict(options).items():
+                setattr(o, k, int(v))
+            options = o
+        self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
+        nbytes = dd_workspace_bytes(self.M, self.B, self.D, self.L, options)
+        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+        self._ctx = _vp()
+        r = _lib.lcsm_dd_init(ctypes.byref(self._ctx), self.M, self.B, self.D, self.L,
+                              self.stream.cuda_stream, self.workspace.data_ptr(), nbytes,
+                              _opts(options))
+        if r:
+            raise LcsmError(r, "lcsm_dd_init")
+
+    def _check(self, r, where):
+        if r:
+            detail = _lib.lcsm_dd_last_error(self._ctx).decode() if self._ctx else ""
+            raise LcsmError(r, where, detail)
+
+    def step(self, y_t, rho_t, z_t=None):
+        import torch
+        shape = (self.M, self.B, self.D)
+        if z_t is None:
+            z_t = torch.empty(shape, dtype=torch.float32, device=self.device)
+        for t, name in ((y_t, "y_t"), (rho_t, "rho_t"), (z_t, "z_t")):
+            if not (t.is_cuda and t.dtype == torch.float32 and t.is_contiguous()
+                    and tuple(t.shape) == shape):
+                raise ValueError(f"{name} must be a contiguous CUDA fp32 tensor of shape {shape}")
+        self._check(_lib.lcsm_dd_step(self._ctx, y_t.data_ptr(), rho_t.data_ptr(), z_t.data_ptr()),
+                    "lcsm_dd_step")
+        return z_t
+
+    def reset(self):
+        self._check(_lib.lcsm_dd_reset(self._ctx), "lcsm_dd_reset")
+
+    @property
+    def position(self) -> int:
+        t = ctypes.c_int()
+        self._check(_lib.lcsm_dd_position(self._ctx, ctypes.byref(t)), "lcsm_dd_position")
+        return t.value
+
+    def close(self):
+        if self._ctx:
+            _lib.lcsm_dd_destroy(self._ctx)
             self._ctx = _vp()
 
     def __del__(self):

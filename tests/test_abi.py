@@ -254,3 +254,45 @@ def test_synth_init_validates_before_touching_the_device():
     assert lib.lcsm_synth_position(None, ctypes.byref(ctypes.c_int())) == lcsm.LCSM_EINVAL
     lib.lcsm_synth_destroy(None)
     assert lib.lcsm_synth_last_error(None) == b""
+
+
+def test_dd_workspace_and_validation():
+    """Data-dependent contexts: two state arrays; options checked; lengths
+    whose largest tile (largest U with 2U < L) fits neither the direct nor
+    the FFT limit rejected -- all host-side."""
+    M, B, D, L = 2, 3, 16, 1000
+    n = lcsm.dd_workspace_bytes(M, B, D, L)
+    assert n >= 2 * 4 * M * L * B * D and n % 256 == 0
+    for opts in ({"half_state": 1}, {"scratch_mib": 4}, {"direct_max_u": 3},
+                 {"lds_fft_max_n": 100}, {"lds_fft_max_n": 16384}):
+        with pytest.raises(lcsm.LcsmError) as e:
+            lcsm.dd_workspace_bytes(M, B, D, L, opts)
+        assert e.value.code == lcsm.LCSM_EINVAL
+    o = lcsm.Options()
+    o.reserved[1] = 5
+    with pytest.raises(lcsm.LcsmError):
+        lcsm.dd_workspace_bytes(M, B, D, L, o)
+    # L = 16384: largest tile U = 4096, 2U = 8192 fits one LDS pass; L = 16385 needs U = 8192
+    lcsm.dd_workspace_bytes(1, 1, 16, 16384)
+    with pytest.raises(lcsm.LcsmError):
+        lcsm.dd_workspace_bytes(1, 1, 16, 16385)
+    lcsm.dd_workspace_bytes(1, 1, 16, 16385, {"direct_max_u": 8192})
+    with pytest.raises(lcsm.LcsmError):
+        lcsm.dd_workspace_bytes(1, 1, 16, 4096, {"lds_fft_max_n": 1024})   # U = 1024 > 32, 2048 > 1024
+    for shape in ((0, 1, 1, 8), (1, 1, 1, 0), (16385, 1, 1, 8)):
+        with pytest.raises(lcsm.LcsmError):
+            lcsm.dd_workspace_bytes(*shape)
+    lib = lcsm.raw()
+    out = ctypes.c_void_p()
+    assert lib.lcsm_dd_init(None, 1, 1, 16, 64, None, None, 0, None) == lcsm.LCSM_EINVAL
+    assert lib.lcsm_dd_init(ctypes.byref(out), 1, 1, 16, 64, None, ctypes.c_void_p(256), 16,
+                            None) == lcsm.LCSM_ENOMEM
+    assert lib.lcsm_dd_init(ctypes.byref(out), 1, 1, 16, 64, None, ctypes.c_void_p(260), 1 << 20,
+                            None) == lcsm.LCSM_EINVAL
+    assert not out.value
+    p = ctypes.c_void_p(256)
+    assert lib.lcsm_dd_step(None, p, p, p) == lcsm.LCSM_EINVAL
+    assert lib.lcsm_dd_reset(None) == lcsm.LCSM_EINVAL
+    assert lib.lcsm_dd_position(None, ctypes.byref(ctypes.c_int())) == lcsm.LCSM_EINVAL
+    lib.lcsm_dd_destroy(None)
+    assert lib.lcsm_dd_last_error(None) == b""

@@ -43,6 +43,9 @@ def test_model_weights_and_noise():
     assert abs(wu.std() * np.sqrt(256) - 1) < 0.01
     assert not np.array_equal(a[1][0, :16], a[3][0])          # distinct streams
     assert np.array_equal(g.filters_np(w, lags=37), g.filters_np(w)[:, :, :37])
+    assert np.array_equal(g.rho_np(w), g.rho_torch(w, "cpu").numpy())
+    assert np.array_equal(g.rho_torch(w, "cpu", 40, 90).numpy(), g.rho_np(w)[40:90])
+    assert np.array_equal(g.rho_np(w, t_idx=[3, 7], b_idx=[1]), g.rho_np(w)[[3, 7]][:, :, [1]])
 
 
 def test_moments_and_ranges():
