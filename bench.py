@@ -27,6 +27,8 @@ Printed: one JSON line, with
                 stepped;
   half_state    the timed generations again with half-state storage (T of
                 the L state rows per layer), and the bytes it saves;
+  data_dependent  generations with data-dependent filters (rho_t revealed
+                with y_t, the parallelogram tiles of Alg. 5);
   synthetic_model  generations of the synthetic end-to-end model (per layer
                 the mixer and an MLP block of hidden 2D with GELU, the next
                 token = last layer's output + noise), with the mixer's share.
@@ -68,6 +70,8 @@ def parse():
     p.add_argument("--no-kernel-pass", action="store_true")
     p.add_argument("--no-prefill", dest="prefill", action="store_false", default=True,
                    help="skip timing the prompt prefill against the same positions stepped online")
+    p.add_argument("--no-dd", dest="dd", action="store_false", default=True,
+                   help="skip the generations with data-dependent filters")
     p.add_argument("--no-synth", dest="synth", action="store_false", default=True,
                    help="skip the synthetic end-to-end model (MLP blocks + noise sampler)")
     p.add_argument("--no-half-state", dest="half_state", action="store_false", default=True,
@@ -282,6 +286,10 @@ def main():
     if args.half_state:
         half = half_state_timing(w, filters, y, z, opts, ms, lcsm, torch, dev, args)
 
+    dd = None
+    if args.dd:
+        dd = dd_timing(w, ms, lcsm, torch, dev, args)
+
     synth = None
     if args.synth:
         synth = synth_timing(w, filters, opts, ms, lcsm, torch, dev, args)
@@ -319,6 +327,8 @@ def main():
         out["half_state"] = half
     if synth:
         out["synthetic_model"] = synth
+    if dd:
+        out["data_dependent"] = dd
     print(json.dumps(out), flush=True)
 
 
@@ -532,6 +542,56 @@ def half_state_timing(w, filters, y, z, opts, ms_full, lcsm, torch, dev, args):
             "time_vs_full_state": round(ms / ms_full, 4),
             "state_bytes": 4 * w.M * T * w.B * w.D, "state_bytes_full": 4 * w.M * w.L * w.B * w.D,
             "workspace_bytes": half_b, "workspace_bytes_full": full_b}
+
+
+def dd_timing(w, ms_fixed, lcsm, torch, dev, args):
+    """Generations with data-dependent filters (lcsm_dd_step: rho_t revealed
+    with y_t; every power of two U dividing t+1 gets a parallelogram tile),
+    teacher-forced y and rho resident in HBM, dispatched like the timed
+    region.  ms_fixed: the data-independent generation, for the ratio."""
+    import datagen
+    try:
+        lcsm.dd_workspace_bytes(w.M, w.B, w.D, w.L)
+    except lcsm.LcsmError as e:   # the largest tile is beyond the single-pass FFT
+        return {"skipped": str(e)}
+    R = min(RING, w.L)
+    y = datagen.y_torch(w, dev, 0, R)
+    rho = datagen.rho_torch(w, dev, 0, R)
+    z = torch.empty_like(y)
+    graph_ok = args.graph and w.L <= GRAPH_MAX_L
+    stream = torch.cuda.Stream(dev) if graph_ok else torch.cuda.current_stream(dev)
+    ctx = lcsm.Dd(w.M, w.B, w.D, w.L, stream=stream)
+    torch.cuda.synchronize()
+
+    def generation():
+        ctx.reset()
+        for t in range(w.L):
+            ctx.step(y[t % R], rho[t % R], z[t % R])
+
+    if graph_ok:
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=stream):
+            generation()
+        torch.cuda.synchronize()
+        one = graph.replay
+    else:
+        one = generation
+    print("# data-dependent generations", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        one()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        one()
+    e1.record()
+    torch.cuda.synchronize()
+    dms = e0.elapsed_time(e1) / args.steps
+    if graph_ok:
+        del graph
+    ctx.close()
+    return {"ms_per_step": round(dms, 4), "tokens_per_s": round(w.B * w.L / (dms / 1e3), 1),
+            "time_vs_fixed_filters": round(dms / ms_fixed, 3), "graph": graph_ok}
 
 
 def synth_timing(w, filters, opts, ms_mixer, lcsm, torch, dev, args):

@@ -144,6 +144,10 @@ Layout layout_for(const Shape& s, const Options& o) {
   return ly;
 }
 
+}  // namespace
+
+namespace lcsm {
+
 // Twiddle table tw[n + m] = exp(-2 pi i m / n) for n = 1, 2, 4, ..., nmax.
 std::vector<float2> twiddle_table(int nmax) {
   std::vector<float2> t(2 * (size_t)nmax);
@@ -157,7 +161,7 @@ std::vector<float2> twiddle_table(int nmax) {
   return t;
 }
 
-}  // namespace
+}  // namespace lcsm
 
 struct lcsm_ctx {
   Shape s;
@@ -219,7 +223,7 @@ hipError_t launch_tile(lcsm_ctx* c, int i, int U, int dst_len) {
 // Filter spectra of every FFT tile size (the cached kernel DFTs).
 hipError_t init_spectra(lcsm_ctx* c) {
   if (!c->ly.nmax) return hipSuccess;
-  std::vector<float2> t = twiddle_table(c->ly.nmax);
+  std::vector<float2> t = lcsm::twiddle_table(c->ly.nmax);
   hipError_t e = hipMemcpyAsync(c->tw, t.data(), t.size() * sizeof(float2), hipMemcpyHostToDevice,
                                 c->stream);
   for (int q = 0; e == hipSuccess && q < kMaxLevels && (1 << q) <= c->s.L - 1; ++q) {

@@ -20,37 +20,81 @@
 #include <new>
 
 #include "lcsm_dd.h"
+#include "lcsm_fft_core.h"
 #include "lcsm_internal.h"
 
 namespace lcsm {
 namespace {
 
+using fft::cadd;
+using fft::cmul;
+using fft::conjf2;
+using fft::csub;
+
 constexpr int kThreads = 256;
 constexpr int kDdJ = 16;            // outputs per thread of the direct tile
 constexpr int kDdDefaultDirectMaxU = 32;
+constexpr int kDdFusedMaxU = 8;      // tiles fused with the red cell
 
-// Red cells of all layers at position t (grid: column blocks x M).
-__global__ __launch_bounds__(kThreads) void k_dd_red(const float* __restrict__ y,
-                                                     const float* __restrict__ rho,
-                                                     float* __restrict__ z, float* __restrict__ Y,
-                                                     float* __restrict__ R, int L, int BD, int t) {
+// The tile of side U of step t for one column, in one thread.
+template <int U>
+__device__ __forceinline__ void dd_tile_in_thread(float* ycol, const float* rcol, size_t rs, int L,
+                                                  int t) {
+  const bool square = t + 1 == 2 * U;
+  const int lo = square ? U : t - U + 1;
+  const int d0 = square ? 2 * U : t + 1;
+  if (d0 >= L) return;
+  float yf[U], rf[U], yr[U], rr[U];
+#pragma unroll
+  for (int k = 0; k < U; ++k) {
+    yf[k] = ycol[(size_t)(U + k) * rs];
+    rf[k] = rcol[(size_t)(U + k) * rs];
+    yr[k] = ycol[(size_t)(lo + k) * rs];
+    rr[k] = rcol[(size_t)(lo + k) * rs];
+  }
+#pragma unroll
+  for (int j = 0; j < 2 * U - 1; ++j) {
+    if (d0 + j < L) {
+      float sum = 0.f;
+#pragma unroll
+      for (int k = 0; k < U; ++k) {
+        if (j - k >= 0 && j - k < U) {
+          sum = fmaf(yf[k], rr[j - k], sum);
+          if (!square) sum = fmaf(rf[k], yr[j - k], sum);
+        }
+      }
+      ycol[(size_t)(d0 + j) * rs] += sum;
+    }
+  }
+}
+
+// Red cell at position t fused with the tiles of every U <= UMAX of step t
+// (U | t+1, 2U <= t+1), one thread per column walking them in increasing U:
+// the blocks (at most 4 x 8 values) are held in registers and every output
+// of a tile is summed in the thread.  Rows written by one tile are not read
+// by a later one (tiles read rows <= t and write rows > t), and the thread's
+// own store of y_t, rho_t is what its tiles read back.
+template <int UMAX>
+__global__ __launch_bounds__(kThreads) void k_dd_step(const float* __restrict__ y,
+                                                      const float* __restrict__ rho,
+                                                      float* __restrict__ z, float* __restrict__ Y,
+                                                      float* __restrict__ R, int L, int BD, int t) {
   const int c = (int)blockIdx.x * kThreads + (int)threadIdx.x;
   if (c >= BD) return;
   const int m = (int)blockIdx.y;
   const size_t e = (size_t)m * BD + c;
+  const size_t rs = (size_t)BD;
   float* ycol = Y + (size_t)m * L * BD + c;
   float* rcol = R + (size_t)m * L * BD + c;
   const float yt = y[e], rt = rho[e];
-  const float acc = ycol[(size_t)t * BD];
-  float zt;
-  if (t == 0) {
-    zt = fmaf(yt, rt, acc);
-  } else {
-    zt = fmaf(yt, rcol[0], fmaf(ycol[0], rt, acc));
-  }
-  z[e] = zt;
-  ycol[(size_t)t * BD] = yt;
-  rcol[(size_t)t * BD] = rt;
+  const float acc = ycol[(size_t)t * rs];
+  z[e] = t == 0 ? fmaf(yt, rt, acc) : fmaf(yt, rcol[0], fmaf(ycol[0], rt, acc));
+  ycol[(size_t)t * rs] = yt;
+  rcol[(size_t)t * rs] = rt;
+  if constexpr (UMAX >= 1) dd_tile_in_thread<1>(ycol, rcol, rs, L, t);
+  if constexpr (UMAX >= 2) dd_tile_in_thread<2>(ycol, rcol, rs, L, t);
+  if constexpr (UMAX >= 4) dd_tile_in_thread<4>(ycol, rcol, rs, L, t);
+  if constexpr (UMAX >= 8) dd_tile_in_thread<8>(ycol, rcol, rs, L, t);
 }
 
 // Direct parallelogram tile of side U for all layers: thread = (column c,
@@ -108,6 +152,169 @@ __global__ __launch_bounds__(kThreads) void k_dd_direct(float* __restrict__ Y,
     if (j0 + jj < dlen) dst[(size_t)jj * rs] += acc[jj];
 }
 
+// ---- FFT parallelogram tiles (2U-point, one LDS-resident pass)
+//
+// Each real column carries its two blocks packed as one complex signal,
+// x = y + i rho (zero-padded to N = 2U).  From X = DFT(x) the spectra of the
+// parts follow by conjugate symmetry: Y[k] = (X[k] + conj X[N-k]) / 2,
+// Rho[k] = (X[k] - conj X[N-k]) / 2i.  The product spectrum of a column is
+// P = YF RhoR + RhoF YR (rectangle; the fixed block F, the recent block R) or
+// YF RhoF (square), Hermitian since the output is real, so two columns a, b
+// share one inverse: Q = Pa + i Pb, out_a + i out_b = IDFT(Q).  The 2U-1
+// outputs of the untruncated convolution are below N, so nothing wraps.
+// Per column: 2 forward transforms (1 for the square) and half an inverse.
+//
+// Launch shape: CW real columns per workgroup (the forward transforms run on
+// CW complex columns, the inverse on CW/2), the LDS buffer N x CW complex;
+// NT threads.
+template <int N>
+struct DdCfg {
+  static constexpr int CW = N <= 2048 ? 8 : (N <= 4096 ? 4 : 2);
+  // at most 512 threads: the spectra held across the second transform need
+  // more than the 128 registers a 1024-thread workgroup leaves
+  static constexpr int NT = N <= 128 ? 64 : (N <= 256 ? 128 : (N <= 512 ? 256 : 512));
+  static constexpr bool TWL = (size_t)N * 8 * (CW + 1) <= 163840;
+  static constexpr bool TWH = !TWL && (size_t)N * 8 * CW + (size_t)N * 4 <= 163840;
+  static constexpr int TWN = TWL ? N : (TWH ? N / 2 : 1);
+};
+
+template <int N>
+using DdTw = typename std::conditional<
+    DdCfg<N>::TWL, fft::TwLds<N>,
+    typename std::conditional<DdCfg<N>::TWH, fft::TwLdsHalf<N>, fft::TwGlobal>::type>::type;
+
+template <int N>
+__device__ __forceinline__ DdTw<N> dd_make_tw(float2* lds, const float2* __restrict__ tw) {
+  if constexpr (DdCfg<N>::TWL) {
+    fft::load_twiddles<N, DdCfg<N>::NT>(lds, tw);
+    return fft::TwLds<N>{lds};
+  } else if constexpr (DdCfg<N>::TWH) {
+    fft::load_twiddles<N, DdCfg<N>::NT, N / 2>(lds, tw);
+    return fft::TwLdsHalf<N>{lds};
+  } else {
+    return fft::TwGlobal{tw};
+  }
+}
+
+// The two packed parts of X at bin k: (first, second) spectra.
+__device__ __forceinline__ void unpack(float2 xk, float2 xnk, float2& a, float2& b) {
+  const float2 c = conjf2(xnk);
+  a = make_float2(0.5f * (xk.x + c.x), 0.5f * (xk.y + c.y));
+  const float2 d = csub(xk, c);  // 2i * b
+  b = make_float2(0.5f * d.y, -0.5f * d.x);
+}
+
+template <int N, bool SQ>
+__global__ __launch_bounds__(DdCfg<N>::NT) void k_dd_fft(float* __restrict__ Y,
+                                                        const float* __restrict__ R,
+                                                        const float2* __restrict__ tw, int L,
+                                                        int BD, int lo, int d0, int dlen,
+                                                        int ppl) {
+  constexpr int CW = DdCfg<N>::CW, NT = DdCfg<N>::NT, U = N / 2, HW = CW / 2;
+  __shared__ float2 buf[N * CW];
+  __shared__ float2 twl[DdCfg<N>::TWN];
+  const auto twz = dd_make_tw<N>(twl, tw);
+  const int q = fft::xcd_logical((int)blockIdx.x, (int)gridDim.x);
+  const int m = q / ppl;
+  const int c0 = (q - m * ppl) * CW;
+  const size_t rs = (size_t)BD;
+  float* Ym = Y + (size_t)m * L * BD;
+  const float* Rm = R + (size_t)m * L * BD;
+
+  // spectra of the fixed blocks [U, 2U) of the unit (bin kk <= U, column col)
+  constexpr int PUN = (U + 1) * CW;
+  constexpr int PU = (PUN + NT - 1) / NT;
+  fft::forward_from_global<N, CW, CW, NT, true>(buf, twz, [&](int row, int col) {
+    const int c = c0 + col;
+    if (c >= BD) return make_float2(0.f, 0.f);
+    const size_t e = (size_t)(U + row) * rs + c;
+    return make_float2(Ym[e], Rm[e]);
+  });
+  float2 yf[PU], rf[PU];
+#pragma unroll
+  for (int a = 0; a < PU; ++a) {
+    const int u = (int)threadIdx.x + a * NT;
+    yf[a] = rf[a] = make_float2(0.f, 0.f);
+    if (PUN % NT == 0 || u < PUN) {
+      const int kk = u / CW, col = u - kk * CW;
+      const int nk = (N - kk) & (N - 1);
+      unpack(buf[kk * CW + col], buf[nk * CW + col], yf[a], rf[a]);
+    }
+  }
+  float2 p[PU];  // product spectrum of the unit's column, scaled by 1/N
+  constexpr float inv_n = 1.0f / (float)N;
+  if constexpr (SQ) {
+#pragma unroll
+    for (int a = 0; a < PU; ++a) {
+      const float2 v = cmul(yf[a], rf[a]);
+      p[a] = make_float2(v.x * inv_n, v.y * inv_n);
+    }
+  } else {
+    __syncthreads();  // every unit has read the fixed spectra
+    fft::forward_from_global<N, CW, CW, NT, true>(buf, twz, [&](int row, int col) {
+      const int c = c0 + col;
+      if (c >= BD) return make_float2(0.f, 0.f);
+      const size_t e = (size_t)(lo + row) * rs + c;
+      return make_float2(Ym[e], Rm[e]);
+    });
+#pragma unroll
+    for (int a = 0; a < PU; ++a) {
+      const int u = (int)threadIdx.x + a * NT;
+      p[a] = make_float2(0.f, 0.f);
+      if (PUN % NT == 0 || u < PUN) {
+        const int kk = u / CW, col = u - kk * CW;
+        const int nk = (N - kk) & (N - 1);
+        float2 yr, rr;
+        unpack(buf[kk * CW + col], buf[nk * CW + col], yr, rr);
+        const float2 v = cadd(cmul(yf[a], rr), cmul(rf[a], yr));
+        p[a] = make_float2(v.x * inv_n, v.y * inv_n);
+      }
+    }
+  }
+  // half spectra P[kk][col], kk <= U, into LDS; then the packed inverse
+  // input Q of every column pair over the whole buffer (after a barrier:
+  // the two layouts overlap)
+  __syncthreads();
+#pragma unroll
+  for (int a = 0; a < PU; ++a) {
+    const int u = (int)threadIdx.x + a * NT;
+    if (PUN % NT == 0 || u < PUN) buf[u] = p[a];  // u = kk * CW + col
+  }
+  __syncthreads();
+  constexpr int QUN = (U + 1) * HW;
+  constexpr int QU = (QUN + NT - 1) / NT;
+  float2 qk[QU], qnk[QU];
+#pragma unroll
+  for (int a = 0; a < QU; ++a) {
+    const int u = (int)threadIdx.x + a * NT;
+    if (QUN % NT == 0 || u < QUN) {
+      const int kk = u / HW, pr = u - kk * HW;
+      const float2 pa = buf[kk * CW + 2 * pr], pb = buf[kk * CW + 2 * pr + 1];
+      qk[a] = make_float2(pa.x - pb.y, pa.y + pb.x);     // Pa + i Pb
+      qnk[a] = make_float2(pa.x + pb.y, pb.x - pa.y);    // conj Pa + i conj Pb
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int a = 0; a < QU; ++a) {
+    const int u = (int)threadIdx.x + a * NT;
+    if (QUN % NT == 0 || u < QUN) {
+      const int kk = u / HW, pr = u - kk * HW;
+      const int nk = (N - kk) & (N - 1);
+      buf[kk * HW + pr] = qk[a];
+      if (nk != kk) buf[nk * HW + pr] = qnk[a];
+    }
+  }
+  __syncthreads();
+  fft::inverse_to_global<N, HW, HW, NT, false>(buf, twz, [&](int row, int pr, float2 v) {
+    if (row >= dlen) return;
+    const int c = c0 + 2 * pr;
+    float* dst = Ym + (size_t)(d0 + row) * rs;
+    if (c < BD) dst[c] += v.x;
+    if (c + 1 < BD) dst[c + 1] += v.y;
+  });
+}
+
 }  // namespace
 }  // namespace lcsm
 
@@ -160,9 +367,18 @@ int resolve(int M, int B, int D, int L, const lcsm_options* o, DdOptions* r) {
   return LCSM_OK;
 }
 
-size_t dd_bytes(int M, int B, int D, int L) {
-  const size_t state = align_up(sizeof(float) * (size_t)M * L * B * D);
-  return 2 * state;
+// Largest FFT length of a context (0: every tile direct).
+int fft_nmax(int L, const DdOptions& o) {
+  const int Umax = largest_u(L);
+  return Umax > o.direct_max_u ? 2 * Umax : 0;
+}
+
+size_t state_bytes(int M, int B, int D, int L) {
+  return align_up(sizeof(float) * (size_t)M * L * B * D);
+}
+
+size_t dd_bytes(int M, int B, int D, int L, const DdOptions& o) {
+  return 2 * state_bytes(M, B, D, L) + align_up(sizeof(float2) * 2 * (size_t)fft_nmax(L, o));
 }
 
 }  // namespace
@@ -175,6 +391,7 @@ struct lcsm_dd {
   char* ws;
   float* Y;
   float* R;
+  float2* tw;  // twiddles of the FFT tiles (nullptr: every tile direct)
   int t;
   bool faulted;
   char msg[256];
@@ -192,8 +409,40 @@ int dd_fail(lcsm_dd* c, int code, const char* what, hipError_t e) {
   return code;
 }
 
-// One tile of side U for all layers.
+template <bool SQ>
+hipError_t dd_fft(lcsm_dd* c, int N, int lo, int d0, int dlen) {
+#define LCSM_CASE(NN)                                                                             \
+  case NN: {                                                                                      \
+    constexpr int CW = lcsm::DdCfg<NN>::CW;                                                       \
+    const int ppl = (c->BD + CW - 1) / CW;                                                        \
+    hipLaunchKernelGGL((lcsm::k_dd_fft<NN, SQ>), dim3((unsigned)(ppl * c->M)),                    \
+                       dim3(lcsm::DdCfg<NN>::NT), 0, c->stream, c->Y, c->R, c->tw, c->L, c->BD,   \
+                       lo, d0, dlen, ppl);                                                        \
+    return hipGetLastError();                                                                     \
+  }
+  switch (N) {
+    LCSM_CASE(4)
+    LCSM_CASE(8)
+    LCSM_CASE(16)
+    LCSM_CASE(32)
+    LCSM_CASE(64)
+    LCSM_CASE(128)
+    LCSM_CASE(256)
+    LCSM_CASE(512)
+    LCSM_CASE(1024)
+    LCSM_CASE(2048)
+    LCSM_CASE(4096)
+    LCSM_CASE(8192)
+  }
+#undef LCSM_CASE
+  return hipErrorInvalidValue;
+}
+
+// One tile of side U for all layers: direct up to the crossover, else the
+// 2U-point FFT tile.
 hipError_t dd_tile(lcsm_dd* c, bool square, int U, int lo, int d0, int dlen) {
+  if (U > c->opt.direct_max_u)
+    return square ? dd_fft<true>(c, 2 * U, lo, d0, dlen) : dd_fft<false>(c, 2 * U, lo, d0, dlen);
   const dim3 grid((unsigned)((c->BD + lcsm::kThreads - 1) / lcsm::kThreads),
                   (unsigned)((dlen + lcsm::kDdJ - 1) / lcsm::kDdJ), (unsigned)c->M);
   if (square)
@@ -214,7 +463,7 @@ int lcsm_dd_workspace_bytes(int M, int B, int D, int L, const lcsm_options* opt,
   DdOptions o;
   int r = resolve(M, B, D, L, opt, &o);
   if (r) return r;
-  *bytes = dd_bytes(M, B, D, L);
+  *bytes = dd_bytes(M, B, D, L, o);
   return LCSM_OK;
 }
 
@@ -225,7 +474,7 @@ int lcsm_dd_init(lcsm_dd** out, int M, int B, int D, int L, void* stream, void* 
   DdOptions o;
   int r = resolve(M, B, D, L, opt, &o);
   if (r) return r;
-  const size_t need = dd_bytes(M, B, D, L);
+  const size_t need = dd_bytes(M, B, D, L, o);
   if (workspace) {
     if (workspace_bytes < need) return LCSM_ENOMEM;
     if (((uintptr_t)workspace) % kAlign) return LCSM_EINVAL;
@@ -253,9 +502,20 @@ int lcsm_dd_init(lcsm_dd** out, int M, int B, int D, int L, void* stream, void* 
     c->ws = (char*)p;
     c->owns_ws = true;
   }
+  const size_t sb = state_bytes(M, B, D, L);
   c->Y = (float*)c->ws;
-  c->R = (float*)(c->ws + need / 2);
-  if (lcsm::launch_zero((float*)c->ws, need / sizeof(float), c->stream) != hipSuccess) {
+  c->R = (float*)(c->ws + sb);
+  const int nmax = fft_nmax(L, o);
+  c->tw = nmax ? (float2*)(c->ws + 2 * sb) : nullptr;
+  hipError_t e = lcsm::launch_zero((float*)c->ws, 2 * sb / sizeof(float), c->stream);
+  if (e == hipSuccess && nmax) {
+    std::vector<float2> t = lcsm::twiddle_table(nmax);
+    e = hipMemcpyAsync(c->tw, t.data(), t.size() * sizeof(float2), hipMemcpyHostToDevice,
+                       c->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(c->stream);  // the host table must outlive the copy
+  }
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
     if (c->owns_ws) (void)hipFree(c->ws);
     delete c;
     return LCSM_EDEVICE;
@@ -273,15 +533,29 @@ int lcsm_dd_step(lcsm_dd* c, const float* y_t, const float* rho_t, float* z_t) {
   if (c->faulted) return LCSM_ESTATE;
   if (c->t >= c->L) return LCSM_EDONE;
   const int t = c->t;
-  hipLaunchKernelGGL(lcsm::k_dd_red,
-                     dim3((unsigned)((c->BD + lcsm::kThreads - 1) / lcsm::kThreads), (unsigned)c->M),
-                     dim3(lcsm::kThreads), 0, c->stream, y_t, rho_t, z_t, c->Y, c->R, c->L, c->BD,
-                     t);
+  // every power of two U dividing t+1 with 2U <= t+1: those up to the fused
+  // limit (and the direct limit) go with the red cell, the rest one launch
+  // per U
+  const int i1 = t + 1;
+  const int fmax = c->opt.direct_max_u < lcsm::kDdFusedMaxU ? c->opt.direct_max_u
+                                                            : lcsm::kDdFusedMaxU;
+  int uf = 0;
+  for (int U = 1; U <= fmax && i1 % U == 0 && 2 * U <= i1; U *= 2) uf = U;
+  const dim3 rgrid((unsigned)((c->BD + lcsm::kThreads - 1) / lcsm::kThreads), (unsigned)c->M);
+#define LCSM_DD_STEP(UU)                                                                        \
+  hipLaunchKernelGGL((lcsm::k_dd_step<UU>), rgrid, dim3(lcsm::kThreads), 0, c->stream, y_t,    \
+                     rho_t, z_t, c->Y, c->R, c->L, c->BD, t)
+  switch (uf) {
+    case 0: LCSM_DD_STEP(0); break;
+    case 1: LCSM_DD_STEP(1); break;
+    case 2: LCSM_DD_STEP(2); break;
+    case 4: LCSM_DD_STEP(4); break;
+    default: LCSM_DD_STEP(8); break;
+  }
+#undef LCSM_DD_STEP
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return dd_fail(c, LCSM_EDEVICE, "red-cell launch", e);
-  // every power of two U dividing t+1 with 2U <= t+1
-  const int i1 = t + 1;
-  for (int U = 1; i1 % U == 0 && 2 * U <= i1; U *= 2) {
+  for (int U = 2 * uf > 0 ? 2 * uf : 1; i1 % U == 0 && 2 * U <= i1; U *= 2) {
     const bool square = i1 == 2 * U;
     const int lo = square ? U : t - U + 1;
     const int d0 = square ? 2 * U : t + 1;
@@ -296,7 +570,7 @@ int lcsm_dd_step(lcsm_dd* c, const float* y_t, const float* rho_t, float* z_t) {
 
 int lcsm_dd_reset(lcsm_dd* c) {
   if (!c) return LCSM_EINVAL;
-  const size_t n = dd_bytes(c->M, c->B, c->D, c->L) / sizeof(float);
+  const size_t n = 2 * state_bytes(c->M, c->B, c->D, c->L) / sizeof(float);
   hipError_t e = lcsm::launch_zero((float*)c->ws, n, c->stream);
   if (e != hipSuccess) return dd_fail(c, LCSM_EDEVICE, "reset", e);
   c->t = 0;

@@ -5,9 +5,15 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <vector>
+
 #include "lcsm.h"
 
 namespace lcsm {
+
+// Host twiddle table of the FFT kernels: tw[n + m] = exp(-2 pi i m / n) for
+// n = 1, 2, 4, ..., nmax and m < n (fp64 evaluation rounded to fp32).
+std::vector<float2> twiddle_table(int nmax);
 
 // Shape of one context.  State rows are indexed [m][t][b*D + d] (time-major:
 // one position of one layer is a contiguous B*D slab), filters [m][k][d].

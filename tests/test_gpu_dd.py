@@ -108,3 +108,35 @@ def test_dd_errors():
     with pytest.raises(lcsm.LcsmError) as ex:
         ctx.step(y[0], rho[0])
     assert ex.value.code == lcsm.LCSM_EDONE
+
+
+@pytest.mark.parametrize("name", ["m1b8d768l8k", "m32b16d2048l16k"])
+def test_dd_workload_sizes_sampled_columns(name):
+    """The bench workload (largest tile 2U = 4096) and the largest length the
+    single-pass tiles allow (L = 16384, 2U = 8192) at full width, default
+    options; the columns are independent, so sampled ones are checked
+    against the definition over all L positions."""
+    from oracle.dd import product_naive
+    w = datagen.WORKLOADS[name]
+    say(f"[dd workload] {name}")
+    ctx = lcsm_mod().Dd(w.M, w.B, w.D, w.L)
+    cols = datagen.sample_columns(w, 8, seed=91)
+    cm, cb, cd = (torch.as_tensor(cols[:, k], device=dev()) for k in range(3))
+    chunk = 256 if w.M * w.B * w.D <= (1 << 17) else 32
+    z = torch.empty((chunk, w.M, w.B, w.D), dtype=torch.float32, device=dev())
+    got, ys, rs = [], [], []
+    for t0 in range(0, w.L, chunk):
+        t1 = min(w.L, t0 + chunk)
+        y = datagen.y_torch(w, dev(), t0, t1)
+        rho = datagen.rho_torch(w, dev(), t0, t1)
+        for k in range(t1 - t0):
+            ctx.step(y[k], rho[k], z[k])
+        got.append(z[: t1 - t0, cm, cb, cd].cpu())
+        ys.append(y[:, cm, cb, cd].cpu())
+        rs.append(rho[:, cm, cb, cd].cpu())
+    torch.cuda.synchronize()
+    zg = torch.cat(got).numpy()
+    zr = product_naive(torch.cat(ys).numpy(), torch.cat(rs).numpy())
+    err = rel_err(zg, zr)
+    say(f"  sampled rel err {err:.3e}")
+    assert err <= TOL
