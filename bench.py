@@ -65,6 +65,9 @@ def parse():
     p.add_argument("--direct-max-u", type=int, default=0, help="0 = library default")
     p.add_argument("--lds-fft-max-n", type=int, default=0, help="0 = library default")
     p.add_argument("--scratch-mib", type=int, default=0, help="0 = library default")
+    p.add_argument("--col-fft-min-n", type=int, default=0,
+                   help="smallest 2U of the column-chunk FFT tiles (0 = library default, "
+                        "above 16384 = off)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work, about")
     p.add_argument("--no-kernel-pass", action="store_true")
@@ -153,7 +156,50 @@ def kernel_key(name):
     m = re.search(r"k_fft_tile<(\d+), (true|false)(, (true|false))*>", name)
     if m:
         return ("fft_lds", int(m.group(1)) // 2)
+    # the column-chunk tile: two transposes around the transform, per chunk
+    m = re.search(r"k_fft_coltile<(\d+)>", name)
+    if m:
+        return ("fft_col", int(m.group(1)) // 2)
+    if "k_rows_to_cols" in name or "k_cols_to_rows" in name:
+        return ("fft_col", None)
     return None
+
+
+def tile_bytes(rows_c):
+    """Counter bytes per (kernel, U) key and dispatch from one counter's rows
+    in dispatch order.  A column-chunk tile is one launch of the per-launch
+    pass made of several dispatches (the red cell before it, then transpose,
+    transform, transpose per chunk): they are summed into one entry per tile."""
+    import collections
+    per = collections.defaultdict(list)
+    rows_c = sorted(rows_c, key=lambda r: int(r["Dispatch_Id"]))
+    tile, red = None, None  # open column tile [U, bytes]; last red-cell dispatch's bytes
+    for r in rows_c:
+        key = kernel_key(r["Kernel_Name"])
+        v = 1024.0 * float(r["Counter_Value"])
+        if key and key[0] == "fft_col":
+            if tile is None:
+                tile = [None, red or 0.0]
+                red = None
+            tile[1] += v
+            if key[1] is not None:
+                tile[0] = key[1]
+            continue
+        if tile is not None:
+            per[("fft_col", tile[0])].append(tile[1])
+            tile = None
+        if red is not None:
+            per[("red", 0)].append(red)
+            red = None
+        if key == ("red", 0):
+            red = v
+        elif key:
+            per[key].append(v)
+    if tile is not None:
+        per[("fft_col", tile[0])].append(tile[1])
+    if red is not None:
+        per[("red", 0)].append(red)
+    return per
 
 
 def traffic_from(args):
@@ -175,10 +221,8 @@ def traffic_from(args):
         scale[c] = known / (sum(vals) / len(vals))
     per = collections.defaultdict(lambda: {"FETCH_SIZE": [], "WRITE_SIZE": []})
     for c in ("FETCH_SIZE", "WRITE_SIZE"):
-        for r in rows(f"pmc_bench_{c}"):
-            key = kernel_key(r["Kernel_Name"])
-            if key:
-                per[key][c].append(1024.0 * float(r["Counter_Value"]) * scale[c])
+        for key, vals in tile_bytes(rows(f"pmc_bench_{c}")).items():
+            per[key][c].extend(v * scale[c] for v in vals)
     kernels = {}
     for (name, U), v in sorted(per.items(), key=lambda kv: (kv[0][1], kv[0][0])):
         if not v["FETCH_SIZE"] or not v["WRITE_SIZE"]:
@@ -252,7 +296,8 @@ def main():
     torch.cuda.set_device(dev)
     opts = {k: v for k, v in (("direct_max_u", args.direct_max_u),
                               ("lds_fft_max_n", args.lds_fft_max_n),
-                              ("scratch_mib", args.scratch_mib)) if v} or None
+                              ("scratch_mib", args.scratch_mib),
+                              ("col_fft_min_n", args.col_fft_min_n)) if v} or None
 
     print(f"# workload {w.name}: M={w.M} B={w.B} D={w.D} L={w.L} graph={args.graph}",
           file=sys.stderr, flush=True)
@@ -340,7 +385,8 @@ def counter_run(args, w, torch, datagen, lcsm):
     torch.cuda.set_device(dev)
     opts = {k: v for k, v in (("direct_max_u", args.direct_max_u),
                               ("lds_fft_max_n", args.lds_fft_max_n),
-                              ("scratch_mib", args.scratch_mib)) if v} or None
+                              ("scratch_mib", args.scratch_mib),
+                              ("col_fft_min_n", args.col_fft_min_n)) if v} or None
     P = min(args.positions, w.L)
     filters = datagen.filters_torch(w, dev)
     R = min(RING, w.L)

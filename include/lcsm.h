@@ -49,6 +49,7 @@ extern "C" {
 #define LCSM_TILE_DIRECT 1  /* direct Toeplitz kernel */
 #define LCSM_TILE_FFT 2     /* 2U-point FFT, one LDS-resident pass */
 #define LCSM_TILE_FFT_HBM 3 /* 2U-point FFT, multi-pass through HBM scratch */
+#define LCSM_TILE_FFT_COL 4 /* 2U-point FFT on column chunks transposed into the scratch */
 
 /* Tuning options.  A NULL pointer, or a field left at 0, selects the
  * library default. */
@@ -63,7 +64,10 @@ typedef struct lcsm_options {
   int half_state;    /* 1: keep only T state rows per layer instead of L, T the largest power
                         of two below L (App. C, "Storing Only Half of the Activations"); see
                         the note below.  0 (default): L rows */
-  int reserved[4];   /* must be zero */
+  int col_fft_min_n; /* FFT tiles with col_fft_min_n <= 2U <= 16384 transpose chunks of their
+                        columns into the scratch and transform each column as one contiguous
+                        run (power of two >= 4; above 16384, the default: never) */
+  int reserved[3];   /* must be zero */
 } lcsm_options;
 
 /* Half-state storage (lcsm_options.half_state = 1).  After position T-1 no

@@ -22,7 +22,12 @@ constexpr size_t kAlign = 256;
 constexpr int kAutoDirectMaxU = 32;
 constexpr int kAutoDirectU64MaxCols = 1 << 17;
 constexpr int kDefaultLdsFftMaxN = 8192;   // 2U <= 8192: one LDS pass
-constexpr int kDefaultScratchMib = 512;    // multi-pass FFT scratch cap
+constexpr int kDefaultScratchMib = 512;    // multi-pass and column-tile FFT scratch cap
+// The column-chunk FFT tiles are off unless asked for: on MI355X they measured
+// slower than the row-panel and three-pass tiles at every size (their
+// transform kernel, one 2U-point column per workgroup, runs at about 0.8
+// TB/s), although their transposes move the rows at 3.5-4 TB/s.
+constexpr int kDefaultColFftMinN = 2 * lcsm::kMaxColFftN;
 constexpr int kMaxL = 1 << 19;             // FFT lengths up to 2^19 are built
 constexpr int kMaxLevels = 20;
 
@@ -37,6 +42,7 @@ struct Options {
   int lds_fft_max_n;
   int scratch_mib;
   int half_state;
+  int col_min_n;
 };
 
 int resolve_options(const lcsm_options* o, Options* r) {
@@ -44,9 +50,14 @@ int resolve_options(const lcsm_options* o, Options* r) {
   r->lds_fft_max_n = kDefaultLdsFftMaxN;
   r->scratch_mib = kDefaultScratchMib;
   r->half_state = 0;
+  r->col_min_n = kDefaultColFftMinN;
   if (!o) return LCSM_OK;
-  for (int k = 0; k < 4; ++k)
+  for (int k = 0; k < 3; ++k)
     if (o->reserved[k] != 0) return LCSM_EINVAL;
+  if (o->col_fft_min_n) {
+    if (!is_pow2(o->col_fft_min_n) || o->col_fft_min_n < 4) return LCSM_EINVAL;
+    r->col_min_n = o->col_fft_min_n;
+  }
   if (o->direct_max_u < 0 || o->lds_fft_max_n < 0 || o->scratch_mib < 0) return LCSM_EINVAL;
   if (o->half_state != 0 && o->half_state != 1) return LCSM_EINVAL;
   r->half_state = o->half_state;
@@ -79,6 +90,7 @@ int tile_kind(const Options& o, const Shape& s, int U) {
   if (dmax == 0)
     dmax = ((long long)s.M * s.BD <= kAutoDirectU64MaxCols) ? 2 * kAutoDirectMaxU : kAutoDirectMaxU;
   if (U <= dmax) return LCSM_TILE_DIRECT;
+  if (2 * U >= o.col_min_n && 2 * U <= lcsm::kMaxColFftN) return LCSM_TILE_FFT_COL;
   return (2 * U <= o.lds_fft_max_n) ? LCSM_TILE_FFT : LCSM_TILE_FFT_HBM;
 }
 
@@ -121,7 +133,7 @@ Layout layout_for(const Shape& s, const Options& o) {
     const int kind = tile_kind(o, s, U);
     if (kind == LCSM_TILE_DIRECT) continue;
     ly.nmax = 2 * U;
-    if (kind == LCSM_TILE_FFT_HBM) multipass = true;
+    if (kind == LCSM_TILE_FFT_HBM || kind == LCSM_TILE_FFT_COL) multipass = true;
     ly.H[q] = off;
     off = align_up(off + sizeof(float2) * (size_t)s.M * (U + 1) * s.D);
   }
@@ -130,7 +142,8 @@ Layout layout_for(const Shape& s, const Options& o) {
     off = align_up(off + sizeof(float2) * 2 * (size_t)ly.nmax);
   }
   if (multipass) {
-    // one chunk: N complex values per complex column
+    // one chunk: N complex values per complex column (column tiles: U
+    // floats per real column, the same bytes)
     const size_t per_col = sizeof(float2) * (size_t)ly.nmax;
     const size_t cols = ((size_t)s.M * ((s.BD + 1) / 2) + 15) / 16 * 16;
     size_t want = (size_t)o.scratch_mib << 20;
@@ -196,6 +209,25 @@ int fail(lcsm_ctx* c, int code, const char* what, hipError_t e) {
   return code;
 }
 
+// Spectra of tile size U, in the layout of the level's tile kernel
+// (channel-major for the column tiles), of the filter delayed by shift rows.
+hipError_t spectra(lcsm_ctx* c, int U, int shift) {
+  const int q = __builtin_ctz((unsigned)U);
+  return lcsm::launch_spectra(c->Hf, (float2*)(c->ws + c->ly.H[q]), c->tw, c->s, U, shift,
+                              c->opt.lds_fft_max_n, c->scratch, c->ly.scratch_bytes, c->stream,
+                              tile_kind(c->opt, c->s, U) == LCSM_TILE_FFT_COL);
+}
+
+// FFT tile of side U for all layers with the level's kernel.
+hipError_t fft_tile(lcsm_ctx* c, float* S, int i, int U, int dst_len, bool in_place) {
+  const float2* H = (const float2*)(c->ws + c->ly.H[__builtin_ctz((unsigned)U)]);
+  if (tile_kind(c->opt, c->s, U) == LCSM_TILE_FFT_COL)
+    return lcsm::launch_fft_col_tile(S, H, c->tw, c->s, i, U, dst_len, c->scratch,
+                                     c->ly.scratch_bytes, c->stream, in_place);
+  return lcsm::launch_fft_tile(S, H, c->tw, c->s, i, U, dst_len, c->opt.lds_fft_max_n, c->scratch,
+                               c->ly.scratch_bytes, c->stream, in_place);
+}
+
 // State pointer of the phase that position p belongs to: the array itself
 // before the half-state swap, the array moved back by T rows from position T
 // on (position p at row p - T; every row touched then is >= T).  Integer
@@ -213,11 +245,7 @@ hipError_t launch_tile(lcsm_ctx* c, int i, int U, int dst_len) {
   const bool swap = c->T && i == c->T;
   if (kind == LCSM_TILE_DIRECT)
     return lcsm::launch_direct_tile(state_base(c, i), c->Hf, c->s, i, U, dst_len, c->stream);
-  const int q = __builtin_ctz((unsigned)U);
-  const float2* H = (const float2*)(c->ws + c->ly.H[q]);
-  return lcsm::launch_fft_tile(swap ? c->S : state_base(c, i), H, c->tw, c->s, i, U, dst_len,
-                               c->opt.lds_fft_max_n, c->scratch, c->ly.scratch_bytes, c->stream,
-                               swap);
+  return fft_tile(c, swap ? c->S : state_base(c, i), i, U, dst_len, swap);
 }
 
 // Filter spectra of every FFT tile size (the cached kernel DFTs).
@@ -229,8 +257,7 @@ hipError_t init_spectra(lcsm_ctx* c) {
   for (int q = 0; e == hipSuccess && q < kMaxLevels && (1 << q) <= c->s.L - 1; ++q) {
     const int U = 1 << q;
     if (tile_kind(c->opt, c->s, U) == LCSM_TILE_DIRECT) continue;
-    e = lcsm::launch_spectra(c->Hf, (float2*)(c->ws + c->ly.H[q]), c->tw, c->s, U, 0,
-                             c->opt.lds_fft_max_n, c->scratch, c->ly.scratch_bytes, c->stream);
+    e = spectra(c, U, 0);
   }
   // the host table must outlive the copy
   if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
@@ -447,22 +474,15 @@ int lcsm_prefill(lcsm_ctx* c, int P, const float* y, size_t y_stride, float* z, 
   // a prompt of a direct tile size: P ordinary steps
   if (tile_kind(c->opt, s, P) == LCSM_TILE_DIRECT) return lcsm_run(c, P, y, y_stride, z, z_stride);
   // P is an FFT tile size, so its cached spectra and the twiddles for 2P exist
-  float2* H = (float2*)(c->ws + c->ly.H[__builtin_ctz((unsigned)P)]);
   // the prompt into state rows [0, P)
   hipError_t e = lcsm::launch_rows_in(y, y_stride, c->S, s, P, c->stream);
   // the tile i = P with the filter delayed by P rows puts, in rows [P, 2P),
   // sum_{k<P} y[k] h[j - k] = z_j for j < P: the prompt's own outputs
-  if (e == hipSuccess)
-    e = lcsm::launch_spectra(c->Hf, H, c->tw, s, P, P, c->opt.lds_fft_max_n, c->scratch,
-                             c->ly.scratch_bytes, c->stream);
-  if (e == hipSuccess)
-    e = lcsm::launch_fft_tile(c->S, H, c->tw, s, P, P, P, c->opt.lds_fft_max_n, c->scratch,
-                              c->ly.scratch_bytes, c->stream);
+  if (e == hipSuccess) e = spectra(c, P, P);
+  if (e == hipSuccess) e = fft_tile(c, c->S, P, P, P, false);
   if (e == hipSuccess) e = lcsm::launch_rows_out_clear(c->S, s, P, P, z, z_stride, c->stream);
   // the tile spectra back, then the gray tile of i = P that P steps would end with
-  if (e == hipSuccess)
-    e = lcsm::launch_spectra(c->Hf, H, c->tw, s, P, 0, c->opt.lds_fft_max_n, c->scratch,
-                             c->ly.scratch_bytes, c->stream);
+  if (e == hipSuccess) e = spectra(c, P, 0);
   if (e == hipSuccess) e = launch_tile(c, P, P, P);
   if (e != hipSuccess) return fail(c, LCSM_EDEVICE, "prefill", e);
   c->t = P;

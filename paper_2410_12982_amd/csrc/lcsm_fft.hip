@@ -330,7 +330,7 @@ template <int N>
 __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_spectra(const float* __restrict__ Hf,
                                                             float2* __restrict__ Hout,
                                                             const float2* __restrict__ tw, int L,
-                                                            int D, int ppl, int shift) {
+                                                            int D, int ppl, int shift, int colmaj) {
   constexpr int WC = Cfg<N>::WC, NT = Cfg<N>::NT, U = N / 2;
   __shared__ float2 buf[N * WC];
   __shared__ float2 twl[Cfg<N>::TWN];
@@ -346,14 +346,17 @@ __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_spectra(const float* __restr
   });
   constexpr float inv_n = 1.0f / (float)N;
   float2* Hm = Hout + (size_t)m * (U + 1) * D;
+  // [k][d] within the layer, or [d][k] (colmaj) for the column tiles
+  const size_t sk = colmaj ? 1 : (size_t)D, sd = colmaj ? (size_t)(U + 1) : 1;
   for (int u = (int)threadIdx.x; u < (U + 1) * WC; u += NT) {
     const int kk = u / WC, col = u - kk * WC;
     const int c = c0 + 2 * col;
     if (c >= D) continue;
     const float2 a = buf[kk * WC + col], b = buf[((N - kk) & (N - 1)) * WC + col];
-    Hm[(size_t)kk * D + c] = make_float2(0.5f * inv_n * (a.x + b.x), 0.5f * inv_n * (a.y - b.y));
+    Hm[kk * sk + c * sd] = make_float2(0.5f * inv_n * (a.x + b.x), 0.5f * inv_n * (a.y - b.y));
     if (c + 1 < D)
-      Hm[(size_t)kk * D + c + 1] = make_float2(0.5f * inv_n * (a.y + b.y), -0.5f * inv_n * (a.x - b.x));
+      Hm[kk * sk + (c + 1) * sd] =
+          make_float2(0.5f * inv_n * (a.y + b.y), -0.5f * inv_n * (a.x - b.x));
   }
 }
 
@@ -422,7 +425,8 @@ template <int N1>
 __global__ __launch_bounds__(kMidNT) void k_fft_mid_spectra(const float2* __restrict__ C,
                                                             float2* __restrict__ Hout, int D,
                                                             Chunk ch,
-                                                            const float2* __restrict__ tw) {
+                                                            const float2* __restrict__ tw,
+                                                            int colmaj) {
   constexpr int G = kMidG, WCM = kMidWC, NT = kMidNT;
   constexpr int W = 2 * G * WCM;  // LDS row stride
   __shared__ float2 buf[N1 * W];
@@ -462,9 +466,11 @@ __global__ __launch_bounds__(kMidNT) void k_fft_mid_spectra(const float2* __rest
     const int m = g / ch.ncc;
     const int c = 2 * (g - m * ch.ncc);
     float2* Hm = Hout + (size_t)m * (U + 1) * D;
-    Hm[(size_t)k * D + c] = make_float2(0.5f * inv_n * (xk.x + xp.x), 0.5f * inv_n * (xk.y - xp.y));
+    const size_t sk = colmaj ? 1 : (size_t)D, sd = colmaj ? (size_t)(U + 1) : 1;
+    Hm[k * sk + c * sd] = make_float2(0.5f * inv_n * (xk.x + xp.x), 0.5f * inv_n * (xk.y - xp.y));
     if (c + 1 < D)
-      Hm[(size_t)k * D + c + 1] = make_float2(0.5f * inv_n * (xk.y + xp.y), -0.5f * inv_n * (xk.x - xp.x));
+      Hm[k * sk + (c + 1) * sd] =
+          make_float2(0.5f * inv_n * (xk.y + xp.y), -0.5f * inv_n * (xk.x - xp.x));
   }
 }
 
@@ -702,12 +708,12 @@ hipError_t tile_single(int N, float* S, const float2* H, const float2* tw, const
 }
 
 hipError_t spectra_single(int N, const float* Hf, float2* Hout, const float2* tw, const Shape& s,
-                          int shift, hipStream_t st) {
+                          int shift, int colmaj, hipStream_t st) {
 #define LCSM_CASE(NN)                                                                            \
   case NN: {                                                                                     \
     const int ppl = (s.D + 2 * Cfg<NN>::WC - 1) / (2 * Cfg<NN>::WC);                             \
     hipLaunchKernelGGL(k_fft_spectra<NN>, dim3((unsigned)(ppl * s.M)), dim3(Cfg<NN>::NT), 0, st, \
-                       Hf, Hout, tw, s.L, s.D, ppl, shift);                                      \
+                       Hf, Hout, tw, s.L, s.D, ppl, shift, colmaj);                                      \
     return hipGetLastError();                                                                    \
   }
   switch (N) { LCSM_POW2_CASES(LCSM_CASE) }
@@ -763,12 +769,12 @@ hipError_t mid_tile(float2* C, const float2* H, int D, const Chunk& ch, const fl
 }
 
 hipError_t mid_spectra(const float2* C, float2* Hout, int D, const Chunk& ch, const float2* tw,
-                       hipStream_t st) {
+                       int colmaj, hipStream_t st) {
   const int npan = (ch.nvalid + kMidWC - 1) / kMidWC;
   const dim3 grid((unsigned)(npan * (ch.N2 / kMidG)));
 #define LCSM_CASE(NN)                                                                             \
   case NN:                                                                                        \
-    hipLaunchKernelGGL(k_fft_mid_spectra<NN>, grid, dim3(kMidNT), 0, st, C, Hout, D, ch, tw);     \
+    hipLaunchKernelGGL(k_fft_mid_spectra<NN>, grid, dim3(kMidNT), 0, st, C, Hout, D, ch, tw, colmaj);     \
     return hipGetLastError();
   switch (ch.N1) { LCSM_MID_CASES(LCSM_CASE) }
 #undef LCSM_CASE
@@ -801,9 +807,9 @@ int fft_multipass_chunk(int N, size_t scratch_bytes, int total_cc) {
 
 hipError_t launch_spectra(const float* Hf, float2* Hout, const float2* tw, const Shape& s, int U,
                           int shift, int lds_max_n, float2* scratch, size_t scratch_bytes,
-                          hipStream_t st) {
+                          hipStream_t st, bool colmaj) {
   const int N = 2 * U;
-  if (N <= lds_max_n) return spectra_single(N, Hf, Hout, tw, s, shift, st);
+  if (N <= lds_max_n) return spectra_single(N, Hf, Hout, tw, s, shift, colmaj ? 1 : 0, st);
   Chunk ch{};
   ch.ncols = s.D;
   ch.ncc = (s.D + 1) / 2;
@@ -817,7 +823,7 @@ hipError_t launch_spectra(const float* Hf, float2* Hout, const float2* tw, const
     ch.g0 = g0;
     ch.nvalid = total - g0 < ch.cstride ? total - g0 : ch.cstride;
     hipError_t e = rows_fwd<false>(Hf, (size_t)s.L * s.D, -shift, s.L, ch, C, tw, st);
-    if (e == hipSuccess) e = mid_spectra(C, Hout, s.D, ch, tw, st);
+    if (e == hipSuccess) e = mid_spectra(C, Hout, s.D, ch, tw, colmaj ? 1 : 0, st);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;

@@ -1,0 +1,222 @@
+// FFT gray tiles on transposed column chunks, for gfx950.
+//
+// The row-panel tile kernels (lcsm_fft.hip) read and write each state row in
+// pieces of WC complex columns, and at 2U >= 2048 LDS leaves room for only
+// 16-64 bytes per row, a run width at which HBM delivers a fraction of its
+// bandwidth.  Here a chunk of columns of the tile's input rows is first
+// transposed into a column-major scratch (64 x 64 tiles through LDS: 256-byte
+// runs on both sides), each workgroup then transforms one complex column --
+// two real state columns packed as real and imaginary part -- reading and
+// writing it as one contiguous run along time, and a second transpose adds
+// the outputs into the destination rows (or stores them, for the in-place
+// swap of half-state storage).  28U bytes move per column instead of 12U, at
+// full run width.  The spectra of these tile sizes are kept channel-major,
+// Hc[m][d][k] (k <= U, pre-scaled by 1/2U), so that a workgroup's spectrum
+// loads are contiguous as well.
+//
+// Transform (as in the row-panel tile, Lemma 1 / App. B): with the two real
+// columns a, b of a pair, z = y_a + i y_b over [0, U) and zero above,
+// Z = DFT_2U(z); P[k] = Z[k] S[k] + conj(Z[2U-k]) D[k] with S = (Ha + Hb)/2,
+// D = (Ha - Hb)/2; the outputs U + j of IDFT_2U(P) are the tile's outputs j
+// of column a (real part) and b (imaginary part).
+#include "lcsm_fft_core.h"
+#include "lcsm_internal.h"
+
+namespace lcsm {
+namespace {
+
+using fft::cadd;
+using fft::cmul;
+using fft::conjf2;
+
+constexpr int kTT = 64;        // transpose tile side
+constexpr int kTThreads = 256;  // 64 x 4
+
+// X[(g - g0) * ldx + r] = S[m][row0 + r][c] for global columns g = m*BD + c
+// in [g0, g0 + ncols) and r < nrows.  lstride: state floats per layer.
+__global__ __launch_bounds__(kTThreads) void k_rows_to_cols(const float* __restrict__ S,
+                                                            size_t lstride, int BD, int row0,
+                                                            int nrows, long long g0, int ncols,
+                                                            float* __restrict__ X, int ldx) {
+  __shared__ float tile[kTT][kTT + 1];
+  const int cb = (int)blockIdx.x * kTT, rb = (int)blockIdx.y * kTT;
+  const int tx = (int)threadIdx.x & (kTT - 1), ty = (int)threadIdx.x / kTT;
+  const int col = cb + tx;
+  if (col < ncols) {
+    const long long g = g0 + col;
+    const long long m = g / BD;
+    const int c = (int)(g - m * BD);
+    const float* src = S + (size_t)m * lstride + (size_t)row0 * BD + c;
+#pragma unroll
+    for (int k = 0; k < kTT / 4; ++k) {
+      const int r = rb + ty + 4 * k;
+      if (r < nrows) tile[ty + 4 * k][tx] = src[(size_t)r * BD];
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < kTT / 4; ++k) {
+    const int cc = cb + ty + 4 * k, r = rb + tx;
+    if (cc < ncols && r < nrows) X[(size_t)cc * ldx + r] = tile[tx][ty + 4 * k];
+  }
+}
+
+// S[m][row0 + r][c] += X[(g - g0) * ldx + r] (STORE: =) for r < nrows.
+template <bool STORE>
+__global__ __launch_bounds__(kTThreads) void k_cols_to_rows(const float* __restrict__ X, int ldx,
+                                                            float* __restrict__ S, size_t lstride,
+                                                            int BD, int row0, int nrows,
+                                                            long long g0, int ncols) {
+  __shared__ float tile[kTT][kTT + 1];
+  const int cb = (int)blockIdx.x * kTT, rb = (int)blockIdx.y * kTT;
+  const int tx = (int)threadIdx.x & (kTT - 1), ty = (int)threadIdx.x / kTT;
+#pragma unroll
+  for (int k = 0; k < kTT / 4; ++k) {
+    const int cc = cb + ty + 4 * k, r = rb + tx;
+    if (cc < ncols && r < nrows) tile[ty + 4 * k][tx] = X[(size_t)cc * ldx + r];
+  }
+  __syncthreads();
+  const int col = cb + tx;
+  if (col >= ncols) return;
+  const long long g = g0 + col;
+  const long long m = g / BD;
+  const int c = (int)(g - m * BD);
+  float* dst = S + (size_t)m * lstride + (size_t)row0 * BD + c;
+#pragma unroll
+  for (int k = 0; k < kTT / 4; ++k) {
+    const int r = rb + ty + 4 * k;
+    if (r < nrows) {
+      float* p = dst + (size_t)r * BD;
+      *p = STORE ? tile[tx][ty + 4 * k] : *p + tile[tx][ty + 4 * k];
+    }
+  }
+}
+
+// One complex column per workgroup (consecutive threads take consecutive
+// time indices: contiguous loads and stores), N/16 threads, at most 512 (a
+// larger workgroup leaves too few registers for the radix-16 passes).  The
+// twiddle table goes to LDS only while it is small (the data alone then
+// bounds the workgroups per CU).
+template <int N>
+struct ColCfg {
+  static constexpr int NT = N / 16 < 64 ? 64 : (N / 16 > 512 ? 512 : N / 16);
+  static constexpr bool TWL = N <= 1024;
+};
+
+template <int N>
+__global__ __launch_bounds__(ColCfg<N>::NT) void k_fft_coltile(float* __restrict__ X, int ldx,
+                                                               const float2* __restrict__ Hc,
+                                                               const float2* __restrict__ tw,
+                                                               long long g0, int ncols, int BD,
+                                                               int D, int B) {
+  constexpr int NT = ColCfg<N>::NT, U = N / 2;
+  using TW = typename std::conditional<ColCfg<N>::TWL, fft::TwLds<N>, fft::TwGlobal>::type;
+  __shared__ float2 buf[N];
+  __shared__ float2 twl[ColCfg<N>::TWL ? N : 1];
+  TW twz;
+  if constexpr (ColCfg<N>::TWL) {
+    fft::load_twiddles<N, NT>(twl, tw);
+    twz = TW{twl};
+  } else {
+    twz = TW{tw};
+  }
+  int pr = fft::xcd_logical((int)blockIdx.x, (int)gridDim.x);
+  // B > 0 (the chunk holds whole layers, D even): consecutive workgroups take
+  // the B batch rows of one channel pair, which share its spectra in L2
+  if (B > 0) {
+    const int ppr = D / 2;  // pairs per batch row
+    const int lp = B * ppr;  // pairs per layer
+    const int l = pr / lp, r = pr - l * lp;
+    const int dp = r / B, b = r - dp * B;
+    pr = l * lp + b * ppr + dp;
+  }
+  const int ca = 2 * pr, cb = ca + 1;  // chunk columns of the pair (cb may be past the chunk)
+  const bool hasb = cb < ncols;
+  float* xa = X + (size_t)ca * ldx;
+  float* xb = X + (size_t)(hasb ? cb : ca) * ldx;
+  fft::forward_from_global<N, 1, 1, NT, true>(buf, twz, [&](int row, int) {
+    return make_float2(xa[row], hasb ? xb[row] : 0.f);
+  });
+  // spectra of the two columns' channels (contiguous along k)
+  const long long ga = g0 + ca, gb = g0 + (hasb ? cb : ca);
+  const long long ma = ga / BD, mb = gb / BD;
+  const int da = (int)(ga - ma * BD) % D, db = (int)(gb - mb * BD) % D;
+  const float2* ha = Hc + ((size_t)ma * D + da) * (U + 1);
+  const float2* hb = Hc + ((size_t)mb * D + db) * (U + 1);
+  for (int kk = (int)threadIdx.x; kk <= U; kk += NT) {
+    const float2 a = ha[kk], b = hasb ? hb[kk] : make_float2(0.f, 0.f);
+    const float2 s = make_float2(0.5f * (a.x + b.x), 0.5f * (a.y + b.y));
+    const float2 d = make_float2(0.5f * (a.x - b.x), 0.5f * (a.y - b.y));
+    const int nk = (N - kk) & (N - 1);
+    const float2 zk = buf[kk], znk = buf[nk];
+    buf[kk] = cadd(cmul(zk, s), cmul(conjf2(znk), d));
+    if (nk != kk) buf[nk] = cadd(cmul(znk, conjf2(s)), cmul(conjf2(zk), conjf2(d)));
+  }
+  __syncthreads();
+  // outputs U + j -> row j of the pair's columns, in place over the inputs
+  // (every input of this workgroup was read in the first pass)
+  fft::inverse_to_global<N, 1, 1, NT, true>(buf, twz, [&](int row, int, float2 v) {
+    const int j = row - U;
+    xa[j] = v.x;
+    if (hasb) xb[j] = v.y;
+  });
+}
+
+}  // namespace
+
+int fft_col_chunk(int U, size_t scratch_bytes, long long total_cols) {
+  long long cap = (long long)(scratch_bytes / (sizeof(float) * (size_t)U));
+  cap = cap / kTT * kTT;
+  const long long need = (total_cols + kTT - 1) / kTT * kTT;
+  if (cap > need) cap = need;
+  if (cap > (1LL << 30)) cap = 1LL << 30;
+  return (int)cap;
+}
+
+hipError_t launch_fft_col_tile(float* S, const float2* Hc, const float2* tw, const Shape& s, int i,
+                               int U, int dst_len, float2* scratch, size_t scratch_bytes,
+                               hipStream_t st, bool in_place) {
+  if (dst_len <= 0) return hipSuccess;
+  const int N = 2 * U;
+  const long long total = (long long)s.M * s.BD;
+  int chunk = fft_col_chunk(U, scratch_bytes, total);
+  if (chunk <= 0) return hipErrorOutOfMemory;
+  // whole layers per chunk where possible (then the pair order can follow
+  // the spectra: see k_fft_coltile)
+  const bool layers = s.D % 2 == 0 && s.BD % 64 == 0 && chunk >= s.BD;
+  if (layers) chunk = chunk / s.BD * s.BD;
+  float* X = reinterpret_cast<float*>(scratch);
+  const size_t lstride = (size_t)s.SL * s.BD;
+  for (long long g0 = 0; g0 < total; g0 += chunk) {
+    const int nc = (int)(total - g0 < chunk ? total - g0 : chunk);
+    const dim3 tin((unsigned)((nc + kTT - 1) / kTT), (unsigned)((U + kTT - 1) / kTT));
+    hipLaunchKernelGGL(k_rows_to_cols, tin, dim3(kTThreads), 0, st, S, lstride, s.BD, i - U, U, g0,
+                       nc, X, U);
+    const dim3 grid((unsigned)((nc + 1) / 2));
+    switch (N) {
+#define LCSM_CASE(NN)                                                                            \
+  case NN:                                                                                       \
+    hipLaunchKernelGGL(k_fft_coltile<NN>, grid, dim3(ColCfg<NN>::NT), 0, st, X, U, Hc, tw, g0, nc, \
+                       s.BD, s.D, layers ? s.B : 0);                                             \
+    break;
+      LCSM_CASE(4) LCSM_CASE(8) LCSM_CASE(16) LCSM_CASE(32) LCSM_CASE(64) LCSM_CASE(128)
+      LCSM_CASE(256) LCSM_CASE(512) LCSM_CASE(1024) LCSM_CASE(2048) LCSM_CASE(4096)
+      LCSM_CASE(8192) LCSM_CASE(16384)
+#undef LCSM_CASE
+      default:
+        return hipErrorInvalidValue;
+    }
+    const dim3 tout((unsigned)((nc + kTT - 1) / kTT), (unsigned)((dst_len + kTT - 1) / kTT));
+    if (in_place)
+      hipLaunchKernelGGL(k_cols_to_rows<true>, tout, dim3(kTThreads), 0, st, X, U, S, lstride, s.BD,
+                         i - U, dst_len, g0, nc);
+    else
+      hipLaunchKernelGGL(k_cols_to_rows<false>, tout, dim3(kTThreads), 0, st, X, U, S, lstride, s.BD,
+                         i, dst_len, g0, nc);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+}  // namespace lcsm

@@ -93,9 +93,27 @@ int fft_multipass_chunk(int N, size_t scratch_bytes, int total_cc);
 // Filter spectra of tile size U (N = 2U): Hout[m][k][d] = DFT_N(g[m,d,0:N))[k]
 // / N for k = 0..U, with g the filter delayed by shift rows (g[r] = h[r -
 // shift], zero for r < shift).  tw: twiddle table (see lcsm_fft_core.h).
+// colmaj: stored channel-major instead, Hout[m][d][k] (the column tiles).
 hipError_t launch_spectra(const float* Hf, float2* Hout, const float2* tw, const Shape& s, int U,
                           int shift, int lds_max_n, float2* scratch, size_t scratch_bytes,
-                          hipStream_t st);
+                          hipStream_t st, bool colmaj = false);
+
+// ---- FFT tiles on transposed column chunks (lcsm_fft_col.hip)
+
+// Largest 2U of the column tiles (one complex column of 2U points in LDS).
+constexpr int kMaxColFftN = 16384;
+
+// Columns per chunk of a column tile of side U with scratch_bytes of
+// scratch (a multiple of 64, 0 if not even 64 columns fit).
+int fft_col_chunk(int U, size_t scratch_bytes, long long total_cols);
+
+// FFT gray tile of all layers on transposed column chunks: y rows [i-U, i)
+// -> z rows [i, i+dst_len) (added), or stored over rows [i-U, i-U+dst_len)
+// when in_place (the half-state swap).  Hc: channel-major spectra [m][d][k]
+// of tile size U.  2U <= kMaxColFftN.
+hipError_t launch_fft_col_tile(float* S, const float2* Hc, const float2* tw, const Shape& s, int i,
+                               int U, int dst_len, float2* scratch, size_t scratch_bytes,
+                               hipStream_t st, bool in_place);
 
 // FFT gray tile of all layers: y rows [i-U, i) -> z rows [i, i+dst_len),
 // with the spectra H of tile size U.  Single LDS pass when 2U <= lds_max_n,

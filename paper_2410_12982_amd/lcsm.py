@@ -20,9 +20,9 @@ LCSM_EDEVICE = -3
 LCSM_EDONE = -4
 LCSM_ESTATE = -5
 
-TILE_NONE, TILE_DIRECT, TILE_FFT, TILE_FFT_HBM = 0, 1, 2, 3
+TILE_NONE, TILE_DIRECT, TILE_FFT, TILE_FFT_HBM, TILE_FFT_COL = 0, 1, 2, 3, 4
 TILE_KIND_NAMES = {TILE_NONE: "none", TILE_DIRECT: "direct", TILE_FFT: "fft_lds",
-                   TILE_FFT_HBM: "fft_hbm"}
+                   TILE_FFT_HBM: "fft_hbm", TILE_FFT_COL: "fft_col"}
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2410_12982_amd.build`")
@@ -54,7 +54,7 @@ class Options(ctypes.Structure):
     """``lcsm_options``: 0 selects the library default."""
     _fields_ = [("direct_max_u", ctypes.c_int), ("lds_fft_max_n", ctypes.c_int),
                 ("scratch_mib", ctypes.c_int), ("half_state", ctypes.c_int),
-                ("reserved", ctypes.c_int * 4)]
+                ("col_fft_min_n", ctypes.c_int), ("reserved", ctypes.c_int * 3)]
 
 
 _c_int_p = ctypes.POINTER(ctypes.c_int)

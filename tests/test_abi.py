@@ -167,6 +167,15 @@ def test_plan_tile_default_kinds_for_workloads():
     assert all(kinds[1 << q] == lcsm.TILE_DIRECT for q in range(7))
     assert all(kinds[1 << q] == lcsm.TILE_FFT for q in range(7, 13))
     assert all(kinds[1 << q] == lcsm.TILE_FFT_HBM for q in range(13, 17))
+    # the column-chunk tiles when asked for: 2U from col_fft_min_n up to 16384
+    on = {"col_fft_min_n": 2048}
+    for q, want in ((9, lcsm.TILE_FFT), (10, lcsm.TILE_FFT_COL), (13, lcsm.TILE_FFT_COL),
+                    (14, lcsm.TILE_FFT_HBM)):
+        t = (1 << q) - 1
+        assert lcsm.plan_tile(18, 1, 1024, L, t, on)[3] == want
+    for bad in (3, 2, -4, 100):
+        with pytest.raises(lcsm.LcsmError):
+            lcsm.workspace_bytes(1, 1, 16, 4096, {"col_fft_min_n": bad})
 
 
 def test_init_validates_before_touching_the_device():

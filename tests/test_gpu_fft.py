@@ -26,11 +26,15 @@ pytestmark = pytest.mark.gpu
 
 FFT_OPTIONS = {
     # every tile with U >= 2 is an FFT tile, in one LDS pass up to 2U = 4096
-    "lds_from_2": {"direct_max_u": 1, "lds_fft_max_n": 4096},
+    "lds_from_2": {"direct_max_u": 1, "lds_fft_max_n": 4096, "col_fft_min_n": 1 << 20},
     # every tile with 2U > 16 goes through the three-pass form
-    "multipass_from_16": {"direct_max_u": 1, "lds_fft_max_n": 16},
+    "multipass_from_16": {"direct_max_u": 1, "lds_fft_max_n": 16, "col_fft_min_n": 1 << 20},
     # multi-pass with a 1 MiB scratch: many chunks per tile
-    "tiny_scratch": {"direct_max_u": 4, "lds_fft_max_n": 32, "scratch_mib": 1},
+    "tiny_scratch": {"direct_max_u": 4, "lds_fft_max_n": 32, "scratch_mib": 1, "col_fft_min_n": 1 << 20},
+    # every FFT tile on transposed column chunks (the column path is off above)
+    "col_from_4": {"direct_max_u": 1, "col_fft_min_n": 4},
+    # column tiles with a 1 MiB scratch: many column chunks per tile
+    "col_tiny_scratch": {"direct_max_u": 4, "col_fft_min_n": 16, "scratch_mib": 1},
     "default": None,
 }
 
@@ -58,7 +62,8 @@ def _run_full(ctx, y):
     return z.cpu().numpy()
 
 
-@pytest.mark.parametrize("opt", ["lds_from_2", "multipass_from_16", "tiny_scratch"])
+@pytest.mark.parametrize("opt", ["lds_from_2", "multipass_from_16", "tiny_scratch", "col_from_4",
+                                 "col_tiny_scratch"])
 @pytest.mark.parametrize("shape", [(2, 3, 40, 300), (1, 1, 5, 257), (3, 2, 33, 1000),
                                    (1, 4, 64, 2048)])
 def test_integer_data_rounds_to_exact(opt, shape):
@@ -74,7 +79,7 @@ def test_integer_data_rounds_to_exact(opt, shape):
     assert np.array_equal(np.rint(z).astype(np.int64), ex)
 
 
-@pytest.mark.parametrize("opt", ["default", "lds_from_2"])
+@pytest.mark.parametrize("opt", ["default", "lds_from_2", "col_from_4"])
 @pytest.mark.parametrize("shape", [(1, 2, 48, 4500), (1, 3, 24, 4200), (2, 1, 10, 6000)])
 def test_integer_data_panel_orders_and_clipped_large_tiles(opt, shape):
     """Shapes whose channel count is not a whole number of 128-byte line
@@ -93,7 +98,8 @@ def test_integer_data_panel_orders_and_clipped_large_tiles(opt, shape):
     assert np.array_equal(np.rint(z).astype(np.int64), ex)
 
 
-@pytest.mark.parametrize("opt", ["lds_from_2", "multipass_from_16", "tiny_scratch", "default"])
+@pytest.mark.parametrize("opt", ["lds_from_2", "multipass_from_16", "tiny_scratch", "default",
+                                 "col_from_4"])
 def test_m1b8d768l8k_teacher_forced_all_columns(opt):
     w = datagen.WORKLOADS["m1b8d768l8k"]
     say(f"[fft teacher-forced all columns] {w.name} options={opt}")
@@ -124,7 +130,7 @@ def test_small_workload_closed_loop(opt):
     assert err <= TOL
 
 
-@pytest.mark.parametrize("opt", ["default", "multipass_from_16"])
+@pytest.mark.parametrize("opt", ["default", "multipass_from_16", "col_tiny_scratch"])
 def test_fft_rerun_bitwise_and_step_layer_path(opt):
     w = datagen.Workload("fftdet", 3, 2, 70, 1500, decay=400.0, seed=12)
     say(f"[fft determinism / step_layer] M=3 B=2 D=70 L=1500 options={opt}")

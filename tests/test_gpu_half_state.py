@@ -26,11 +26,13 @@ pytestmark = pytest.mark.gpu
 OPTIONS = {
     "default": {},
     # every tile above U = 1 an FFT tile, one LDS pass up to 2U = 8192
-    "lds_from_2": {"direct_max_u": 1, "lds_fft_max_n": 8192},
+    "lds_from_2": {"direct_max_u": 1, "lds_fft_max_n": 8192, "col_fft_min_n": 1 << 20},
     # every tile with 2U > 16, the swap included, in three passes
-    "multipass_from_16": {"direct_max_u": 1, "lds_fft_max_n": 16},
+    "multipass_from_16": {"direct_max_u": 1, "lds_fft_max_n": 16, "col_fft_min_n": 1 << 20},
     # three passes with a 1 MiB scratch: the swap in many column chunks
-    "tiny_scratch": {"direct_max_u": 4, "lds_fft_max_n": 32, "scratch_mib": 1},
+    "tiny_scratch": {"direct_max_u": 4, "lds_fft_max_n": 32, "scratch_mib": 1, "col_fft_min_n": 1 << 20},
+    # the swap (and every FFT tile) on transposed column chunks, many chunks
+    "col_tiny_scratch": {"direct_max_u": 4, "col_fft_min_n": 16, "scratch_mib": 1},
 }
 
 
@@ -51,7 +53,8 @@ def _oracle(w, y):
                                 h.reshape(h.shape[0], -1))
 
 
-@pytest.mark.parametrize("opt", ["default", "lds_from_2", "multipass_from_16", "tiny_scratch"])
+@pytest.mark.parametrize("opt", ["default", "lds_from_2", "multipass_from_16", "tiny_scratch",
+                                 "col_tiny_scratch"])
 @pytest.mark.parametrize("shape", [(2, 3, 40, 300), (1, 4, 64, 2048), (3, 2, 33, 1000),
                                    (1, 2, 48, 4500), (2, 2, 24, 8192)])
 def test_half_state_matches_oracle_and_full_state(opt, shape):
@@ -71,7 +74,7 @@ def test_half_state_matches_oracle_and_full_state(opt, shape):
     assert err <= TOL
 
 
-@pytest.mark.parametrize("opt", ["default", "multipass_from_16", "tiny_scratch"])
+@pytest.mark.parametrize("opt", ["default", "multipass_from_16", "tiny_scratch", "col_tiny_scratch"])
 def test_half_state_integer_data_rounds_to_exact(opt):
     M, B, D, L = 2, 3, 20, 1500
     w = datagen.Workload("halfint", M, B, D, L, decay=1.0, seed=9)

@@ -21,7 +21,7 @@ pytestmark = pytest.mark.gpu
 OPTION_SETS = {
     "all_direct": {"direct_max_u": 1 << 20},
     "default": None,
-    "fft_from_2": {"direct_max_u": 1, "lds_fft_max_n": 64},
+    "fft_from_2": {"direct_max_u": 1, "lds_fft_max_n": 64, "col_fft_min_n": 1 << 20},
     "fft_from_64": {"direct_max_u": 32},
 }
 

@@ -23,9 +23,11 @@ pytestmark = pytest.mark.gpu
 OPTIONS = {
     "default": None,
     # every tile above U = 1 is an FFT tile, one LDS pass up to 2U = 4096
-    "fft_from_2": {"direct_max_u": 1, "lds_fft_max_n": 4096},
+    "fft_from_2": {"direct_max_u": 1, "lds_fft_max_n": 4096, "col_fft_min_n": 1 << 20},
     # every tile with 2U > 16 (and the prompt's transform) in three passes
-    "multipass_from_16": {"direct_max_u": 1, "lds_fft_max_n": 16},
+    "multipass_from_16": {"direct_max_u": 1, "lds_fft_max_n": 16, "col_fft_min_n": 1 << 20},
+    # every FFT tile (and the prompt's transform) on transposed column chunks
+    "col_from_4": {"direct_max_u": 1, "col_fft_min_n": 4},
 }
 
 
@@ -39,7 +41,7 @@ def _prefill_then_run(ctx, y, P):
     return z.cpu().numpy()
 
 
-@pytest.mark.parametrize("opt", ["default", "fft_from_2", "multipass_from_16"])
+@pytest.mark.parametrize("opt", ["default", "fft_from_2", "multipass_from_16", "col_from_4"])
 @pytest.mark.parametrize("case", [(2, 3, 40, 1024, 256), (3, 2, 33, 2048, 64), (1, 1, 5, 300, 128),
                                   (2, 2, 24, 4096, 2048)])
 def test_prefill_then_generate_matches_oracle(opt, case):
@@ -73,7 +75,7 @@ def test_prefill_bench_workload_half_prompt():
     assert err <= TOL
 
 
-@pytest.mark.parametrize("opt", ["default", "multipass_from_16"])
+@pytest.mark.parametrize("opt", ["default", "multipass_from_16", "col_from_4"])
 def test_prefill_integer_data_rounds_to_exact(opt):
     M, B, D, L, P = 2, 2, 16, 2048, 512
     w = datagen.Workload("int", M, B, D, L, decay=1.0, seed=7)
