@@ -101,10 +101,12 @@ template <int N>
 struct ColCfg {
   static constexpr int NT = N / 16 < 64 ? 64 : (N / 16 > 512 ? 512 : N / 16);
   static constexpr bool TWL = N <= 1024;
+  // waves per SIMD the registers must allow: two 512-thread workgroups per CU
+  static constexpr int MINB = N >= 4096 && N <= 8192 ? 4 : 1;
 };
 
 template <int N>
-__global__ __launch_bounds__(ColCfg<N>::NT) void k_fft_coltile(float* __restrict__ X, int ldx,
+__global__ __launch_bounds__(ColCfg<N>::NT, ColCfg<N>::MINB) void k_fft_coltile(float* __restrict__ X, int ldx,
                                                                const float2* __restrict__ Hc,
                                                                const float2* __restrict__ tw,
                                                                long long g0, int ncols, int BD,
