@@ -42,8 +42,10 @@ def _ctx(w, opt):
 
 @pytest.mark.parametrize("opt", ["direct_all", "fft_from_2", "default"])
 @pytest.mark.parametrize("shape", [(1, 1, 16, 300), (2, 3, 20, 1000), (3, 2, 33, 513),
-                                   (1, 4, 64, 2048)])
+                                   (1, 4, 64, 2048), (2, 1, 15, 400)])
 def test_dd_matches_oracle(opt, shape):
+    """Includes an odd column count per layer (15: the FFT tile's last real
+    column has no partner in its pair)."""
     M, B, D, L = shape
     say(f"[dd] M={M} B={B} D={D} L={L} options={opt}")
     w = datagen.Workload("dd", M, B, D, L, decay=L / 4, seed=60 + L % 89)
