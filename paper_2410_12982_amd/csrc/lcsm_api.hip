@@ -23,11 +23,12 @@ constexpr int kAutoDirectMaxU = 32;
 constexpr int kAutoDirectU64MaxCols = 1 << 17;
 constexpr int kDefaultLdsFftMaxN = 8192;   // 2U <= 8192: one LDS pass
 constexpr int kDefaultScratchMib = 512;    // multi-pass and column-tile FFT scratch cap
-// The column-chunk FFT tiles are off unless asked for: on MI355X they measured
-// slower than the row-panel and three-pass tiles at every size (their
-// transform kernel, one 2U-point column per workgroup, runs at about 0.8
-// TB/s), although their transposes move the rows at 3.5-4 TB/s.
-constexpr int kDefaultColFftMinN = 2 * lcsm::kMaxColFftN;
+// FFT tiles from 2U = 8192 up run on transposed column chunks when there are
+// at least 2^14 columns (M*B*D): there the row-panel tile's 16-byte row runs
+// (and above 8192 the three-pass tile's extra passes) cost more than the two
+// transposes; below that size, or with fewer columns, the row panels win.
+constexpr int kDefaultColFftMinN = 8192;
+constexpr long long kAutoColMinCols = 1LL << 14;
 constexpr int kMaxL = 1 << 19;             // FFT lengths up to 2^19 are built
 constexpr int kMaxLevels = 20;
 
@@ -43,6 +44,7 @@ struct Options {
   int scratch_mib;
   int half_state;
   int col_min_n;
+  bool col_auto;  // col_min_n is the default: applies from kAutoColMinCols columns
 };
 
 int resolve_options(const lcsm_options* o, Options* r) {
@@ -51,12 +53,14 @@ int resolve_options(const lcsm_options* o, Options* r) {
   r->scratch_mib = kDefaultScratchMib;
   r->half_state = 0;
   r->col_min_n = kDefaultColFftMinN;
+  r->col_auto = true;
   if (!o) return LCSM_OK;
   for (int k = 0; k < 3; ++k)
     if (o->reserved[k] != 0) return LCSM_EINVAL;
   if (o->col_fft_min_n) {
     if (!is_pow2(o->col_fft_min_n) || o->col_fft_min_n < 4) return LCSM_EINVAL;
     r->col_min_n = o->col_fft_min_n;
+    r->col_auto = false;
   }
   if (o->direct_max_u < 0 || o->lds_fft_max_n < 0 || o->scratch_mib < 0) return LCSM_EINVAL;
   if (o->half_state != 0 && o->half_state != 1) return LCSM_EINVAL;
@@ -90,7 +94,9 @@ int tile_kind(const Options& o, const Shape& s, int U) {
   if (dmax == 0)
     dmax = ((long long)s.M * s.BD <= kAutoDirectU64MaxCols) ? 2 * kAutoDirectMaxU : kAutoDirectMaxU;
   if (U <= dmax) return LCSM_TILE_DIRECT;
-  if (2 * U >= o.col_min_n && 2 * U <= lcsm::kMaxColFftN) return LCSM_TILE_FFT_COL;
+  if (2 * U >= o.col_min_n && 2 * U <= lcsm::kMaxColFftN &&
+      (!o.col_auto || (long long)s.M * s.BD >= kAutoColMinCols))
+    return LCSM_TILE_FFT_COL;
   return (2 * U <= o.lds_fft_max_n) ? LCSM_TILE_FFT : LCSM_TILE_FFT_HBM;
 }
 

@@ -92,11 +92,28 @@ __global__ __launch_bounds__(kTThreads) void k_cols_to_rows(const float* __restr
   }
 }
 
+// Two-level twiddles in LDS: w_N^f = hi[f >> 6] * lo[f & 63] with
+// hi[j] = w_N^{64 j} (N/64 entries) and lo[l] = w_N^l (64 entries), both
+// copied from the fp64-derived global table; one complex product per
+// twiddle instead of N entries of LDS.
+template <int N>
+struct TwSplit {
+  static constexpr int NH = N / 64;
+  const float2* hi;
+  const float2* lo;
+  template <bool INV, int NN>
+  __device__ __forceinline__ float2 get(int e) const {
+    const int f = e * (N / NN);
+    const float2 w = cmul(hi[f >> 6], lo[f & 63]);
+    return INV ? conjf2(w) : w;
+  }
+};
+
 // One complex column per workgroup (consecutive threads take consecutive
 // time indices: contiguous loads and stores), N/16 threads, at most 512 (a
 // larger workgroup leaves too few registers for the radix-16 passes).  The
-// twiddle table goes to LDS only while it is small (the data alone then
-// bounds the workgroups per CU).
+// full twiddle table goes to LDS while it is small, the two-level one above
+// that (the data alone then bounds the workgroups per CU).
 template <int N>
 struct ColCfg {
   static constexpr int NT = N / 16 < 64 ? 64 : (N / 16 > 512 ? 512 : N / 16);
@@ -112,15 +129,17 @@ __global__ __launch_bounds__(ColCfg<N>::NT, ColCfg<N>::MINB) void k_fft_coltile(
                                                                long long g0, int ncols, int BD,
                                                                int D, int B) {
   constexpr int NT = ColCfg<N>::NT, U = N / 2;
-  using TW = typename std::conditional<ColCfg<N>::TWL, fft::TwLds<N>, fft::TwGlobal>::type;
+  using TW = typename std::conditional<ColCfg<N>::TWL, fft::TwLds<N>, TwSplit<N>>::type;
   __shared__ float2 buf[N];
-  __shared__ float2 twl[ColCfg<N>::TWL ? N : 1];
+  __shared__ float2 twl[ColCfg<N>::TWL ? N : N / 64 + 64];
   TW twz;
   if constexpr (ColCfg<N>::TWL) {
     fft::load_twiddles<N, NT>(twl, tw);
     twz = TW{twl};
   } else {
-    twz = TW{tw};
+    for (int j = (int)threadIdx.x; j < N / 64; j += NT) twl[j] = tw[N + 64 * j];
+    for (int l = (int)threadIdx.x; l < 64; l += NT) twl[N / 64 + l] = tw[N + l];
+    twz = TW{twl, twl + N / 64};
   }
   int pr = fft::xcd_logical((int)blockIdx.x, (int)gridDim.x);
   // B > 0 (the chunk holds whole layers, D even): consecutive workgroups take

@@ -158,15 +158,19 @@ def test_workspace_grows_with_fft_levels():
 
 
 def test_plan_tile_default_kinds_for_workloads():
-    # default: direct up to U = 64, one LDS pass up to 2U = 8192, multi-pass above
+    # default at 18432 columns: direct up to U = 64, one LDS pass up to 2U = 4096,
+    # transposed column chunks at 2U = 8192 and 16384, multi-pass above
     L = 1 << 17
     kinds = {}
     for t in range(L - 1):
         _, U, _, k = lcsm.plan_tile(18, 1, 1024, L, t)
         kinds[U] = k
     assert all(kinds[1 << q] == lcsm.TILE_DIRECT for q in range(7))
-    assert all(kinds[1 << q] == lcsm.TILE_FFT for q in range(7, 13))
-    assert all(kinds[1 << q] == lcsm.TILE_FFT_HBM for q in range(13, 17))
+    assert all(kinds[1 << q] == lcsm.TILE_FFT for q in range(7, 12))
+    assert all(kinds[1 << q] == lcsm.TILE_FFT_COL for q in range(12, 14))
+    assert all(kinds[1 << q] == lcsm.TILE_FFT_HBM for q in range(14, 17))
+    # fewer than 2^14 columns (the 6144-column workload): no column chunks
+    assert lcsm.plan_tile(1, 8, 768, 8192, 4095)[3] == lcsm.TILE_FFT
     # the column-chunk tiles when asked for: 2U from col_fft_min_n up to 16384
     on = {"col_fft_min_n": 2048}
     for q, want in ((9, lcsm.TILE_FFT), (10, lcsm.TILE_FFT_COL), (13, lcsm.TILE_FFT_COL),
