@@ -122,13 +122,23 @@ struct ColCfg {
   static constexpr int MINB = N >= 4096 && N <= 8192 ? 4 : 1;
 };
 
+// mode: how the complex columns pair the chunk's real columns.
+//   2 (the chunk holds whole layers, B even): batch rows 2p and 2p+1 of one
+//     channel -- both share its spectrum, the product is P = Z H, and the
+//     workgroups of one channel are consecutive (its spectrum stays in L2);
+//   1 (whole layers, D even): channels 2q and 2q+1 of one batch row, the
+//     workgroups of one channel pair consecutive over the batch rows;
+//   0: neighbouring chunk columns.
 template <int N>
 __global__ __launch_bounds__(ColCfg<N>::NT, ColCfg<N>::MINB) void k_fft_coltile(float* __restrict__ X, int ldx,
                                                                const float2* __restrict__ Hc,
                                                                const float2* __restrict__ tw,
                                                                long long g0, int ncols, int BD,
-                                                               int D, int B) {
+                                                               int D, int B, int mode) {
   constexpr int NT = ColCfg<N>::NT, U = N / 2;
+  // one channel's spectrum loaded into registers before the transform
+  constexpr int HU = (U + 1 + NT - 1) / NT;
+  constexpr bool PRE = N <= 8192;
   using TW = typename std::conditional<ColCfg<N>::TWL, fft::TwLds<N>, TwSplit<N>>::type;
   __shared__ float2 buf[N];
   __shared__ float2 twl[ColCfg<N>::TWL ? N : N / 64 + 64];
@@ -142,36 +152,66 @@ __global__ __launch_bounds__(ColCfg<N>::NT, ColCfg<N>::MINB) void k_fft_coltile(
     twz = TW{twl, twl + N / 64};
   }
   int pr = fft::xcd_logical((int)blockIdx.x, (int)gridDim.x);
-  // B > 0 (the chunk holds whole layers, D even): consecutive workgroups take
-  // the B batch rows of one channel pair, which share its spectra in L2
-  if (B > 0) {
-    const int ppr = D / 2;  // pairs per batch row
-    const int lp = B * ppr;  // pairs per layer
+  int ca, cb;  // chunk columns of the pair (cb may be past the chunk in mode 0)
+  if (mode == 2) {
+    const int half = B / 2, lp = half * D;  // pairs per layer
     const int l = pr / lp, r = pr - l * lp;
-    const int dp = r / B, b = r - dp * B;
-    pr = l * lp + b * ppr + dp;
+    const int d = r / half, bp = r - d * half;
+    ca = l * BD + 2 * bp * D + d;
+    cb = ca + D;
+  } else {
+    if (mode == 1) {
+      const int ppr = D / 2, lp = B * ppr;
+      const int l = pr / lp, r = pr - l * lp;
+      const int dp = r / B, b = r - dp * B;
+      pr = l * lp + b * ppr + dp;
+    }
+    ca = 2 * pr;
+    cb = ca + 1;
   }
-  const int ca = 2 * pr, cb = ca + 1;  // chunk columns of the pair (cb may be past the chunk)
   const bool hasb = cb < ncols;
   float* xa = X + (size_t)ca * ldx;
   float* xb = X + (size_t)(hasb ? cb : ca) * ldx;
-  fft::forward_from_global<N, 1, 1, NT, true>(buf, twz, [&](int row, int) {
-    return make_float2(xa[row], hasb ? xb[row] : 0.f);
-  });
   // spectra of the two columns' channels (contiguous along k)
   const long long ga = g0 + ca, gb = g0 + (hasb ? cb : ca);
   const long long ma = ga / BD, mb = gb / BD;
   const int da = (int)(ga - ma * BD) % D, db = (int)(gb - mb * BD) % D;
   const float2* ha = Hc + ((size_t)ma * D + da) * (U + 1);
   const float2* hb = Hc + ((size_t)mb * D + db) * (U + 1);
-  for (int kk = (int)threadIdx.x; kk <= U; kk += NT) {
-    const float2 a = ha[kk], b = hasb ? hb[kk] : make_float2(0.f, 0.f);
-    const float2 s = make_float2(0.5f * (a.x + b.x), 0.5f * (a.y + b.y));
-    const float2 d = make_float2(0.5f * (a.x - b.x), 0.5f * (a.y - b.y));
-    const int nk = (N - kk) & (N - 1);
-    const float2 zk = buf[kk], znk = buf[nk];
-    buf[kk] = cadd(cmul(zk, s), cmul(conjf2(znk), d));
-    if (nk != kk) buf[nk] = cadd(cmul(znk, conjf2(s)), cmul(conjf2(zk), conjf2(d)));
+  float2 hv[PRE ? HU : 1];
+  if constexpr (PRE) {
+    if (mode == 2) {
+#pragma unroll
+      for (int j = 0; j < HU; ++j) {
+        const int kk = (int)threadIdx.x + j * NT;
+        hv[j] = kk <= U ? ha[kk] : make_float2(0.f, 0.f);
+      }
+    }
+  }
+  fft::forward_from_global<N, 1, 1, NT, true>(buf, twz, [&](int row, int) {
+    return make_float2(xa[row], hasb ? xb[row] : 0.f);
+  });
+  if (mode == 2) {
+#pragma unroll
+    for (int j = 0; j < HU; ++j) {
+      const int kk = (int)threadIdx.x + j * NT;
+      if (kk <= U) {
+        const float2 h = PRE ? hv[PRE ? j : 0] : ha[kk];
+        const int nk = (N - kk) & (N - 1);
+        buf[kk] = cmul(buf[kk], h);
+        if (nk != kk) buf[nk] = cmul(buf[nk], conjf2(h));
+      }
+    }
+  } else {
+    for (int kk = (int)threadIdx.x; kk <= U; kk += NT) {
+      const float2 a = ha[kk], b = hasb ? hb[kk] : make_float2(0.f, 0.f);
+      const float2 s = make_float2(0.5f * (a.x + b.x), 0.5f * (a.y + b.y));
+      const float2 d = make_float2(0.5f * (a.x - b.x), 0.5f * (a.y - b.y));
+      const int nk = (N - kk) & (N - 1);
+      const float2 zk = buf[kk], znk = buf[nk];
+      buf[kk] = cadd(cmul(zk, s), cmul(conjf2(znk), d));
+      if (nk != kk) buf[nk] = cadd(cmul(znk, conjf2(s)), cmul(conjf2(zk), conjf2(d)));
+    }
   }
   __syncthreads();
   // outputs U + j -> row j of the pair's columns, in place over the inputs
@@ -202,10 +242,11 @@ hipError_t launch_fft_col_tile(float* S, const float2* Hc, const float2* tw, con
   const long long total = (long long)s.M * s.BD;
   int chunk = fft_col_chunk(U, scratch_bytes, total);
   if (chunk <= 0) return hipErrorOutOfMemory;
-  // whole layers per chunk where possible (then the pair order can follow
-  // the spectra: see k_fft_coltile)
-  const bool layers = s.D % 2 == 0 && s.BD % 64 == 0 && chunk >= s.BD;
+  // whole layers per chunk where possible (then the pairs and their order can
+  // follow the spectra: see k_fft_coltile)
+  const bool layers = s.BD % 64 == 0 && chunk >= s.BD;
   if (layers) chunk = chunk / s.BD * s.BD;
+  const int mode = layers && s.B % 2 == 0 ? 2 : (layers && s.D % 2 == 0 ? 1 : 0);
   float* X = reinterpret_cast<float*>(scratch);
   const size_t lstride = (size_t)s.SL * s.BD;
   for (long long g0 = 0; g0 < total; g0 += chunk) {
@@ -218,7 +259,7 @@ hipError_t launch_fft_col_tile(float* S, const float2* Hc, const float2* tw, con
 #define LCSM_CASE(NN)                                                                            \
   case NN:                                                                                       \
     hipLaunchKernelGGL(k_fft_coltile<NN>, grid, dim3(ColCfg<NN>::NT), 0, st, X, U, Hc, tw, g0, nc, \
-                       s.BD, s.D, layers ? s.B : 0);                                             \
+                       s.BD, s.D, s.B, mode);                                                    \
     break;
       LCSM_CASE(4) LCSM_CASE(8) LCSM_CASE(16) LCSM_CASE(32) LCSM_CASE(64) LCSM_CASE(128)
       LCSM_CASE(256) LCSM_CASE(512) LCSM_CASE(1024) LCSM_CASE(2048) LCSM_CASE(4096)
