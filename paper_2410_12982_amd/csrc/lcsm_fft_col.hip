@@ -99,6 +99,7 @@ __global__ __launch_bounds__(kTThreads) void k_cols_to_rows(const float* __restr
 template <int N>
 struct TwSplit {
   static constexpr int NH = N / 64;
+  static constexpr bool kRow = true;
   const float2* hi;
   const float2* lo;
   template <bool INV, int NN>
@@ -107,19 +108,43 @@ struct TwSplit {
     const float2 w = cmul(hi[f >> 6], lo[f & 63]);
     return INV ? conjf2(w) : w;
   }
+  // The twiddles w^{qk}, 0 < q < R, of one butterfly: the powers of two of
+  // q from the table, every other q as the product of its highest power of
+  // two and the rest (at most three products deep at R = 16): 2 log2 R LDS
+  // reads instead of 2 (R - 1).
+  template <bool INV, int NN, int R>
+  __device__ __forceinline__ void row(int k, float2 (&w)[R]) const {
+#pragma unroll
+    for (int p = 1; p < R; p *= 2) w[p] = get<INV, NN>(p * k);
+#pragma unroll
+    for (int q = 3; q < R; ++q) {
+      if (q & (q - 1)) {
+        int hb = 1;
+        while (2 * hb <= q) hb *= 2;
+        w[q] = cmul(w[hb], w[q - hb]);
+      }
+    }
+  }
 };
 
 // One complex column per workgroup (consecutive threads take consecutive
-// time indices: contiguous loads and stores), N/16 threads, at most 512 (a
-// larger workgroup leaves too few registers for the radix-16 passes).  The
-// full twiddle table goes to LDS while it is small, the two-level one above
-// that (the data alone then bounds the workgroups per CU).
+// time indices: contiguous loads and stores), N/16 threads: one radix-16
+// butterfly per thread and pass, at most 128 registers from 2U = 4096 on
+// (four waves per SIMD: two workgroups per CU at 4096 and 8192, one of 1024
+// threads at 16384, whose data fills most of LDS).  The full twiddle table
+// goes to LDS while it is small, the two-level one above that.
 template <int N>
 struct ColCfg {
-  static constexpr int NT = N / 16 < 64 ? 64 : (N / 16 > 512 ? 512 : N / 16);
+  static constexpr int NT = N / 16 < 64 ? 64 : (N / 16 > 1024 ? 1024 : N / 16);
   static constexpr bool TWL = N <= 1024;
-  // waves per SIMD the registers must allow: two 512-thread workgroups per CU
-  static constexpr int MINB = N >= 4096 && N <= 8192 ? 4 : 1;
+  // waves per SIMD the registers must allow
+  static constexpr int MINB = N >= 4096 ? 4 : 1;
+  // LDS padding: one slot after every 16 elements.  With one column per
+  // workgroup the first pass writes at a stride of 16 elements (128 bytes)
+  // and the second in runs of 16 a power of two apart: without it all lanes
+  // of a wave meet on one bank, with it at most three share one.
+  static constexpr int SH = 4;
+  static constexpr int SLOTS = N + (N >> SH);
 };
 
 // mode: how the complex columns pair the chunk's real columns.
@@ -140,7 +165,8 @@ __global__ __launch_bounds__(ColCfg<N>::NT, ColCfg<N>::MINB) void k_fft_coltile(
   constexpr int HU = (U + 1 + NT - 1) / NT;
   constexpr bool PRE = N <= 8192;
   using TW = typename std::conditional<ColCfg<N>::TWL, fft::TwLds<N>, TwSplit<N>>::type;
-  __shared__ float2 buf[N];
+  constexpr int SH = ColCfg<N>::SH;
+  __shared__ float2 buf[ColCfg<N>::SLOTS];
   __shared__ float2 twl[ColCfg<N>::TWL ? N : N / 64 + 64];
   TW twz;
   if constexpr (ColCfg<N>::TWL) {
@@ -188,7 +214,7 @@ __global__ __launch_bounds__(ColCfg<N>::NT, ColCfg<N>::MINB) void k_fft_coltile(
       }
     }
   }
-  fft::forward_from_global<N, 1, 1, NT, true>(buf, twz, [&](int row, int) {
+  fft::forward_from_global<N, 1, 1, NT, true, SH>(buf, twz, [&](int row, int) {
     return make_float2(xa[row], hasb ? xb[row] : 0.f);
   });
   if (mode == 2) {
@@ -198,8 +224,9 @@ __global__ __launch_bounds__(ColCfg<N>::NT, ColCfg<N>::MINB) void k_fft_coltile(
       if (kk <= U) {
         const float2 h = PRE ? hv[PRE ? j : 0] : ha[kk];
         const int nk = (N - kk) & (N - 1);
-        buf[kk] = cmul(buf[kk], h);
-        if (nk != kk) buf[nk] = cmul(buf[nk], conjf2(h));
+        const int sk = fft::lds_slot<SH>(kk), snk = fft::lds_slot<SH>(nk);
+        buf[sk] = cmul(buf[sk], h);
+        if (nk != kk) buf[snk] = cmul(buf[snk], conjf2(h));
       }
     }
   } else {
@@ -208,15 +235,16 @@ __global__ __launch_bounds__(ColCfg<N>::NT, ColCfg<N>::MINB) void k_fft_coltile(
       const float2 s = make_float2(0.5f * (a.x + b.x), 0.5f * (a.y + b.y));
       const float2 d = make_float2(0.5f * (a.x - b.x), 0.5f * (a.y - b.y));
       const int nk = (N - kk) & (N - 1);
-      const float2 zk = buf[kk], znk = buf[nk];
-      buf[kk] = cadd(cmul(zk, s), cmul(conjf2(znk), d));
-      if (nk != kk) buf[nk] = cadd(cmul(znk, conjf2(s)), cmul(conjf2(zk), conjf2(d)));
+      const int sk = fft::lds_slot<SH>(kk), snk = fft::lds_slot<SH>(nk);
+      const float2 zk = buf[sk], znk = buf[snk];
+      buf[sk] = cadd(cmul(zk, s), cmul(conjf2(znk), d));
+      if (nk != kk) buf[snk] = cadd(cmul(znk, conjf2(s)), cmul(conjf2(zk), conjf2(d)));
     }
   }
   __syncthreads();
   // outputs U + j -> row j of the pair's columns, in place over the inputs
   // (every input of this workgroup was read in the first pass)
-  fft::inverse_to_global<N, 1, 1, NT, true>(buf, twz, [&](int row, int, float2 v) {
+  fft::inverse_to_global<N, 1, 1, NT, true, SH>(buf, twz, [&](int row, int, float2 v) {
     const int j = row - U;
     xa[j] = v.x;
     if (hasb) xb[j] = v.y;

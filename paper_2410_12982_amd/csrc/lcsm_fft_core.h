@@ -20,6 +20,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 namespace lcsm {
 namespace fft {
 
@@ -75,6 +77,23 @@ struct TwLdsHalf {
     return INV ? make_float2(s * w.x, -s * w.y) : make_float2(s * w.x, s * w.y);
   }
 };
+
+// A twiddle source with a member row<INV, NN, R>(k, w), filling w[q] =
+// w_NN^{q k} for 0 < q < R in one call, gives the passes all twiddles of a
+// butterfly at once (its own way of deriving them from fewer table reads);
+// other sources are asked one twiddle at a time.
+template <class TW, class = void>
+struct HasRow : std::false_type {};
+template <class TW>
+struct HasRow<TW, std::void_t<decltype(TW::kRow)>> : std::true_type {};
+
+template <bool INV, int NN, int R, class TW>
+__device__ __forceinline__ void apply_twiddle_row(const TW& tw, int k, float2 (&v)[R]) {
+  float2 w[R];
+  tw.template row<INV, NN, R>(k, w);
+#pragma unroll
+  for (int q = 1; q < R; ++q) v[q] = cmul(v[q], w[q]);
+}
 
 // Copy w_N^m, m < NM, from the global table of the N-point twiddles into LDS
 // (no synchronisation).
@@ -248,10 +267,28 @@ struct Plan {
   }
 };
 
+// LDS slot of element i: with SH > 0 one padding slot follows every 2^SH
+// elements, which spreads the power-of-two strides of the butterfly outputs
+// over the banks (a buffer of n elements then needs n + n / 2^SH slots).
+template <int SH>
+__device__ __forceinline__ int lds_slot(int i) {
+  if constexpr (SH > 0) return i + (i >> SH);
+  return i;
+}
+
+// Slot distance of an element distance that is a multiple of 2^SH (the
+// padding below the element carries over), a constant where off is one: the
+// passes take their unrolled accesses as immediate offsets from one slot.
+template <int SH>
+__device__ __forceinline__ int lds_step(int off) {
+  if constexpr (SH > 0) return off + (off >> SH);
+  return off;
+}
+
 // One radix-R pass (pass index PS of Plan<N>) in LDS, in place: every thread
 // loads the inputs of all its butterflies, the workgroup synchronises, then
 // every thread writes its outputs.  Callers synchronise before the first pass.
-template <int N, int PS, int WC, int LDSW, int NT, bool INV, class TW>
+template <int N, int PS, int WC, int LDSW, int NT, bool INV, int SH = 0, class TW>
 __device__ __forceinline__ void lds_pass(float2* buf, const TW& tw) {
   constexpr int R = Plan<N>::radix(PS);
   constexpr int P = Plan<N>::p_before(PS);
@@ -263,8 +300,20 @@ __device__ __forceinline__ void lds_pass(float2* buf, const TW& tw) {
     const int u = (int)threadIdx.x + a * NT;
     if (UNITS % NT == 0 || u < UNITS) {
       const int j = u / WC, col = u % WC;
+      if constexpr (SH == 0) {
 #pragma unroll
-      for (int q = 0; q < R; ++q) v[a][q] = buf[(j + q * (N / R)) * LDSW + col];
+        for (int q = 0; q < R; ++q) v[a][q] = buf[(j + q * (N / R)) * LDSW + col];
+      } else {
+        constexpr int ST = N / R * LDSW;
+        const int b = lds_slot<SH>(j * LDSW + col);
+#pragma unroll
+        for (int q = 0; q < R; ++q) {
+          if constexpr (ST % (1 << SH) == 0)
+            v[a][q] = buf[b + lds_step<SH>(q * ST)];
+          else
+            v[a][q] = buf[lds_slot<SH>((j + q * (N / R)) * LDSW + col)];
+        }
+      }
     }
   }
   __syncthreads();
@@ -274,23 +323,37 @@ __device__ __forceinline__ void lds_pass(float2* buf, const TW& tw) {
     if (UNITS % NT == 0 || u < UNITS) {
       const int j = u / WC, col = u % WC;
       const int k = j & (P - 1);
-      if constexpr (P > 1) {
+      if constexpr (P > 1 && HasRow<TW>::value) {
+        apply_twiddle_row<INV, P * R>(tw, k, v[a]);
+      } else if constexpr (P > 1) {
 #pragma unroll
         for (int q = 1; q < R; ++q) v[a][q] = cmul(v[a][q], tw.template get<INV, P * R>(q * k));
       }
       dft<R, INV>(v[a]);
+      if constexpr (SH == 0) {
 #pragma unroll
-      for (int s = 0; s < R; ++s) buf[((j - k) * R + k + s * P) * LDSW + col] = v[a][s];
+        for (int s = 0; s < R; ++s) buf[((j - k) * R + k + s * P) * LDSW + col] = v[a][s];
+      } else {
+        constexpr int PL = P * LDSW;
+        const int b = lds_slot<SH>(((j - k) * R + k) * LDSW + col);
+#pragma unroll
+        for (int s = 0; s < R; ++s) {
+          if constexpr (PL % (1 << SH) == 0)
+            buf[b + lds_step<SH>(s * PL)] = v[a][s];
+          else
+            buf[lds_slot<SH>(((j - k) * R + k + s * P) * LDSW + col)] = v[a][s];
+        }
+      }
     }
   }
   __syncthreads();
 }
 
-template <int N, int PS, int PE, int WC, int LDSW, int NT, bool INV, class TW>
+template <int N, int PS, int PE, int WC, int LDSW, int NT, bool INV, int SH = 0, class TW>
 __device__ __forceinline__ void lds_passes(float2* buf, const TW& tw) {
   if constexpr (PS < PE) {
-    lds_pass<N, PS, WC, LDSW, NT, INV>(buf, tw);
-    lds_passes<N, PS + 1, PE, WC, LDSW, NT, INV>(buf, tw);
+    lds_pass<N, PS, WC, LDSW, NT, INV, SH>(buf, tw);
+    lds_passes<N, PS + 1, PE, WC, LDSW, NT, INV, SH>(buf, tw);
   }
 }
 
@@ -298,7 +361,7 @@ __device__ __forceinline__ void lds_passes(float2* buf, const TW& tw) {
 // load(row, col) instead of from LDS; only rows < N*QIN/R are fetched (the
 // rest are zero: QIN = R/2 for a zero-padded upper half, R for full input).
 // Writes its outputs to LDS and synchronises.
-template <int N, int WC, int LDSW, int NT, bool INV, bool HALF, class Load>
+template <int N, int WC, int LDSW, int NT, bool INV, bool HALF, int SH = 0, class Load>
 __device__ __forceinline__ void first_pass_global(float2* buf, const Load& load) {
   constexpr int R = Plan<N>::radix(0);
   constexpr int QIN = HALF ? R / 2 : R;
@@ -320,8 +383,22 @@ __device__ __forceinline__ void first_pass_global(float2* buf, const Load& load)
     if (UNITS % NT == 0 || u < UNITS) {
       const int j = u / WC, col = u % WC;
       dft<R, INV>(v[a]);
+      if constexpr (SH == 0) {
 #pragma unroll
-      for (int s = 0; s < R; ++s) buf[(j * R + s) * LDSW + col] = v[a][s];
+        for (int s = 0; s < R; ++s) buf[(j * R + s) * LDSW + col] = v[a][s];
+      } else {
+        // one column only: j R is a multiple of R, so for s < R the slot of
+        // j R + s is that of j R plus s plus the padding within s
+        static_assert(LDSW == 1, "padded LDS holds one column");
+        const int b = lds_slot<SH>(j * R);
+#pragma unroll
+        for (int s = 0; s < R; ++s) {
+          if constexpr (R <= (1 << SH))
+            buf[b + s] = v[a][s];
+          else
+            buf[b + s + (s >> SH)] = v[a][s];
+        }
+      }
     }
   }
   __syncthreads();
@@ -330,7 +407,8 @@ __device__ __forceinline__ void first_pass_global(float2* buf, const Load& load)
 // Last pass (index NP-1, p = N/R) reading LDS and handing the outputs of
 // rows >= N/2 (HALF) or of all rows to store(row, col, value) instead of
 // writing LDS.  No synchronisation at the end (LDS is only read).
-template <int N, int WC, int LDSW, int NT, bool INV, bool HALF, class TW, class Store>
+template <int N, int WC, int LDSW, int NT, bool INV, bool HALF, int SH = 0, class TW,
+          class Store>
 __device__ __forceinline__ void last_pass_global(const float2* buf, const TW& tw,
                                                  const Store& store) {
   constexpr int PS = Plan<N>::NP - 1;
@@ -346,9 +424,23 @@ __device__ __forceinline__ void last_pass_global(const float2* buf, const TW& tw
     if (UNITS % NT == 0 || u < UNITS) {
       const int j = u / WC, col = u % WC;  // j < P, so k = j
       float2 v[R];
+      if constexpr (SH == 0) {
 #pragma unroll
-      for (int q = 0; q < R; ++q) v[q] = buf[(j + q * (N / R)) * LDSW + col];
-      if constexpr (P > 1) {
+        for (int q = 0; q < R; ++q) v[q] = buf[(j + q * (N / R)) * LDSW + col];
+      } else {
+        constexpr int ST = N / R * LDSW;
+        const int b = lds_slot<SH>(j * LDSW + col);
+#pragma unroll
+        for (int q = 0; q < R; ++q) {
+          if constexpr (ST % (1 << SH) == 0)
+            v[q] = buf[b + lds_step<SH>(q * ST)];
+          else
+            v[q] = buf[lds_slot<SH>((j + q * (N / R)) * LDSW + col)];
+        }
+      }
+      if constexpr (P > 1 && HasRow<TW>::value) {
+        apply_twiddle_row<INV, N>(tw, j, v);
+      } else if constexpr (P > 1) {
 #pragma unroll
         for (int q = 1; q < R; ++q) v[q] = cmul(v[q], tw.template get<INV, N>(q * j));
       }
@@ -361,18 +453,18 @@ __device__ __forceinline__ void last_pass_global(const float2* buf, const TW& tw
 
 // Forward transform whose input is fetched by load(): first pass from
 // global, the rest in LDS.  Result in LDS, natural order.
-template <int N, int WC, int LDSW, int NT, bool HALF, class TW, class Load>
+template <int N, int WC, int LDSW, int NT, bool HALF, int SH = 0, class TW, class Load>
 __device__ __forceinline__ void forward_from_global(float2* buf, const TW& tw, const Load& load) {
-  first_pass_global<N, WC, LDSW, NT, false, HALF>(buf, load);
-  lds_passes<N, 1, Plan<N>::NP, WC, LDSW, NT, false>(buf, tw);
+  first_pass_global<N, WC, LDSW, NT, false, HALF, SH>(buf, load);
+  lds_passes<N, 1, Plan<N>::NP, WC, LDSW, NT, false, SH>(buf, tw);
 }
 
 // Inverse transform of the LDS contents whose outputs go to store() (rows >=
 // N/2 only when HALF).  The caller synchronises before.
-template <int N, int WC, int LDSW, int NT, bool HALF, class TW, class Store>
+template <int N, int WC, int LDSW, int NT, bool HALF, int SH = 0, class TW, class Store>
 __device__ __forceinline__ void inverse_to_global(float2* buf, const TW& tw, const Store& store) {
-  lds_passes<N, 0, Plan<N>::NP - 1, WC, LDSW, NT, true>(buf, tw);
-  last_pass_global<N, WC, LDSW, NT, true, HALF>(buf, tw, store);
+  lds_passes<N, 0, Plan<N>::NP - 1, WC, LDSW, NT, true, SH>(buf, tw);
+  last_pass_global<N, WC, LDSW, NT, true, HALF, SH>(buf, tw, store);
 }
 
 // Hardware dispatches workgroup b to XCD b mod 8.  Remap so that XCD x runs a
