@@ -160,7 +160,7 @@ def kernel_key(name):
         if m.group(2) == "false":
             return ("direct", u)
         return ("fused", u) if u else ("red", 0)
-    m = re.search(r"k_fft_tile<(\d+), (true|false)(, (true|false))*>", name)
+    m = re.search(r"k_fft_tile<(\d+), (true|false)(, (true|false))*(, \d+)?>", name)
     if m:
         return ("fft_lds", int(m.group(1)) // 2)
     # the column-chunk tile: two transposes around the transform, per chunk

@@ -157,7 +157,7 @@ __device__ __forceinline__ int panel_of(int r, int B, int hgroup) {
 // i-U+dst_len) instead of added into rows [i, i+dst_len).  The workgroup has
 // read all inputs of its columns (the first pass, before the barriers of the
 // LDS passes) before it stores, and no other workgroup touches its columns.
-template <int N, bool RED, bool FAST, bool STORE = false>
+template <int N, bool RED, bool FAST, bool STORE = false, int WCX = Cfg<N>::WC>
 __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_tile(float* __restrict__ S,
                                                          const float2* __restrict__ H,
                                                          const float2* __restrict__ tw,
@@ -167,7 +167,7 @@ __global__ __launch_bounds__(Cfg<N>::NT) void k_fft_tile(float* __restrict__ S,
                                                          int BD, int D, int B, int i, int dst_len,
                                                          int ppl, int hgroup) {
   static_assert(!(RED && STORE), "the in-place store has no red cell");
-  constexpr int WC = Cfg<N>::WC, NT = Cfg<N>::NT, U = N / 2;
+  constexpr int WC = WCX, NT = Cfg<N>::NT, U = N / 2;
   using P = fft::Plan<N>;
   __shared__ float2 buf[N * WC];
   __shared__ float2 twl[Cfg<N>::TWN];
@@ -667,43 +667,60 @@ __global__ __launch_bounds__(Cfg<N2>::NT) void k_fft_rows_inv(const float2* __re
 #define LCSM_POW2_CASES(X) \
   X(4) X(8) X(16) X(32) X(64) X(128) X(256) X(512) X(1024) X(2048) X(4096) X(8192)
 
+// Panel width WC of the single-pass tiles is Cfg<N>::WC, except at 2U = 128
+// and 256 when the launch has many columns: there 8-column panels (64-byte
+// row runs instead of 32) take the tile 25 % faster at 55K and 1M columns,
+// while at a few thousand columns the halved workgroup count leaves CUs idle.
+constexpr int kWideWC = 8;
+constexpr long long kWideMinCols = 1LL << 14;  // M*B*D
+
+template <int NN, int WC>
+hipError_t tile_panels(float* S, const float2* H, const float2* tw, const float* Hf,
+                       const float* yt, float* zt, const Shape& s, int i, int dst_len,
+                       bool in_place, hipStream_t st) {
+  const int ppl = (s.BD + 2 * WC - 1) / (2 * WC);
+  const int hgroup = (s.D % (2 * WC) == 0) ? s.D / (2 * WC) : 0;
+  const dim3 grid((unsigned)(ppl * s.M)), block(Cfg<NN>::NT);
+  const bool fast = hgroup > 0 && dst_len == NN / 2;
+#define LCSM_TILE(RED, FAST, STORE)                                                          \
+  hipLaunchKernelGGL((k_fft_tile<NN, RED, FAST, STORE, WC>), grid, block, 0, st, S, H, tw, Hf, \
+                     yt, zt, s.L, s.SL, s.BD, s.D, s.B, i, dst_len, ppl, hgroup)
+  if (yt) {
+    if constexpr (NN <= kMaxRedFftN) {
+      if (fast)
+        LCSM_TILE(true, true, false);
+      else
+        LCSM_TILE(true, false, false);
+    } else {
+      return hipErrorInvalidValue;
+    }
+  } else if (in_place) {
+    if (fast)
+      LCSM_TILE(false, true, true);
+    else
+      LCSM_TILE(false, false, true);
+  } else if (fast) {
+    LCSM_TILE(false, true, false);
+  } else {
+    LCSM_TILE(false, false, false);
+  }
+#undef LCSM_TILE
+  return hipGetLastError();
+}
+
 hipError_t tile_single(int N, float* S, const float2* H, const float2* tw, const float* Hf,
                        const float* yt, float* zt, const Shape& s, int i, int dst_len,
                        bool in_place, hipStream_t st) {
-#define LCSM_TILE_ARGS S, H, tw, Hf, yt, zt, s.L, s.SL, s.BD, s.D, s.B, i, dst_len, ppl, hgroup
-#define LCSM_CASE(NN)                                                                             \
-  case NN: {                                                                                      \
-    constexpr int WC = Cfg<NN>::WC;                                                               \
-    const int ppl = (s.BD + 2 * WC - 1) / (2 * WC);                                               \
-    const int hgroup = (s.D % (2 * WC) == 0) ? s.D / (2 * WC) : 0;                                \
-    const dim3 grid((unsigned)(ppl * s.M)), block(Cfg<NN>::NT);                                   \
-    const bool fast = hgroup > 0 && dst_len == NN / 2;                                            \
-    if (yt) {                                                                                     \
-      if constexpr (NN <= kMaxRedFftN) {                                                          \
-        if (fast)                                                                                 \
-          hipLaunchKernelGGL((k_fft_tile<NN, true, true>), grid, block, 0, st, LCSM_TILE_ARGS);   \
-        else                                                                                      \
-          hipLaunchKernelGGL((k_fft_tile<NN, true, false>), grid, block, 0, st, LCSM_TILE_ARGS);  \
-      } else {                                                                                    \
-        return hipErrorInvalidValue;                                                              \
-      }                                                                                           \
-    } else if (in_place) {                                                                        \
-      if (fast)                                                                                   \
-        hipLaunchKernelGGL((k_fft_tile<NN, false, true, true>), grid, block, 0, st,               \
-                           LCSM_TILE_ARGS);                                                       \
-      else                                                                                        \
-        hipLaunchKernelGGL((k_fft_tile<NN, false, false, true>), grid, block, 0, st,              \
-                           LCSM_TILE_ARGS);                                                       \
-    } else if (fast) {                                                                            \
-      hipLaunchKernelGGL((k_fft_tile<NN, false, true>), grid, block, 0, st, LCSM_TILE_ARGS);      \
-    } else {                                                                                      \
-      hipLaunchKernelGGL((k_fft_tile<NN, false, false>), grid, block, 0, st, LCSM_TILE_ARGS);     \
-    }                                                                                             \
-    return hipGetLastError();                                                                     \
-  }
+  const bool wide = (long long)s.M * s.BD >= kWideMinCols;
+#define LCSM_CASE(NN)                                                                      \
+  case NN:                                                                                 \
+    if constexpr (NN == 128 || NN == 256) {                                                \
+      if (wide)                                                                            \
+        return tile_panels<NN, kWideWC>(S, H, tw, Hf, yt, zt, s, i, dst_len, in_place, st); \
+    }                                                                                      \
+    return tile_panels<NN, Cfg<NN>::WC>(S, H, tw, Hf, yt, zt, s, i, dst_len, in_place, st);
   switch (N) { LCSM_POW2_CASES(LCSM_CASE) }
 #undef LCSM_CASE
-#undef LCSM_TILE_ARGS
   return hipErrorInvalidValue;
 }
 

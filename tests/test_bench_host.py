@@ -1,0 +1,108 @@
+"""Host logic of bench.py (no GPU): the mapping of profiled kernel names to
+the per-launch pass's (kernel, U) keys, the aggregation of counter rows into
+one entry per tile, the algorithmic-bytes formula on hand-counted cases, the
+digest's file list, and the refusal of more than one GPU."""
+import os
+import subprocess
+import sys
+
+import pytest
+
+import bench
+import datagen
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.mark.parametrize("name,key", [
+    ("void lcsm::(anonymous namespace)::k_step_fused<1, true>(float*, int)", ("fused", 1)),
+    ("lcsm::k_step_fused<32, true>", ("fused", 32)),
+    ("lcsm::k_step_fused<0, true>", ("red", 0)),
+    ("lcsm::k_step_fused<8, false>", ("direct", 8)),
+    ("lcsm::k_fft_tile<8192, false, true, false>", ("fft_lds", 4096)),
+    ("lcsm::k_fft_tile<4096, true, true, false, 4>", ("fft_lds", 2048)),
+    ("lcsm::k_fft_tile<128, true, false, false, 8>(float*, float2 const*)", ("fft_lds", 64)),
+    ("lcsm::k_fft_coltile<16384>", ("fft_col", 8192)),
+    ("lcsm::k_rows_to_cols", ("fft_col", None)),
+    ("lcsm::k_cols_to_rows<false>", ("fft_col", None)),
+    ("at::native::vectorized_elementwise_kernel<4, ...>", None),
+    ("lcsm::k_fft_spectra<1024>", None),
+])
+def test_kernel_key(name, key):
+    assert bench.kernel_key(name) == key
+
+
+def _row(i, name, kib):
+    return {"Dispatch_Id": str(i), "Kernel_Name": name, "Counter_Value": str(kib)}
+
+
+def test_tile_bytes_sums_a_column_tile_with_its_red_cell():
+    """Dispatch order of two positions: a fused step; then the red cell and
+    two column chunks (transpose, transform, transpose each) of the U = 4096
+    tile; then a fused step and a wide-panel FFT tile.  The column tile's
+    entry is the red cell plus its six dispatches; the other launches stay
+    separate; rows arrive out of order and are sorted by dispatch id."""
+    order = [
+        ("lcsm::k_step_fused<1, true>", 1.0),
+        ("lcsm::k_step_fused<0, true>", 0.5),
+        ("lcsm::k_rows_to_cols", 20.0),
+        ("lcsm::k_fft_coltile<8192>", 100.0),
+        ("lcsm::k_cols_to_rows<false>", 30.0),
+        ("lcsm::k_rows_to_cols", 21.0),
+        ("lcsm::k_fft_coltile<8192>", 101.0),
+        ("lcsm::k_cols_to_rows<false>", 31.0),
+        ("lcsm::k_step_fused<1, true>", 2.0),
+        ("lcsm::k_fft_tile<256, true, true, false, 8>", 7.0),
+    ]
+    rows = [_row(i, n, v) for i, (n, v) in enumerate(order)]
+    per = bench.tile_bytes(rows[::-1])
+    assert per[("fft_col", 4096)] == [1024.0 * (0.5 + 20 + 100 + 30 + 21 + 101 + 31)]
+    assert per[("fused", 1)] == [1024.0, 2048.0]
+    assert per[("fft_lds", 128)] == [7 * 1024.0]
+    assert ("red", 0) not in per
+
+
+def test_tile_bytes_keeps_a_lone_red_cell():
+    rows = [_row(1, "lcsm::k_step_fused<0, true>", 0.25),
+            _row(2, "lcsm::k_fft_tile<8192, false, true, false>", 50.0)]
+    per = bench.tile_bytes(rows)
+    assert per[("red", 0)] == [256.0]
+    assert per[("fft_lds", 4096)] == [50 * 1024.0]
+
+
+def test_launch_bytes_hand_counted():
+    """One layer, B = 1, D = 2 (2 columns): red cell 16 B per column; a
+    fused U = 2 step adds 4 (U - 1) + 8U per column and 4 (2U - 1) lags per
+    channel; an FFT tile of U = 4 adds 4 (U - 1) + 8U per column and
+    8 (U + 1) spectrum bytes per channel."""
+    w = datagen.Workload("hand", 1, 1, 2, 64, decay=1.0, seed=0)
+    assert bench.launch_bytes("red", 0, w) == 2 * 16
+    assert bench.launch_bytes("fused", 2, w) == 2 * (16 + 4 + 16) + 2 * 4 * 3
+    assert bench.launch_bytes("fft_lds", 4, w) == 2 * (16 + 12 + 32) + 2 * 8 * 5
+
+
+def test_source_digest_files_exist_and_change_with_content(tmp_path, monkeypatch):
+    csrc = os.path.join(ROOT, "paper_2410_12982_amd", "csrc")
+    for f in bench.COUNTED_SOURCES:
+        assert os.path.isfile(os.path.join(csrc, f)), f
+    d0 = bench.source_digest()
+    assert len(d0) == 16 and d0 == bench.source_digest()
+    # the same digest over a copy, then over the copy with one byte changed
+    fake = tmp_path / "paper_2410_12982_amd" / "csrc"
+    fake.mkdir(parents=True)
+    for f in bench.COUNTED_SOURCES:
+        with open(os.path.join(csrc, f), "rb") as src:
+            (fake / f).write_bytes(src.read())
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    assert bench.source_digest() == d0
+    p = fake / bench.COUNTED_SOURCES[0]
+    p.write_bytes(p.read_bytes() + b" ")
+    assert bench.source_digest() != d0
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+    assert r.stdout == ""

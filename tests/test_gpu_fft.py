@@ -98,6 +98,31 @@ def test_integer_data_panel_orders_and_clipped_large_tiles(opt, shape):
     assert np.array_equal(np.rint(z).astype(np.int64), ex)
 
 
+@pytest.mark.parametrize("half", [False, True])
+@pytest.mark.parametrize("opt", ["default", "lds_from_2"])
+@pytest.mark.parametrize("shape", [(1, 2, 8192, 260), (2, 3, 2731, 200), (1, 5, 3300, 140)])
+def test_integer_data_wide_panels(opt, shape, half):
+    """From 2^14 columns the single-pass tiles of 2U = 128 and 256 use panels
+    of 8 complex columns: whole panels inside a batch row (8192 channels),
+    an odd column count per layer (2731 channels, 3 batch rows), channels
+    not a whole number of panels (3300), a clipped destination (L = 260 cuts
+    the U = 128 tile of i = 256), and, with half-state storage, the in-place
+    tile of i = T = 128 at 2U = 256."""
+    M, B, D, L = shape
+    say(f"[int fft wide panels] M={M} B={B} D={D} L={L} options={opt} half_state={half}")
+    w, h, y = _int_case(M, B, D, L, 3, seed=7 * sum(shape))
+    opts = dict(FFT_OPTIONS[opt] or {})
+    if half:
+        opts["half_state"] = 1
+    ctx, _ = make_ctx(w, torch.from_numpy(h).to(dev()), opts or None)
+    z = _run_full(ctx, torch.from_numpy(y).to(dev()))
+    ex = _exact(h, y)
+    err = np.abs(z.astype(np.float64) - ex).max()
+    say(f"  max abs err {err:.3e}")
+    assert err < 0.25
+    assert np.array_equal(np.rint(z).astype(np.int64), ex)
+
+
 @pytest.mark.parametrize("opt", ["lds_from_2", "multipass_from_16", "tiny_scratch", "default",
                                  "col_from_4"])
 def test_m1b8d768l8k_teacher_forced_all_columns(opt):
