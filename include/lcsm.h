@@ -138,6 +138,34 @@ int lcsm_step_layer(lcsm_ctx* ctx, int layer, const float* y, float* z);
  * every layer at position t; advances t.  Errors: LCSM_ESTATE otherwise. */
 int lcsm_advance(lcsm_ctx* ctx);
 
+/* Views for callers that fuse the red cell into their own kernel (the
+ * kernel that produces y_t, e.g. a block's epilogue), as the red line of
+ * Alg. 1 / Alg. 3 allows: z^m_t = fmaf(h^m_0[d], y^m_t[b,d], acc^m_t[b,d]).
+ *
+ * lcsm_h0: *h0 = device pointer to the lag-0 taps, h^m_0[d] at
+ *   (*h0)[m * *layer_stride + d] (the library's lag-major filter copy; valid
+ *   until lcsm_destroy).  Host only.  Errors: LCSM_EINVAL for null pointers.
+ *
+ * lcsm_pending: *acc = device pointer to the accumulators of the current
+ *   position t, acc^m_t[b,d] at (*acc)[m * *layer_stride + b*D + d]: the sum
+ *   of all contributions of earlier positions (every one of them comes from
+ *   a gray tile queued before step t, so the values are complete once the
+ *   context's stream has passed the work queued so far).  The pointer is
+ *   valid for position t only: the row moves with every step (and, with
+ *   half_state, wraps at T).  Host only.  Errors: LCSM_EINVAL, LCSM_EDONE
+ *   once t = L, LCSM_ESTATE after a fault.
+ *
+ * lcsm_commit: the caller has done the red cell of every layer at t in
+ *   place, in stream order before this call: read acc^m_t from the pending
+ *   row, computed z^m_t with the fmaf above, and written y^m_t over it (the
+ *   slot of position t holds the input from then on, Sec. 3.3).  Queues the
+ *   gray tiles of i = t+1 for all layers and advances t, as lcsm_advance.
+ *   Errors: LCSM_EDONE once t = L, LCSM_ESTATE after a fault or between
+ *   lcsm_step_layer calls, LCSM_EDEVICE. */
+int lcsm_h0(const lcsm_ctx* ctx, const float** h0, size_t* layer_stride);
+int lcsm_pending(lcsm_ctx* ctx, float** acc, size_t* layer_stride);
+int lcsm_commit(lcsm_ctx* ctx);
+
 /* Run n consecutive lcsm_step calls: step k reads y + k*y_stride and writes
  * z + k*z_stride (strides in floats).  Equivalent to the loop of single
  * steps, with one host call.  Errors as lcsm_step; stops at the first. */
@@ -179,6 +207,11 @@ int lcsm_position(const lcsm_ctx* ctx, int* t);
  * other outputs are 0.  Errors: LCSM_EINVAL. */
 int lcsm_plan_tile(int M, int B, int D, int L, const lcsm_options* opt, int t, int* i, int* U,
                    int* dst_len, int* kind);
+
+/* The same schedule query for this context's shape and options (Alg. 3's
+ * gray phase after step t; outputs as lcsm_plan_tile).  Host only.
+ * Errors: LCSM_EINVAL for null pointers or t outside [0, L). */
+int lcsm_tile(const lcsm_ctx* ctx, int t, int* i, int* U, int* dst_len, int* kind);
 
 /* Release the context and, if the library allocated it, the workspace.
  * Waits for the context's stream.  NULL is ignored. */

@@ -537,6 +537,50 @@ int lcsm_plan_tile(int M, int B, int D, int L, const lcsm_options* opt, int t, i
   return LCSM_OK;
 }
 
+int lcsm_tile(const lcsm_ctx* c, int t, int* i, int* U, int* dst_len, int* kind) {
+  if (!c || !i || !U || !dst_len || !kind) return LCSM_EINVAL;
+  if (t < 0 || t >= c->s.L) return LCSM_EINVAL;
+  const int ii = t + 1;
+  if (ii >= c->s.L) {
+    *i = *U = *dst_len = 0;
+    *kind = LCSM_TILE_NONE;
+    return LCSM_OK;
+  }
+  const int u = lowbit(ii);
+  *i = ii;
+  *U = u;
+  *dst_len = u < c->s.L - ii ? u : c->s.L - ii;
+  *kind = tile_kind(c->opt, c->s, u);
+  return LCSM_OK;
+}
+
+int lcsm_h0(const lcsm_ctx* c, const float** h0, size_t* layer_stride) {
+  if (!c || !h0 || !layer_stride) return LCSM_EINVAL;
+  *h0 = c->Hf;
+  *layer_stride = (size_t)c->s.L * c->s.D;
+  return LCSM_OK;
+}
+
+int lcsm_pending(lcsm_ctx* c, float** acc, size_t* layer_stride) {
+  if (!c || !acc || !layer_stride) return LCSM_EINVAL;
+  if (c->faulted) return LCSM_ESTATE;
+  if (c->t >= c->s.L) return LCSM_EDONE;
+  const int row = (c->T && c->t >= c->T) ? c->t - c->T : c->t;  // half-state: rows wrap at T
+  *acc = c->S + (size_t)row * c->s.BD;
+  *layer_stride = (size_t)c->s.SL * c->s.BD;
+  return LCSM_OK;
+}
+
+int lcsm_commit(lcsm_ctx* c) {
+  if (!c) return LCSM_EINVAL;
+  if (c->faulted) return LCSM_ESTATE;
+  if (c->t >= c->s.L) return LCSM_EDONE;
+  if (c->layers_done != 0)
+    return fail(c, LCSM_ESTATE, "lcsm_commit during a per-layer position", hipSuccess);
+  c->layers_done = c->s.M;
+  return lcsm_advance(c);
+}
+
 void lcsm_destroy(lcsm_ctx* c) {
   if (!c) return;
   (void)hipStreamSynchronize(c->stream);

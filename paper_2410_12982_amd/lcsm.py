@@ -75,6 +75,10 @@ _SIGS = {
     "lcsm_position": (ctypes.c_int, [_vp, _c_int_p]),
     "lcsm_plan_tile": (ctypes.c_int, [ctypes.c_int] * 4 + [ctypes.POINTER(Options), ctypes.c_int]
                        + [_c_int_p] * 4),
+    "lcsm_tile": (ctypes.c_int, [_vp, ctypes.c_int] + [_c_int_p] * 4),
+    "lcsm_h0": (ctypes.c_int, [_vp, ctypes.POINTER(_vp), ctypes.POINTER(ctypes.c_size_t)]),
+    "lcsm_pending": (ctypes.c_int, [_vp, ctypes.POINTER(_vp), ctypes.POINTER(ctypes.c_size_t)]),
+    "lcsm_commit": (ctypes.c_int, [_vp]),
     "lcsm_destroy": (None, [_vp]),
     "lcsm_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "lcsm_last_error": (ctypes.c_char_p, [_vp]),
@@ -272,6 +276,46 @@ class Lcsm:
 
     def plan(self, t):
         return plan_tile(self.M, self.B, self.D, self.L, t, self._opts_obj)
+
+    def tile(self, t):
+        """(i, U, dst_len, kind) of the gray tile this context queues after step t."""
+        i, U, n, k = (ctypes.c_int() for _ in range(4))
+        self._check(_lib.lcsm_tile(self._ctx, int(t), ctypes.byref(i), ctypes.byref(U),
+                                   ctypes.byref(n), ctypes.byref(k)), "lcsm_tile")
+        return i.value, U.value, n.value, k.value
+
+    def _ws_view(self, ptr, stride, rows, rowlen, what):
+        """[rows, rowlen] fp32 view of the workspace at device address ptr,
+        row k at ptr + k*stride floats (the library's buffers live in the
+        workspace tensor this object owns)."""
+        import torch
+        base = self.workspace.data_ptr()
+        off = ptr - base
+        end = off + 4 * ((rows - 1) * stride + rowlen)
+        if off < 0 or off % 4 or end > self.workspace.numel():
+            raise LcsmError(LCSM_EINVAL, what, "view outside the workspace")
+        flat = self.workspace.view(torch.float32)
+        return flat.as_strided((rows, rowlen), (stride, 1), off // 4)
+
+    def h0(self):
+        """Lag-0 taps h[m, d, 0] as a [M, D] view of the library's filter copy."""
+        p, st = _vp(), ctypes.c_size_t()
+        self._check(_lib.lcsm_h0(self._ctx, ctypes.byref(p), ctypes.byref(st)), "lcsm_h0")
+        return self._ws_view(p.value, st.value, self.M, self.D, "lcsm_h0")
+
+    def pending(self):
+        """Accumulators of the current position t as a [M, B, D] view of the
+        state (valid for this position only); see lcsm_commit."""
+        p, st = _vp(), ctypes.c_size_t()
+        self._check(_lib.lcsm_pending(self._ctx, ctypes.byref(p), ctypes.byref(st)),
+                    "lcsm_pending")
+        v = self._ws_view(p.value, st.value, self.M, self.B * self.D, "lcsm_pending")
+        return v.view(self.M, self.B, self.D)
+
+    def commit(self):
+        """After the caller's own red cells at t (z = fmaf(h0, y, acc), y
+        written over the pending row): queue the gray tiles, advance t."""
+        self._check(_lib.lcsm_commit(self._ctx), "lcsm_commit")
 
     def close(self):
         if self._ctx:

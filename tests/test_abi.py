@@ -19,7 +19,7 @@ def _declared():
     names = set()
     for path in glob.glob(os.path.join(ROOT, "include", "*.h")):
         text = re.sub(r"/\*.*?\*/", "", open(path).read(), flags=re.S)
-        names |= set(re.findall(r"\b(lcsm_[a-z_]+)\s*\(", text))
+        names |= set(re.findall(r"\b(lcsm_[a-z0-9_]+)\s*\(", text))
     return sorted(names)
 
 
@@ -208,6 +208,13 @@ def test_null_context_calls():
     assert lib.lcsm_run(None, 1, fake, 0, fake, 0) == lcsm.LCSM_EINVAL
     t = ctypes.c_int()
     assert lib.lcsm_position(None, ctypes.byref(t)) == lcsm.LCSM_EINVAL
+    i, U, n, k = (ctypes.c_int() for _ in range(4))
+    assert lib.lcsm_tile(None, 0, ctypes.byref(i), ctypes.byref(U), ctypes.byref(n),
+                         ctypes.byref(k)) == lcsm.LCSM_EINVAL
+    p, st = ctypes.c_void_p(), ctypes.c_size_t()
+    assert lib.lcsm_h0(None, ctypes.byref(p), ctypes.byref(st)) == lcsm.LCSM_EINVAL
+    assert lib.lcsm_pending(None, ctypes.byref(p), ctypes.byref(st)) == lcsm.LCSM_EINVAL
+    assert lib.lcsm_commit(None) == lcsm.LCSM_EINVAL
     lib.lcsm_destroy(None)
     assert lib.lcsm_last_error(None) == b""
 
