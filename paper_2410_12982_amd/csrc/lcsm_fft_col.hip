@@ -92,6 +92,91 @@ __global__ __launch_bounds__(kTThreads) void k_cols_to_rows(const float* __restr
   }
 }
 
+// The two transposes with 16-byte accesses on both sides, for B*D, the
+// column length ldx and the row count multiples of 4 (then every float4 lies
+// in one layer's row and is aligned): a wavefront moves four 256-byte row
+// segments (or four column runs) per instruction instead of one.  LDS keeps
+// 4-byte elements with a pitch of 65: the row-side lanes (4 rows x 16 float4)
+// and the column-side lanes (16 x 4 rows of 4 columns) both meet 64 distinct
+// banks.
+__global__ __launch_bounds__(kTThreads) void k_rows_to_cols4(const float* __restrict__ S,
+                                                             size_t lstride, int BD, int row0,
+                                                             int nrows, long long g0, int ncols,
+                                                             float* __restrict__ X, int ldx) {
+  __shared__ float tile[kTT][kTT + 1];
+  const int cb = (int)blockIdx.x * kTT, rb = (int)blockIdx.y * kTT;
+  const int q4 = (int)threadIdx.x & 15, r16 = (int)threadIdx.x >> 4;
+  const int col = cb + 4 * q4;
+  if (col < ncols) {
+    const long long g = g0 + col;
+    const long long m = g / BD;
+    const int c = (int)(g - m * BD);
+    const float* src = S + (size_t)m * lstride + (size_t)row0 * BD + c;
+#pragma unroll
+    for (int k = 0; k < kTT / 16; ++k) {
+      const int r = r16 + 16 * k;
+      if (rb + r < nrows) {
+        const float4 v = *reinterpret_cast<const float4*>(src + (size_t)(rb + r) * BD);
+        tile[r][4 * q4] = v.x;
+        tile[r][4 * q4 + 1] = v.y;
+        tile[r][4 * q4 + 2] = v.z;
+        tile[r][4 * q4 + 3] = v.w;
+      }
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < kTT / 16; ++k) {
+    const int cc = r16 + 16 * k, r = 4 * q4;
+    if (cb + cc < ncols && rb + r < nrows) {
+      const float4 v = make_float4(tile[r][cc], tile[r + 1][cc], tile[r + 2][cc], tile[r + 3][cc]);
+      *reinterpret_cast<float4*>(X + (size_t)(cb + cc) * ldx + rb + r) = v;
+    }
+  }
+}
+
+template <bool STORE>
+__global__ __launch_bounds__(kTThreads) void k_cols_to_rows4(const float* __restrict__ X, int ldx,
+                                                             float* __restrict__ S, size_t lstride,
+                                                             int BD, int row0, int nrows,
+                                                             long long g0, int ncols) {
+  __shared__ float tile[kTT][kTT + 1];
+  const int cb = (int)blockIdx.x * kTT, rb = (int)blockIdx.y * kTT;
+  const int q4 = (int)threadIdx.x & 15, r16 = (int)threadIdx.x >> 4;
+#pragma unroll
+  for (int k = 0; k < kTT / 16; ++k) {
+    const int cc = r16 + 16 * k, r = 4 * q4;
+    if (cb + cc < ncols && rb + r < nrows) {
+      const float4 v = *reinterpret_cast<const float4*>(X + (size_t)(cb + cc) * ldx + rb + r);
+      tile[r][cc] = v.x;
+      tile[r + 1][cc] = v.y;
+      tile[r + 2][cc] = v.z;
+      tile[r + 3][cc] = v.w;
+    }
+  }
+  __syncthreads();
+  const int col = cb + 4 * q4;
+  if (col >= ncols) return;
+  const long long g = g0 + col;
+  const long long m = g / BD;
+  const int c = (int)(g - m * BD);
+  float* dst = S + (size_t)m * lstride + (size_t)row0 * BD + c;
+#pragma unroll
+  for (int k = 0; k < kTT / 16; ++k) {
+    const int r = r16 + 16 * k;
+    if (rb + r < nrows) {
+      float4* p = reinterpret_cast<float4*>(dst + (size_t)(rb + r) * BD);
+      float4 o = make_float4(tile[r][4 * q4], tile[r][4 * q4 + 1], tile[r][4 * q4 + 2],
+                             tile[r][4 * q4 + 3]);
+      if constexpr (!STORE) {
+        const float4 a = *p;
+        o = make_float4(a.x + o.x, a.y + o.y, a.z + o.z, a.w + o.w);
+      }
+      *p = o;
+    }
+  }
+}
+
 // Two-level twiddles in LDS: w_N^f = hi[f >> 6] * lo[f & 63] with
 // hi[j] = w_N^{64 j} (N/64 entries) and lo[l] = w_N^l (64 entries), both
 // copied from the fp64-derived global table; one complex product per
@@ -277,11 +362,20 @@ hipError_t launch_fft_col_tile(float* S, const float2* Hc, const float2* tw, con
   const int mode = layers && s.B % 2 == 0 ? 2 : (layers && s.D % 2 == 0 ? 1 : 0);
   float* X = reinterpret_cast<float*>(scratch);
   const size_t lstride = (size_t)s.SL * s.BD;
+  // 16-byte transposes: whole float4s in one layer's rows (B*D, and with it
+  // every chunk start, a multiple of 4) and in the columns (U and the rows
+  // moved back multiples of 4)
+  const bool vin = s.BD % 4 == 0 && U % 4 == 0;
+  const bool vout = vin && dst_len % 4 == 0;
   for (long long g0 = 0; g0 < total; g0 += chunk) {
     const int nc = (int)(total - g0 < chunk ? total - g0 : chunk);
     const dim3 tin((unsigned)((nc + kTT - 1) / kTT), (unsigned)((U + kTT - 1) / kTT));
-    hipLaunchKernelGGL(k_rows_to_cols, tin, dim3(kTThreads), 0, st, S, lstride, s.BD, i - U, U, g0,
-                       nc, X, U);
+    if (vin)
+      hipLaunchKernelGGL(k_rows_to_cols4, tin, dim3(kTThreads), 0, st, S, lstride, s.BD, i - U, U,
+                         g0, nc, X, U);
+    else
+      hipLaunchKernelGGL(k_rows_to_cols, tin, dim3(kTThreads), 0, st, S, lstride, s.BD, i - U, U,
+                         g0, nc, X, U);
     const dim3 grid((unsigned)((nc + 1) / 2));
     switch (N) {
 #define LCSM_CASE(NN)                                                                            \
@@ -297,9 +391,15 @@ hipError_t launch_fft_col_tile(float* S, const float2* Hc, const float2* tw, con
         return hipErrorInvalidValue;
     }
     const dim3 tout((unsigned)((nc + kTT - 1) / kTT), (unsigned)((dst_len + kTT - 1) / kTT));
-    if (in_place)
+    if (in_place && vout)
+      hipLaunchKernelGGL(k_cols_to_rows4<true>, tout, dim3(kTThreads), 0, st, X, U, S, lstride,
+                         s.BD, i - U, dst_len, g0, nc);
+    else if (in_place)
       hipLaunchKernelGGL(k_cols_to_rows<true>, tout, dim3(kTThreads), 0, st, X, U, S, lstride, s.BD,
                          i - U, dst_len, g0, nc);
+    else if (vout)
+      hipLaunchKernelGGL(k_cols_to_rows4<false>, tout, dim3(kTThreads), 0, st, X, U, S, lstride,
+                         s.BD, i, dst_len, g0, nc);
     else
       hipLaunchKernelGGL(k_cols_to_rows<false>, tout, dim3(kTThreads), 0, st, X, U, S, lstride, s.BD,
                          i, dst_len, g0, nc);

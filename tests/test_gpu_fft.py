@@ -123,6 +123,28 @@ def test_integer_data_wide_panels(opt, shape, half):
     assert np.array_equal(np.rint(z).astype(np.int64), ex)
 
 
+@pytest.mark.parametrize("half", [False, True])
+@pytest.mark.parametrize("opt", ["col_from_4", "col_tiny_scratch"])
+@pytest.mark.parametrize("shape", [(2, 3, 40, 301), (1, 2, 64, 1027), (1, 1, 12, 1028)])
+def test_integer_data_column_transposes(opt, shape, half):
+    """Column tiles whose transposes move 16-byte vectors (B*D a multiple of
+    4) next to clipped destinations of a length that is not (L = 301 and
+    1027: the outputs go back element by element), and, with half-state
+    storage, the in-place tile of i = T with both kinds of destination
+    (45 rows at L = 301, 4 rows at L = 1028)."""
+    M, B, D, L = shape
+    say(f"[int fft column transposes] M={M} B={B} D={D} L={L} options={opt} half_state={half}")
+    w, h, y = _int_case(M, B, D, L, 3, seed=11 * sum(shape))
+    opts = dict(FFT_OPTIONS[opt], half_state=int(half))
+    ctx, _ = make_ctx(w, torch.from_numpy(h).to(dev()), opts)
+    z = _run_full(ctx, torch.from_numpy(y).to(dev()))
+    ex = _exact(h, y)
+    err = np.abs(z.astype(np.float64) - ex).max()
+    say(f"  max abs err {err:.3e}")
+    assert err < 0.25
+    assert np.array_equal(np.rint(z).astype(np.int64), ex)
+
+
 @pytest.mark.parametrize("opt", ["lds_from_2", "multipass_from_16", "tiny_scratch", "default",
                                  "col_from_4"])
 def test_m1b8d768l8k_teacher_forced_all_columns(opt):
