@@ -56,7 +56,7 @@ extern "C" {
 typedef struct lcsm_options {
   int direct_max_u;  /* tiles with U <= direct_max_u use the direct kernel (power of two, >= 1),
                         larger ones the FFT.  0: by shape -- direct up to U = 32, and at U = 64
-                        while M*B*D <= 2^17 */
+                        while M*B*D < 2^14 */
   int lds_fft_max_n; /* FFT tiles with 2U <= lds_fft_max_n run in one LDS pass, larger ones in
                         three passes through scratch (power of two in [16, 8192]; default 8192) */
   int scratch_mib;   /* cap of the multi-pass FFT scratch in MiB (default 512); the scratch is

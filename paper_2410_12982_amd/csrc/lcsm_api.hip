@@ -17,10 +17,9 @@ namespace {
 constexpr size_t kAlign = 256;
 // Default tile-kind choice (the paper's per-shape "Hybrid" choice of tau, from
 // MI355X measurements): direct tiles (fused with the red cell) up to U = 32,
-// and at U = 64 while the launch is small enough to be bound by its latency
-// (M*B*D <= 2^17 columns; above that the FFT tile moves the bytes faster).
+// and at U = 64 below kWidePanelMinCols columns, where the FFT tile of
+// 2U = 128 runs in narrow panels and the launch is bound by its latency.
 constexpr int kAutoDirectMaxU = 32;
-constexpr int kAutoDirectU64MaxCols = 1 << 17;
 constexpr int kDefaultLdsFftMaxN = 8192;   // 2U <= 8192: one LDS pass
 constexpr int kDefaultScratchMib = 512;    // multi-pass and column-tile FFT scratch cap
 // FFT tiles from 2U = 8192 up run on transposed column chunks when there are
@@ -92,7 +91,7 @@ int tile_kind(const Options& o, const Shape& s, int U) {
   if (U <= 0) return LCSM_TILE_NONE;
   int dmax = o.direct_max_u;
   if (dmax == 0)
-    dmax = ((long long)s.M * s.BD <= kAutoDirectU64MaxCols) ? 2 * kAutoDirectMaxU : kAutoDirectMaxU;
+    dmax = ((long long)s.M * s.BD < lcsm::kWidePanelMinCols) ? 2 * kAutoDirectMaxU : kAutoDirectMaxU;
   if (U <= dmax) return LCSM_TILE_DIRECT;
   if (2 * U >= o.col_min_n && 2 * U <= lcsm::kMaxColFftN &&
       (!o.col_auto || (long long)s.M * s.BD >= kAutoColMinCols))

@@ -672,7 +672,6 @@ __global__ __launch_bounds__(Cfg<N2>::NT) void k_fft_rows_inv(const float2* __re
 // row runs instead of 32) take the tile 25 % faster at 55K and 1M columns,
 // while at a few thousand columns the halved workgroup count leaves CUs idle.
 constexpr int kWideWC = 8;
-constexpr long long kWideMinCols = 1LL << 14;  // M*B*D
 
 template <int NN, int WC>
 hipError_t tile_panels(float* S, const float2* H, const float2* tw, const float* Hf,
@@ -711,7 +710,7 @@ hipError_t tile_panels(float* S, const float2* H, const float2* tw, const float*
 hipError_t tile_single(int N, float* S, const float2* H, const float2* tw, const float* Hf,
                        const float* yt, float* zt, const Shape& s, int i, int dst_len,
                        bool in_place, hipStream_t st) {
-  const bool wide = (long long)s.M * s.BD >= kWideMinCols;
+  const bool wide = (long long)s.M * s.BD >= kWidePanelMinCols;
 #define LCSM_CASE(NN)                                                                      \
   case NN:                                                                                 \
     if constexpr (NN == 128 || NN == 256) {                                                \

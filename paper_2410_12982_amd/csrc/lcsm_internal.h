@@ -103,6 +103,11 @@ hipError_t launch_spectra(const float* Hf, float2* Hout, const float2* tw, const
 // Largest 2U of the column tiles (one complex column of 2U points in LDS).
 constexpr int kMaxColFftN = 16384;
 
+// From this many columns (M*B*D) a launch has workgroups enough for FFT tile
+// panels of 8 complex columns at 2U = 128 and 256 (64-byte row runs), and
+// with them the FFT tile of U = 64 is faster than the direct one.
+constexpr long long kWidePanelMinCols = 1LL << 14;
+
 // Columns per chunk of a column tile of side U with scratch_bytes of
 // scratch (a multiple of 64, 0 if not even 64 columns fit).
 int fft_col_chunk(int U, size_t scratch_bytes, long long total_cols);

@@ -158,15 +158,15 @@ def test_workspace_grows_with_fft_levels():
 
 
 def test_plan_tile_default_kinds_for_workloads():
-    # default at 18432 columns: direct up to U = 64, one LDS pass up to 2U = 4096,
+    # default at 18432 columns: direct up to U = 32, one LDS pass up to 2U = 4096,
     # transposed column chunks at 2U = 8192 and 16384, multi-pass above
     L = 1 << 17
     kinds = {}
     for t in range(L - 1):
         _, U, _, k = lcsm.plan_tile(18, 1, 1024, L, t)
         kinds[U] = k
-    assert all(kinds[1 << q] == lcsm.TILE_DIRECT for q in range(7))
-    assert all(kinds[1 << q] == lcsm.TILE_FFT for q in range(7, 12))
+    assert all(kinds[1 << q] == lcsm.TILE_DIRECT for q in range(6))
+    assert all(kinds[1 << q] == lcsm.TILE_FFT for q in range(6, 12))
     assert all(kinds[1 << q] == lcsm.TILE_FFT_COL for q in range(12, 14))
     assert all(kinds[1 << q] == lcsm.TILE_FFT_HBM for q in range(14, 17))
     # fewer than 2^14 columns (the 6144-column workload): no column chunks
@@ -231,14 +231,19 @@ def test_single_hip_runtime_in_process():
 
 
 def test_default_crossover_depends_on_shape():
-    """Direct tiles up to U = 32 always; U = 64 direct only while M*B*D <= 2^17
-    (small launches are latency-bound), FFT above."""
+    """Direct tiles up to U = 32 always; U = 64 direct only below 2^14 columns
+    (small launches are latency-bound; from 2^14 columns the FFT tile of
+    2U = 128 runs in wide panels and is faster), FFT above."""
     def kind_at_u(M, B, D, L, u):
         # the tile after step t = u - 1 has i = u, side lowbit(u) = u
         return lcsm.plan_tile(M, B, D, L, u - 1)[3]
-    for shape in [(1, 8, 768, 8192), (18, 4, 768, 32768), (18, 1, 1024, 1 << 17)]:
+    for shape in [(1, 8, 768, 8192), (1, 1, 16383, 1024)]:
         assert kind_at_u(*shape, 32) == lcsm.TILE_DIRECT
         assert kind_at_u(*shape, 64) == lcsm.TILE_DIRECT
+        assert kind_at_u(*shape, 128) == lcsm.TILE_FFT
+    for shape in [(18, 4, 768, 32768), (18, 1, 1024, 1 << 17), (1, 1, 16384, 1024)]:
+        assert kind_at_u(*shape, 32) == lcsm.TILE_DIRECT
+        assert kind_at_u(*shape, 64) == lcsm.TILE_FFT
         assert kind_at_u(*shape, 128) == lcsm.TILE_FFT
     wide = (32, 16, 2048, 16384)
     assert kind_at_u(*wide, 32) == lcsm.TILE_DIRECT
