@@ -67,7 +67,7 @@ typedef struct lcsm_options {
   int col_fft_min_n; /* FFT tiles with col_fft_min_n <= 2U <= 16384 transpose chunks of their
                         columns into the scratch and transform each column as one contiguous
                         run (power of two >= 4; above 16384: never).  0: by shape -- from
-                        2U = 8192 while M*B*D >= 2^14 */
+                        2U = 8192 while M*B*D >= 2^14, from 2U = 4096 while M*B*D >= 2^15 */
   int reserved[3];   /* must be zero */
 } lcsm_options;
 

@@ -28,6 +28,9 @@ constexpr int kDefaultScratchMib = 512;    // multi-pass and column-tile FFT scr
 // transposes; below that size, or with fewer columns, the row panels win.
 constexpr int kDefaultColFftMinN = 8192;
 constexpr long long kAutoColMinCols = 1LL << 14;
+// and the 2U = 4096 tile too from this many columns (at 18K columns its row
+// panels are still ahead, at 55K and 1M the column tile)
+constexpr long long kAutoCol4096MinCols = 1LL << 15;
 constexpr int kMaxL = 1 << 19;             // FFT lengths up to 2^19 are built
 constexpr int kMaxLevels = 20;
 
@@ -93,8 +96,9 @@ int tile_kind(const Options& o, const Shape& s, int U) {
   if (dmax == 0)
     dmax = ((long long)s.M * s.BD < lcsm::kWidePanelMinCols) ? 2 * kAutoDirectMaxU : kAutoDirectMaxU;
   if (U <= dmax) return LCSM_TILE_DIRECT;
-  if (2 * U >= o.col_min_n && 2 * U <= lcsm::kMaxColFftN &&
-      (!o.col_auto || (long long)s.M * s.BD >= kAutoColMinCols))
+  const long long cols = (long long)s.M * s.BD;
+  const int col_min = (o.col_auto && cols >= kAutoCol4096MinCols) ? 4096 : o.col_min_n;
+  if (2 * U >= col_min && 2 * U <= lcsm::kMaxColFftN && (!o.col_auto || cols >= kAutoColMinCols))
     return LCSM_TILE_FFT_COL;
   return (2 * U <= o.lds_fft_max_n) ? LCSM_TILE_FFT : LCSM_TILE_FFT_HBM;
 }

@@ -171,6 +171,11 @@ def test_plan_tile_default_kinds_for_workloads():
     assert all(kinds[1 << q] == lcsm.TILE_FFT_HBM for q in range(14, 17))
     # fewer than 2^14 columns (the 6144-column workload): no column chunks
     assert lcsm.plan_tile(1, 8, 768, 8192, 4095)[3] == lcsm.TILE_FFT
+    # from 2^15 columns the 2U = 4096 tile is a column tile too, not 2U = 2048
+    for shape in ((18, 4, 768, 32768), (32, 16, 2048, 16384), (1, 1, 32768, 8192)):
+        assert lcsm.plan_tile(*shape, 2047)[3] == lcsm.TILE_FFT_COL
+        assert lcsm.plan_tile(*shape, 1023)[3] == lcsm.TILE_FFT
+    assert lcsm.plan_tile(1, 1, 32767, 8192, 2047)[3] == lcsm.TILE_FFT
     # the column-chunk tiles when asked for: 2U from col_fft_min_n up to 16384
     on = {"col_fft_min_n": 2048}
     for q, want in ((9, lcsm.TILE_FFT), (10, lcsm.TILE_FFT_COL), (13, lcsm.TILE_FFT_COL),
