@@ -80,3 +80,18 @@ def oracle_sampled(w: datagen.Workload, cols, filters_np_fn=None, y_cols=None):
 def rel_err(z_gpu, z_ref):
     scale = np.abs(z_ref).max()
     return float(np.abs(z_gpu.astype(np.float64) - z_ref).max() / max(scale, 1e-300))
+
+
+def say_maxima(z_gpu, z_ref, cols):
+    """Log, beside the gated maximum, the error maximum of each layer and the
+    worst column (z_* are [L, n] over the sampled columns ``cols`` [n, 3] of
+    (m, b, d)), each relative to the config's max|z_ref|."""
+    scale = max(float(np.abs(z_ref).max()), 1e-300)
+    err = np.abs(z_gpu.astype(np.float64) - z_ref).max(axis=0) / scale
+    per_layer = {}
+    for k, (m, _, _) in enumerate(np.asarray(cols)):
+        per_layer[int(m)] = max(per_layer.get(int(m), 0.0), float(err[k]))
+    worst = int(np.argmax(err))
+    say("  per-layer max rel err: " + ", ".join(f"m{m}={e:.2e}" for m, e in sorted(per_layer.items())))
+    m, b, d = (int(v) for v in np.asarray(cols)[worst])
+    say(f"  worst column (m={m}, b={b}, d={d}): {err[worst]:.3e}; median column {np.median(err):.3e}")

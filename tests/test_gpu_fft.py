@@ -20,7 +20,7 @@ import datagen
 from oracle import conv, feedback
 from oracle.relaxed import filters_to_columns, relaxed_online
 
-from gpu_harness import TOL, dev, make_ctx, rel_err, say
+from gpu_harness import TOL, dev, make_ctx, rel_err, say, say_maxima
 
 pytestmark = pytest.mark.gpu
 
@@ -157,6 +157,8 @@ def test_m1b8d768l8k_teacher_forced_all_columns(opt):
     zr = conv.causal_conv_fft(y.cpu().numpy().reshape(w.L, -1).astype(np.float64), h[:, 0])
     err = rel_err(z.reshape(w.L, -1), zr)
     say(f"  rel err {err:.3e}")
+    cols = np.array([(m, b, d) for m in range(w.M) for b in range(w.B) for d in range(w.D)])
+    say_maxima(z.reshape(w.L, -1), zr, cols)
     assert err <= TOL
 
 

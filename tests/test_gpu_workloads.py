@@ -8,7 +8,7 @@ first and last layer."""
 import pytest
 
 import datagen
-from gpu_harness import TOL, make_ctx, oracle_sampled, rel_err, run_sampled, say
+from gpu_harness import TOL, make_ctx, oracle_sampled, rel_err, run_sampled, say, say_maxima
 
 pytestmark = pytest.mark.gpu
 
@@ -25,6 +25,7 @@ def test_workload_sampled_columns(name):
     zr = oracle_sampled(w, cols)
     err = rel_err(z, zr)
     say(f"  rel err {err:.3e} over {len(cols)} columns")
+    say_maxima(z, zr, cols)
     assert err <= TOL
 
 
