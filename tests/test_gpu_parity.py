@@ -54,8 +54,11 @@ def _run_full(ctx, y):
 
 
 @pytest.mark.parametrize("shape", [(2, 3, 40, 300), (1, 2, 64, 256), (3, 1, 5, 1), (1, 1, 1, 77),
-                                   (2, 2, 300, 129)])
+                                   (2, 2, 300, 129), (1, 4, 8200, 100), (2, 3, 5462, 70)])
 def test_integer_data_bit_exact_direct(shape):
+    """The last two shapes have more than 2^15 columns, channel counts that
+    leave a partial block of 256, and clipped direct tiles (i = 96 at L = 100:
+    4 rows; i = 64 at L = 70: 6 rows)."""
     M, B, D, L = shape
     say(f"[int-exact direct] M={M} B={B} D={D} L={L}")
     w, h, y = _int_case(M, B, D, L, 3, seed=sum(shape))
