@@ -64,9 +64,10 @@ typedef struct lcsm_options {
   int half_state;    /* 1: keep only T state rows per layer instead of L, T the largest power
                         of two below L (App. C, "Storing Only Half of the Activations"); see
                         the note below.  0 (default): L rows */
-  int col_fft_min_n; /* FFT tiles with col_fft_min_n <= 2U <= 16384 transpose chunks of their
+  int col_fft_min_n; /* FFT tiles with col_fft_min_n <= 2U <= 32768 transpose chunks of their
                         columns into the scratch and transform each column as one contiguous
-                        run (power of two >= 4; above 16384: never).  0: by shape -- from
+                        run (2U = 32768: as its even and odd bins, two 16384-point halves;
+                        power of two >= 4; above 32768: never).  0: by shape -- from
                         2U = 8192 while M*B*D >= 2^14, from 2U = 4096 while M*B*D >= 2^15 */
   int reserved[3];   /* must be zero */
 } lcsm_options;

@@ -136,13 +136,14 @@ Layout layout_for(const Shape& s, const Options& o) {
   off = align_up(off + sizeof(float) * (size_t)s.M * s.L * s.D);
   ly.prev = off;
   off = align_up(off + sizeof(float) * (size_t)s.BD);
-  bool multipass = false;
+  bool multipass = false, colsplit = false;
   for (int q = 0; q < kMaxLevels && (1 << q) <= s.L - 1; ++q) {
     const int U = 1 << q;
     const int kind = tile_kind(o, s, U);
     if (kind == LCSM_TILE_DIRECT) continue;
     ly.nmax = 2 * U;
     if (kind == LCSM_TILE_FFT_HBM || kind == LCSM_TILE_FFT_COL) multipass = true;
+    if (kind == LCSM_TILE_FFT_COL && 2 * U > lcsm::kMaxColFftN1) colsplit = true;
     ly.H[q] = off;
     off = align_up(off + sizeof(float2) * (size_t)s.M * (U + 1) * s.D);
   }
@@ -152,12 +153,14 @@ Layout layout_for(const Shape& s, const Options& o) {
   }
   if (multipass) {
     // one chunk: N complex values per complex column (column tiles: U
-    // floats per real column, the same bytes)
+    // floats per real column, the same bytes; split column tiles 2U, so 64
+    // real columns need 32 complex columns' worth)
     const size_t per_col = sizeof(float2) * (size_t)ly.nmax;
     const size_t cols = ((size_t)s.M * ((s.BD + 1) / 2) + 15) / 16 * 16;
+    const size_t min_cols = colsplit ? 32 : 16;
     size_t want = (size_t)o.scratch_mib << 20;
     if (want > per_col * cols) want = per_col * cols;
-    if (want < per_col * 16) want = per_col * 16;
+    if (want < per_col * min_cols) want = per_col * min_cols;
     ly.scratch = off;
     ly.scratch_bytes = want;
     off = align_up(off + want);

@@ -232,6 +232,27 @@ struct ColCfg {
   static constexpr int SLOTS = N + (N >> SH);
 };
 
+// Chunk columns (ca, cb) of the complex column pr, in the order `mode` sets
+// (below); cb may lie past the chunk in mode 0.
+__device__ __forceinline__ void col_pair(int pr, int mode, int BD, int D, int B, int& ca, int& cb) {
+  if (mode == 2) {
+    const int half = B / 2, lp = half * D;  // pairs per layer
+    const int l = pr / lp, r = pr - l * lp;
+    const int d = r / half, bp = r - d * half;
+    ca = l * BD + 2 * bp * D + d;
+    cb = ca + D;
+  } else {
+    if (mode == 1) {
+      const int ppr = D / 2, lp = B * ppr;
+      const int l = pr / lp, r = pr - l * lp;
+      const int dp = r / B, b = r - dp * B;
+      pr = l * lp + b * ppr + dp;
+    }
+    ca = 2 * pr;
+    cb = ca + 1;
+  }
+}
+
 // mode: how the complex columns pair the chunk's real columns.
 //   2 (the chunk holds whole layers, B even): batch rows 2p and 2p+1 of one
 //     channel -- both share its spectrum, the product is P = Z H, and the
@@ -262,24 +283,8 @@ __global__ __launch_bounds__(ColCfg<N>::NT, ColCfg<N>::MINB) void k_fft_coltile(
     for (int l = (int)threadIdx.x; l < 64; l += NT) twl[N / 64 + l] = tw[N + l];
     twz = TW{twl, twl + N / 64};
   }
-  int pr = fft::xcd_logical((int)blockIdx.x, (int)gridDim.x);
   int ca, cb;  // chunk columns of the pair (cb may be past the chunk in mode 0)
-  if (mode == 2) {
-    const int half = B / 2, lp = half * D;  // pairs per layer
-    const int l = pr / lp, r = pr - l * lp;
-    const int d = r / half, bp = r - d * half;
-    ca = l * BD + 2 * bp * D + d;
-    cb = ca + D;
-  } else {
-    if (mode == 1) {
-      const int ppr = D / 2, lp = B * ppr;
-      const int l = pr / lp, r = pr - l * lp;
-      const int dp = r / B, b = r - dp * B;
-      pr = l * lp + b * ppr + dp;
-    }
-    ca = 2 * pr;
-    cb = ca + 1;
-  }
+  col_pair(fft::xcd_logical((int)blockIdx.x, (int)gridDim.x), mode, BD, D, B, ca, cb);
   const bool hasb = cb < ncols;
   float* xa = X + (size_t)ca * ldx;
   float* xb = X + (size_t)(hasb ? cb : ca) * ldx;
@@ -336,6 +341,88 @@ __global__ __launch_bounds__(ColCfg<N>::NT, ColCfg<N>::MINB) void k_fft_coltile(
   });
 }
 
+// The column tile of 2U = 2 NS points, above the largest transform a column
+// can hold in LDS, as two NS-point transforms (U = NS): the even and the odd
+// bins of the 2U-point spectrum.  With z[n] the complex column (zero for
+// n >= U, so every input row is one of the NS points),
+//   Z[2k + p] = DFT_NS(z[n] w_2U^{p n})[k],
+// and the outputs U + j of the inverse 2U-point transform of the product are
+//   A[j] + w_2U^{-(U + j)} B[j] = A[j] - w_2U^{-j} B[j],
+// A and B the NS-point inverses of the even and the odd products.  PAR = 1
+// stores -w_2U^{-j} B[j] into Y; PAR = 0, launched after it, stores
+// A[j] + Y[j] into X over its own inputs (all read in its first pass).  The
+// bins k > U of the filter spectra follow from H[2U - k] = conj(H[k]); for
+// pairs of two channels the mirror bin 2U - k of bin k lies in the same half.
+template <int NS, int PAR>
+__global__ __launch_bounds__(ColCfg<NS>::NT, ColCfg<NS>::MINB) void k_fft_coltile2(
+    float* __restrict__ X, float* __restrict__ Y, int ldx, const float2* __restrict__ Hc,
+    const float2* __restrict__ tw, long long g0, int ncols, int BD, int D, int B, int mode) {
+  constexpr int NT = ColCfg<NS>::NT, U = NS, N = 2 * NS;
+  constexpr int SH = ColCfg<NS>::SH;
+  static_assert(!ColCfg<NS>::TWL, "two-level twiddles");
+  __shared__ float2 buf[ColCfg<NS>::SLOTS];
+  __shared__ float2 twl[NS / 64 + 64];
+  for (int j = (int)threadIdx.x; j < NS / 64; j += NT) twl[j] = tw[NS + 64 * j];
+  for (int l = (int)threadIdx.x; l < 64; l += NT) twl[NS / 64 + l] = tw[NS + l];
+  const TwSplit<NS> twz{twl, twl + NS / 64};
+  // w_2U^m for m < U, as w_2U^(m mod C) w_32^(m div C) with C = NS/16: the
+  // rows of one butterfly share the first factor (one table read each)
+  constexpr int C = NS / 16;
+  auto w2u = [&](int m) { return cmul(tw[N + (m & (C - 1))], tw[32 + m / C]); };
+  int ca, cb;
+  col_pair(fft::xcd_logical((int)blockIdx.x, (int)gridDim.x), mode, BD, D, B, ca, cb);
+  const bool hasb = cb < ncols;
+  float* xa = X + (size_t)ca * ldx;
+  float* xb = X + (size_t)(hasb ? cb : ca) * ldx;
+  float* ya = Y + (size_t)ca * ldx;
+  float* yb = Y + (size_t)(hasb ? cb : ca) * ldx;
+  const long long ga = g0 + ca, gb = g0 + (hasb ? cb : ca);
+  const long long ma = ga / BD, mb = gb / BD;
+  const int da = (int)(ga - ma * BD) % D, db = (int)(gb - mb * BD) % D;
+  const float2* ha = Hc + ((size_t)ma * D + da) * (U + 1);
+  const float2* hb = Hc + ((size_t)mb * D + db) * (U + 1);
+
+  fft::forward_from_global<NS, 1, 1, NT, false, SH>(buf, twz, [&](int row, int) -> float2 {
+    const float2 v = make_float2(xa[row], hasb ? xb[row] : 0.f);
+    if constexpr (PAR == 1) return cmul(v, w2u(row));
+    return v;
+  });
+  if (mode == 2) {
+    // one channel: P = Z H at every bin k = 2 kk + PAR
+    for (int kk = (int)threadIdx.x; kk < NS; kk += NT) {
+      const int k = 2 * kk + PAR;
+      const float2 h = k <= U ? ha[k] : conjf2(ha[N - k]);
+      const int sk = fft::lds_slot<SH>(kk);
+      buf[sk] = cmul(buf[sk], h);
+    }
+  } else {
+    // bin k = 2 kk + PAR <= U with its mirror 2U - k = bin (NS - kk - PAR) mod NS
+    constexpr int KH = PAR ? NS / 2 : NS / 2 + 1;
+    for (int kk = (int)threadIdx.x; kk < KH; kk += NT) {
+      const int k = 2 * kk + PAR;
+      const int nk = (NS - kk - PAR) & (NS - 1);
+      const float2 a = ha[k], b = hasb ? hb[k] : make_float2(0.f, 0.f);
+      const float2 s = make_float2(0.5f * (a.x + b.x), 0.5f * (a.y + b.y));
+      const float2 d = make_float2(0.5f * (a.x - b.x), 0.5f * (a.y - b.y));
+      const int sk = fft::lds_slot<SH>(kk), snk = fft::lds_slot<SH>(nk);
+      const float2 zk = buf[sk], znk = buf[snk];
+      buf[sk] = cadd(cmul(zk, s), cmul(conjf2(znk), d));
+      if (nk != kk) buf[snk] = cadd(cmul(znk, conjf2(s)), cmul(conjf2(zk), conjf2(d)));
+    }
+  }
+  __syncthreads();
+  fft::inverse_to_global<NS, 1, 1, NT, false, SH>(buf, twz, [&](int row, int, float2 v) {
+    if constexpr (PAR == 1) {
+      const float2 b = cmul(v, conjf2(w2u(row)));
+      ya[row] = -b.x;
+      if (hasb) yb[row] = -b.y;
+    } else {
+      xa[row] = v.x + ya[row];
+      if (hasb) xb[row] = v.y + yb[row];
+    }
+  });
+}
+
 }  // namespace
 
 int fft_col_chunk(int U, size_t scratch_bytes, long long total_cols) {
@@ -353,7 +440,10 @@ hipError_t launch_fft_col_tile(float* S, const float2* Hc, const float2* tw, con
   if (dst_len <= 0) return hipSuccess;
   const int N = 2 * U;
   const long long total = (long long)s.M * s.BD;
-  int chunk = fft_col_chunk(U, scratch_bytes, total);
+  // above one column's LDS transform: two halves (k_fft_coltile2), with a
+  // second U floats per column in the scratch for the odd half's outputs
+  const bool split = N > kMaxColFftN1;
+  int chunk = fft_col_chunk(U, split ? scratch_bytes / 2 : scratch_bytes, total);
   if (chunk <= 0) return hipErrorOutOfMemory;
   // whole layers per chunk where possible (then the pairs and their order can
   // follow the spectra: see k_fft_coltile)
@@ -361,6 +451,7 @@ hipError_t launch_fft_col_tile(float* S, const float2* Hc, const float2* tw, con
   if (layers) chunk = chunk / s.BD * s.BD;
   const int mode = layers && s.B % 2 == 0 ? 2 : (layers && s.D % 2 == 0 ? 1 : 0);
   float* X = reinterpret_cast<float*>(scratch);
+  float* Y = X + (size_t)chunk * U;  // the odd half's outputs (split tiles only)
   const size_t lstride = (size_t)s.SL * s.BD;
   // 16-byte transposes: whole float4s in one layer's rows (B*D, and with it
   // every chunk start, a multiple of 4) and in the columns (U and the rows
@@ -387,6 +478,12 @@ hipError_t launch_fft_col_tile(float* S, const float2* Hc, const float2* tw, con
       LCSM_CASE(256) LCSM_CASE(512) LCSM_CASE(1024) LCSM_CASE(2048) LCSM_CASE(4096)
       LCSM_CASE(8192) LCSM_CASE(16384)
 #undef LCSM_CASE
+      case 2 * kMaxColFftN1:
+        hipLaunchKernelGGL((k_fft_coltile2<kMaxColFftN1, 1>), grid, dim3(ColCfg<kMaxColFftN1>::NT), 0,
+                           st, X, Y, U, Hc, tw, g0, nc, s.BD, s.D, s.B, mode);
+        hipLaunchKernelGGL((k_fft_coltile2<kMaxColFftN1, 0>), grid, dim3(ColCfg<kMaxColFftN1>::NT), 0,
+                           st, X, Y, U, Hc, tw, g0, nc, s.BD, s.D, s.B, mode);
+        break;
       default:
         return hipErrorInvalidValue;
     }

@@ -100,8 +100,11 @@ hipError_t launch_spectra(const float* Hf, float2* Hout, const float2* tw, const
 
 // ---- FFT tiles on transposed column chunks (lcsm_fft_col.hip)
 
-// Largest 2U of the column tiles (one complex column of 2U points in LDS).
-constexpr int kMaxColFftN = 16384;
+// Largest 2U of the column tiles.
+constexpr int kMaxColFftN = 32768;
+// Largest 2U transformed as one column in LDS; the next size runs as two
+// halves of this size (even and odd bins).
+constexpr int kMaxColFftN1 = 16384;
 
 // From this many columns (M*B*D) a launch has workgroups enough for FFT tile
 // panels of 8 complex columns at 2U = 128 and 256 (64-byte row runs), and
@@ -115,7 +118,8 @@ int fft_col_chunk(int U, size_t scratch_bytes, long long total_cols);
 // FFT gray tile of all layers on transposed column chunks: y rows [i-U, i)
 // -> z rows [i, i+dst_len) (added), or stored over rows [i-U, i-U+dst_len)
 // when in_place (the half-state swap).  Hc: channel-major spectra [m][d][k]
-// of tile size U.  2U <= kMaxColFftN.
+// of tile size U.  2U <= kMaxColFftN; above kMaxColFftN1 the tile needs
+// scratch for 2U floats per column of a chunk (at least 64 columns).
 hipError_t launch_fft_col_tile(float* S, const float2* Hc, const float2* tw, const Shape& s, int i,
                                int U, int dst_len, float2* scratch, size_t scratch_bytes,
                                hipStream_t st, bool in_place);

@@ -159,7 +159,8 @@ def test_workspace_grows_with_fft_levels():
 
 def test_plan_tile_default_kinds_for_workloads():
     # default at 18432 columns: direct up to U = 32, one LDS pass up to 2U = 4096,
-    # transposed column chunks at 2U = 8192 and 16384, multi-pass above
+    # transposed column chunks at 2U = 8192, 16384 and 32768 (the last as two
+    # halves), multi-pass above
     L = 1 << 17
     kinds = {}
     for t in range(L - 1):
@@ -167,8 +168,8 @@ def test_plan_tile_default_kinds_for_workloads():
         kinds[U] = k
     assert all(kinds[1 << q] == lcsm.TILE_DIRECT for q in range(6))
     assert all(kinds[1 << q] == lcsm.TILE_FFT for q in range(6, 12))
-    assert all(kinds[1 << q] == lcsm.TILE_FFT_COL for q in range(12, 14))
-    assert all(kinds[1 << q] == lcsm.TILE_FFT_HBM for q in range(14, 17))
+    assert all(kinds[1 << q] == lcsm.TILE_FFT_COL for q in range(12, 15))
+    assert all(kinds[1 << q] == lcsm.TILE_FFT_HBM for q in range(15, 17))
     # fewer than 2^14 columns (the 6144-column workload): no column chunks
     assert lcsm.plan_tile(1, 8, 768, 8192, 4095)[3] == lcsm.TILE_FFT
     # from 2^15 columns the 2U = 4096 tile is a column tile too, not 2U = 2048
@@ -176,10 +177,10 @@ def test_plan_tile_default_kinds_for_workloads():
         assert lcsm.plan_tile(*shape, 2047)[3] == lcsm.TILE_FFT_COL
         assert lcsm.plan_tile(*shape, 1023)[3] == lcsm.TILE_FFT
     assert lcsm.plan_tile(1, 1, 32767, 8192, 2047)[3] == lcsm.TILE_FFT
-    # the column-chunk tiles when asked for: 2U from col_fft_min_n up to 16384
+    # the column-chunk tiles when asked for: 2U from col_fft_min_n up to 32768
     on = {"col_fft_min_n": 2048}
     for q, want in ((9, lcsm.TILE_FFT), (10, lcsm.TILE_FFT_COL), (13, lcsm.TILE_FFT_COL),
-                    (14, lcsm.TILE_FFT_HBM)):
+                    (14, lcsm.TILE_FFT_COL), (15, lcsm.TILE_FFT_HBM)):
         t = (1 << q) - 1
         assert lcsm.plan_tile(18, 1, 1024, L, t, on)[3] == want
     for bad in (3, 2, -4, 100):

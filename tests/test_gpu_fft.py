@@ -20,7 +20,7 @@ import datagen
 from oracle import conv, feedback
 from oracle.relaxed import filters_to_columns, relaxed_online
 
-from gpu_harness import TOL, dev, make_ctx, rel_err, say, say_maxima
+from gpu_harness import TOL, dev, lcsm_mod, make_ctx, rel_err, say, say_maxima
 
 pytestmark = pytest.mark.gpu
 
@@ -139,6 +139,36 @@ def test_integer_data_column_transposes(opt, shape, half):
     ctx, _ = make_ctx(w, torch.from_numpy(h).to(dev()), opts)
     z = _run_full(ctx, torch.from_numpy(y).to(dev()))
     ex = _exact(h, y)
+    err = np.abs(z.astype(np.float64) - ex).max()
+    say(f"  max abs err {err:.3e}")
+    assert err < 0.25
+    assert np.array_equal(np.rint(z).astype(np.int64), ex)
+
+
+@pytest.mark.parametrize("half", [False, True])
+@pytest.mark.parametrize("opt", ["col_from_4", "col_top"])
+@pytest.mark.parametrize("shape", [(1, 4, 16, 16500), (1, 1, 64, 17000), (1, 1, 5, 16390)])
+def test_integer_data_split_column_tile(opt, shape, half):
+    """The column tile of 2U = 32768 (i = 16384, clipped at L), transformed as
+    its even and odd bins in two 16384-point halves: batch-row pairs of one
+    channel (B*D = 64, B even), channel pairs (B = 1), neighbouring columns
+    with an odd count; every FFT tile on column chunks or only this one; with
+    half-state storage it is the in-place tile of i = T = 16384."""
+    M, B, D, L = shape
+    say(f"[int split column tile] M={M} B={B} D={D} L={L} options={opt} half_state={half}")
+    w, h, y = _int_case(M, B, D, L, 2, seed=13 * sum(shape))
+    opts = dict(FFT_OPTIONS[opt] if opt in FFT_OPTIONS else {"col_fft_min_n": 32768},
+                half_state=int(half))
+    ctx, _ = make_ctx(w, torch.from_numpy(h).to(dev()), opts)
+    assert ctx.tile(16383)[1:] == (16384, L - 16384, lcsm_mod().TILE_FFT_COL)
+    z = _run_full(ctx, torch.from_numpy(y).to(dev()))
+    # the exact integers: the oracle's fp64 FFT convolution, rounded (|z| stays
+    # near 10^3, where fp64 rounding is far below 1/2)
+    hc = filters_to_columns(h.astype(np.float64), B).reshape(L, -1)
+    zf = conv.causal_conv_fft(y.reshape(L, -1).astype(np.float64), hc)
+    ex = np.rint(zf).astype(np.int64)
+    assert np.abs(zf - ex).max() < 1e-3
+    ex = ex.reshape(L, M, B, D)
     err = np.abs(z.astype(np.float64) - ex).max()
     say(f"  max abs err {err:.3e}")
     assert err < 0.25
