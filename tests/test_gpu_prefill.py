@@ -43,8 +43,10 @@ def _prefill_then_run(ctx, y, P):
 
 @pytest.mark.parametrize("opt", ["default", "fft_from_2", "multipass_from_16", "col_from_4"])
 @pytest.mark.parametrize("case", [(2, 3, 40, 1024, 256), (3, 2, 33, 2048, 64), (1, 1, 5, 300, 128),
-                                  (2, 2, 24, 4096, 2048)])
+                                  (2, 2, 24, 4096, 2048), (1, 2, 8, 32768, 16384)])
 def test_prefill_then_generate_matches_oracle(opt, case):
+    """The last case's prompt tile is 2U = 32768: with column tiles it runs as
+    the two 16384-point halves, with the filter spectrum delayed by P."""
     M, B, D, L, P = case
     w = datagen.Workload("prefill", M, B, D, L, decay=L / 4, seed=31 + P)
     say(f"[prefill] M={M} B={B} D={D} L={L} P={P} options={opt}")
