@@ -14,13 +14,13 @@
 //
 // The products are matrix-vector products over B <= 16 rows at a time: their
 // time is the weight read (4 bytes per weight, 2B flops), so they run on the
-// vector ALUs with coalesced weight rows, not on the matrix cores.  A wave
-// takes one output unit: its 64 lanes stride the unit's weight row in
-// 16-byte pieces (1 KB contiguous per load), multiply them with the same
-// pieces of the B input rows (shared through L1 by the block's 4 waves) and
-// reduce over the wave with butterfly shuffles, after which lane r stores
-// row r.  The K loop is unrolled so that one memory round trip covers several
-// pieces per lane.
+// vector ALUs with coalesced weight rows, not on the matrix cores.  They are
+// bound by how many loads are in flight, not by bytes: a workgroup takes one
+// output unit and splits its weight row over K/256 waves, one 1 KB piece per
+// wave (its 64 lanes in 16-byte parts), multiplied with the same pieces of
+// the B input rows; each wave reduces with butterfly shuffles and wave 0 sums
+// the waves' partials from LDS in wave order (deterministic), after which
+// lane r stores row r.
 #include <math.h>
 #include <stdio.h>
 #include <string.h>
@@ -33,8 +33,7 @@
 namespace lcsm {
 namespace {
 
-constexpr int kGemvWaves = 4;    // output units per block, one per wave
-constexpr int kGemvThreads = 64 * kGemvWaves;
+constexpr int kGemvMaxThreads = 1024;  // 16 waves: K up to 4096 in one piece per wave
 constexpr int kMaxRows = 16;     // batch rows per product launch
 
 enum { kUp = 0, kDown = 1 };
@@ -58,70 +57,67 @@ __device__ __forceinline__ float gelu(float v) {
 // red cell of the next layer or the sampler copy.  NR >= nrows, a power of
 // two <= kMaxRows; rows nrows..NR-1 are computed from row nrows-1 and not
 // stored.  K must be a multiple of 4 and the rows 16-byte aligned.
+// One output unit per workgroup: its WPU waves take consecutive 256-float
+// pieces of the unit's weight row (wave w: pieces w, w + WPU, ...), reduce
+// over the wave with butterfly shuffles, and wave 0 sums the WPU partials of
+// each row from LDS (in wave order: deterministic).
 template <int NR, int MODE>
-__global__ __launch_bounds__(kGemvThreads) void k_gemv(const float* __restrict__ x,
-                                                       const float* __restrict__ W,
-                                                       const float* __restrict__ bias,
-                                                       float* __restrict__ out, int N, int K,
-                                                       int nrows, RedNext rn) {
-  constexpr int UNR = NR <= 8 ? 4 : 2;  // pieces per lane and round trip
-  const int lane = (int)threadIdx.x & 63;
-  const int n = (int)blockIdx.x * kGemvWaves + ((int)threadIdx.x >> 6);
-  const bool live = n < N;
-  const float* wr = W + (size_t)(live ? n : N - 1) * K;
+__global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(const float* __restrict__ x,
+                                                          const float* __restrict__ W,
+                                                          const float* __restrict__ bias,
+                                                          float* __restrict__ out, int N, int K,
+                                                          int nrows, RedNext rn) {
+  __shared__ float part[kGemvMaxThreads / 64][NR];
+  const int lane = (int)threadIdx.x & 63, wv = (int)threadIdx.x >> 6;
+  const int wpu = (int)blockDim.x >> 6;
+  const int n = (int)blockIdx.x;
+  const float* wr = W + (size_t)n * K;
   const float* xr[NR];
 #pragma unroll
   for (int r = 0; r < NR; ++r) xr[r] = x + (size_t)(r < nrows ? r : nrows - 1) * K;
   float acc[NR];
 #pragma unroll
   for (int r = 0; r < NR; ++r) acc[r] = 0.f;
-  for (int k0 = lane * 4; k0 < K; k0 += 256 * UNR) {
-    float4 w[UNR];
-    float4 v[UNR][NR];
+  for (int k = wv * 256 + lane * 4; k < K; k += wpu * 256) {
+    const float4 w = *reinterpret_cast<const float4*>(wr + k);
+    float4 v[NR];
 #pragma unroll
-    for (int u = 0; u < UNR; ++u) {
-      const int k = k0 + 256 * u;
-      const bool in = k < K;
-      w[u] = in ? *reinterpret_cast<const float4*>(wr + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int r = 0; r < NR; ++r) v[r] = *reinterpret_cast<const float4*>(xr[r] + k);
 #pragma unroll
-      for (int r = 0; r < NR; ++r)
-        v[u][r] = in ? *reinterpret_cast<const float4*>(xr[r] + k) : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-#pragma unroll
-    for (int u = 0; u < UNR; ++u) {
-#pragma unroll
-      for (int r = 0; r < NR; ++r) {
-        acc[r] = fmaf(w[u].x, v[u][r].x, acc[r]);
-        acc[r] = fmaf(w[u].y, v[u][r].y, acc[r]);
-        acc[r] = fmaf(w[u].z, v[u][r].z, acc[r]);
-        acc[r] = fmaf(w[u].w, v[u][r].w, acc[r]);
-      }
+    for (int r = 0; r < NR; ++r) {
+      acc[r] = fmaf(w.x, v[r].x, acc[r]);
+      acc[r] = fmaf(w.y, v[r].y, acc[r]);
+      acc[r] = fmaf(w.z, v[r].z, acc[r]);
+      acc[r] = fmaf(w.w, v[r].w, acc[r]);
     }
   }
-  // sum over the wave: every lane ends with the totals
 #pragma unroll
   for (int r = 0; r < NR; ++r) {
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) acc[r] += __shfl_xor(acc[r], off, 64);
   }
-  if (!live) return;
-  const float bn = bias[n];
+  if (lane < NR) {
 #pragma unroll
-  for (int r = 0; r < NR; ++r) {
-    if (r != lane || r >= nrows) continue;
-    const float s = acc[r] + bn;
-    const size_t e = (size_t)r * N + n;
-    if constexpr (MODE == kUp) {
-      out[e] = gelu(s);
+    for (int r = 0; r < NR; ++r)
+      if (r == lane) part[wv][r] = acc[r];
+  }
+  __syncthreads();
+  if (wv != 0 || lane >= nrows) return;
+  const int r = lane;
+  float s = 0.f;
+  for (int q = 0; q < wpu; ++q) s += part[q][r];
+  s += bias[n];
+  const size_t e = (size_t)r * N + n;
+  if constexpr (MODE == kUp) {
+    out[e] = gelu(s);
+  } else {
+    out[e] = s;
+    if (rn.S) {
+      float* slot = rn.S + e;
+      rn.z[e] = fmaf(rn.h0[n], s, *slot);
+      *slot = s;
     } else {
-      out[e] = s;
-      if (rn.S) {
-        float* slot = rn.S + e;
-        rn.z[e] = fmaf(rn.h0[n], s, *slot);
-        *slot = s;
-      } else {
-        rn.last[e] = s;
-      }
+      rn.last[e] = s;
     }
   }
 }
@@ -143,7 +139,9 @@ __global__ __launch_bounds__(256) void k_synth_red0(const float* __restrict__ ep
 template <int MODE>
 hipError_t gemv(const float* x, const float* W, const float* bias, float* out, int N, int K,
                 int nrows, const RedNext& rn, hipStream_t st) {
-  const dim3 grid((unsigned)((N + kGemvWaves - 1) / kGemvWaves)), block(kGemvThreads);
+  int wpu = (K + 255) / 256;  // waves per unit: one 256-float piece each
+  if (wpu > kGemvMaxThreads / 64) wpu = kGemvMaxThreads / 64;
+  const dim3 grid((unsigned)N), block((unsigned)(64 * wpu));
 #define LCSM_GEMV(NR) \
   hipLaunchKernelGGL((k_gemv<NR, MODE>), grid, block, 0, st, x, W, bias, out, N, K, nrows, rn)
   if (nrows <= 1)
