@@ -152,6 +152,56 @@ __global__ __launch_bounds__(kThreads) void k_dd_direct(float* __restrict__ Y,
     if (j0 + jj < dlen) dst[(size_t)jj * rs] += acc[jj];
 }
 
+// The same tile for a side UT known at compile time: every value it reads --
+// the two fixed blocks and the window j0-UT+1 .. j0+J-1 of the two recent
+// blocks -- is loaded before the first product (one memory round trip, rows
+// clamped into range and zero-selected, since a load under a condition would
+// wait for the earlier ones), and the window offsets become register names.
+template <int J, int UT, bool SQ>
+__global__ __launch_bounds__(kThreads) void k_dd_direct_u(float* __restrict__ Y,
+                                                          const float* __restrict__ R, int L,
+                                                          int BD, int lo, int d0, int dlen) {
+  constexpr int NW = J + UT - 1;  // window: recent index j0 - UT + 1 + i, i < NW
+  const int c = (int)blockIdx.x * kThreads + (int)threadIdx.x;
+  const int j0 = (int)blockIdx.y * J;
+  const int m = (int)blockIdx.z;
+  if (c >= BD || j0 >= dlen) return;
+  const size_t rs = (size_t)BD;
+  float* ycol = Y + (size_t)m * L * BD + c;
+  const float* rcol = R + (size_t)m * L * BD + c;
+  const float* yR = ycol + (size_t)lo * rs;
+  const float* rR = rcol + (size_t)lo * rs;
+  const float* yF = ycol + (size_t)UT * rs;
+  const float* rF = rcol + (size_t)UT * rs;
+  float fy[UT], fr[UT], wy[NW], wr[NW];
+#pragma unroll
+  for (int k = 0; k < UT; ++k) {
+    fy[k] = yF[(size_t)k * rs];
+    fr[k] = SQ ? 0.f : rF[(size_t)k * rs];
+  }
+#pragma unroll
+  for (int i = 0; i < NW; ++i) {
+    const int idx = j0 - UT + 1 + i;
+    const int cl = idx < 0 ? 0 : (idx >= UT ? UT - 1 : idx);
+    const float vr = rR[(size_t)cl * rs];
+    const float vy = SQ ? 0.f : yR[(size_t)cl * rs];
+    const bool in = idx >= 0 && idx < UT;
+    wr[i] = in ? vr : 0.f;
+    wy[i] = in ? vy : 0.f;
+  }
+  float* dst = ycol + (size_t)(d0 + j0) * rs;
+#pragma unroll
+  for (int jj = 0; jj < J; ++jj) {
+    float a = 0.f;
+#pragma unroll
+    for (int k = 0; k < UT; ++k) {
+      a = fmaf(fy[k], wr[jj - k + UT - 1], a);
+      if constexpr (!SQ) a = fmaf(fr[k], wy[jj - k + UT - 1], a);
+    }
+    if (j0 + jj < dlen) dst[(size_t)jj * rs] += a;
+  }
+}
+
 // ---- FFT parallelogram tiles (2U-point, one LDS-resident pass)
 //
 // Each real column carries its two blocks packed as one complex signal,
@@ -445,6 +495,19 @@ hipError_t dd_tile(lcsm_dd* c, bool square, int U, int lo, int d0, int dlen) {
     return square ? dd_fft<true>(c, 2 * U, lo, d0, dlen) : dd_fft<false>(c, 2 * U, lo, d0, dlen);
   const dim3 grid((unsigned)((c->BD + lcsm::kThreads - 1) / lcsm::kThreads),
                   (unsigned)((dlen + lcsm::kDdJ - 1) / lcsm::kDdJ), (unsigned)c->M);
+#define LCSM_DD_U(UU)                                                                              \
+  if (U == UU) {                                                                                   \
+    if (square)                                                                                    \
+      hipLaunchKernelGGL((lcsm::k_dd_direct_u<lcsm::kDdJ, UU, true>), grid, dim3(lcsm::kThreads), 0, \
+                         c->stream, c->Y, c->R, c->L, c->BD, lo, d0, dlen);                        \
+    else                                                                                           \
+      hipLaunchKernelGGL((lcsm::k_dd_direct_u<lcsm::kDdJ, UU, false>), grid, dim3(lcsm::kThreads),   \
+                         0, c->stream, c->Y, c->R, c->L, c->BD, lo, d0, dlen);                     \
+    return hipGetLastError();                                                                      \
+  }
+  LCSM_DD_U(16)
+  LCSM_DD_U(32)
+#undef LCSM_DD_U
   if (square)
     hipLaunchKernelGGL((lcsm::k_dd_direct<lcsm::kDdJ, true>), grid, dim3(lcsm::kThreads), 0,
                        c->stream, c->Y, c->R, c->L, c->BD, U, lo, d0, dlen);
