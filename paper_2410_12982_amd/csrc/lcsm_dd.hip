@@ -36,44 +36,44 @@ constexpr int kDdJ = 16;            // outputs per thread of the direct tile
 constexpr int kDdDefaultDirectMaxU = 32;
 constexpr int kDdFusedMaxU = 8;      // tiles fused with the red cell
 
-// The tile of side U of step t for one column, in one thread.
-template <int U>
-__device__ __forceinline__ void dd_tile_in_thread(float* ycol, const float* rcol, size_t rs, int L,
-                                                  int t) {
-  const bool square = t + 1 == 2 * U;
-  const int lo = square ? U : t - U + 1;
-  const int d0 = square ? 2 * U : t + 1;
-  if (d0 >= L) return;
-  float yf[U], rf[U], yr[U], rr[U];
-#pragma unroll
-  for (int k = 0; k < U; ++k) {
-    yf[k] = ycol[(size_t)(U + k) * rs];
-    rf[k] = rcol[(size_t)(U + k) * rs];
-    yr[k] = ycol[(size_t)(lo + k) * rs];
-    rr[k] = rcol[(size_t)(lo + k) * rs];
-  }
+// Contributions of the tile of side U of step t (t + 1 a multiple of U,
+// 2U <= t + 1) to the destination rows t + 1 + j, j < 2U - 1, added into dz
+// in that order.  fy, fr: the rows 1 .. 2 UMAX - 1 of y and rho (index =
+// row); wy, wr: the rows t - UMAX + 1 .. t (index i = row - t + UMAX - 1).
+// The square tile (t + 1 = 2U) has the fixed block as its recent block and
+// one product.
+template <int U, int UMAX>
+__device__ __forceinline__ void dd_tile_regs(const float* fy, const float* fr, const float* wy,
+                                             const float* wr, float* dz, bool square) {
 #pragma unroll
   for (int j = 0; j < 2 * U - 1; ++j) {
-    if (d0 + j < L) {
-      float sum = 0.f;
+    float sum = 0.f;
+    if (square) {
+#pragma unroll
+      for (int k = 0; k < U; ++k)
+        if (j - k >= 0 && j - k < U) sum = fmaf(fy[U + k], fr[U + j - k], sum);
+    } else {
 #pragma unroll
       for (int k = 0; k < U; ++k) {
         if (j - k >= 0 && j - k < U) {
-          sum = fmaf(yf[k], rr[j - k], sum);
-          if (!square) sum = fmaf(rf[k], yr[j - k], sum);
+          // recent row t - U + 1 + (j - k) is window index UMAX - U + (j - k)
+          sum = fmaf(fy[U + k], wr[UMAX - U + j - k], sum);
+          sum = fmaf(fr[U + k], wy[UMAX - U + j - k], sum);
         }
       }
-      ycol[(size_t)(d0 + j) * rs] += sum;
     }
+    dz[j] += sum;
   }
 }
 
 // Red cell at position t fused with the tiles of every U <= UMAX of step t
-// (U | t+1, 2U <= t+1), one thread per column walking them in increasing U:
-// the blocks (at most 4 x 8 values) are held in registers and every output
-// of a tile is summed in the thread.  Rows written by one tile are not read
-// by a later one (tiles read rows <= t and write rows > t), and the thread's
-// own store of y_t, rho_t is what its tiles read back.
+// (U | t+1, 2U <= t+1), one thread per column.  Every value the step reads
+// -- y_0, rho_0 and the accumulator of row t, the fixed rows 1 .. 2UMAX-1,
+// the recent rows t-UMAX+1 .. t-1 (row t is the new input, in registers) and
+// the destination rows t+1 .. t+2UMAX-1 -- is loaded before the first store
+// (one memory round trip; destination rows past L clamped and not stored).
+// The tiles' sums are added into the destination in increasing U, as
+// separate read-modify-writes per tile would.
 template <int UMAX>
 __global__ __launch_bounds__(kThreads) void k_dd_step(const float* __restrict__ y,
                                                       const float* __restrict__ rho,
@@ -88,13 +88,46 @@ __global__ __launch_bounds__(kThreads) void k_dd_step(const float* __restrict__ 
   float* rcol = R + (size_t)m * L * BD + c;
   const float yt = y[e], rt = rho[e];
   const float acc = ycol[(size_t)t * rs];
-  z[e] = t == 0 ? fmaf(yt, rt, acc) : fmaf(yt, rcol[0], fmaf(ycol[0], rt, acc));
+  const float y0 = ycol[0], r0 = rcol[0];
+  constexpr int NF = UMAX > 0 ? 2 * UMAX : 1;
+  constexpr int NW = UMAX > 0 ? UMAX : 1;
+  constexpr int ND = UMAX > 0 ? 2 * UMAX - 1 : 1;
+  float fy[NF], fr[NF], wy[NW], wr[NW], dz[ND];
+  if constexpr (UMAX > 0) {
+#pragma unroll
+    for (int row = 1; row < 2 * UMAX; ++row) {
+      const float vy = ycol[(size_t)row * rs], vr = rcol[(size_t)row * rs];
+      fy[row] = row == t ? yt : vy;  // row t (the square tile's last fixed row) is the new input
+      fr[row] = row == t ? rt : vr;
+    }
+#pragma unroll
+    for (int i = 0; i < UMAX - 1; ++i) {
+      const size_t row = (size_t)(t - UMAX + 1 + i);
+      wy[i] = ycol[row * rs];
+      wr[i] = rcol[row * rs];
+    }
+    wy[UMAX - 1] = yt;
+    wr[UMAX - 1] = rt;
+#pragma unroll
+    for (int j = 0; j < 2 * UMAX - 1; ++j) {
+      const int row = t + 1 + j;
+      dz[j] = ycol[(size_t)(row < L ? row : L - 1) * rs];
+    }
+  }
+  z[e] = t == 0 ? fmaf(yt, rt, acc) : fmaf(yt, r0, fmaf(y0, rt, acc));
   ycol[(size_t)t * rs] = yt;
   rcol[(size_t)t * rs] = rt;
-  if constexpr (UMAX >= 1) dd_tile_in_thread<1>(ycol, rcol, rs, L, t);
-  if constexpr (UMAX >= 2) dd_tile_in_thread<2>(ycol, rcol, rs, L, t);
-  if constexpr (UMAX >= 4) dd_tile_in_thread<4>(ycol, rcol, rs, L, t);
-  if constexpr (UMAX >= 8) dd_tile_in_thread<8>(ycol, rcol, rs, L, t);
+  if constexpr (UMAX > 0) {
+    // only the largest tile can be the square one (t + 1 = 2 UMAX)
+    const bool sq = t + 1 == 2 * UMAX;
+    if constexpr (UMAX >= 1) dd_tile_regs<1, UMAX>(fy, fr, wy, wr, dz, sq && UMAX == 1);
+    if constexpr (UMAX >= 2) dd_tile_regs<2, UMAX>(fy, fr, wy, wr, dz, sq && UMAX == 2);
+    if constexpr (UMAX >= 4) dd_tile_regs<4, UMAX>(fy, fr, wy, wr, dz, sq && UMAX == 4);
+    if constexpr (UMAX >= 8) dd_tile_regs<8, UMAX>(fy, fr, wy, wr, dz, sq && UMAX == 8);
+#pragma unroll
+    for (int j = 0; j < 2 * UMAX - 1; ++j)
+      if (t + 1 + j < L) ycol[(size_t)(t + 1 + j) * rs] = dz[j];
+  }
 }
 
 // Direct parallelogram tile of side U for all layers: thread = (column c,
