@@ -114,11 +114,12 @@ def test_small_workload_closed_loop():
 
 
 @pytest.mark.parametrize("opt", ["default", "fft_from_2", "all_direct"])
-@pytest.mark.parametrize("shape", [(4, 2, 24, 300), (11, 1, 8, 130)])
+@pytest.mark.parametrize("shape", [(4, 2, 24, 300), (11, 1, 8, 130), (18, 1, 8, 100), (33, 1, 4, 70)])
 def test_multilayer_closed_loop(opt, shape):
     """The chain across layers (y^m_t from z^{m-1}_t, layer 0 from the last
     layer's z_{t-1}): with several layers the red cells walk the layers in
-    chunks of loads and the tiles run in the separate all-layer launch.
+    chunks of loads (8, 16 or 32 layers: 11 and 18 layers in one chunk, 33 in
+    two) and the tiles run in the separate all-layer launch.
     Filters decay fast (as in the 1024-position workload), so the fp32 closed
     loop stays close to the fp64 one over these lengths."""
     M, B, D, L = shape
