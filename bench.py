@@ -167,6 +167,10 @@ def kernel_key(name):
     m = re.search(r"k_fft_coltile<(\d+)>", name)
     if m:
         return ("fft_col", int(m.group(1)) // 2)
+    # the 2U = 2 NS tile as its even and odd halves: U = NS
+    m = re.search(r"k_fft_coltile2<(\d+), \d+>", name)
+    if m:
+        return ("fft_col", int(m.group(1)))
     if "k_rows_to_cols" in name or "k_cols_to_rows" in name:
         return ("fft_col", None)
     return None
@@ -230,6 +234,17 @@ def traffic_from(args):
     for c in ("FETCH_SIZE", "WRITE_SIZE"):
         for key, vals in tile_bytes(rows(f"pmc_bench_{c}")).items():
             per[key][c].extend(v * scale[c] for v in vals)
+    # entries of other workloads taken on the same sources are kept
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    kept = {}
+    try:
+        with open(path) as f:
+            old = json.load(f)
+        if old.get("source_digest") == source_digest():
+            kept = {k: v for k, v in old.get("kernels", {}).items()
+                    if not k.startswith(args.workload + ":")}
+    except (OSError, ValueError):
+        pass
     kernels = {}
     for (name, U), v in sorted(per.items(), key=lambda kv: (kv[0][1], kv[0][0])):
         if not v["FETCH_SIZE"] or not v["WRITE_SIZE"]:
@@ -239,7 +254,8 @@ def traffic_from(args):
         kernels[f"{args.workload}:{name}:U={U}"] = {"bytes_per_launch": round(fb + wb),
                                                     "read_bytes": round(fb), "write_bytes": round(wb),
                                                     "dispatches": len(v["FETCH_SIZE"])}
-    out = {"source_digest": source_digest(), "workload": args.workload,
+    workloads = sorted({k.split(":")[0] for k in kept} | {args.workload})
+    out = {"source_digest": source_digest(), "workloads": workloads,
            "fetch_scale": round(scale["FETCH_SIZE"], 4), "write_scale": round(scale["WRITE_SIZE"], 4),
            "commands": ["cd /tmp && export TMPDIR=/tmp && rocprofv3 --pmc {C} --output-format csv "
                         "-d <dir>/pmc_copy_{C} -o run -- python3 bench.py --copy-probe 1024",
@@ -248,7 +264,7 @@ def traffic_from(args):
                         f"--positions {args.positions or '<P>'}",
                         "  for C in FETCH_SIZE, WRITE_SIZE; then: python3 bench.py --traffic-from <dir> "
                         f"--workload {args.workload}"],
-           "kernels": kernels}
+           "kernels": dict(sorted({**kept, **kernels}.items()))}
     prof = os.path.join(ROOT, "profiles")
     os.makedirs(prof, exist_ok=True)
     with open(os.path.join(prof, "traffic.json"), "w") as f:

@@ -23,6 +23,8 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
     ("lcsm::k_fft_tile<4096, true, true, false, 4>", ("fft_lds", 2048)),
     ("lcsm::k_fft_tile<128, true, false, false, 8>(float*, float2 const*)", ("fft_lds", 64)),
     ("lcsm::k_fft_coltile<16384>", ("fft_col", 8192)),
+    ("lcsm::(anonymous namespace)::k_fft_coltile2<16384, 1>(float*, float*)", ("fft_col", 16384)),
+    ("lcsm::k_fft_coltile2<16384, 0>", ("fft_col", 16384)),
     ("lcsm::k_rows_to_cols", ("fft_col", None)),
     ("lcsm::k_cols_to_rows<false>", ("fft_col", None)),
     ("at::native::vectorized_elementwise_kernel<4, ...>", None),
