@@ -46,12 +46,14 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-DEFAULT_WORKLOAD = "m1b8d768l8k"
+# The largest single-GPU workload (1M columns, 68.7 GB of state, 1.77 TB of
+# algorithmic traffic per generation).
+DEFAULT_WORKLOAD = "m32b16d2048l16k"
 RING = 256  # input slabs kept resident
-# Longest generation replayed from one HIP graph.  A single graph of the
-# 131072-position workload (about 131k kernel nodes) crashed the process
-# during capture/instantiation; runs up to 32768 positions are known good.
-GRAPH_MAX_L = 32768
+# Positions per HIP graph: a generation is replayed as a chain of graphs of
+# at most this many positions (the library's lcsm_graph_capture; the bench's
+# own GraphChain for the data-dependent and synthetic-model contexts).
+GRAPH_SEG = 16384
 
 
 def parse():
@@ -62,6 +64,8 @@ def parse():
     p.add_argument("--workload", default=DEFAULT_WORKLOAD)
     p.add_argument("--graph", dest="graph", action="store_true", default=True)
     p.add_argument("--no-graph", dest="graph", action="store_false")
+    p.add_argument("--graph-seg", type=int, default=GRAPH_SEG,
+                   help="positions per HIP graph of a replayed generation")
     p.add_argument("--direct-max-u", type=int, default=0, help="0 = library default")
     p.add_argument("--lds-fft-max-n", type=int, default=0, help="0 = library default")
     p.add_argument("--scratch-mib", type=int, default=0, help="0 = library default")
@@ -87,6 +91,9 @@ def parse():
     p.add_argument("--traffic-from", metavar="DIR", default=None,
                    help="only convert rocprofv3 FETCH_SIZE/WRITE_SIZE runs under DIR (pmc_copy_*, "
                         "pmc_bench_*) into profiles/traffic.json and a text summary")
+    p.add_argument("--trace-from", metavar="DIR", default=None,
+                   help="only summarise a rocprofv3 kernel trace under DIR per (kernel, U), "
+                        "grouped as the per-launch pass groups launches")
     p.add_argument("--copy-mib", type=int, default=1024, help="size the copy probe ran with")
     p.add_argument("--copy-scalar", action="store_true",
                    help="copy probe with 4-byte accesses per lane (a one-element offset keeps torch "
@@ -176,18 +183,19 @@ def kernel_key(name):
     return None
 
 
-def tile_bytes(rows_c):
-    """Counter bytes per (kernel, U) key and dispatch from one counter's rows
-    in dispatch order.  A column-chunk tile is one launch of the per-launch
-    pass made of several dispatches (the red cell before it, then transpose,
-    transform, transpose per chunk): they are summed into one entry per tile."""
+def group_tiles(rows, value, order_key="Dispatch_Id"):
+    """Per (kernel, U) key, one summed value per launch of the per-launch
+    pass, from profiler rows in dispatch order.  A column-chunk tile is one
+    launch made of several dispatches (the red cell before it, then
+    transpose, transform, transpose per chunk): their values are summed into
+    one entry per tile.  value(row) gives a row's number."""
     import collections
     per = collections.defaultdict(list)
-    rows_c = sorted(rows_c, key=lambda r: int(r["Dispatch_Id"]))
-    tile, red = None, None  # open column tile [U, bytes]; last red-cell dispatch's bytes
-    for r in rows_c:
+    rows = sorted(rows, key=lambda r: int(r[order_key]))
+    tile, red = None, None  # open column tile [U, value]; last red-cell dispatch's value
+    for r in rows:
         key = kernel_key(r["Kernel_Name"])
-        v = 1024.0 * float(r["Counter_Value"])
+        v = value(r)
         if key and key[0] == "fft_col":
             if tile is None:
                 tile = [None, red or 0.0]
@@ -211,6 +219,40 @@ def tile_bytes(rows_c):
     if red is not None:
         per[("red", 0)].append(red)
     return per
+
+
+def tile_bytes(rows_c):
+    """Counter bytes per (kernel, U) key and launch from one counter's rows."""
+    return group_tiles(rows_c, lambda r: 1024.0 * float(r["Counter_Value"]))
+
+
+def trace_summary(args):
+    """Per (kernel, U) launch durations from a rocprofv3 kernel trace
+    (<dir>/run_kernel_trace.csv) of a bench command: the same grouping as the
+    per-launch pass (a column tile = its red cell + every chunk's dispatches),
+    with algorithmic GB/s and the fraction of 8 TB/s."""
+    import csv
+    import glob
+
+    import datagen
+    w = datagen.WORKLOADS[args.workload]
+    path = glob.glob(os.path.join(args.trace_from, "**", "*kernel_trace.csv"), recursive=True)[0]
+    with open(path) as f:
+        rows = list(csv.DictReader(f))
+    per = group_tiles(rows, lambda r: (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3,
+                      order_key="Start_Timestamp")
+    lines = [f"# per-launch durations from the kernel trace, workload {w.name} "
+             f"(M={w.M} B={w.B} D={w.D} L={w.L})",
+             "# kernel        U   launches    avg_us   total_ms  algorithmic_GB_s  frac_of_8TB_s"]
+    for (name, U), v in sorted(per.items(), key=lambda kv: (kv[0][1] or 0, kv[0][0])):
+        if U is None:
+            continue
+        name = "fused" if name == "red" else name
+        avg = sum(v) / len(v)
+        gbs = launch_bytes(name, U, w) / (avg * 1e-6) / 1e9
+        lines.append(f"{name:12s} {U:5d} {len(v):10d} {avg:9.2f} {sum(v) / 1e3:10.2f} "
+                     f"{gbs:17.1f} {gbs / HBM_PEAK_GBS:14.4f}")
+    print("\n".join(lines))
 
 
 def traffic_from(args):
@@ -293,6 +335,9 @@ def main():
     if args.traffic_from:
         traffic_from(args)
         return
+    if args.trace_from:
+        trace_summary(args)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
               "(this build has no multi-GPU path).", file=sys.stderr)
@@ -311,10 +356,6 @@ def main():
     if args.positions:
         counter_run(args, w, torch, datagen, lcsm)
         return
-    if args.graph and w.L > GRAPH_MAX_L:
-        print(f"# L={w.L} > {GRAPH_MAX_L}: launching from the host (no whole-generation graph)",
-              file=sys.stderr, flush=True)
-        args.graph = False
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     opts = {k: v for k, v in (("direct_max_u", args.direct_max_u),
@@ -341,6 +382,10 @@ def main():
             "us_per_launch": round(floor_us, 3),
             "how": "graph-replayed elementwise kernels on a tensor of one position's M*B*D floats",
             "generation_us_per_position": round(1e3 * ms / w.L, 3)}
+        # a kernel whose launches last about as long as an almost empty
+        # graph-replayed launch is bound by the launch, not by HBM
+        if roofline["avg_launch_us"] < 2.0 * floor_us:
+            roofline["bound"] = "launch"
 
     closed = None
     if args.closed_loop:
@@ -402,8 +447,12 @@ def main():
 
 def counter_run(args, w, torch, datagen, lcsm):
     """The first P positions of one generation, launched from the host (the
-    dispatches a counter run should see), with a progress line every 256
-    positions.  No timing and no metric."""
+    dispatches a counter run should see), with a progress line after every
+    set-up phase and every 256 positions.  No timing and no metric.  Under a
+    counter profiler every dispatch is serialised, so the set-up keeps its
+    dispatch count small: filters generated 8 layers per pass (a few hundred
+    elementwise kernels instead of a few thousand) and a ring of 16 input
+    slabs (the counted kernels' traffic does not depend on the values)."""
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     opts = {k: v for k, v in (("direct_max_u", args.direct_max_u),
@@ -411,17 +460,28 @@ def counter_run(args, w, torch, datagen, lcsm):
                               ("scratch_mib", args.scratch_mib),
                               ("col_fft_min_n", args.col_fft_min_n)) if v} or None
     P = min(args.positions, w.L)
-    filters = datagen.filters_torch(w, dev)
-    R = min(RING, w.L)
+
+    def say(msg):
+        print(f"# {msg}", file=sys.stderr, flush=True)
+
+    say(f"counter run {w.name}: {P} positions")
+    filters = datagen.filters_torch(w, dev, m_chunk=8)
+    torch.cuda.synchronize()
+    say("filters generated")
+    R = min(16, w.L)
     y = datagen.y_torch(w, dev, 0, R)
     z = torch.empty_like(y)
+    torch.cuda.synchronize()
+    say(f"input ring of {R} slabs generated")
     ctx = lcsm.Lcsm(filters, w.B, options=opts)
     torch.cuda.synchronize()
+    say("context initialised (filter re-layout, state cleared, spectra of every FFT tile size)")
+    del filters
     for t in range(P):
         ctx.step(y[t % R], z[t % R])
         if (t + 1) % 256 == 0 or t + 1 == P:
             torch.cuda.synchronize()
-            print(f"# position {t + 1} of {P}", file=sys.stderr, flush=True)
+            say(f"position {t + 1} of {P}")
     ctx.close()
     print(json.dumps({"counter_run": True, "workload": w.name, "positions": P}), flush=True)
 
@@ -538,39 +598,23 @@ def kernel_pass(w, filters, y, z, opts, lcsm, torch):
                                     "achieved": round(bbytes / bavg / 1e9, 2),
                                     "frac": round(bbytes / bavg / 1e9 / HBM_PEAK_GBS, 5),
                                     "traffic": committed_traffic(bname, bU, w)}
+    # every FFT tile size against the 50 % HBM gate on algorithmic bytes
+    roofline["fft_tiles_vs_gate"] = {
+        f"{k[0]} U={k[1]}": round(launch_bytes(k[0], k[1], w) / (v[0] / v[1] / 1e3) / 1e9
+                                  / HBM_PEAK_GBS, 4)
+        for k, v in sorted(agg.items(), key=lambda kv: kv[0][1]) if k[0] != "fused" and v[0] > 0}
     return roofline, levels
 
 
-def timed_generations(w, filters, y, z, opts, lcsm, torch, dev, args, verbose=False):
-    """Teacher-forced generations of all L positions (inputs from the ring y
-    resident in HBM), one HIP graph per generation up to GRAPH_MAX_L positions
-    (host launches above): warmup untimed, then args.steps timed with events.
-    Returns ms per generation."""
-    R = y.shape[0]
-    stream = torch.cuda.Stream(dev) if args.graph else torch.cuda.current_stream(dev)
-    ctx = lcsm.Lcsm(filters, w.B, options=opts, stream=stream)
-    torch.cuda.synchronize()
-
-    def generation():
-        ctx.reset()
-        for t0 in range(0, w.L, R):
-            ctx.run(y, z, n=min(R, w.L - t0))
-
-    if args.graph:
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph, stream=stream):
-            generation()
-        torch.cuda.synchronize()
-        one_step = graph.replay
-    else:
-        one_step = generation
-
+def time_steps(one_step, torch, args, verbose=False):
+    """args.warmup untimed calls of one_step, then args.steps timed with
+    events on the current stream (bracketing the whole timed region).
+    Returns ms per step."""
     for _ in range(args.warmup):
         one_step()
     torch.cuda.synchronize()
     if verbose:
         print(f"# warmup done ({args.warmup})", file=sys.stderr, flush=True)
-
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_wall = time.perf_counter()
@@ -584,8 +628,60 @@ def timed_generations(w, filters, y, z, opts, lcsm, torch, dev, args, verbose=Fa
     if verbose:
         print(f"# timed {args.steps} steps: {ms:.3f} ms/step (wall {1e3 * t_wall / args.steps:.3f})",
               file=sys.stderr, flush=True)
+    return ms
+
+
+class GraphChain:
+    """A generation of a context without the library's own recorder (the
+    data-dependent and synthetic-model contexts) as a chain of torch HIP graphs
+    of at most seg positions each: issue(p0, p1) queues positions [p0, p1)
+    (the reset with p0 = 0) on the capture stream."""
+
+    def __init__(self, torch, stream, L, seg, issue):
+        self.graphs = []
+        for p0 in range(0, L, seg):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=stream):
+                issue(p0, min(L, p0 + seg))
+            self.graphs.append(g)
+        torch.cuda.synchronize()
+
+    def replay(self):
+        for g in self.graphs:
+            g.replay()
+
+    def close(self):
+        self.graphs = []
+
+
+def timed_generations(w, filters, y, z, opts, lcsm, torch, dev, args, verbose=False):
+    """Teacher-forced generations of all L positions (inputs from the ring y
+    resident in HBM), recorded once by the library as a chain of HIP graphs
+    (lcsm_graph_capture: reset + L steps, at most args.graph_seg positions per
+    graph) and replayed per step, or launched from the host with --no-graph:
+    warmup untimed, then args.steps timed with events.  Returns ms per
+    generation."""
+    R = y.shape[0]
+    stream = torch.cuda.Stream(dev) if args.graph else torch.cuda.current_stream(dev)
+    ctx = lcsm.Lcsm(filters, w.B, options=opts, stream=stream)
+    torch.cuda.synchronize()
+    graph = None
     if args.graph:
-        del graph
+        graph = ctx.capture(y, z, n=w.L, seg=args.graph_seg)
+        torch.cuda.synchronize()
+        if verbose:
+            print(f"# recorded: {graph.segments} graph(s) of <= {args.graph_seg} positions",
+                  file=sys.stderr, flush=True)
+        one_step = graph.launch
+    else:
+        def one_step():
+            ctx.reset()
+            for t0 in range(0, w.L, R):
+                ctx.run(y, z, n=min(R, w.L - t0))
+    with torch.cuda.stream(stream):
+        ms = time_steps(one_step, torch, args, verbose)
+    if graph is not None:
+        graph.close()
     ctx.close()
     del ctx
     torch.cuda.synchronize()
@@ -617,7 +713,8 @@ def dd_timing(w, ms_fixed, lcsm, torch, dev, args):
     """Generations with data-dependent filters (lcsm_dd_step: rho_t revealed
     with y_t; every power of two U dividing t+1 gets a parallelogram tile),
     teacher-forced y and rho resident in HBM, dispatched like the timed
-    region.  ms_fixed: the data-independent generation, for the ratio."""
+    region (a chain of HIP graphs).  ms_fixed: the data-independent
+    generation, for the ratio."""
     import datagen
     try:
         lcsm.dd_workspace_bytes(w.M, w.B, w.D, w.L)
@@ -627,84 +724,57 @@ def dd_timing(w, ms_fixed, lcsm, torch, dev, args):
     y = datagen.y_torch(w, dev, 0, R)
     rho = datagen.rho_torch(w, dev, 0, R)
     z = torch.empty_like(y)
-    graph_ok = args.graph and w.L <= GRAPH_MAX_L
-    stream = torch.cuda.Stream(dev) if graph_ok else torch.cuda.current_stream(dev)
+    stream = torch.cuda.Stream(dev) if args.graph else torch.cuda.current_stream(dev)
     ctx = lcsm.Dd(w.M, w.B, w.D, w.L, stream=stream)
     torch.cuda.synchronize()
 
-    def generation():
-        ctx.reset()
-        for t in range(w.L):
+    def issue(p0, p1):
+        if p0 == 0:
+            ctx.reset()
+        for t in range(p0, p1):
             ctx.step(y[t % R], rho[t % R], z[t % R])
 
-    if graph_ok:
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph, stream=stream):
-            generation()
-        torch.cuda.synchronize()
-        one = graph.replay
-    else:
-        one = generation
+    chain = GraphChain(torch, stream, w.L, args.graph_seg, issue) if args.graph else None
+    one = chain.replay if chain else (lambda: issue(0, w.L))
     print("# data-dependent generations", file=sys.stderr, flush=True)
-    for _ in range(args.warmup):
-        one()
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(args.steps):
-        one()
-    e1.record()
-    torch.cuda.synchronize()
-    dms = e0.elapsed_time(e1) / args.steps
-    if graph_ok:
-        del graph
+    with torch.cuda.stream(stream):
+        dms = time_steps(one, torch, args)
+    if chain:
+        chain.close()
     ctx.close()
     return {"ms_per_step": round(dms, 4), "tokens_per_s": round(w.B * w.L / (dms / 1e3), 1),
-            "time_vs_fixed_filters": round(dms / ms_fixed, 3), "graph": graph_ok}
+            "time_vs_fixed_filters": round(dms / ms_fixed, 3), "graph": bool(chain)}
 
 
 def synth_timing(w, filters, opts, ms_mixer, lcsm, torch, dev, args):
     """Generations of the synthetic end-to-end model (lcsm_synth_step: per
     layer the mixer and an MLP block of hidden 2D with GELU; the next token
-    = last layer's output + noise), dispatched like the timed region: warmup
-    untimed, then args.steps timed with events.  ms_mixer: the teacher-forced
-    mixer generation time, for the mixer's share of the model's time."""
+    = last layer's output + noise), dispatched like the timed region (a chain
+    of HIP graphs): warmup untimed, then args.steps timed with events.
+    ms_mixer: the teacher-forced mixer generation time, for the mixer's share
+    of the model's time."""
     import datagen
     R = min(RING, w.L)
     weights = datagen.mlp_weights_torch(w, dev)
     eps = datagen.noise_torch(w, dev, 0, R)
     act = torch.empty((R, w.M, w.B, w.D), dtype=torch.float32, device=dev)
-    graph_ok = args.graph and w.L <= GRAPH_MAX_L
-    stream = torch.cuda.Stream(dev) if graph_ok else torch.cuda.current_stream(dev)
+    stream = torch.cuda.Stream(dev) if args.graph else torch.cuda.current_stream(dev)
     model = lcsm.Synth(filters, *weights, w.B, options=opts, stream=stream)
     torch.cuda.synchronize()
 
-    def generation():
-        model.reset()
-        for t in range(w.L):
+    def issue(p0, p1):
+        if p0 == 0:
+            model.reset()
+        for t in range(p0, p1):
             model.step(eps[t % R], act[t % R])
 
-    if graph_ok:
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph, stream=stream):
-            generation()
-        torch.cuda.synchronize()
-        one = graph.replay
-    else:
-        one = generation
+    chain = GraphChain(torch, stream, w.L, args.graph_seg, issue) if args.graph else None
+    one = chain.replay if chain else (lambda: issue(0, w.L))
     print("# synthetic-model generations", file=sys.stderr, flush=True)
-    for _ in range(args.warmup):
-        one()
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(args.steps):
-        one()
-    e1.record()
-    torch.cuda.synchronize()
-    sms = e0.elapsed_time(e1) / args.steps
-    if graph_ok:
-        del graph
+    with torch.cuda.stream(stream):
+        sms = time_steps(one, torch, args)
+    if chain:
+        chain.close()
     model.close()
     wbytes = 4 * w.M * (4 * w.D * w.D + 3 * w.D)
     return {"ms_per_step": round(sms, 4), "tokens_per_s": round(w.B * w.L / (sms / 1e3), 1),
@@ -712,51 +782,36 @@ def synth_timing(w, filters, opts, ms_mixer, lcsm, torch, dev, args):
             "mixer_share": round(ms_mixer / sms, 4),
             "weight_bytes_per_position": wbytes,
             "launches_per_position": 2 * w.M + 2,
-            "graph": graph_ok}
+            "graph": bool(chain)}
 
 
 def closed_loop(w, filters, opts, lcsm, torch, dev, args):
     """Closed-loop generations (lcsm_step_chain: y^0_t = 0.5 tanh(z^{M-1}_{t-1})
     + x^0_t, y^m_t = 0.5 tanh(z^{m-1}_t) + x^m_t), dispatched like the timed
-    region (one HIP graph per generation up to GRAPH_MAX_L positions, host
-    launches above): warmup untimed, then steps timed with events."""
+    region (recorded by the library as a chain of HIP graphs): warmup untimed,
+    then steps timed with events."""
     import datagen
     R = min(RING, w.L)
     x = datagen.x_torch(w, dev, 0, R)
     z = torch.empty_like(x)
-    graph_ok = args.graph and w.L <= GRAPH_MAX_L
-    stream = torch.cuda.Stream(dev) if graph_ok else torch.cuda.current_stream(dev)
+    stream = torch.cuda.Stream(dev) if args.graph else torch.cuda.current_stream(dev)
     ctx = lcsm.Lcsm(filters, w.B, options=opts, stream=stream)
     torch.cuda.synchronize()
+    graph = ctx.capture(x, z, n=w.L, chain=True, seg=args.graph_seg) if args.graph else None
 
-    def generation():
+    def host_generation():
         ctx.reset()
         for t in range(w.L):
             ctx.step_chain(x[t % R], z[t % R])
 
-    if graph_ok:
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph, stream=stream):
-            generation()
-        torch.cuda.synchronize()
-        one = graph.replay
-    else:
-        one = generation
-    for _ in range(args.warmup):
-        one()
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(args.steps):
-        one()
-    e1.record()
-    torch.cuda.synchronize()
-    cms = e0.elapsed_time(e1) / args.steps
-    if graph_ok:
-        del graph
+    one = graph.launch if graph else host_generation
+    with torch.cuda.stream(stream):
+        cms = time_steps(one, torch, args)
+    if graph:
+        graph.close()
     ctx.close()
     return {"ms_per_step": round(cms, 4), "tokens_per_s": round(w.B * w.L / (cms / 1e3), 1),
-            "graph": graph_ok}
+            "graph": bool(graph)}
 
 
 def prefill_timing(w, filters, opts, lcsm, torch, dev, max_bytes=2 << 30):
@@ -820,15 +875,34 @@ def _oracle_shard(arg):
     return time.perf_counter() - t0
 
 
+def cpu_model():
+    """The host CPU's model name (first 'model name' line of /proc/cpuinfo)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+# Worker processes of the CPU baseline: the host's CPU share per GPU (a
+# one-GPU box grants 16 CPUs whatever os.cpu_count() reports).
+CPU_SHARE = 16
+
+
 def cpu_baseline(w, budget_s):
     """Time the CPU oracle (relaxed tiling, fp64 numpy, as it stands) on a
     bounded sample: all positions of a set of (b, d) columns, sharded over
     worker processes (one thread each); the sample grows until it takes
-    about budget_s / 4 seconds of wall time or covers every column."""
+    about budget_s / 4 seconds of wall time or covers every column.  The rate
+    is extrapolated linearly to all columns when the sample is smaller."""
     import multiprocessing as mp
 
     import numpy as np
-    workers = max(1, min(16, os.cpu_count() or 1))
+    host = os.cpu_count() or 1
+    workers = max(1, min(CPU_SHARE, host))
     total_cols = w.M * w.B * w.D
     env_keys = ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS")
     saved = {k: os.environ.get(k) for k in env_keys}
@@ -856,11 +930,16 @@ def cpu_baseline(w, budget_s):
                 os.environ.pop(k, None)
             else:
                 os.environ[k] = v
+    n = min(n, total_cols)
     value = w.B * w.L / (wall * total_cols / n)
+    extrap = n < total_cols
     return {"value": round(value, 2), "unit": "tokens/s", "cores": workers, "kind": "oracle",
-            "sample": f"relaxed-tiling oracle (fp64 numpy), all {w.L} positions of {n} columns "
-                      f"({workers} processes x {n // workers} columns of layer 0, in parallel) in "
-                      f"{wall:.1f} s (slowest process), scaled linearly to all {total_cols} columns"}
+            "host_cpus": host, "cpu_model": cpu_model(), "extrapolated": extrap,
+            "sample": f"relaxed-tiling oracle (fp64 numpy), all {w.L} positions of {n} of the "
+                      f"{total_cols} columns ({workers} single-thread processes x {n // workers} "
+                      f"columns of layer 0, in parallel; {workers} of the host's {host} CPUs, the "
+                      f"CPU share of one GPU) in {wall:.1f} s (slowest process)"
+                      + (f", extrapolated linearly to all {total_cols} columns" if extrap else "")}
 
 
 if __name__ == "__main__":

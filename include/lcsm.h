@@ -87,9 +87,12 @@ typedef struct lcsm_options {
 
 typedef struct lcsm_ctx lcsm_ctx;
 
-/* Device bytes of the workspace a context of this shape needs (state
- * M*L*B*D fp32 -- M*T*B*D with half_state --, filters M*L*D fp32, filter spectra of the FFT tile sizes, FFT
- * scratch and a few small buffers).  Host only: touches no device.
+/* Device bytes of the workspace a context of this shape needs: the state
+ * M*L*B*D fp32 (M*T*B*D with half_state) -- the activations of Sec. 3.3,
+ * one slot per position that holds the accumulator until the position's
+ * input overwrites it --, filters M*L*D fp32, the filter spectra of the FFT
+ * tile sizes (App. B's cached DFTs), FFT scratch and a few small buffers.
+ * Host only: touches no device.
  * Errors: LCSM_EINVAL for sizes < 1, M > 16384, B > 65535, M*B*D >= 2^31, L > 2^19 or
  * bad options (half_state not 0 or 1, or 1 where the tile of side T would be
  * a direct tile). */
@@ -167,12 +170,59 @@ int lcsm_h0(const lcsm_ctx* ctx, const float** h0, size_t* layer_stride);
 int lcsm_pending(lcsm_ctx* ctx, float** acc, size_t* layer_stride);
 int lcsm_commit(lcsm_ctx* ctx);
 
-/* Run n consecutive lcsm_step calls: step k reads y + k*y_stride and writes
- * z + k*z_stride (strides in floats).  Equivalent to the loop of single
- * steps, with one host call.  Errors as lcsm_step; stops at the first. */
+/* Run n consecutive lcsm_step calls (n iterations of Alg. 3's loop over
+ * positions): step k reads y + k*y_stride and writes z + k*z_stride (strides
+ * in floats).  Equivalent to the loop of single steps, with one host call.
+ * Errors as lcsm_step; stops at the first. */
 int lcsm_run(lcsm_ctx* ctx, int n, const float* y, size_t y_stride, float* z, size_t z_stride);
 
-/* Prompt prefill (Sec. 2.2.1 "The Inference Problem"; the appendix on the
+/* ---- Replayed generations (App. B.2, "CPU Overhead: The silent performance
+ * killer": the per-token launches of a generation are recorded once as HIP
+ * graphs and replayed, so the host submits a few graph launches per
+ * generation instead of one or two kernel launches per position).
+ *
+ * lcsm_graph_capture records lcsm_reset followed by n consecutive steps into
+ * a chain of HIP graphs of at most seg_positions positions each (a bounded
+ * node count per graph, whatever n is).  Step k (k < n) reads
+ *   in + (k mod in_ring) * in_stride      (device, [M][B][D] fp32)
+ * and writes
+ *   z + (k mod z_ring) * z_stride         (device, [M][B][D] fp32),
+ * strides in floats; in_ring / z_ring = 0 mean n (no wrap-around).  flags = 0
+ * records lcsm_step (in = y_t); flags = LCSM_GRAPH_CHAIN records
+ * lcsm_step_chain (in = x_t, the built-in tanh chain).  seg_positions = 0
+ * selects LCSM_GRAPH_DEFAULT_SEG; at most LCSM_GRAPH_MAX_SEG.
+ * Nothing runs on the device during the call; the context's stream must be
+ * a created stream (not the null stream) that is not capturing, and the
+ * context must not be faulted or between lcsm_step_layer calls.  Afterwards
+ * the context's position is n, as if the recorded work had been queued.
+ * The graphs keep the pointers they were recorded with: in, z and the
+ * context's workspace must stay valid while the graph object lives.
+ * Errors: LCSM_EINVAL (null pointers, n outside [1, L], bad rings or
+ * seg_positions, the null stream), LCSM_ESTATE, LCSM_EDEVICE (the capture or
+ * the instantiation failed; nothing is left recorded, the context is
+ * faulted until lcsm_reset). */
+#define LCSM_GRAPH_CHAIN 1
+#define LCSM_GRAPH_DEFAULT_SEG 16384
+#define LCSM_GRAPH_MAX_SEG 32768
+typedef struct lcsm_graph lcsm_graph;
+int lcsm_graph_capture(lcsm_ctx* ctx, int flags, int n, const float* in, size_t in_stride,
+                       int in_ring, float* z, size_t z_stride, int z_ring, int seg_positions,
+                       lcsm_graph** out);
+
+/* Queue every graph of the chain, in order, on the context's stream: the same
+ * device work as lcsm_reset followed by the n recorded steps.  Leaves the
+ * context at position n.  Errors: LCSM_EINVAL, LCSM_EDEVICE (the context is
+ * then faulted). */
+int lcsm_graph_launch(lcsm_graph* g);
+
+/* Number of graphs in the chain (ceil(n / seg_positions)).  Host only. */
+int lcsm_graph_segments(const lcsm_graph* g, int* nseg);
+
+/* Release the graphs (after the stream has passed their last launch).  NULL
+ * is ignored.  Must come before lcsm_destroy of its context. */
+void lcsm_graph_destroy(lcsm_graph* g);
+
+/* Prompt prefill (Sec. 2.3.1 "The Inference Problem"; the appendix on the
  * prefilling and autoregressive stages): with all P prompt inputs known, the
  * prompt's own outputs come from one transform instead of P online steps.
  *   y  device [P][M][B][D] prompt inputs y^m_t, position k at y + k*y_stride;
@@ -193,8 +243,11 @@ int lcsm_run(lcsm_ctx* ctx, int n, const float* y, size_t y_stride, float* z, si
  * LCSM_ESTATE (not at position 0, or faulted), LCSM_EDEVICE. */
 int lcsm_prefill(lcsm_ctx* ctx, int P, const float* y, size_t y_stride, float* z, size_t z_stride);
 
-/* Restart at position 0 with all activations zero; keeps filters and
- * spectra and clears a fault.  Errors: LCSM_EDEVICE. */
+/* Restart at position 0 with all activations zero (the initial state of
+ * Alg. 1 / Alg. 3: every accumulator z_t = 0 before the first position);
+ * keeps filters and spectra and clears a fault.  The state is cleared by a
+ * fill kernel (no memset), so the call may be recorded into a graph.
+ * Errors: LCSM_EDEVICE. */
 int lcsm_reset(lcsm_ctx* ctx);
 
 /* Current position t (the next step emits z_t).  Host only. */

@@ -11,7 +11,7 @@ Contents (all indices 0-based: positions 0..L-1, z_t = sum_{s<=t} y_s h_{t-s}):
 * ``schedule``  -- the tile order of the relaxed algorithm (Alg. 1; Prop. 1).
 * ``conv``      -- the plain definitions: the lazy O(L^2) sum (Eq. onlineConv,
   the "lazy approach" of Sec. 3.1.1), the static FFT convolution used at
-  training time (Sec. 2.2.1) and the one-pole recurrence of a geometric
+  training time (Sec. 2.3.1) and the one-pole recurrence of a geometric
   filter (the LTI-SSM view, App. "State Space Models").
 * ``relaxed``   -- the relaxed tiling itself: red cells and gray tiles in the
   order of Alg. 1 / Alg. 3, with the contribution block tau (Eq. taus)

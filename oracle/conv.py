@@ -30,7 +30,7 @@ def causal_conv_fft(y, h):
     """Static (whole-sequence) FFT evaluation of the same sum.
 
     This is how the convolution is computed when all of y is known in advance
-    (Sec. 2.2.1, "The Inference Problem"): a linear convolution via a
+    (Sec. 2.3.1, "The Inference Problem"): a linear convolution via a
     zero-padded transform of length >= 2L, truncated to the first L outputs.
     """
     y = np.asarray(y, dtype=np.float64)

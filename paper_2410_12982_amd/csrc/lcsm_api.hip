@@ -471,6 +471,114 @@ int lcsm_run(lcsm_ctx* c, int n, const float* y, size_t y_stride, float* z, size
   return LCSM_OK;
 }
 
+}  // extern "C"
+
+// A recorded generation: lcsm_reset plus n steps, split into graphs of at
+// most seg positions so that no graph's node count grows with n (one graph
+// per generation of 131072 positions, about 131k kernel nodes, crashed the
+// process during capture; graphs of 32768 positions are known good).
+struct lcsm_graph {
+  lcsm_ctx* ctx;
+  int n;
+  std::vector<hipGraph_t> graphs;
+  std::vector<hipGraphExec_t> execs;
+};
+
+namespace {
+
+void release_graphs(lcsm_graph* g) {
+  for (hipGraphExec_t e : g->execs) (void)hipGraphExecDestroy(e);
+  for (hipGraph_t gr : g->graphs) (void)hipGraphDestroy(gr);
+  g->execs.clear();
+  g->graphs.clear();
+}
+
+}  // namespace
+
+extern "C" {
+
+int lcsm_graph_capture(lcsm_ctx* c, int flags, int n, const float* in, size_t in_stride,
+                       int in_ring, float* z, size_t z_stride, int z_ring, int seg,
+                       lcsm_graph** out) {
+  if (!out) return LCSM_EINVAL;
+  *out = nullptr;
+  if (!c) return LCSM_EINVAL;
+  if (!in || !z) return fail(c, LCSM_EINVAL, "null input or output pointer", hipSuccess);
+  if (flags != 0 && flags != LCSM_GRAPH_CHAIN)
+    return fail(c, LCSM_EINVAL, "unknown graph flags", hipSuccess);
+  if (n < 1 || n > c->s.L) return fail(c, LCSM_EINVAL, "position count outside [1, L]", hipSuccess);
+  if (in_ring < 0 || z_ring < 0) return fail(c, LCSM_EINVAL, "negative ring length", hipSuccess);
+  if (seg == 0) seg = LCSM_GRAPH_DEFAULT_SEG;
+  if (seg < 1 || seg > LCSM_GRAPH_MAX_SEG)
+    return fail(c, LCSM_EINVAL, "positions per graph outside [1, LCSM_GRAPH_MAX_SEG]", hipSuccess);
+  if (!c->stream) return fail(c, LCSM_EINVAL, "graphs need a created stream, not the null stream", hipSuccess);
+  if (c->faulted) return LCSM_ESTATE;
+  if (c->layers_done != 0)
+    return fail(c, LCSM_ESTATE, "capture during a per-layer position", hipSuccess);
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  hipError_t e = hipStreamIsCapturing(c->stream, &cs);
+  if (e != hipSuccess) return fail(c, LCSM_EDEVICE, "stream capture status", e);
+  if (cs != hipStreamCaptureStatusNone)
+    return fail(c, LCSM_ESTATE, "the stream is already capturing", hipSuccess);
+  const int ir = in_ring ? in_ring : n, zr = z_ring ? z_ring : n;
+  const bool chain = flags == LCSM_GRAPH_CHAIN;
+  lcsm_graph* g = new (std::nothrow) lcsm_graph();
+  if (!g) return LCSM_ENOMEM;
+  g->ctx = c;
+  g->n = n;
+  for (int p0 = 0; p0 < n; p0 += seg) {
+    const int p1 = n - p0 < seg ? n : p0 + seg;
+    e = hipStreamBeginCapture(c->stream, hipStreamCaptureModeThreadLocal);
+    if (e != hipSuccess) break;
+    int r = LCSM_OK;
+    if (p0 == 0) r = lcsm_reset(c);
+    for (int t = p0; r == LCSM_OK && t < p1; ++t)
+      r = step_common(c, in + (size_t)(t % ir) * in_stride, z + (size_t)(t % zr) * z_stride, chain);
+    hipGraph_t gr = nullptr;
+    e = hipStreamEndCapture(c->stream, &gr);
+    if (gr) g->graphs.push_back(gr);
+    if (r != LCSM_OK && e == hipSuccess) e = hipErrorLaunchFailure;
+    if (e != hipSuccess) break;
+    hipGraphExec_t ex = nullptr;
+    e = hipGraphInstantiate(&ex, gr, nullptr, nullptr, 0);
+    if (e != hipSuccess) break;
+    g->execs.push_back(ex);
+  }
+  if (e != hipSuccess) {
+    release_graphs(g);
+    delete g;
+    (void)hipGetLastError();
+    return fail(c, LCSM_EDEVICE, "graph capture", e);
+  }
+  *out = g;
+  return LCSM_OK;
+}
+
+int lcsm_graph_launch(lcsm_graph* g) {
+  if (!g || !g->ctx) return LCSM_EINVAL;
+  lcsm_ctx* c = g->ctx;
+  for (hipGraphExec_t ex : g->execs) {
+    const hipError_t e = hipGraphLaunch(ex, c->stream);
+    if (e != hipSuccess) return fail(c, LCSM_EDEVICE, "graph launch", e);
+  }
+  c->t = g->n;
+  c->layers_done = 0;
+  c->faulted = false;
+  return LCSM_OK;
+}
+
+int lcsm_graph_segments(const lcsm_graph* g, int* nseg) {
+  if (!g || !nseg) return LCSM_EINVAL;
+  *nseg = (int)g->execs.size();
+  return LCSM_OK;
+}
+
+void lcsm_graph_destroy(lcsm_graph* g) {
+  if (!g) return;
+  release_graphs(g);
+  delete g;
+}
+
 int lcsm_prefill(lcsm_ctx* c, int P, const float* y, size_t y_stride, float* z, size_t z_stride) {
   if (!c) return LCSM_EINVAL;
   if (!y || !z) return fail(c, LCSM_EINVAL, "null input or output pointer", hipSuccess);

@@ -9,6 +9,7 @@ from __future__ import annotations
 
 import ctypes
 import os
+import weakref
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "liblcsm.so")
@@ -21,6 +22,8 @@ LCSM_EDONE = -4
 LCSM_ESTATE = -5
 
 TILE_NONE, TILE_DIRECT, TILE_FFT, TILE_FFT_HBM, TILE_FFT_COL = 0, 1, 2, 3, 4
+GRAPH_CHAIN = 1
+GRAPH_DEFAULT_SEG, GRAPH_MAX_SEG = 16384, 32768
 TILE_KIND_NAMES = {TILE_NONE: "none", TILE_DIRECT: "direct", TILE_FFT: "fft_lds",
                    TILE_FFT_HBM: "fft_hbm", TILE_FFT_COL: "fft_col"}
 
@@ -80,6 +83,12 @@ _SIGS = {
     "lcsm_pending": (ctypes.c_int, [_vp, ctypes.POINTER(_vp), ctypes.POINTER(ctypes.c_size_t)]),
     "lcsm_commit": (ctypes.c_int, [_vp]),
     "lcsm_destroy": (None, [_vp]),
+    "lcsm_graph_capture": (ctypes.c_int, [_vp, ctypes.c_int, ctypes.c_int, _vp, ctypes.c_size_t,
+                                          ctypes.c_int, _vp, ctypes.c_size_t, ctypes.c_int,
+                                          ctypes.c_int, ctypes.POINTER(_vp)]),
+    "lcsm_graph_launch": (ctypes.c_int, [_vp]),
+    "lcsm_graph_segments": (ctypes.c_int, [_vp, _c_int_p]),
+    "lcsm_graph_destroy": (None, [_vp]),
     "lcsm_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "lcsm_last_error": (ctypes.c_char_p, [_vp]),
     # include/lcsm_dd.h
@@ -190,6 +199,7 @@ class Lcsm:
         if r:
             raise LcsmError(r, "lcsm_init")
         self._filters_keepalive = filters
+        self._graphs = weakref.WeakSet()  # recorded generations, released before the context
 
     # -- helpers
     def _check(self, r, where):
@@ -268,6 +278,27 @@ class Lcsm:
     def reset(self):
         self._check(_lib.lcsm_reset(self._ctx), "lcsm_reset")
 
+    def capture(self, x, z, n=None, chain=False, seg=0):
+        """Record lcsm_reset + n steps as a chain of HIP graphs (lcsm_graph_capture).
+        x, z: [R, M, B, D] tensors used as rings (step k reads x[k % R], writes
+        z[k % Rz]); chain: record lcsm_step_chain (x = additive inputs) instead of
+        lcsm_step (x = y).  Returns a Graph; nothing runs until Graph.launch()."""
+        shape = (self.M, self.B, self.D)
+        n = self.L if n is None else int(n)
+        if tuple(x.shape[1:]) != shape or tuple(z.shape[1:]) != shape:
+            raise ValueError("x and z must be [R, M, B, D]")
+        if not (x.is_contiguous() and z.is_contiguous() and x.is_cuda and z.is_cuda):
+            raise ValueError("x and z must be contiguous CUDA tensors")
+        slab = self.M * self.B * self.D
+        g = _vp()
+        self._check(_lib.lcsm_graph_capture(self._ctx, GRAPH_CHAIN if chain else 0, n,
+                                            x.data_ptr(), slab, int(x.shape[0]), z.data_ptr(),
+                                            slab, int(z.shape[0]), int(seg), ctypes.byref(g)),
+                    "lcsm_graph_capture")
+        graph = Graph(self, g, (x, z))
+        self._graphs.add(graph)
+        return graph
+
     @property
     def position(self) -> int:
         t = ctypes.c_int()
@@ -319,8 +350,40 @@ class Lcsm:
 
     def close(self):
         if self._ctx:
+            for g in list(getattr(self, "_graphs", ())):
+                g.close()
             _lib.lcsm_destroy(self._ctx)
             self._ctx = _vp()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class Graph:
+    """A recorded generation (``lcsm_graph``): ``launch()`` queues lcsm_reset +
+    the recorded steps on the context's stream as a chain of HIP graphs."""
+
+    def __init__(self, ctx, handle, keepalive):
+        self._ctx = ctx
+        self._g = handle
+        self._keepalive = keepalive
+
+    def launch(self):
+        self._ctx._check(_lib.lcsm_graph_launch(self._g), "lcsm_graph_launch")
+
+    @property
+    def segments(self) -> int:
+        n = ctypes.c_int()
+        self._ctx._check(_lib.lcsm_graph_segments(self._g, ctypes.byref(n)), "lcsm_graph_segments")
+        return n.value
+
+    def close(self):
+        if self._g:
+            _lib.lcsm_graph_destroy(self._g)
+            self._g = _vp()
 
     def __del__(self):
         try:

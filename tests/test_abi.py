@@ -221,6 +221,13 @@ def test_null_context_calls():
     assert lib.lcsm_h0(None, ctypes.byref(p), ctypes.byref(st)) == lcsm.LCSM_EINVAL
     assert lib.lcsm_pending(None, ctypes.byref(p), ctypes.byref(st)) == lcsm.LCSM_EINVAL
     assert lib.lcsm_commit(None) == lcsm.LCSM_EINVAL
+    g = ctypes.c_void_p(1234)
+    assert lib.lcsm_graph_capture(None, 0, 8, fake, 0, 0, fake, 0, 0, 0,
+                                  ctypes.byref(g)) == lcsm.LCSM_EINVAL
+    assert g.value is None  # *out is cleared before any other check
+    assert lib.lcsm_graph_launch(None) == lcsm.LCSM_EINVAL
+    assert lib.lcsm_graph_segments(None, ctypes.byref(t)) == lcsm.LCSM_EINVAL
+    lib.lcsm_graph_destroy(None)
     lib.lcsm_destroy(None)
     assert lib.lcsm_last_error(None) == b""
 
