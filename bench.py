@@ -83,6 +83,12 @@ def parse():
                    help="skip the synthetic end-to-end model (MLP blocks + noise sampler)")
     p.add_argument("--no-half-state", dest="half_state", action="store_false", default=True,
                    help="skip the generations with half-state storage")
+    p.add_argument("--baselines", default="",
+                   help="comma-separated lazy/eager baselines to time over whole generations "
+                        "(lazy, lazy_np, eager, eager_np; 'all' for the four), reported as the "
+                        "paper's speed-up over parallel Lazy")
+    p.add_argument("--baseline-warmup", type=int, default=0,
+                   help="untimed baseline generations before the timed one")
     p.add_argument("--no-closed-loop", dest="closed_loop", action="store_false", default=True,
                    help="skip timing the closed-loop generation (the built-in tanh chain feeding each "
                         "layer's output into the next input)")
@@ -407,6 +413,12 @@ def main():
     if args.synth:
         synth = synth_timing(w, filters, opts, ms, lcsm, torch, dev, args)
 
+    base = None
+    if args.baselines:
+        kinds = (["lazy", "lazy_np", "eager", "eager_np"] if args.baselines == "all"
+                 else [k for k in args.baselines.split(",") if k])
+        base = baselines_timing(w, filters, y, ms, kinds, lcsm, torch, dev, args, synth)
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(w, args.cpu_budget)
@@ -442,6 +454,8 @@ def main():
         out["synthetic_model"] = synth
     if dd:
         out["data_dependent"] = dd
+    if base:
+        out["baselines"] = base
     print(json.dumps(out), flush=True)
 
 
@@ -686,6 +700,58 @@ def timed_generations(w, filters, y, z, opts, lcsm, torch, dev, args, verbose=Fa
     del ctx
     torch.cuda.synchronize()
     return ms
+
+
+def baselines_timing(w, filters, y, ms_relaxed, kinds, lcsm, torch, dev, args, synth=None):
+    """Whole generations of the lazy and eager baselines (lcsm_base_step, the
+    paper's Lazy/Eager and their per-layer *_NP variants) on the same
+    teacher-forced ring inputs, each replayed as a chain of HIP graphs like
+    the timed region: args.baseline_warmup untimed, then one timed
+    generation (a lazy generation is O(L^2): tens of seconds at 32K
+    positions).  Reports each one's time and the relaxed generation's
+    speed-up over it; with the synthetic model's time, the end-to-end
+    speed-up over a model whose mixer is parallel Lazy, taking the model's
+    non-mixer time as unchanged."""
+    R = y.shape[0]
+    out = {}
+    for kind in kinds:
+        stream = torch.cuda.Stream(dev)
+        ctx = lcsm.Base(kind, filters, w.B, stream=stream)
+        z = torch.empty_like(y)
+        torch.cuda.synchronize()
+
+        def issue(p0, p1):
+            if p0 == 0:
+                ctx.reset()
+            for t in range(p0, p1):
+                ctx.step(y[t % R], z[t % R])
+
+        print(f"# baseline {kind}: recording", file=sys.stderr, flush=True)
+        chain = GraphChain(torch, stream, w.L, args.graph_seg, issue)
+        with torch.cuda.stream(stream):
+            for _ in range(args.baseline_warmup):
+                chain.replay()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            chain.replay()
+            e1.record()
+        torch.cuda.synchronize()
+        bms = e0.elapsed_time(e1)
+        chain.close()
+        ctx.close()
+        print(f"# baseline {kind}: {bms:.1f} ms per generation", file=sys.stderr, flush=True)
+        out[kind] = {"ms_per_step": round(bms, 3), "tokens_per_s": round(w.B * w.L / (bms / 1e3), 1),
+                     "relaxed_speedup": round(bms / ms_relaxed, 2)}
+    if "lazy" in out:
+        out["speedup_over_parallel_lazy"] = out["lazy"]["relaxed_speedup"]
+        if synth and "ms_per_step" in synth:
+            lazy_model = synth["ms_per_step"] - ms_relaxed + out["lazy"]["ms_per_step"]
+            out["end_to_end_speedup_over_parallel_lazy"] = {
+                "value": round(lazy_model / synth["ms_per_step"], 2),
+                "how": "synthetic model with the parallel-Lazy mixer estimated as the model's time "
+                       "minus the relaxed mixer's plus the Lazy mixer's, over the model's time"}
+    return out
 
 
 def half_state_timing(w, filters, y, z, opts, ms_full, lcsm, torch, dev, args):

@@ -1,4 +1,4 @@
-"""Python binding of the C ABI in ``include/lcsm.h``, ``lcsm_dd.h`` and ``lcsm_synth.h`` (ctypes).
+"""Python binding of the C ABI in ``include/lcsm.h``, ``lcsm_base.h``, ``lcsm_dd.h`` and ``lcsm_synth.h`` (ctypes).
 
 Argument marshalling only: every step of the computation runs in the HIP
 kernels of ``liblcsm.so``.  PyTorch supplies device memory (the workspace and
@@ -23,6 +23,9 @@ LCSM_ESTATE = -5
 
 TILE_NONE, TILE_DIRECT, TILE_FFT, TILE_FFT_HBM, TILE_FFT_COL = 0, 1, 2, 3, 4
 GRAPH_CHAIN = 1
+BASE_LAZY, BASE_EAGER, BASE_NP = 0, 1, 2
+BASE_KINDS = {"lazy": BASE_LAZY, "lazy_np": BASE_LAZY | BASE_NP, "eager": BASE_EAGER,
+              "eager_np": BASE_EAGER | BASE_NP}
 GRAPH_DEFAULT_SEG, GRAPH_MAX_SEG = 16384, 32768
 TILE_KIND_NAMES = {TILE_NONE: "none", TILE_DIRECT: "direct", TILE_FFT: "fft_lds",
                    TILE_FFT_HBM: "fft_hbm", TILE_FFT_COL: "fft_col"}
@@ -91,6 +94,15 @@ _SIGS = {
     "lcsm_graph_destroy": (None, [_vp]),
     "lcsm_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "lcsm_last_error": (ctypes.c_char_p, [_vp]),
+    # include/lcsm_base.h
+    "lcsm_base_workspace_bytes": (ctypes.c_int, [ctypes.c_int] * 5 + [ctypes.POINTER(ctypes.c_size_t)]),
+    "lcsm_base_init": (ctypes.c_int, [ctypes.POINTER(_vp), ctypes.c_int, _vp] + [ctypes.c_int] * 4
+                       + [_vp, _vp, ctypes.c_size_t]),
+    "lcsm_base_step": (ctypes.c_int, [_vp, _vp, _vp]),
+    "lcsm_base_reset": (ctypes.c_int, [_vp]),
+    "lcsm_base_position": (ctypes.c_int, [_vp, _c_int_p]),
+    "lcsm_base_destroy": (None, [_vp]),
+    "lcsm_base_last_error": (ctypes.c_char_p, [_vp]),
     # include/lcsm_dd.h
     "lcsm_dd_workspace_bytes": (ctypes.c_int, [ctypes.c_int] * 4
                                 + [ctypes.POINTER(Options), ctypes.POINTER(ctypes.c_size_t)]),
@@ -166,6 +178,16 @@ def raw():
     return _lib
 
 
+def _after_current(stream, device):
+    """Order work queued next on ``stream`` after everything already queued on
+    torch's current stream (where callers produce filters and inputs), when
+    the two differ: the library's calls are asynchronous on their own stream."""
+    import torch
+    cur = torch.cuda.current_stream(device)
+    if cur.cuda_stream != stream.cuda_stream:
+        stream.wait_stream(cur)
+
+
 class Lcsm:
     """One relaxed online convolution context.
 
@@ -193,6 +215,7 @@ class Lcsm:
         nbytes = workspace_bytes(self.M, self.B, self.D, self.L, options)
         self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
         self._ctx = _vp()
+        _after_current(self.stream, self.device)
         r = _lib.lcsm_init(ctypes.byref(self._ctx), filters.data_ptr(), self.M, self.B, self.D,
                            self.L, self.stream.cuda_stream, self.workspace.data_ptr(), nbytes,
                            _opts(options))
@@ -221,6 +244,7 @@ class Lcsm:
         shape = (self.M, self.B, self.D)
         if z_t is None:
             z_t = torch.empty(shape, dtype=torch.float32, device=self.device)
+        _after_current(self.stream, self.device)
         self._check(_lib.lcsm_step(self._ctx, self._slab(y_t, shape, "y_t"),
                                    self._slab(z_t, shape, "z_t")), "lcsm_step")
         return z_t
@@ -231,6 +255,7 @@ class Lcsm:
         shape = (self.M, self.B, self.D)
         if z_t is None:
             z_t = torch.empty(shape, dtype=torch.float32, device=self.device)
+        _after_current(self.stream, self.device)
         self._check(_lib.lcsm_step_chain(self._ctx, self._slab(x_t, shape, "x_t"),
                                          self._slab(z_t, shape, "z_t")), "lcsm_step_chain")
         return z_t
@@ -240,6 +265,7 @@ class Lcsm:
         shape = (self.B, self.D)
         if z is None:
             z = torch.empty(shape, dtype=torch.float32, device=self.device)
+        _after_current(self.stream, self.device)
         self._check(_lib.lcsm_step_layer(self._ctx, int(layer), self._slab(y, shape, "y"),
                                          self._slab(z, shape, "z")), "lcsm_step_layer")
         return z
@@ -256,6 +282,7 @@ class Lcsm:
         if not (y.is_contiguous() and z.is_contiguous() and y.is_cuda and z.is_cuda):
             raise ValueError("y and z must be contiguous CUDA tensors")
         slab = self.M * self.B * self.D
+        _after_current(self.stream, self.device)
         self._check(_lib.lcsm_run(self._ctx, int(n), y.data_ptr(), slab, z.data_ptr(), slab),
                     "lcsm_run")
         return z
@@ -271,6 +298,7 @@ class Lcsm:
         if not (y.is_contiguous() and z.is_contiguous() and y.is_cuda and z.is_cuda):
             raise ValueError("y and z must be contiguous CUDA tensors")
         slab = self.M * self.B * self.D
+        _after_current(self.stream, self.device)
         self._check(_lib.lcsm_prefill(self._ctx, int(P), y.data_ptr(), slab, z.data_ptr(), slab),
                     "lcsm_prefill")
         return z
@@ -372,6 +400,7 @@ class Graph:
         self._keepalive = keepalive
 
     def launch(self):
+        _after_current(self._ctx.stream, self._ctx.device)
         self._ctx._check(_lib.lcsm_graph_launch(self._g), "lcsm_graph_launch")
 
     @property
@@ -384,6 +413,80 @@ class Graph:
         if self._g:
             _lib.lcsm_graph_destroy(self._g)
             self._g = _vp()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def base_workspace_bytes(kind, M, B, D, L) -> int:
+    n = ctypes.c_size_t(0)
+    r = _lib.lcsm_base_workspace_bytes(int(kind), M, B, D, L, ctypes.byref(n))
+    if r:
+        raise LcsmError(r, "lcsm_base_workspace_bytes")
+    return n.value
+
+
+class Base:
+    """A lazy or eager online convolution context (``include/lcsm_base.h``), the
+    baselines of Sec. 3.1.1: ``kind`` is one of BASE_KINDS' names or codes.
+    ``filters`` [M, D, L] fp32 CUDA tensor; the workspace is a torch uint8
+    tensor owned by this object."""
+
+    def __init__(self, kind, filters, B: int, stream=None):
+        import torch
+        if not (filters.is_cuda and filters.dtype == torch.float32 and filters.dim() == 3):
+            raise ValueError("filters must be a CUDA fp32 tensor [M, D, L]")
+        self.kind = BASE_KINDS[kind] if isinstance(kind, str) else int(kind)
+        filters = filters.contiguous()
+        self.M, self.D, self.L = (int(v) for v in filters.shape)
+        self.B = int(B)
+        self.device = filters.device
+        self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
+        nbytes = base_workspace_bytes(self.kind, self.M, self.B, self.D, self.L)
+        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+        self._ctx = _vp()
+        _after_current(self.stream, self.device)
+        r = _lib.lcsm_base_init(ctypes.byref(self._ctx), self.kind, filters.data_ptr(), self.M,
+                                self.B, self.D, self.L, self.stream.cuda_stream,
+                                self.workspace.data_ptr(), nbytes)
+        if r:
+            raise LcsmError(r, "lcsm_base_init")
+        self._filters_keepalive = filters
+
+    def _check(self, r, where):
+        if r:
+            detail = _lib.lcsm_base_last_error(self._ctx).decode() if self._ctx else ""
+            raise LcsmError(r, where, detail)
+
+    def step(self, y_t, z_t=None):
+        import torch
+        shape = (self.M, self.B, self.D)
+        if z_t is None:
+            z_t = torch.empty(shape, dtype=torch.float32, device=self.device)
+        for t, name in ((y_t, "y_t"), (z_t, "z_t")):
+            if not (t.is_cuda and t.dtype == torch.float32 and t.is_contiguous()
+                    and tuple(t.shape) == shape):
+                raise ValueError(f"{name} must be a contiguous CUDA fp32 tensor of shape {shape}")
+        _after_current(self.stream, self.device)
+        self._check(_lib.lcsm_base_step(self._ctx, y_t.data_ptr(), z_t.data_ptr()), "lcsm_base_step")
+        return z_t
+
+    def reset(self):
+        self._check(_lib.lcsm_base_reset(self._ctx), "lcsm_base_reset")
+
+    @property
+    def position(self) -> int:
+        t = ctypes.c_int()
+        self._check(_lib.lcsm_base_position(self._ctx, ctypes.byref(t)), "lcsm_base_position")
+        return t.value
+
+    def close(self):
+        if self._ctx:
+            _lib.lcsm_base_destroy(self._ctx)
+            self._ctx = _vp()
 
     def __del__(self):
         try:
@@ -419,6 +522,7 @@ class Dd:
         nbytes = dd_workspace_bytes(self.M, self.B, self.D, self.L, options)
         self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
         self._ctx = _vp()
+        _after_current(self.stream, self.device)
         r = _lib.lcsm_dd_init(ctypes.byref(self._ctx), self.M, self.B, self.D, self.L,
                               self.stream.cuda_stream, self.workspace.data_ptr(), nbytes,
                               _opts(options))
@@ -439,6 +543,7 @@ class Dd:
             if not (t.is_cuda and t.dtype == torch.float32 and t.is_contiguous()
                     and tuple(t.shape) == shape):
                 raise ValueError(f"{name} must be a contiguous CUDA fp32 tensor of shape {shape}")
+        _after_current(self.stream, self.device)
         self._check(_lib.lcsm_dd_step(self._ctx, y_t.data_ptr(), rho_t.data_ptr(), z_t.data_ptr()),
                     "lcsm_dd_step")
         return z_t
@@ -495,6 +600,7 @@ class Synth:
             options = o
         self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
         self._ctx = _vp()
+        _after_current(self.stream, self.device)
         r = _lib.lcsm_synth_init(ctypes.byref(self._ctx), filters.data_ptr(), w_up.data_ptr(),
                                  b_up.data_ptr(), w_down.data_ptr(), b_down.data_ptr(), M, self.B,
                                  D, self.L, self.stream.cuda_stream, _opts(options))
@@ -519,6 +625,7 @@ class Synth:
             if not (t.is_cuda and t.dtype == torch.float32 and t.is_contiguous()
                     and tuple(t.shape) == shape):
                 raise ValueError(f"{name} must be a contiguous CUDA fp32 tensor of shape {shape}")
+        _after_current(self.stream, self.device)
         self._check(_lib.lcsm_synth_step(self._ctx, eps_t.data_ptr(), act_t.data_ptr()),
                     "lcsm_synth_step")
         return act_t

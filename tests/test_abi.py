@@ -334,3 +334,36 @@ def test_dd_workspace_and_validation():
     assert lib.lcsm_dd_position(None, ctypes.byref(ctypes.c_int())) == lcsm.LCSM_EINVAL
     lib.lcsm_dd_destroy(None)
     assert lib.lcsm_dd_last_error(None) == b""
+
+
+def test_base_workspace_and_validation():
+    """The lazy/eager baselines (include/lcsm_base.h): workspace sizes and
+    argument checks, on the host."""
+    M, B, D, L = 3, 2, 40, 1000
+    lazy = lcsm.base_workspace_bytes(lcsm.BASE_LAZY, M, B, D, L)
+    eager = lcsm.base_workspace_bytes(lcsm.BASE_EAGER, M, B, D, L)
+    state, filt = 4 * M * L * B * D, 4 * M * L * D
+    assert eager >= state + filt and eager - (state + filt) < 1024
+    # lazy also holds ceil(L/256) partial sums per column
+    assert lazy - eager >= 4 * 4 * M * B * D
+    assert lcsm.base_workspace_bytes(lcsm.BASE_LAZY | lcsm.BASE_NP, M, B, D, L) == lazy
+    for kind, shape in ((4, (1, 1, 1, 8)), (-1, (1, 1, 1, 8)), (0, (0, 1, 1, 8)),
+                        (0, (1, 1, 1, (1 << 19) + 1)), (1, (1, 1 << 16, 1, 8))):
+        with pytest.raises(lcsm.LcsmError) as e:
+            lcsm.base_workspace_bytes(kind, *shape)
+        assert e.value.code == lcsm.LCSM_EINVAL
+    lib = lcsm.raw()
+    ctx = ctypes.c_void_p(1234)
+    fake = ctypes.c_void_p(4096)
+    assert lib.lcsm_base_init(ctypes.byref(ctx), 0, None, 1, 1, 1, 8, None, None, 0) == lcsm.LCSM_EINVAL
+    assert ctx.value is None
+    assert lib.lcsm_base_init(ctypes.byref(ctx), 7, fake, 1, 1, 1, 8, None, None, 0) == lcsm.LCSM_EINVAL
+    need = lcsm.base_workspace_bytes(0, 1, 1, 1, 8)
+    assert lib.lcsm_base_init(ctypes.byref(ctx), 0, fake, 1, 1, 1, 8, None, fake,
+                              need - 1) == lcsm.LCSM_ENOMEM
+    assert lib.lcsm_base_step(None, fake, fake) == lcsm.LCSM_EINVAL
+    assert lib.lcsm_base_reset(None) == lcsm.LCSM_EINVAL
+    t = ctypes.c_int()
+    assert lib.lcsm_base_position(None, ctypes.byref(t)) == lcsm.LCSM_EINVAL
+    lib.lcsm_base_destroy(None)
+    assert lib.lcsm_base_last_error(None) == b""
