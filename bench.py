@@ -50,10 +50,16 @@ HBM_PEAK_GBS = 8000.0
 # algorithmic traffic per generation).
 DEFAULT_WORKLOAD = "m32b16d2048l16k"
 RING = 256  # input slabs kept resident
-# Positions per HIP graph: a generation is replayed as a chain of graphs of
-# at most this many positions (the library's lcsm_graph_capture; the bench's
-# own GraphChain for the data-dependent and synthetic-model contexts).
-GRAPH_SEG = 16384
+# A generation is replayed as a chain of HIP graphs, none larger than a
+# bounded number of kernel nodes: a single graph of about 131k nodes (one
+# generation of 131072 positions) and one of about 1.08M nodes (16384
+# positions of the 32-layer synthetic model, 66 launches each) crashed the
+# process while it was recorded or instantiated; graphs of up to about 33k
+# nodes are known good.  Positions per graph of the library's recorder
+# (lcsm_graph_capture: one or two launches per position, a few hundred at
+# the rare largest tiles), and the node budget of the bench's own chains.
+GRAPH_SEG = 8192
+GRAPH_MAX_NODES = 16384
 
 
 def parse():
@@ -393,31 +399,46 @@ def main():
         if roofline["avg_launch_us"] < 2.0 * floor_us:
             roofline["bound"] = "launch"
 
+    def release():
+        # each leg's contexts hold tens of GB; give torch's cached blocks back
+        # so that the next leg's library-allocated workspace fits
+        import gc
+        gc.collect()
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+
+    release()
     closed = None
     if args.closed_loop:
         closed = closed_loop(w, filters, opts, lcsm, torch, dev, args)
+        release()
 
     prefill = None
     if args.prefill:
         prefill = prefill_timing(w, filters, opts, lcsm, torch, dev)
+        release()
 
     half = None
     if args.half_state:
         half = half_state_timing(w, filters, y, z, opts, ms, lcsm, torch, dev, args)
+        release()
 
     dd = None
     if args.dd:
         dd = dd_timing(w, ms, lcsm, torch, dev, args)
+        release()
 
     synth = None
     if args.synth:
         synth = synth_timing(w, filters, opts, ms, lcsm, torch, dev, args)
+        release()
 
     base = None
     if args.baselines:
         kinds = (["lazy", "lazy_np", "eager", "eager_np"] if args.baselines == "all"
                  else [k for k in args.baselines.split(",") if k])
         base = baselines_timing(w, filters, y, ms, kinds, lcsm, torch, dev, args, synth)
+        release()
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -647,16 +668,19 @@ def time_steps(one_step, torch, args, verbose=False):
 
 class GraphChain:
     """A generation of a context without the library's own recorder (the
-    data-dependent and synthetic-model contexts) as a chain of torch HIP graphs
-    of at most seg positions each: issue(p0, p1) queues positions [p0, p1)
-    (the reset with p0 = 0) on the capture stream."""
+    data-dependent, synthetic-model and baseline contexts) as a chain of
+    torch HIP graphs: issue(p0, p1) queues positions [p0, p1) (the reset with
+    p0 = 0) on the capture stream, and each graph takes as many positions as
+    keep it within GRAPH_MAX_NODES kernel nodes given at most per_position
+    launches per position (and at most seg positions)."""
 
-    def __init__(self, torch, stream, L, seg, issue):
+    def __init__(self, torch, stream, L, seg, issue, per_position):
+        self.positions = max(1, min(seg, GRAPH_MAX_NODES // max(1, per_position)))
         self.graphs = []
-        for p0 in range(0, L, seg):
+        for p0 in range(0, L, self.positions):
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g, stream=stream):
-                issue(p0, min(L, p0 + seg))
+                issue(p0, min(L, p0 + self.positions))
             self.graphs.append(g)
         torch.cuda.synchronize()
 
@@ -727,7 +751,9 @@ def baselines_timing(w, filters, y, ms_relaxed, kinds, lcsm, torch, dev, args, s
                 ctx.step(y[t % R], z[t % R])
 
         print(f"# baseline {kind}: recording", file=sys.stderr, flush=True)
-        chain = GraphChain(torch, stream, w.L, args.graph_seg, issue)
+        # lazy: partial sums + reduction; eager: one launch; per layer with _np
+        per_pos = (2 if kind.startswith("lazy") else 1) * (w.M if kind.endswith("_np") else 1)
+        chain = GraphChain(torch, stream, w.L, args.graph_seg, issue, per_pos)
         with torch.cuda.stream(stream):
             for _ in range(args.baseline_warmup):
                 chain.replay()
@@ -800,7 +826,9 @@ def dd_timing(w, ms_fixed, lcsm, torch, dev, args):
         for t in range(p0, p1):
             ctx.step(y[t % R], rho[t % R], z[t % R])
 
-    chain = GraphChain(torch, stream, w.L, args.graph_seg, issue) if args.graph else None
+    # the red cell with the small tiles, plus one launch per larger U dividing t+1
+    per_pos = 1 + max(1, (w.L - 1).bit_length())
+    chain = GraphChain(torch, stream, w.L, args.graph_seg, issue, per_pos) if args.graph else None
     one = chain.replay if chain else (lambda: issue(0, w.L))
     print("# data-dependent generations", file=sys.stderr, flush=True)
     with torch.cuda.stream(stream):
@@ -834,7 +862,9 @@ def synth_timing(w, filters, opts, ms_mixer, lcsm, torch, dev, args):
         for t in range(p0, p1):
             model.step(eps[t % R], act[t % R])
 
-    chain = GraphChain(torch, stream, w.L, args.graph_seg, issue) if args.graph else None
+    # sampler/red cell, two products per layer and 16 batch rows, the gray tiles
+    per_pos = 2 + 2 * w.M * (-(-w.B // 16)) + 8
+    chain = GraphChain(torch, stream, w.L, args.graph_seg, issue, per_pos) if args.graph else None
     one = chain.replay if chain else (lambda: issue(0, w.L))
     print("# synthetic-model generations", file=sys.stderr, flush=True)
     with torch.cuda.stream(stream):

@@ -182,8 +182,9 @@ int lcsm_run(lcsm_ctx* ctx, int n, const float* y, size_t y_stride, float* z, si
  * generation instead of one or two kernel launches per position).
  *
  * lcsm_graph_capture records lcsm_reset followed by n consecutive steps into
- * a chain of HIP graphs of at most seg_positions positions each (a bounded
- * node count per graph, whatever n is).  Step k (k < n) reads
+ * a chain of HIP graphs of at most seg_positions positions each (a step is
+ * one or two kernel launches, a few hundred only at the largest tiles, so
+ * every graph holds about 2 * seg_positions nodes, whatever n is).  Step k (k < n) reads
  *   in + (k mod in_ring) * in_stride      (device, [M][B][D] fp32)
  * and writes
  *   z + (k mod z_ring) * z_stride         (device, [M][B][D] fp32),
@@ -202,8 +203,8 @@ int lcsm_run(lcsm_ctx* ctx, int n, const float* y, size_t y_stride, float* z, si
  * the instantiation failed; nothing is left recorded, the context is
  * faulted until lcsm_reset). */
 #define LCSM_GRAPH_CHAIN 1
-#define LCSM_GRAPH_DEFAULT_SEG 16384
-#define LCSM_GRAPH_MAX_SEG 32768
+#define LCSM_GRAPH_DEFAULT_SEG 8192
+#define LCSM_GRAPH_MAX_SEG 16384
 typedef struct lcsm_graph lcsm_graph;
 int lcsm_graph_capture(lcsm_ctx* ctx, int flags, int n, const float* in, size_t in_stride,
                        int in_ring, float* z, size_t z_stride, int z_ring, int seg_positions,

@@ -474,9 +474,12 @@ int lcsm_run(lcsm_ctx* c, int n, const float* y, size_t y_stride, float* z, size
 }  // extern "C"
 
 // A recorded generation: lcsm_reset plus n steps, split into graphs of at
-// most seg positions so that no graph's node count grows with n (one graph
-// per generation of 131072 positions, about 131k kernel nodes, crashed the
-// process during capture; graphs of 32768 positions are known good).
+// most seg positions so that no graph's node count grows with n.  A step is
+// one or two kernel launches, a few hundred only at the rare largest tiles,
+// so a graph holds about 2 seg nodes (at most 16384 positions: about 33k
+// nodes).  Graphs of about 131k and 1.08M nodes crashed the process while
+// they were recorded or instantiated; graphs of about 33k nodes are known
+// good.
 struct lcsm_graph {
   lcsm_ctx* ctx;
   int n;

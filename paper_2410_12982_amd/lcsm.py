@@ -26,7 +26,7 @@ GRAPH_CHAIN = 1
 BASE_LAZY, BASE_EAGER, BASE_NP = 0, 1, 2
 BASE_KINDS = {"lazy": BASE_LAZY, "lazy_np": BASE_LAZY | BASE_NP, "eager": BASE_EAGER,
               "eager_np": BASE_EAGER | BASE_NP}
-GRAPH_DEFAULT_SEG, GRAPH_MAX_SEG = 16384, 32768
+GRAPH_DEFAULT_SEG, GRAPH_MAX_SEG = 8192, 16384
 TILE_KIND_NAMES = {TILE_NONE: "none", TILE_DIRECT: "direct", TILE_FFT: "fft_lds",
                    TILE_FFT_HBM: "fft_hbm", TILE_FFT_COL: "fft_col"}
 

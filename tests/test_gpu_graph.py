@@ -8,7 +8,7 @@ graph's node count growing with the generation).  Checks:
 * replays equal host-launched steps on the same ring inputs bit for bit,
   again on a second replay (the reset is inside the recording), for
   teacher-forced and chained inputs and for several segment lengths;
-* the benchmark's own recording (a ring of 256 input slabs, graphs of 16384
+* the benchmark's own recording (a ring of 256 input slabs, graphs of 8192
   positions) on the 32768- and 131072-position workloads, every position of
   sampled columns against the fp64 oracle on the same ring-periodic inputs;
 * argument errors leave the context usable.
@@ -51,7 +51,7 @@ def test_replay_equals_host_launches(shape, seg):
     torch.cuda.synchronize()
     z = torch.full_like(z_host, float("nan"))
     g = ctx.capture(y, z, n=L, seg=seg)
-    expect = -(-L // (seg or 16384))
+    expect = -(-L // (seg or lcsm_mod().GRAPH_DEFAULT_SEG))
     assert g.segments == expect
     assert ctx.position == L
     for rep in range(2):
@@ -89,8 +89,8 @@ def test_replay_chain_equals_host_launches(shape):
 
 @pytest.mark.parametrize("name", ["m18b4d768l32k", "m18b1d1024l128k"])
 def test_benchmark_recording_against_oracle(name):
-    """The benchmark's recording: a ring of 256 input slabs, graphs of 16384
-    positions (2 and 8 of them here).  Outputs go to a buffer of all L
+    """The benchmark's recording: a ring of 256 input slabs, graphs of 8192
+    positions (4 and 16 of them here).  Outputs go to a buffer of all L
     positions so that every position of the sampled columns is compared."""
     w = datagen.WORKLOADS[name]
     say(f"[benchmark recording vs oracle] {w.name} M={w.M} B={w.B} D={w.D} L={w.L}")
@@ -98,9 +98,9 @@ def test_benchmark_recording_against_oracle(name):
     y = datagen.y_torch(w, dev(), 0, R)
     z = torch.empty((w.L, w.M, w.B, w.D), dtype=torch.float32, device=dev())
     ctx = _ctx(w)
-    g = ctx.capture(y, z, n=w.L, seg=16384)
+    g = ctx.capture(y, z, n=w.L, seg=8192)
     say(f"  {g.segments} graphs recorded")
-    assert g.segments == w.L // 16384
+    assert g.segments == w.L // 8192
     g.launch()
     torch.cuda.synchronize()
     cols = datagen.sample_columns(w, 48)
