@@ -89,6 +89,13 @@ def parse():
                    help="skip the synthetic end-to-end model (MLP blocks + noise sampler)")
     p.add_argument("--no-half-state", dest="half_state", action="store_false", default=True,
                    help="skip the generations with half-state storage")
+    p.add_argument("--extra-steps", type=int, default=1,
+                   help="timed generations of each extra leg (closed loop, half-state, "
+                        "data-dependent, synthetic model)")
+    p.add_argument("--extra-warmup", type=int, default=1, help="untimed generations of each extra leg")
+    p.add_argument("--synth-max-bytes", type=float, default=8e12,
+                   help="the synthetic model is timed over the first positions whose MLP weight "
+                        "reads stay below this many bytes (all L when they do)")
     p.add_argument("--baselines", default="",
                    help="comma-separated lazy/eager baselines to time over whole generations "
                         "(lazy, lazy_np, eager, eager_np; 'all' for the four), reported as the "
@@ -641,28 +648,34 @@ def kernel_pass(w, filters, y, z, opts, lcsm, torch):
     return roofline, levels
 
 
-def time_steps(one_step, torch, args, verbose=False):
-    """args.warmup untimed calls of one_step, then args.steps timed with
-    events on the current stream (bracketing the whole timed region).
-    Returns ms per step."""
-    for _ in range(args.warmup):
+def time_steps(one_step, torch, args, verbose=False, extra=None):
+    """Untimed warm-up calls of one_step, then timed ones, bracketed by events
+    on the current stream.  The timed region uses args.warmup / args.steps;
+    an extra leg (extra = its name) uses args.extra_warmup / args.extra_steps
+    and prints a line per generation.  Returns ms per step."""
+    warmup, steps = (args.warmup, args.steps) if extra is None else (args.extra_warmup,
+                                                                     args.extra_steps)
+    for k in range(warmup):
         one_step()
+        if extra:
+            torch.cuda.synchronize()
+            print(f"# {extra}: warm-up {k + 1}/{warmup}", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     if verbose:
-        print(f"# warmup done ({args.warmup})", file=sys.stderr, flush=True)
+        print(f"# warmup done ({warmup})", file=sys.stderr, flush=True)
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_wall = time.perf_counter()
     ev0.record()
-    for _ in range(args.steps):
+    for _ in range(steps):
         one_step()
     ev1.record()
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
-    ms = ev0.elapsed_time(ev1) / args.steps
-    if verbose:
-        print(f"# timed {args.steps} steps: {ms:.3f} ms/step (wall {1e3 * t_wall / args.steps:.3f})",
-              file=sys.stderr, flush=True)
+    ms = ev0.elapsed_time(ev1) / steps
+    if verbose or extra:
+        print(f"# {extra or 'timed'}: {steps} steps, {ms:.3f} ms/step (wall "
+              f"{1e3 * t_wall / steps:.3f})", file=sys.stderr, flush=True)
     return ms
 
 
@@ -692,7 +705,7 @@ class GraphChain:
         self.graphs = []
 
 
-def timed_generations(w, filters, y, z, opts, lcsm, torch, dev, args, verbose=False):
+def timed_generations(w, filters, y, z, opts, lcsm, torch, dev, args, verbose=False, extra=None):
     """Teacher-forced generations of all L positions (inputs from the ring y
     resident in HBM), recorded once by the library as a chain of HIP graphs
     (lcsm_graph_capture: reset + L steps, at most args.graph_seg positions per
@@ -717,7 +730,7 @@ def timed_generations(w, filters, y, z, opts, lcsm, torch, dev, args, verbose=Fa
             for t0 in range(0, w.L, R):
                 ctx.run(y, z, n=min(R, w.L - t0))
     with torch.cuda.stream(stream):
-        ms = time_steps(one_step, torch, args, verbose)
+        ms = time_steps(one_step, torch, args, verbose, extra)
     if graph is not None:
         graph.close()
     ctx.close()
@@ -771,7 +784,7 @@ def baselines_timing(w, filters, y, ms_relaxed, kinds, lcsm, torch, dev, args, s
                      "relaxed_speedup": round(bms / ms_relaxed, 2)}
     if "lazy" in out:
         out["speedup_over_parallel_lazy"] = out["lazy"]["relaxed_speedup"]
-        if synth and "ms_per_step" in synth:
+        if synth and synth.get("positions") == w.L:
             lazy_model = synth["ms_per_step"] - ms_relaxed + out["lazy"]["ms_per_step"]
             out["end_to_end_speedup_over_parallel_lazy"] = {
                 "value": round(lazy_model / synth["ms_per_step"], 2),
@@ -791,7 +804,7 @@ def half_state_timing(w, filters, y, z, opts, ms_full, lcsm, torch, dev, args):
     except lcsm.LcsmError as e:  # the tile of side T is a direct tile here
         return {"skipped": str(e)}
     print("# half-state generations", file=sys.stderr, flush=True)
-    ms = timed_generations(w, filters, y, z, hopts, lcsm, torch, dev, args)
+    ms = timed_generations(w, filters, y, z, hopts, lcsm, torch, dev, args, extra="half-state")
     T = 1
     while 2 * T < w.L:
         T *= 2
@@ -832,7 +845,7 @@ def dd_timing(w, ms_fixed, lcsm, torch, dev, args):
     one = chain.replay if chain else (lambda: issue(0, w.L))
     print("# data-dependent generations", file=sys.stderr, flush=True)
     with torch.cuda.stream(stream):
-        dms = time_steps(one, torch, args)
+        dms = time_steps(one, torch, args, extra="data-dependent")
     if chain:
         chain.close()
     ctx.close()
@@ -844,10 +857,19 @@ def synth_timing(w, filters, opts, ms_mixer, lcsm, torch, dev, args):
     """Generations of the synthetic end-to-end model (lcsm_synth_step: per
     layer the mixer and an MLP block of hidden 2D with GELU; the next token
     = last layer's output + noise), dispatched like the timed region (a chain
-    of HIP graphs): warmup untimed, then args.steps timed with events.
+    of HIP graphs): args.extra_warmup untimed, then args.extra_steps timed
+    with events.  When a generation would read more than args.synth_max_bytes
+    of MLP weights (the 1M-column workload reads 2.1 GB per position), the
+    model is timed over its first P positions (P a power of two) instead.
     ms_mixer: the teacher-forced mixer generation time, for the mixer's share
-    of the model's time."""
+    of the model's time (per position, over the whole generation)."""
     import datagen
+    wbytes = 4 * w.M * (4 * w.D * w.D + 3 * w.D)
+    P = w.L
+    if wbytes * w.L > args.synth_max_bytes:
+        P = 256
+        while 2 * P < w.L and 2 * P * wbytes <= args.synth_max_bytes:
+            P *= 2
     R = min(RING, w.L)
     weights = datagen.mlp_weights_torch(w, dev)
     eps = datagen.noise_torch(w, dev, 0, R)
@@ -864,21 +886,26 @@ def synth_timing(w, filters, opts, ms_mixer, lcsm, torch, dev, args):
 
     # sampler/red cell, two products per layer and 16 batch rows, the gray tiles
     per_pos = 2 + 2 * w.M * (-(-w.B // 16)) + 8
-    chain = GraphChain(torch, stream, w.L, args.graph_seg, issue, per_pos) if args.graph else None
-    one = chain.replay if chain else (lambda: issue(0, w.L))
-    print("# synthetic-model generations", file=sys.stderr, flush=True)
+    chain = GraphChain(torch, stream, P, args.graph_seg, issue, per_pos) if args.graph else None
+    one = chain.replay if chain else (lambda: issue(0, P))
+    print(f"# synthetic-model generations ({P} of {w.L} positions)", file=sys.stderr, flush=True)
     with torch.cuda.stream(stream):
-        sms = time_steps(one, torch, args)
+        sms = time_steps(one, torch, args, extra="synthetic model")
     if chain:
         chain.close()
     model.close()
-    wbytes = 4 * w.M * (4 * w.D * w.D + 3 * w.D)
-    return {"ms_per_step": round(sms, 4), "tokens_per_s": round(w.B * w.L / (sms / 1e3), 1),
-            "us_per_position": round(1e3 * sms / w.L, 3),
-            "mixer_share": round(ms_mixer / sms, 4),
-            "weight_bytes_per_position": wbytes,
-            "launches_per_position": 2 * w.M + 2,
-            "graph": bool(chain)}
+    us_pos = 1e3 * sms / P
+    out = {"positions": P, "ms_per_step": round(sms, 4), "tokens_per_s": round(w.B * P / (sms / 1e3), 1),
+           "us_per_position": round(us_pos, 3),
+           "mixer_share": round(1e3 * ms_mixer / w.L / us_pos, 4),
+           "weight_bytes_per_position": wbytes,
+           "weight_GB_s": round(wbytes / (us_pos * 1e-6) / 1e9, 1),
+           "launches_per_position": 2 * w.M + 2,
+           "graph": bool(chain)}
+    if P < w.L:
+        out["note"] = (f"timed over the first {P} positions (whole generations would read "
+                       f"{wbytes * w.L / 1e12:.1f} TB of weights)")
+    return out
 
 
 def closed_loop(w, filters, opts, lcsm, torch, dev, args):
@@ -902,7 +929,7 @@ def closed_loop(w, filters, opts, lcsm, torch, dev, args):
 
     one = graph.launch if graph else host_generation
     with torch.cuda.stream(stream):
-        cms = time_steps(one, torch, args)
+        cms = time_steps(one, torch, args, extra="closed loop")
     if graph:
         graph.close()
     ctx.close()
@@ -1016,6 +1043,7 @@ def cpu_baseline(w, budget_s):
                 # oracle time only (input generation excluded); shards run in parallel
                 wall = max(pool.map(_oracle_shard, shards))
                 n = len(b_idx) * nd * workers
+                print(f"# cpu baseline: {n} columns in {wall:.1f} s", file=sys.stderr, flush=True)
                 if wall * 4 > budget_s or n >= total_cols or per >= 4096:
                     break
                 # the oracle vectorises over columns: fewer, wider shards are cheaper

@@ -14,7 +14,6 @@
 //
 // Gray tile (Eq. taus) for i = t+1, side U: for j < dst_len,
 //   S[i+j] += sum_{k<U} y[i-U+k] * h[U+j-k]     (lags 1..2U-1).
-#include "lcsm_fft_core.h"
 #include "lcsm_internal.h"
 
 namespace lcsm {
@@ -38,35 +37,28 @@ struct Split {
 // Every load (inputs, lags, the red cell's accumulator and the tile's
 // destination accumulators) is issued before the first store, so the step
 // costs one memory round trip; the slots read and written are distinct rows.
-// Grid (channel blocks, B, M * SPLIT): consecutive lanes take consecutive
-// channels.  The hardware puts workgroup n (x fastest) on XCD n mod 8; the B
-// batch rows of one channel block read the same filter lags, so they should
-// share one XCD's L2.  That holds by itself when the channel-block count is
-// a multiple of 8; otherwise (xcd_remap) the workgroup ids are remapped so
-// that each XCD runs a contiguous range of a batch-row-fastest order.
+// Grid (channel blocks, B, M * SPLIT): no integer division on the critical
+// path, consecutive lanes take consecutive channels.  With a channel-block
+// count that is not a multiple of 8 the batch rows of one block run on
+// different XCDs, and each XCD's L2 fetches the same lag rows.  Remapping the
+// workgroup ids so that they share one XCD removes those reads, but its
+// integer divisions ahead of the first load cost about 0.5 us per launch on
+// these latency-bound steps (a 32768-position, 18-layer generation: 135 ->
+// 151 ms), so the grid keeps the hardware order.
 template <int U, bool RED>
 __global__ __launch_bounds__(kThreads) void k_step_fused(const float* __restrict__ y,
                                                         float* __restrict__ z,
                                                         float* __restrict__ S,
                                                         const float* __restrict__ Hf, int m0, int L,
-                                                        int SL, int BD, int D, int t, int dst_len,
-                                                        int xcd_remap) {
+                                                        int SL, int BD, int D, int t, int dst_len) {
   constexpr int SP = U > 0 ? Split<U>::value : 1;
   constexpr int UJ = U > 0 ? U / SP : 1;  // outputs per thread
-  int bx = (int)blockIdx.x, by = (int)blockIdx.y, bz = (int)blockIdx.z;
-  if (xcd_remap) {
-    const int nb = (int)gridDim.x, nr = (int)gridDim.y;
-    const int lg = fft::xcd_logical(bx + nb * (by + nr * bz), nb * nr * (int)gridDim.z);
-    by = lg % nr;
-    bx = (lg / nr) % nb;
-    bz = lg / (nr * nb);
-  }
-  const int d = bx * kThreads + (int)threadIdx.x;
+  const int d = (int)blockIdx.x * kThreads + (int)threadIdx.x;
   if (d >= D) return;
-  const int m = m0 + bz / SP;
-  const int part = bz - (m - m0) * SP;
+  const int m = m0 + (int)blockIdx.z / SP;
+  const int part = (int)blockIdx.z - (m - m0) * SP;
   const int j0 = part * UJ;
-  const int c = by * D + d;
+  const int c = (int)blockIdx.y * D + d;
   const size_t e = (size_t)m * BD + c;
   float* col = S + (size_t)m * SL * BD + c;
   const float* hc = Hf + (size_t)m * L * D + d;
@@ -353,8 +345,6 @@ template <bool RED>
 hipError_t dispatch_fused(int U, const float* y, float* z, float* S, const float* Hf,
                           const Shape& s, int t, int dst_len, hipStream_t st) {
   const dim3 block(kThreads);
-  // batch rows of a channel block on one XCD (see k_step_fused)
-  const int remap = (s.B > 1 && blocks_for(s.D) % 8 != 0) ? 1 : 0;
 #define LCSM_FUSED_CASE(UU)                                                                      \
   case UU: {                                                                                     \
     constexpr int SP = UU > 0 ? Split<UU>::value : 1;                                            \
@@ -363,7 +353,7 @@ hipError_t dispatch_fused(int U, const float* y, float* z, float* S, const float
       const int mc = s.M - m0 < MC ? s.M - m0 : MC;                                              \
       hipLaunchKernelGGL((k_step_fused<UU, RED>),                                                \
                          dim3(blocks_for(s.D), (unsigned)s.B, (unsigned)(mc * SP)), block, 0,    \
-                         st, y, z, S, Hf, m0, s.L, s.SL, s.BD, s.D, t, dst_len, remap);         \
+                         st, y, z, S, Hf, m0, s.L, s.SL, s.BD, s.D, t, dst_len);                \
     }                                                                                            \
     break;                                                                                       \
   }
