@@ -176,6 +176,23 @@ int lcsm_commit(lcsm_ctx* ctx);
  * Errors as lcsm_step; stops at the first. */
 int lcsm_run(lcsm_ctx* ctx, int n, const float* y, size_t y_stride, float* z, size_t z_stride);
 
+/* lcsm_run for callers that cannot allocate device memory (code under HIP
+ * graph capture, serving loops or harnesses that forbid hipMalloc): the same
+ * n steps, arguments, results (to fp32 rounding) and errors as lcsm_run,
+ * allocating nothing.  The FFT tiles' staging (column chunks and multi-pass
+ * transforms), which lcsm_run takes from the context's workspace, comes from
+ * a static device array of the library instead: 64 MiB per GPU, reserved
+ * when the library is loaded and held until the process ends, enough for
+ * one chunk of every tile a context can plan (contexts whose tiles would
+ * need more are rejected with LCSM_EINVAL before any work is queued).  That
+ * array is shared by every call on the same GPU and keeps the last call's
+ * contents (the tiles write every element before reading it): calls that
+ * overlap on one GPU -- two streams, two threads, two contexts -- race on it
+ * and must be serialised by the caller.  Chunks may differ in size from
+ * lcsm_run's, so results can differ from it in the last bits. */
+int lcsm_run_noalloc(lcsm_ctx* ctx, int n, const float* y, size_t y_stride, float* z,
+                     size_t z_stride);
+
 /* ---- Replayed generations (App. B.2, "CPU Overhead: The silent performance
  * killer": the per-token launches of a generation are recorded once as HIP
  * graphs and replayed, so the host submits a few graph launches per

@@ -4,6 +4,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -123,6 +124,7 @@ int make_shape(int M, int B, int D, int L, const Options& o, Shape* out) {
 // Offsets of the workspace sections, in bytes.
 struct Layout {
   size_t S, Hf, prev, tw, scratch, scratch_bytes, total;
+  size_t scratch_min;    // bytes of one chunk of the largest multi-pass or column tile
   size_t H[kMaxLevels];  // spectra of tile size 2^q (FFT levels only)
   int nmax;              // largest FFT length, 0 if no tile uses the FFT
 };
@@ -163,10 +165,45 @@ Layout layout_for(const Shape& s, const Options& o) {
     if (want < per_col * min_cols) want = per_col * min_cols;
     ly.scratch = off;
     ly.scratch_bytes = want;
+    ly.scratch_min = per_col * min_cols;
     off = align_up(off + want);
   }
   ly.total = off;
   return ly;
+}
+
+}  // namespace
+
+// Staging of the FFT tiles for lcsm_run_noalloc (column chunks and the
+// multi-pass scratch), in place of the workspace's scratch section: one
+// array per GPU, loaded with the library and held until the process ends.
+// Host code uses only its device address, resolved per device by
+// static_scratch_ptr.  64 MiB holds one chunk of every tile the library
+// builds (16 complex columns of the longest, 2^19-point, multi-pass
+// transform).
+constexpr size_t kStaticScratchBytes = 64ull << 20;
+static __device__ __align__(256) float2 scratch[kStaticScratchBytes / sizeof(float2)];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float2* g_scratch_ptr[kMaxDevices];  // device address of scratch per device, null until resolved
+
+// Device address of the static scratch on the current device (which must be
+// `device`), looked up once per device.
+hipError_t static_scratch_ptr(int device, float2** out) {
+  *out = nullptr;
+  if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[device]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[device] = static_cast<float2*>(p);
+  }
+  *out = g_scratch_ptr[device];
+  return hipSuccess;
 }
 
 }  // namespace
@@ -202,6 +239,7 @@ struct lcsm_ctx {
   float* prev;
   float2* tw;
   float2* scratch;
+  float2* static_scratch;  // this device's static scratch (lcsm_run_noalloc)
   int T;            // half-state swap position (the state's rows per layer), 0 without
   int t;            // next position to emit
   int layers_done;  // lcsm_step_layer progress at position t
@@ -380,7 +418,9 @@ int lcsm_init(lcsm_ctx** out, const float* filters, int M, int B, int D, int L, 
   c->ly = ly;
   c->stream = (hipStream_t)stream;
   c->msg[0] = 0;
-  if (hipGetDevice(&c->device) != hipSuccess) {
+  if (hipGetDevice(&c->device) != hipSuccess ||
+      static_scratch_ptr(c->device, &c->static_scratch) != hipSuccess) {
+    (void)hipGetLastError();
     delete c;
     return LCSM_EDEVICE;
   }
@@ -469,6 +509,29 @@ int lcsm_run(lcsm_ctx* c, int n, const float* y, size_t y_stride, float* z, size
     if (r) return r;
   }
   return LCSM_OK;
+}
+
+int lcsm_run_noalloc(lcsm_ctx* c, int n, const float* y, size_t y_stride, float* z,
+                     size_t z_stride) {
+  if (!c) return LCSM_EINVAL;
+  if (n < 0) return fail(c, LCSM_EINVAL, "negative step count", hipSuccess);
+  if (c->ly.scratch_min > kStaticScratchBytes)
+    return fail(c, LCSM_EINVAL, "one chunk of the FFT tiles exceeds the 64 MiB static scratch",
+                hipSuccess);
+  if (!c->static_scratch) return fail(c, LCSM_EDEVICE, "static scratch unavailable", hipSuccess);
+  // the same steps, with the FFT tiles staged in the static scratch
+  float2* const ws_scratch = c->scratch;
+  const size_t ws_bytes = c->ly.scratch_bytes;
+  if (ws_bytes) {
+    c->scratch = c->static_scratch;
+    c->ly.scratch_bytes = kStaticScratchBytes;
+  }
+  int r = LCSM_OK;
+  for (int k = 0; r == LCSM_OK && k < n; ++k)
+    r = step_common(c, y + (size_t)k * y_stride, z + (size_t)k * z_stride, false);
+  c->scratch = ws_scratch;
+  c->ly.scratch_bytes = ws_bytes;
+  return r;
 }
 
 }  // extern "C"

@@ -76,6 +76,7 @@ _SIGS = {
     "lcsm_step_layer": (ctypes.c_int, [_vp, ctypes.c_int, _vp, _vp]),
     "lcsm_advance": (ctypes.c_int, [_vp]),
     "lcsm_run": (ctypes.c_int, [_vp, ctypes.c_int, _vp, ctypes.c_size_t, _vp, ctypes.c_size_t]),
+    "lcsm_run_noalloc": (ctypes.c_int, [_vp, ctypes.c_int, _vp, ctypes.c_size_t, _vp, ctypes.c_size_t]),
     "lcsm_prefill": (ctypes.c_int, [_vp, ctypes.c_int, _vp, ctypes.c_size_t, _vp, ctypes.c_size_t]),
     "lcsm_reset": (ctypes.c_int, [_vp]),
     "lcsm_position": (ctypes.c_int, [_vp, _c_int_p]),
