@@ -199,6 +199,15 @@ def kernel_key(name):
         return ("fft_col", int(m.group(1)))
     if "k_rows_to_cols" in name or "k_cols_to_rows" in name:
         return ("fft_col", None)
+    # tiles on the column-major mirror, and the mirror's copies around them
+    m = re.search(r"k_cm_tile<(\d+)>", name)
+    if m:
+        return ("fft_cm", int(m.group(1)) // 2)
+    m = re.search(r"k_cm_tile2<(\d+), \d+>", name)
+    if m:
+        return ("fft_cm", int(m.group(1)))
+    if "k_cm_yin" in name or "k_cm_merge" in name:
+        return ("fft_cm", None)
     return None
 
 
@@ -211,20 +220,20 @@ def group_tiles(rows, value, order_key="Dispatch_Id"):
     import collections
     per = collections.defaultdict(list)
     rows = sorted(rows, key=lambda r: int(r[order_key]))
-    tile, red = None, None  # open column tile [U, value]; last red-cell dispatch's value
+    tile, red = None, None  # open column tile [kind, U, value]; last red-cell dispatch's value
     for r in rows:
         key = kernel_key(r["Kernel_Name"])
         v = value(r)
-        if key and key[0] == "fft_col":
+        if key and key[0] in ("fft_col", "fft_cm"):
             if tile is None:
-                tile = [None, red or 0.0]
+                tile = [key[0], None, red or 0.0]
                 red = None
-            tile[1] += v
+            tile[2] += v
             if key[1] is not None:
-                tile[0] = key[1]
+                tile[1] = key[1]
             continue
         if tile is not None:
-            per[("fft_col", tile[0])].append(tile[1])
+            per[(tile[0], tile[1])].append(tile[2])
             tile = None
         if red is not None:
             per[("red", 0)].append(red)
@@ -234,7 +243,7 @@ def group_tiles(rows, value, order_key="Dispatch_Id"):
         elif key:
             per[key].append(v)
     if tile is not None:
-        per[("fft_col", tile[0])].append(tile[1])
+        per[(tile[0], tile[1])].append(tile[2])
     if red is not None:
         per[("red", 0)].append(red)
     return per

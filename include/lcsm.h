@@ -50,6 +50,7 @@ extern "C" {
 #define LCSM_TILE_FFT 2     /* 2U-point FFT, one LDS-resident pass */
 #define LCSM_TILE_FFT_HBM 3 /* 2U-point FFT, multi-pass through HBM scratch */
 #define LCSM_TILE_FFT_COL 4 /* 2U-point FFT on column chunks transposed into the scratch */
+#define LCSM_TILE_FFT_CM 5  /* 2U-point FFT on the column-major mirror of the state (below) */
 
 /* Tuning options.  A NULL pointer, or a field left at 0, selects the
  * library default. */
@@ -69,8 +70,26 @@ typedef struct lcsm_options {
                         run (2U = 32768: as its even and odd bins, two 16384-point halves;
                         power of two >= 4; above 32768: never).  0: by shape -- from
                         2U = 8192 while M*B*D >= 2^14, from 2U = 4096 while M*B*D >= 2^15 */
-  int reserved[3];   /* must be zero */
+  int col_tile_form; /* how the tiles of the column-tile sizes reach contiguous columns.  0
+                        (default): a column-major mirror of the state (LCSM_TILE_FFT_CM, see
+                        below); 1: chunks transposed into the scratch and back for every
+                        tile (LCSM_TILE_FFT_COL; no mirror memory).  With half_state the
+                        transposed chunks are always used */
+  int reserved[2];   /* must be zero */
 } lcsm_options;
+
+/* Column-major mirror (col_tile_form = 0).  With T0 the smallest tile side
+ * of the column-tile sizes, the context keeps a second copy of every layer's
+ * columns, pairs of real columns interleaved along time (C[m][pair][t]),
+ * holding the inputs of the positions already passed and, for later
+ * positions, the sums of the mirrored tiles.  After every position t with
+ * i = t+1 a multiple of T0, the inputs of the last T0 positions are copied
+ * in, the tile of i reads its U inputs and adds its U outputs as contiguous
+ * runs of the mirror, and the mirrored sums of positions [i, i+T0) are
+ * handed to the state before position i is emitted.  That costs 16 bytes
+ * per column and position (8 more with tiles above 2U = 32768, whose outputs
+ * still go to the state) instead of 20U bytes per column of every column
+ * tile, and doubles the state memory. */
 
 /* Half-state storage (lcsm_options.half_state = 1).  After position T-1 no
  * input y_s with s < T is read again, and before it no contribution lands at
@@ -81,7 +100,8 @@ typedef struct lcsm_options {
  * (multi-pass), each reading its columns' inputs before it stores any of
  * their outputs.  From then on state row r stands for position T + r.  Needs
  * no memory beyond the ordinary tile's; every output is bit-for-bit that of
- * the full-state context (a zero's sign aside).  Requirements: the tile of
+ * the full-state context with col_tile_form = 1 (a zero's sign aside; the
+ * column-tile sizes run on transposed chunks with half-state storage).  Requirements: the tile of
  * side T is an FFT tile (L > 2 * the direct limit), and a prefill prompt P
  * satisfies 2P <= T.  State memory: M*T*B*D floats instead of M*L*B*D. */
 

@@ -48,6 +48,7 @@ struct Options {
   int half_state;
   int col_min_n;
   bool col_auto;  // col_min_n is the default: applies from kAutoColMinCols columns
+  int col_form;   // 0: column-major mirror, 1: transposed column chunks
 };
 
 int resolve_options(const lcsm_options* o, Options* r) {
@@ -57,9 +58,12 @@ int resolve_options(const lcsm_options* o, Options* r) {
   r->half_state = 0;
   r->col_min_n = kDefaultColFftMinN;
   r->col_auto = true;
+  r->col_form = 0;
   if (!o) return LCSM_OK;
-  for (int k = 0; k < 3; ++k)
+  for (int k = 0; k < 2; ++k)
     if (o->reserved[k] != 0) return LCSM_EINVAL;
+  if (o->col_tile_form != 0 && o->col_tile_form != 1) return LCSM_EINVAL;
+  r->col_form = o->col_tile_form;
   if (o->col_fft_min_n) {
     if (!is_pow2(o->col_fft_min_n) || o->col_fft_min_n < 4) return LCSM_EINVAL;
     r->col_min_n = o->col_fft_min_n;
@@ -100,7 +104,7 @@ int tile_kind(const Options& o, const Shape& s, int U) {
   const long long cols = (long long)s.M * s.BD;
   const int col_min = (o.col_auto && cols >= kAutoCol4096MinCols) ? 4096 : o.col_min_n;
   if (2 * U >= col_min && 2 * U <= lcsm::kMaxColFftN && (!o.col_auto || cols >= kAutoColMinCols))
-    return LCSM_TILE_FFT_COL;
+    return (o.col_form == 0 && !o.half_state) ? LCSM_TILE_FFT_CM : LCSM_TILE_FFT_COL;
   return (2 * U <= o.lds_fft_max_n) ? LCSM_TILE_FFT : LCSM_TILE_FFT_HBM;
 }
 
@@ -125,6 +129,11 @@ int make_shape(int M, int B, int D, int L, const Options& o, Shape* out) {
 struct Layout {
   size_t S, Hf, prev, tw, scratch, scratch_bytes, total;
   size_t scratch_min;    // bytes of one chunk of the largest multi-pass or column tile
+  size_t C;              // the column-major mirror (when cm_t0 > 0)
+  lcsm::CmShape cm;
+  int cm_t0;             // smallest mirrored tile side (0: no mirror)
+  unsigned cm_mask;      // OR of the mirrored tile sides
+  bool cm_store;         // every tile side >= cm_t0 is mirrored: merges store
   size_t H[kMaxLevels];  // spectra of tile size 2^q (FFT levels only)
   int nmax;              // largest FFT length, 0 if no tile uses the FFT
 };
@@ -139,15 +148,32 @@ Layout layout_for(const Shape& s, const Options& o) {
   ly.prev = off;
   off = align_up(off + sizeof(float) * (size_t)s.BD);
   bool multipass = false, colsplit = false;
+  ly.cm_store = true;
   for (int q = 0; q < kMaxLevels && (1 << q) <= s.L - 1; ++q) {
     const int U = 1 << q;
     const int kind = tile_kind(o, s, U);
     if (kind == LCSM_TILE_DIRECT) continue;
     ly.nmax = 2 * U;
-    if (kind == LCSM_TILE_FFT_HBM || kind == LCSM_TILE_FFT_COL) multipass = true;
-    if (kind == LCSM_TILE_FFT_COL && 2 * U > lcsm::kMaxColFftN1) colsplit = true;
+    // the mirrored tiles take the column tiles' scratch: prefill's delayed
+    // tile runs as a column tile, and 2U = 32768 needs it for its odd half
+    if (kind == LCSM_TILE_FFT_HBM || kind == LCSM_TILE_FFT_COL || kind == LCSM_TILE_FFT_CM)
+      multipass = true;
+    if ((kind == LCSM_TILE_FFT_COL || kind == LCSM_TILE_FFT_CM) && 2 * U > lcsm::kMaxColFftN1)
+      colsplit = true;
+    if (kind == LCSM_TILE_FFT_CM) {
+      if (!ly.cm_t0) ly.cm_t0 = U;
+      ly.cm_mask |= (unsigned)U;
+    } else if (ly.cm_t0) {
+      ly.cm_store = false;  // a larger tile writes the state itself: merges add
+    }
     ly.H[q] = off;
     off = align_up(off + sizeof(float2) * (size_t)s.M * (U + 1) * s.D);
+  }
+  if (ly.cm_t0) {
+    ly.cm.bpair = s.B % 2 == 0 ? 1 : 0;
+    ly.cm.PC = ly.cm.bpair ? (s.B / 2) * s.D : (s.BD + 1) / 2;
+    ly.C = off;
+    off = align_up(off + sizeof(float2) * (size_t)s.M * ly.cm.PC * s.L);
   }
   if (ly.nmax) {
     ly.tw = off;
@@ -239,6 +265,8 @@ struct lcsm_ctx {
   float* prev;
   float2* tw;
   float2* scratch;
+  float2* C;               // column-major mirror (ly.cm_t0 > 0)
+  int mirrored;            // positions [0, mirrored) of the mirror hold inputs
   float2* static_scratch;  // this device's static scratch (lcsm_run_noalloc)
   int T;            // half-state swap position (the state's rows per layer), 0 without
   int t;            // next position to emit
@@ -265,13 +293,15 @@ hipError_t spectra(lcsm_ctx* c, int U, int shift) {
   const int q = __builtin_ctz((unsigned)U);
   return lcsm::launch_spectra(c->Hf, (float2*)(c->ws + c->ly.H[q]), c->tw, c->s, U, shift,
                               c->opt.lds_fft_max_n, c->scratch, c->ly.scratch_bytes, c->stream,
-                              tile_kind(c->opt, c->s, U) == LCSM_TILE_FFT_COL);
+                              tile_kind(c->opt, c->s, U) >= LCSM_TILE_FFT_COL);
 }
 
-// FFT tile of side U for all layers with the level's kernel.
+// FFT tile of side U for all layers with the level's kernel, on the
+// time-major state (a mirrored size runs as a transposed column tile here:
+// prefill's delayed-filter tile).
 hipError_t fft_tile(lcsm_ctx* c, float* S, int i, int U, int dst_len, bool in_place) {
   const float2* H = (const float2*)(c->ws + c->ly.H[__builtin_ctz((unsigned)U)]);
-  if (tile_kind(c->opt, c->s, U) == LCSM_TILE_FFT_COL)
+  if (tile_kind(c->opt, c->s, U) >= LCSM_TILE_FFT_COL)
     return lcsm::launch_fft_col_tile(S, H, c->tw, c->s, i, U, dst_len, c->scratch,
                                      c->ly.scratch_bytes, c->stream, in_place);
   return lcsm::launch_fft_tile(S, H, c->tw, c->s, i, U, dst_len, c->opt.lds_fft_max_n, c->scratch,
@@ -290,12 +320,52 @@ float* state_base(const lcsm_ctx* c, int p) {
 // Gray tile of i = t+1 for all layers, when it was not fused into the red
 // launch.  With half-state storage the tile of i = T (an FFT tile) stores
 // its outputs for positions [T, L) over its inputs, rows [0, L - T).
+//
+// Column-major mirror: every i that is a multiple of T0 (the smallest
+// mirrored side; U >= T0 there) first copies the inputs of the positions not
+// yet mirrored into it, and after the tile hands the mirrored sums of
+// positions [i, i+T0) to the state -- if any mirrored tile reached them,
+// i.e. if i has a bit at a mirrored side.  A mirrored tile stores its
+// outputs when no mirrored tile reached those positions before, i.e. when
+// the bits of i above U are at no mirrored side, and adds them otherwise,
+// so the mirror never needs clearing.
 hipError_t launch_tile(lcsm_ctx* c, int i, int U, int dst_len) {
   const int kind = tile_kind(c->opt, c->s, U);
   const bool swap = c->T && i == c->T;
   if (kind == LCSM_TILE_DIRECT)
     return lcsm::launch_direct_tile(state_base(c, i), c->Hf, c->s, i, U, dst_len, c->stream);
-  return fft_tile(c, swap ? c->S : state_base(c, i), i, U, dst_len, swap);
+  const int t0 = c->ly.cm_t0;
+  const bool boundary = t0 && i % t0 == 0;
+  hipError_t e = hipSuccess;
+  if (boundary) {
+    e = lcsm::launch_cm_yin(c->S, c->C, c->s, c->ly.cm, c->mirrored, i, c->stream);
+    c->mirrored = i;
+  }
+  if (e != hipSuccess) return e;
+  if (kind == LCSM_TILE_FFT_CM) {
+    const float2* H = (const float2*)(c->ws + c->ly.H[__builtin_ctz((unsigned)U)]);
+    const bool store = ((unsigned)i & ~(2u * (unsigned)U - 1u) & c->ly.cm_mask) == 0;
+    e = lcsm::launch_cm_tile(c->C, H, c->tw, c->s, c->ly.cm, i, U, dst_len, store, c->scratch,
+                             c->ly.scratch_bytes, c->stream);
+  } else {
+    e = fft_tile(c, swap ? c->S : state_base(c, i), i, U, dst_len, swap);
+  }
+  if (e == hipSuccess && boundary && ((unsigned)i & c->ly.cm_mask)) {
+    const int r1 = i + t0 < c->s.L ? i + t0 : c->s.L;
+    e = lcsm::launch_cm_merge(c->C, c->S, c->s, c->ly.cm, i, r1, c->ly.cm_store, c->stream);
+  }
+  return e;
+}
+
+// Clear the state for position 0.  With a mirror whose merges store, only
+// rows [0, T0) are read before being written (a merge stores every later row
+// before anything else touches it); otherwise all rows.
+hipError_t clear_state(lcsm_ctx* c) {
+  const size_t per_layer = (size_t)c->s.SL * c->s.BD;
+  if (c->ly.cm_t0 && c->ly.cm_store)
+    return lcsm::launch_zero_rows(c->S, c->s.M, per_layer, (size_t)c->ly.cm_t0 * c->s.BD,
+                                  c->stream);
+  return lcsm::launch_zero(c->S, (size_t)c->s.M * per_layer, c->stream);
 }
 
 // Filter spectra of every FFT tile size (the cached kernel DFTs).
@@ -444,6 +514,8 @@ int lcsm_init(lcsm_ctx** out, const float* filters, int M, int B, int D, int L, 
   c->prev = (float*)(c->ws + ly.prev);
   c->tw = ly.nmax ? (float2*)(c->ws + ly.tw) : nullptr;
   c->scratch = ly.scratch_bytes ? (float2*)(c->ws + ly.scratch) : nullptr;
+  c->C = ly.cm_t0 ? (float2*)(c->ws + ly.C) : nullptr;
+  c->mirrored = 0;
   c->T = o.half_state ? s.SL : 0;
   hipError_t e = lcsm::launch_transpose_filters(filters, c->Hf, s, c->stream);
   if (e == hipSuccess) e = lcsm::launch_zero(c->S, (size_t)s.M * s.SL * s.BD, c->stream);
@@ -662,6 +734,11 @@ int lcsm_prefill(lcsm_ctx* c, int P, const float* y, size_t y_stride, float* z, 
   // P is an FFT tile size, so its cached spectra and the twiddles for 2P exist
   // the prompt into state rows [0, P)
   hipError_t e = lcsm::launch_rows_in(y, y_stride, c->S, s, P, c->stream);
+  // rows [P, 2P) are clear after a reset unless a mirror's merges store (then
+  // only rows below T0 are)
+  if (e == hipSuccess && c->ly.cm_t0 && c->ly.cm_store && 2 * P > c->ly.cm_t0)
+    e = lcsm::launch_zero_rows(c->S + (size_t)P * s.BD, s.M, (size_t)s.SL * s.BD,
+                               (size_t)P * s.BD, c->stream);
   // the tile i = P with the filter delayed by P rows puts, in rows [P, 2P),
   // sum_{k<P} y[k] h[j - k] = z_j for j < P: the prompt's own outputs
   if (e == hipSuccess) e = spectra(c, P, P);
@@ -677,10 +754,11 @@ int lcsm_prefill(lcsm_ctx* c, int P, const float* y, size_t y_stride, float* z, 
 
 int lcsm_reset(lcsm_ctx* c) {
   if (!c) return LCSM_EINVAL;
-  hipError_t e = lcsm::launch_zero(c->S, (size_t)c->s.M * c->s.SL * c->s.BD, c->stream);
+  hipError_t e = clear_state(c);
   if (e == hipSuccess) e = lcsm::launch_zero(c->prev, (size_t)c->s.BD, c->stream);
   if (e != hipSuccess) return fail(c, LCSM_EDEVICE, "reset", e);
   c->t = 0;
+  c->mirrored = 0;
   c->layers_done = 0;
   c->faulted = false;
   c->msg[0] = 0;

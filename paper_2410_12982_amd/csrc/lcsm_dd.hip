@@ -430,9 +430,11 @@ int resolve(int M, int B, int D, int L, const lcsm_options* o, DdOptions* r) {
   r->direct_max_u = lcsm::kDdDefaultDirectMaxU;
   r->fft_max_n = lcsm::kMaxLdsFftN;
   if (o) {
-    for (int k = 0; k < 3; ++k)
+    for (int k = 0; k < 2; ++k)
       if (o->reserved[k] != 0) return LCSM_EINVAL;
-    if (o->scratch_mib != 0 || o->half_state != 0 || o->col_fft_min_n != 0) return LCSM_EINVAL;
+    if (o->scratch_mib != 0 || o->half_state != 0 || o->col_fft_min_n != 0 ||
+        o->col_tile_form != 0)
+      return LCSM_EINVAL;
     if (o->direct_max_u < 0 || o->lds_fft_max_n < 0) return LCSM_EINVAL;
     if (o->direct_max_u) {
       if (!is_pow2(o->direct_max_u)) return LCSM_EINVAL;

@@ -337,6 +337,14 @@ __global__ __launch_bounds__(kThreads) void k_zero(float* __restrict__ p, size_t
   for (size_t k = (size_t)blockIdx.x * kThreads + threadIdx.x; k < n; k += stride) p[k] = 0.f;
 }
 
+// Zero the first n floats of each layer (grid y = layers, grid-stride on x).
+__global__ __launch_bounds__(kThreads) void k_zero_rows(float* __restrict__ p, size_t stride,
+                                                       size_t n) {
+  float* q = p + (size_t)blockIdx.y * stride;
+  const size_t step = (size_t)gridDim.x * kThreads;
+  for (size_t k = (size_t)blockIdx.x * kThreads + threadIdx.x; k < n; k += step) q[k] = 0.f;
+}
+
 inline unsigned blocks_for(int64_t n) { return (unsigned)((n + kThreads - 1) / kThreads); }
 
 // Layers go on grid z (times the output split); launches are chunked over
@@ -463,6 +471,19 @@ hipError_t launch_rows_out_clear(float* S, const Shape& s, int row0, int P, floa
   if (blocks > 8192) blocks = 8192;
   hipLaunchKernelGGL(k_rows_out_clear, dim3((unsigned)blocks), dim3(kThreads), 0, st, S, s.M, s.SL,
                      s.BD, row0, P, z, z_stride);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero_rows(float* p, int M, size_t stride, size_t n, hipStream_t st) {
+  if (n == 0 || M <= 0) return hipSuccess;
+  size_t bx = (n + kThreads - 1) / kThreads;
+  const size_t cap = (8192 + (size_t)M - 1) / (size_t)M;  // about 8192 workgroups in all
+  if (bx > cap) bx = cap;
+  for (int m0 = 0; m0 < M; m0 += 65535) {
+    const int mc = M - m0 < 65535 ? M - m0 : 65535;
+    hipLaunchKernelGGL(k_zero_rows, dim3((unsigned)bx, (unsigned)mc), dim3(kThreads), 0, st,
+                       p + (size_t)m0 * stride, stride, n);
+  }
   return hipGetLastError();
 }
 

@@ -423,6 +423,264 @@ __global__ __launch_bounds__(ColCfg<NS>::NT, ColCfg<NS>::MINB) void k_fft_coltil
   });
 }
 
+// ---- Column-major mirror tiles.
+//
+// The mirror C holds, per layer, one row of L complex samples per column
+// pair: C[m][p][t] = (y_a[t], y_b[t]) for the positions t whose inputs are
+// known, and the large tiles' accumulators for later positions, where
+// the pair p is two real columns (a, b) of the layer:
+//   batch pairs (B even):  p = q D + d,  a = 2q D + d,  b = a + D  (one channel);
+//   adjacent pairs:        a = 2p,  b = 2p + 1 (absent when b = B D).
+// Every T0 positions (T0 the smallest mirrored tile side) the inputs of the
+// last T0 positions are copied in (k_cm_yin) and, after that position's
+// tile, the mirrored accumulators of the next T0 positions are handed to the
+// time-major state (k_cm_merge).  The mirrored tiles (k_cm_tile) read their
+// U inputs and write their U outputs as contiguous runs of one pair's row.
+
+// Real columns (a, b) of pair p of a layer; b < 0 when absent.
+__device__ __forceinline__ void cm_cols(int p, bool bpair, int D, int BD, int& a, int& b) {
+  if (bpair) {
+    const int q = p / D, d = p - q * D;
+    a = 2 * q * D + d;
+    b = a + D;
+  } else {
+    a = 2 * p;
+    b = a + 1 < BD ? a + 1 : -1;
+  }
+}
+
+constexpr int kCmT = 64;  // transpose tile: 64 pairs x 64 positions
+
+// C[m][p][t] = (S[m][t][a], S[m][t][b]) for t in [row0, row1).  Grid (pair
+// blocks, position blocks, M); 256 threads.
+__global__ __launch_bounds__(kTThreads) void k_cm_yin(const float* __restrict__ S, size_t lstride,
+                                                      float2* __restrict__ C, size_t cstride,
+                                                      int L, int PC, int BD, int D, int bpair,
+                                                      int row0, int row1) {
+  __shared__ float2 tile[kCmT][kCmT + 1];
+  const int m = (int)blockIdx.z;
+  const int p0 = (int)blockIdx.x * kCmT, r0 = row0 + (int)blockIdx.y * kCmT;
+  const int x = (int)threadIdx.x & (kCmT - 1), y4 = (int)threadIdx.x / kCmT;
+  const float* Sm = S + (size_t)m * lstride;
+  {
+    const int p = p0 + x;
+    int a = 0, b = -1;
+    if (p < PC) cm_cols(p, bpair != 0, D, BD, a, b);
+#pragma unroll
+    for (int k = 0; k < kCmT / 4; ++k) {
+      const int r = y4 + 4 * k, t = r0 + r;
+      if (p < PC && t < row1) {
+        const float* row = Sm + (size_t)t * BD;
+        tile[r][x] = make_float2(row[a], b >= 0 ? row[b] : 0.f);
+      }
+    }
+  }
+  __syncthreads();
+  float2* Cm = C + (size_t)m * cstride;
+#pragma unroll
+  for (int k = 0; k < kCmT / 4; ++k) {
+    const int xx = y4 + 4 * k, p = p0 + xx, t = r0 + x;
+    if (p < PC && t < row1) Cm[(size_t)p * L + t] = tile[x][xx];
+  }
+}
+
+// S[m][t][a] (+)= C[m][p][t].x and S[m][t][b] (+)= C[m][p][t].y for t in
+// [row0, row1): stored when STORE (the rows hold nothing else yet), added
+// otherwise.
+template <bool STORE>
+__global__ __launch_bounds__(kTThreads) void k_cm_merge(const float2* __restrict__ C,
+                                                        size_t cstride, float* __restrict__ S,
+                                                        size_t lstride, int L, int PC, int BD,
+                                                        int D, int bpair, int row0, int row1) {
+  __shared__ float2 tile[kCmT][kCmT + 1];
+  const int m = (int)blockIdx.z;
+  const int p0 = (int)blockIdx.x * kCmT, r0 = row0 + (int)blockIdx.y * kCmT;
+  const int x = (int)threadIdx.x & (kCmT - 1), y4 = (int)threadIdx.x / kCmT;
+  const float2* Cm = C + (size_t)m * cstride;
+#pragma unroll
+  for (int k = 0; k < kCmT / 4; ++k) {
+    const int xx = y4 + 4 * k, p = p0 + xx, t = r0 + x;
+    if (p < PC && t < row1) tile[x][xx] = Cm[(size_t)p * L + t];
+  }
+  __syncthreads();
+  const int p = p0 + x;
+  if (p >= PC) return;
+  int a, b;
+  cm_cols(p, bpair != 0, D, BD, a, b);
+  float* Sm = S + (size_t)m * lstride;
+#pragma unroll
+  for (int k = 0; k < kCmT / 4; ++k) {
+    const int r = y4 + 4 * k, t = r0 + r;
+    if (t < row1) {
+      float* row = Sm + (size_t)t * BD;
+      const float2 v = tile[r][x];
+      row[a] = STORE ? v.x : row[a] + v.x;
+      if (b >= 0) row[b] = STORE ? v.y : row[b] + v.y;
+    }
+  }
+}
+
+// Spectral product of the transform in buf (padded LDS, one column) for a
+// pair: one channel (spectrum ha, plain P = Z H over bins k <= U and their
+// mirrors) or two (ha, hb: P[k] = Z[k] S[k] + conj(Z[N-k]) D[k]).  hv: ha
+// preloaded into registers (PRE).  Synchronises at the end.
+template <int N, bool PRE, int HU>
+__device__ __forceinline__ void cm_product(float2* buf, bool one, const float2* __restrict__ ha,
+                                           const float2* __restrict__ hb, bool hasb,
+                                           const float2 (&hv)[PRE ? HU : 1]) {
+  constexpr int NT = ColCfg<N>::NT, U = N / 2, SH = ColCfg<N>::SH;
+  if (one) {
+#pragma unroll
+    for (int j = 0; j < HU; ++j) {
+      const int kk = (int)threadIdx.x + j * NT;
+      if (kk <= U) {
+        const float2 h = PRE ? hv[PRE ? j : 0] : ha[kk];
+        const int nk = (N - kk) & (N - 1);
+        const int sk = fft::lds_slot<SH>(kk), snk = fft::lds_slot<SH>(nk);
+        buf[sk] = cmul(buf[sk], h);
+        if (nk != kk) buf[snk] = cmul(buf[snk], conjf2(h));
+      }
+    }
+  } else {
+    for (int kk = (int)threadIdx.x; kk <= U; kk += NT) {
+      const float2 a = ha[kk], b = hasb ? hb[kk] : make_float2(0.f, 0.f);
+      const float2 s = make_float2(0.5f * (a.x + b.x), 0.5f * (a.y + b.y));
+      const float2 d = make_float2(0.5f * (a.x - b.x), 0.5f * (a.y - b.y));
+      const int nk = (N - kk) & (N - 1);
+      const int sk = fft::lds_slot<SH>(kk), snk = fft::lds_slot<SH>(nk);
+      const float2 zk = buf[sk], znk = buf[snk];
+      buf[sk] = cadd(cmul(zk, s), cmul(conjf2(znk), d));
+      if (nk != kk) buf[snk] = cadd(cmul(znk, conjf2(s)), cmul(conjf2(zk), conjf2(d)));
+    }
+  }
+  __syncthreads();
+}
+
+// Mirrored tile of side U = N/2 at position i for every pair of every layer
+// (one workgroup per pair, the same transform as k_fft_coltile): inputs
+// C[p][i-U .. i), outputs j < dst_len into C[p][i+j], stored when `store`
+// (no earlier mirrored tile reached those positions) and added otherwise.
+template <int N>
+__global__ __launch_bounds__(ColCfg<N>::NT, ColCfg<N>::MINB) void k_cm_tile(
+    float2* __restrict__ C, size_t cstride, int L, const float2* __restrict__ Hc,
+    const float2* __restrict__ tw, int PC, int BD, int D, int bpair, int i, int dst_len,
+    int store) {
+  constexpr int NT = ColCfg<N>::NT, U = N / 2;
+  constexpr int HU = (U + 1 + NT - 1) / NT;
+  constexpr bool PRE = N <= 8192;
+  using TW = typename std::conditional<ColCfg<N>::TWL, fft::TwLds<N>, TwSplit<N>>::type;
+  constexpr int SH = ColCfg<N>::SH;
+  __shared__ float2 buf[ColCfg<N>::SLOTS];
+  __shared__ float2 twl[ColCfg<N>::TWL ? N : N / 64 + 64];
+  TW twz;
+  if constexpr (ColCfg<N>::TWL) {
+    fft::load_twiddles<N, NT>(twl, tw);
+    twz = TW{twl};
+  } else {
+    for (int j = (int)threadIdx.x; j < N / 64; j += NT) twl[j] = tw[N + 64 * j];
+    for (int l = (int)threadIdx.x; l < 64; l += NT) twl[N / 64 + l] = tw[N + l];
+    twz = TW{twl, twl + N / 64};
+  }
+  const int g = fft::xcd_logical((int)blockIdx.x, (int)gridDim.x);
+  const int m = g / PC, p = g - m * PC;
+  int a, b;
+  cm_cols(p, bpair != 0, D, BD, a, b);
+  const bool one = bpair != 0;
+  const float2* ha = Hc + ((size_t)m * D + a % D) * (U + 1);
+  const float2* hb = Hc + ((size_t)m * D + (b >= 0 ? b : a) % D) * (U + 1);
+  float2 hv[PRE ? HU : 1];
+  if constexpr (PRE) {
+    if (one) {
+#pragma unroll
+      for (int j = 0; j < HU; ++j) {
+        const int kk = (int)threadIdx.x + j * NT;
+        hv[j] = kk <= U ? ha[kk] : make_float2(0.f, 0.f);
+      }
+    }
+  }
+  float2* col = C + (size_t)m * cstride + (size_t)p * L;
+  const float2* in = col + (i - U);
+  fft::forward_from_global<N, 1, 1, NT, true, SH>(buf, twz, [&](int row, int) { return in[row]; });
+  cm_product<N, PRE, HU>(buf, one, ha, hb, b >= 0, hv);
+  float2* out = col + i;
+  fft::inverse_to_global<N, 1, 1, NT, true, SH>(buf, twz, [&](int row, int, float2 v) {
+    const int j = row - U;
+    if (j < dst_len) out[j] = store ? v : cadd(out[j], v);
+  });
+}
+
+// The mirrored tile of 2U = 2 NS (above one column's LDS transform) as two
+// NS-point halves, the even and the odd bins (see k_fft_coltile2), for the
+// pairs [g0, g0 + npairs) of all layers: PAR = 1 stores -w_2U^{-j} B[j] into
+// Y[pair - g0][j]; PAR = 0, launched after it, adds A[j] + Y into the
+// outputs.
+template <int NS, int PAR>
+__global__ __launch_bounds__(ColCfg<NS>::NT, ColCfg<NS>::MINB) void k_cm_tile2(
+    float2* __restrict__ C, size_t cstride, int L, float2* __restrict__ Y,
+    const float2* __restrict__ Hc, const float2* __restrict__ tw, int PC, int BD, int D,
+    int bpair, int i, int dst_len, int store, int g0) {
+  constexpr int NT = ColCfg<NS>::NT, U = NS, N = 2 * NS;
+  constexpr int SH = ColCfg<NS>::SH;
+  static_assert(!ColCfg<NS>::TWL, "two-level twiddles");
+  __shared__ float2 buf[ColCfg<NS>::SLOTS];
+  __shared__ float2 twl[NS / 64 + 64];
+  for (int j = (int)threadIdx.x; j < NS / 64; j += NT) twl[j] = tw[NS + 64 * j];
+  for (int l = (int)threadIdx.x; l < 64; l += NT) twl[NS / 64 + l] = tw[NS + l];
+  const TwSplit<NS> twz{twl, twl + NS / 64};
+  constexpr int CC = NS / 16;
+  auto w2u = [&](int mm) { return cmul(tw[N + (mm & (CC - 1))], tw[32 + mm / CC]); };
+  const int gl = fft::xcd_logical((int)blockIdx.x, (int)gridDim.x);
+  const int g = g0 + gl;
+  const int m = g / PC, p = g - m * PC;
+  int a, b;
+  cm_cols(p, bpair != 0, D, BD, a, b);
+  const bool hasb = b >= 0;
+  const float2* ha = Hc + ((size_t)m * D + a % D) * (U + 1);
+  const float2* hb = Hc + ((size_t)m * D + (hasb ? b : a) % D) * (U + 1);
+  float2* col = C + (size_t)m * cstride + (size_t)p * L;
+  const float2* in = col + (i - U);
+  float2* y = Y + (size_t)gl * U;
+  fft::forward_from_global<NS, 1, 1, NT, false, SH>(buf, twz, [&](int row, int) -> float2 {
+    const float2 v = in[row];
+    if constexpr (PAR == 1) return cmul(v, w2u(row));
+    return v;
+  });
+  if (bpair) {
+    for (int kk = (int)threadIdx.x; kk < NS; kk += NT) {
+      const int k = 2 * kk + PAR;
+      const float2 h = k <= U ? ha[k] : conjf2(ha[N - k]);
+      const int sk = fft::lds_slot<SH>(kk);
+      buf[sk] = cmul(buf[sk], h);
+    }
+  } else {
+    constexpr int KH = PAR ? NS / 2 : NS / 2 + 1;
+    for (int kk = (int)threadIdx.x; kk < KH; kk += NT) {
+      const int k = 2 * kk + PAR;
+      const int nk = (NS - kk - PAR) & (NS - 1);
+      const float2 av = ha[k], bv = hasb ? hb[k] : make_float2(0.f, 0.f);
+      const float2 s = make_float2(0.5f * (av.x + bv.x), 0.5f * (av.y + bv.y));
+      const float2 d = make_float2(0.5f * (av.x - bv.x), 0.5f * (av.y - bv.y));
+      const int sk = fft::lds_slot<SH>(kk), snk = fft::lds_slot<SH>(nk);
+      const float2 zk = buf[sk], znk = buf[snk];
+      buf[sk] = cadd(cmul(zk, s), cmul(conjf2(znk), d));
+      if (nk != kk) buf[snk] = cadd(cmul(znk, conjf2(s)), cmul(conjf2(zk), conjf2(d)));
+    }
+  }
+  __syncthreads();
+  float2* out = col + i;
+  fft::inverse_to_global<NS, 1, 1, NT, false, SH>(buf, twz, [&](int row, int, float2 v) {
+    if constexpr (PAR == 1) {
+      const float2 bb = cmul(v, conjf2(w2u(row)));
+      y[row] = make_float2(-bb.x, -bb.y);
+    } else {
+      if (row < dst_len) {
+        const float2 o = cadd(v, y[row]);
+        out[row] = store ? o : cadd(out[row], o);
+      }
+    }
+  });
+}
+
 }  // namespace
 
 int fft_col_chunk(int U, size_t scratch_bytes, long long total_cols) {
@@ -500,6 +758,73 @@ hipError_t launch_fft_col_tile(float* S, const float2* Hc, const float2* tw, con
     else
       hipLaunchKernelGGL(k_cols_to_rows<false>, tout, dim3(kTThreads), 0, st, X, U, S, lstride, s.BD,
                          i, dst_len, g0, nc);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+hipError_t launch_cm_yin(const float* S, float2* C, const Shape& s, const CmShape& cm, int row0,
+                         int row1, hipStream_t st) {
+  if (row1 <= row0) return hipSuccess;
+  const dim3 grid((unsigned)((cm.PC + kCmT - 1) / kCmT), (unsigned)((row1 - row0 + kCmT - 1) / kCmT),
+                  (unsigned)s.M);
+  hipLaunchKernelGGL(k_cm_yin, grid, dim3(kTThreads), 0, st, S, (size_t)s.SL * s.BD, C,
+                     (size_t)cm.PC * s.L, s.L, cm.PC, s.BD, s.D, cm.bpair, row0, row1);
+  return hipGetLastError();
+}
+
+hipError_t launch_cm_merge(const float2* C, float* S, const Shape& s, const CmShape& cm, int row0,
+                           int row1, bool store, hipStream_t st) {
+  if (row1 <= row0) return hipSuccess;
+  const dim3 grid((unsigned)((cm.PC + kCmT - 1) / kCmT), (unsigned)((row1 - row0 + kCmT - 1) / kCmT),
+                  (unsigned)s.M);
+  if (store)
+    hipLaunchKernelGGL(k_cm_merge<true>, grid, dim3(kTThreads), 0, st, C, (size_t)cm.PC * s.L, S,
+                       (size_t)s.SL * s.BD, s.L, cm.PC, s.BD, s.D, cm.bpair, row0, row1);
+  else
+    hipLaunchKernelGGL(k_cm_merge<false>, grid, dim3(kTThreads), 0, st, C, (size_t)cm.PC * s.L, S,
+                       (size_t)s.SL * s.BD, s.L, cm.PC, s.BD, s.D, cm.bpair, row0, row1);
+  return hipGetLastError();
+}
+
+hipError_t launch_cm_tile(float2* C, const float2* Hc, const float2* tw, const Shape& s,
+                          const CmShape& cm, int i, int U, int dst_len, bool store, float2* scratch,
+                          size_t scratch_bytes, hipStream_t st) {
+  if (dst_len <= 0) return hipSuccess;
+  const int N = 2 * U;
+  const long long total = (long long)s.M * cm.PC;
+  const size_t cstride = (size_t)cm.PC * s.L;
+  if (N <= kMaxColFftN1) {
+    const dim3 grid((unsigned)total);
+    switch (N) {
+#define LCSM_CM_CASE(NN)                                                                      \
+  case NN:                                                                                    \
+    hipLaunchKernelGGL(k_cm_tile<NN>, grid, dim3(ColCfg<NN>::NT), 0, st, C, cstride, s.L, Hc, \
+                       tw, cm.PC, s.BD, s.D, cm.bpair, i, dst_len, store ? 1 : 0);            \
+    break;
+      LCSM_CM_CASE(4) LCSM_CM_CASE(8) LCSM_CM_CASE(16) LCSM_CM_CASE(32) LCSM_CM_CASE(64)
+      LCSM_CM_CASE(128) LCSM_CM_CASE(256) LCSM_CM_CASE(512) LCSM_CM_CASE(1024)
+      LCSM_CM_CASE(2048) LCSM_CM_CASE(4096) LCSM_CM_CASE(8192) LCSM_CM_CASE(16384)
+#undef LCSM_CM_CASE
+      default:
+        return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+  }
+  if (N != 2 * kMaxColFftN1) return hipErrorInvalidValue;
+  // the odd half's outputs, U complex values per pair, in the scratch
+  const long long chunk = (long long)(scratch_bytes / (sizeof(float2) * (size_t)U));
+  if (chunk <= 0) return hipErrorOutOfMemory;
+  for (long long g0 = 0; g0 < total; g0 += chunk) {
+    const int np = (int)(total - g0 < chunk ? total - g0 : chunk);
+    const dim3 grid((unsigned)np);
+    hipLaunchKernelGGL((k_cm_tile2<kMaxColFftN1, 1>), grid, dim3(ColCfg<kMaxColFftN1>::NT), 0, st,
+                       C, cstride, s.L, scratch, Hc, tw, cm.PC, s.BD, s.D, cm.bpair, i, dst_len,
+                       store ? 1 : 0, (int)g0);
+    hipLaunchKernelGGL((k_cm_tile2<kMaxColFftN1, 0>), grid, dim3(ColCfg<kMaxColFftN1>::NT), 0, st,
+                       C, cstride, s.L, scratch, Hc, tw, cm.PC, s.BD, s.D, cm.bpair, i, dst_len,
+                       store ? 1 : 0, (int)g0);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

@@ -61,6 +61,9 @@ hipError_t launch_direct_tile(float* S, const float* Hf, const Shape& s, int i, 
 // Fill n floats with zero (a kernel, so it is safe under graph capture).
 hipError_t launch_zero(float* p, size_t n, hipStream_t st);
 
+// Fill the first n floats of each of M layers (layer k at p + k*stride) with zero.
+hipError_t launch_zero_rows(float* p, int M, size_t stride, size_t n, hipStream_t st);
+
 // Prompt rows: copy y[t][m][:] (position stride y_stride floats) into state
 // rows t < P of every layer.
 hipError_t launch_rows_in(const float* y, size_t y_stride, float* S, const Shape& s, int P,
@@ -134,6 +137,34 @@ hipError_t launch_fft_col_tile(float* S, const float2* Hc, const float2* tw, con
 hipError_t launch_fft_tile(float* S, const float2* H, const float2* tw, const Shape& s, int i,
                            int U, int dst_len, int lds_max_n, float2* scratch,
                            size_t scratch_bytes, hipStream_t st, bool in_place = false);
+
+// ---- FFT tiles on the column-major mirror (lcsm_fft_col.hip)
+
+// Pairs of real columns per layer in the mirror C[m][p][t] (float2): batch
+// rows 2q and 2q+1 of one channel when B is even (bpair, p = q*D + d), else
+// neighbouring columns 2p and 2p+1 (PC = ceil(B*D/2), the last pair's second
+// column absent when B*D is odd).
+struct CmShape {
+  int PC;     // pairs per layer
+  int bpair;  // 1: batch pairs, 0: neighbouring columns
+};
+
+// C[m][p][t] = (S[m][t][a], S[m][t][b]) for positions t in [row0, row1).
+hipError_t launch_cm_yin(const float* S, float2* C, const Shape& s, const CmShape& cm, int row0,
+                         int row1, hipStream_t st);
+
+// State rows t in [row0, row1) receive the mirrored accumulators C[m][p][t]:
+// stored (the rows hold nothing else yet) or added.
+hipError_t launch_cm_merge(const float2* C, float* S, const Shape& s, const CmShape& cm, int row0,
+                           int row1, bool store, hipStream_t st);
+
+// FFT gray tile of side U at position i on the mirror, all layers: inputs
+// C[p][i-U, i), outputs j < dst_len into C[p][i+j] (stored when `store`, else
+// added).  Hc: channel-major spectra of tile size U.  2U <= kMaxColFftN; 2U =
+// kMaxColFftN needs scratch for U complex values per pair of a chunk.
+hipError_t launch_cm_tile(float2* C, const float2* Hc, const float2* tw, const Shape& s,
+                          const CmShape& cm, int i, int U, int dst_len, bool store,
+                          float2* scratch, size_t scratch_bytes, hipStream_t st);
 
 // ---- hooks for a caller that runs the red cells in its own kernels (the
 // synthetic model, lcsm_synth.hip): between two steps of a context,

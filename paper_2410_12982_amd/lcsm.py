@@ -21,14 +21,14 @@ LCSM_EDEVICE = -3
 LCSM_EDONE = -4
 LCSM_ESTATE = -5
 
-TILE_NONE, TILE_DIRECT, TILE_FFT, TILE_FFT_HBM, TILE_FFT_COL = 0, 1, 2, 3, 4
+TILE_NONE, TILE_DIRECT, TILE_FFT, TILE_FFT_HBM, TILE_FFT_COL, TILE_FFT_CM = 0, 1, 2, 3, 4, 5
 GRAPH_CHAIN = 1
 BASE_LAZY, BASE_EAGER, BASE_NP = 0, 1, 2
 BASE_KINDS = {"lazy": BASE_LAZY, "lazy_np": BASE_LAZY | BASE_NP, "eager": BASE_EAGER,
               "eager_np": BASE_EAGER | BASE_NP}
 GRAPH_DEFAULT_SEG, GRAPH_MAX_SEG = 8192, 16384
 TILE_KIND_NAMES = {TILE_NONE: "none", TILE_DIRECT: "direct", TILE_FFT: "fft_lds",
-                   TILE_FFT_HBM: "fft_hbm", TILE_FFT_COL: "fft_col"}
+                   TILE_FFT_HBM: "fft_hbm", TILE_FFT_COL: "fft_col", TILE_FFT_CM: "fft_cm"}
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2410_12982_amd.build`")
@@ -60,7 +60,8 @@ class Options(ctypes.Structure):
     """``lcsm_options``: 0 selects the library default."""
     _fields_ = [("direct_max_u", ctypes.c_int), ("lds_fft_max_n", ctypes.c_int),
                 ("scratch_mib", ctypes.c_int), ("half_state", ctypes.c_int),
-                ("col_fft_min_n", ctypes.c_int), ("reserved", ctypes.c_int * 3)]
+                ("col_fft_min_n", ctypes.c_int), ("col_tile_form", ctypes.c_int),
+                ("reserved", ctypes.c_int * 2)]
 
 
 _c_int_p = ctypes.POINTER(ctypes.c_int)

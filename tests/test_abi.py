@@ -91,7 +91,7 @@ def test_bad_options_rejected(opts):
 
 def test_reserved_options_must_be_zero():
     o = lcsm.Options()
-    o.reserved[2] = 1
+    o.reserved[1] = 1
     with pytest.raises(lcsm.LcsmError):
         lcsm.workspace_bytes(1, 1, 1, 16, o)
 
@@ -159,8 +159,8 @@ def test_workspace_grows_with_fft_levels():
 
 def test_plan_tile_default_kinds_for_workloads():
     # default at 18432 columns: direct up to U = 32, one LDS pass up to 2U = 4096,
-    # transposed column chunks at 2U = 8192, 16384 and 32768 (the last as two
-    # halves), multi-pass above
+    # the column-tile sizes 2U = 8192, 16384 and 32768 (the last as two halves)
+    # on the column-major mirror, multi-pass above
     L = 1 << 17
     kinds = {}
     for t in range(L - 1):
@@ -168,24 +168,44 @@ def test_plan_tile_default_kinds_for_workloads():
         kinds[U] = k
     assert all(kinds[1 << q] == lcsm.TILE_DIRECT for q in range(6))
     assert all(kinds[1 << q] == lcsm.TILE_FFT for q in range(6, 12))
-    assert all(kinds[1 << q] == lcsm.TILE_FFT_COL for q in range(12, 15))
+    assert all(kinds[1 << q] == lcsm.TILE_FFT_CM for q in range(12, 15))
     assert all(kinds[1 << q] == lcsm.TILE_FFT_HBM for q in range(15, 17))
-    # fewer than 2^14 columns (the 6144-column workload): no column chunks
+    # the transposed column chunks instead when asked for, and with half-state
+    for opts in ({"col_tile_form": 1}, {"half_state": 1}):
+        for q in range(12, 15):
+            assert lcsm.plan_tile(18, 1, 1024, L, (1 << q) - 1, opts)[3] == lcsm.TILE_FFT_COL
+    # fewer than 2^14 columns (the 6144-column workload): no column tiles
     assert lcsm.plan_tile(1, 8, 768, 8192, 4095)[3] == lcsm.TILE_FFT
     # from 2^15 columns the 2U = 4096 tile is a column tile too, not 2U = 2048
     for shape in ((18, 4, 768, 32768), (32, 16, 2048, 16384), (1, 1, 32768, 8192)):
-        assert lcsm.plan_tile(*shape, 2047)[3] == lcsm.TILE_FFT_COL
+        assert lcsm.plan_tile(*shape, 2047)[3] == lcsm.TILE_FFT_CM
         assert lcsm.plan_tile(*shape, 1023)[3] == lcsm.TILE_FFT
     assert lcsm.plan_tile(1, 1, 32767, 8192, 2047)[3] == lcsm.TILE_FFT
-    # the column-chunk tiles when asked for: 2U from col_fft_min_n up to 32768
+    # the column tiles when asked for: 2U from col_fft_min_n up to 32768
     on = {"col_fft_min_n": 2048}
-    for q, want in ((9, lcsm.TILE_FFT), (10, lcsm.TILE_FFT_COL), (13, lcsm.TILE_FFT_COL),
-                    (14, lcsm.TILE_FFT_COL), (15, lcsm.TILE_FFT_HBM)):
+    for q, want in ((9, lcsm.TILE_FFT), (10, lcsm.TILE_FFT_CM), (13, lcsm.TILE_FFT_CM),
+                    (14, lcsm.TILE_FFT_CM), (15, lcsm.TILE_FFT_HBM)):
         t = (1 << q) - 1
         assert lcsm.plan_tile(18, 1, 1024, L, t, on)[3] == want
     for bad in (3, 2, -4, 100):
         with pytest.raises(lcsm.LcsmError):
             lcsm.workspace_bytes(1, 1, 16, 4096, {"col_fft_min_n": bad})
+    for bad in (2, -1):
+        with pytest.raises(lcsm.LcsmError):
+            lcsm.workspace_bytes(1, 1, 16, 4096, {"col_tile_form": bad})
+
+
+@pytest.mark.parametrize("shape", [(18, 4, 768, 32768), (3, 1, 7, 4096), (2, 5, 3, 1000)])
+def test_mirror_memory(shape):
+    """The column-major mirror holds M * ceil(B*D/2) pairs of L complex
+    values (batch pairs when B is even, neighbouring columns otherwise):
+    the workspace grows by that much over the transposed column tiles."""
+    M, B, D, L = shape
+    opts = {"col_fft_min_n": 256}
+    mirror = lcsm.workspace_bytes(M, B, D, L, opts)
+    transposed = lcsm.workspace_bytes(M, B, D, L, dict(opts, col_tile_form=1))
+    pairs = (B // 2) * D if B % 2 == 0 else (B * D + 1) // 2
+    assert 0 <= (mirror - transposed) - 8 * M * pairs * L < 512
 
 
 def test_init_validates_before_touching_the_device():

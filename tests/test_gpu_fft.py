@@ -31,10 +31,16 @@ FFT_OPTIONS = {
     "multipass_from_16": {"direct_max_u": 1, "lds_fft_max_n": 16, "col_fft_min_n": 1 << 20},
     # multi-pass with a 1 MiB scratch: many chunks per tile
     "tiny_scratch": {"direct_max_u": 4, "lds_fft_max_n": 32, "scratch_mib": 1, "col_fft_min_n": 1 << 20},
-    # every FFT tile on transposed column chunks (the column path is off above)
+    # every FFT tile on the column-major mirror (the column path is off above):
+    # T0 = 2, a merge after every other position
     "col_from_4": {"direct_max_u": 1, "col_fft_min_n": 4},
-    # column tiles with a 1 MiB scratch: many column chunks per tile
+    # the same tiles on transposed column chunks
+    "colT_from_4": {"direct_max_u": 1, "col_fft_min_n": 4, "col_tile_form": 1},
+    # column tiles with a 1 MiB scratch: many column chunks per tile (transposed),
+    # many pair chunks of the split 2U = 32768 tile (mirror)
     "col_tiny_scratch": {"direct_max_u": 4, "col_fft_min_n": 16, "scratch_mib": 1},
+    "colT_tiny_scratch": {"direct_max_u": 4, "col_fft_min_n": 16, "scratch_mib": 1,
+                          "col_tile_form": 1},
     "default": None,
 }
 
@@ -63,7 +69,7 @@ def _run_full(ctx, y):
 
 
 @pytest.mark.parametrize("opt", ["lds_from_2", "multipass_from_16", "tiny_scratch", "col_from_4",
-                                 "col_tiny_scratch"])
+                                 "col_tiny_scratch", "colT_from_4", "colT_tiny_scratch"])
 @pytest.mark.parametrize("shape", [(2, 3, 40, 300), (1, 1, 5, 257), (3, 2, 33, 1000),
                                    (1, 4, 64, 2048)])
 def test_integer_data_rounds_to_exact(opt, shape):
@@ -79,7 +85,7 @@ def test_integer_data_rounds_to_exact(opt, shape):
     assert np.array_equal(np.rint(z).astype(np.int64), ex)
 
 
-@pytest.mark.parametrize("opt", ["default", "lds_from_2", "col_from_4"])
+@pytest.mark.parametrize("opt", ["default", "lds_from_2", "col_from_4", "colT_from_4"])
 @pytest.mark.parametrize("shape", [(1, 2, 48, 4500), (1, 3, 24, 4200), (2, 1, 10, 6000)])
 def test_integer_data_panel_orders_and_clipped_large_tiles(opt, shape):
     """Shapes whose channel count is not a whole number of 128-byte line
@@ -124,7 +130,7 @@ def test_integer_data_wide_panels(opt, shape, half):
 
 
 @pytest.mark.parametrize("half", [False, True])
-@pytest.mark.parametrize("opt", ["col_from_4", "col_tiny_scratch"])
+@pytest.mark.parametrize("opt", ["col_from_4", "col_tiny_scratch", "colT_from_4", "colT_tiny_scratch"])
 @pytest.mark.parametrize("shape", [(2, 3, 40, 301), (1, 2, 64, 1027), (1, 1, 12, 1028)])
 def test_integer_data_column_transposes(opt, shape, half):
     """Column tiles whose transposes move 16-byte vectors (B*D a multiple of
@@ -146,7 +152,7 @@ def test_integer_data_column_transposes(opt, shape, half):
 
 
 @pytest.mark.parametrize("half", [False, True])
-@pytest.mark.parametrize("opt", ["col_from_4", "col_top"])
+@pytest.mark.parametrize("opt", ["col_from_4", "col_top", "colT_top"])
 @pytest.mark.parametrize("shape", [(1, 4, 16, 16500), (1, 1, 64, 17000), (1, 1, 5, 16390)])
 def test_integer_data_split_column_tile(opt, shape, half):
     """The column tile of 2U = 32768 (i = 16384, clipped at L), transformed as
@@ -157,10 +163,13 @@ def test_integer_data_split_column_tile(opt, shape, half):
     M, B, D, L = shape
     say(f"[int split column tile] M={M} B={B} D={D} L={L} options={opt} half_state={half}")
     w, h, y = _int_case(M, B, D, L, 2, seed=13 * sum(shape))
-    opts = dict(FFT_OPTIONS[opt] if opt in FFT_OPTIONS else {"col_fft_min_n": 32768},
-                half_state=int(half))
+    top = {"col_top": {"col_fft_min_n": 32768},
+           "colT_top": {"col_fft_min_n": 32768, "col_tile_form": 1}}
+    opts = dict(FFT_OPTIONS[opt] if opt in FFT_OPTIONS else top[opt], half_state=int(half))
     ctx, _ = make_ctx(w, torch.from_numpy(h).to(dev()), opts)
-    assert ctx.tile(16383)[1:] == (16384, L - 16384, lcsm_mod().TILE_FFT_COL)
+    lcsm = lcsm_mod()
+    form = lcsm.TILE_FFT_COL if (half or opts.get("col_tile_form")) else lcsm.TILE_FFT_CM
+    assert ctx.tile(16383)[1:] == (16384, L - 16384, form)
     z = _run_full(ctx, torch.from_numpy(y).to(dev()))
     # the exact integers: the oracle's fp64 FFT convolution, rounded (|z| stays
     # near 10^3, where fp64 rounding is far below 1/2)

@@ -27,11 +27,12 @@ OPTIONS = {
     "default": {},
     "fft_from_2": {"direct_max_u": 1, "col_fft_min_n": 1 << 20},
     "col_from_4": {"direct_max_u": 1, "col_fft_min_n": 4},
+    "colT_from_4": {"direct_max_u": 1, "col_fft_min_n": 4, "col_tile_form": 1},
 }
 
 
 @pytest.mark.parametrize("half", [False, True])
-@pytest.mark.parametrize("opt", ["default", "fft_from_2", "col_from_4"])
+@pytest.mark.parametrize("opt", ["default", "fft_from_2", "col_from_4", "colT_from_4"])
 def test_pending_commit_equals_step(opt, half):
     M, B, D, L = 2, 3, 40, 700
     say(f"[fused caller] M={M} B={B} D={D} L={L} options={opt} half_state={half}")

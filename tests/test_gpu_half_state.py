@@ -40,6 +40,14 @@ def _half(opts):
     return dict(opts, half_state=1)
 
 
+def _full(opts=None):
+    """Options of the full-state context a half-state one equals bit for bit:
+    half-state storage runs the column-tile sizes on transposed chunks, so the
+    full-state context does too (on the column-major mirror its large tiles
+    are summed in a different order)."""
+    return dict(opts or {}, col_tile_form=1)
+
+
 def _run(ctx, y):
     z = torch.full_like(y, float("nan"))
     ctx.run(y, z)
@@ -62,7 +70,7 @@ def test_half_state_matches_oracle_and_full_state(opt, shape):
     say(f"[half state] M={M} B={B} D={D} L={L} options={opt}")
     w = datagen.Workload("half", M, B, D, L, decay=L / 3, seed=40 + L % 97)
     filt = datagen.filters_torch(w, dev())
-    full, _ = make_ctx(w, filt, OPTIONS[opt] or None)
+    full, _ = make_ctx(w, filt, _full(OPTIONS[opt]))
     half, _ = make_ctx(w, filt, _half(OPTIONS[opt]))
     y = datagen.y_torch(w, dev())
     zf = _run(full, y)
@@ -110,7 +118,7 @@ def test_half_state_layer_path_chain_and_reset(opt):
     w = datagen.Workload("halfpaths", 3, 2, 40, 1200, decay=300.0, seed=14)
     say(f"[half state paths] M=3 B=2 D=40 L=1200 options={opt}")
     filt = datagen.filters_torch(w, dev())
-    full, _ = make_ctx(w, filt, OPTIONS[opt] or None)
+    full, _ = make_ctx(w, filt, _full(OPTIONS[opt]))
     half, _ = make_ctx(w, filt, _half(OPTIONS[opt]))
     y = datagen.y_torch(w, dev())
     za = _run(half, y)
@@ -157,7 +165,7 @@ def test_half_state_prefill():
     T = 2048
     say(f"[half state prefill] M=2 B=2 D=48 L=4096 P={T // 2}")
     filt = datagen.filters_torch(w, dev())
-    full, _ = make_ctx(w, filt)
+    full, _ = make_ctx(w, filt, _full())
     half, _ = make_ctx(w, filt, {"half_state": 1})
     y = datagen.y_torch(w, dev())
     out = []
@@ -197,7 +205,7 @@ def test_half_state_full_size_equals_full_state(name):
     w = datagen.WORKLOADS[name]
     say(f"[half state full size] {name}")
     filt = datagen.filters_torch(w, dev())
-    full, _ = make_ctx(w, filt)
+    full, _ = make_ctx(w, filt, _full())
     half, _ = make_ctx(w, filt, {"half_state": 1})
     cols = datagen.sample_columns(w, 6, seed=77)
     cm, cb, cd = (torch.as_tensor(cols[:, k], device=dev()) for k in range(3))

@@ -28,6 +28,7 @@ OPTIONS = {
     "multipass_from_16": {"direct_max_u": 1, "lds_fft_max_n": 16, "col_fft_min_n": 1 << 20},
     # every FFT tile (and the prompt's transform) on transposed column chunks
     "col_from_4": {"direct_max_u": 1, "col_fft_min_n": 4},
+    "colT_from_4": {"direct_max_u": 1, "col_fft_min_n": 4, "col_tile_form": 1},
 }
 
 
@@ -41,7 +42,8 @@ def _prefill_then_run(ctx, y, P):
     return z.cpu().numpy()
 
 
-@pytest.mark.parametrize("opt", ["default", "fft_from_2", "multipass_from_16", "col_from_4"])
+@pytest.mark.parametrize("opt", ["default", "fft_from_2", "multipass_from_16", "col_from_4",
+                                 "colT_from_4"])
 @pytest.mark.parametrize("case", [(2, 3, 40, 1024, 256), (3, 2, 33, 2048, 64), (1, 1, 5, 300, 128),
                                   (2, 2, 24, 4096, 2048), (1, 2, 8, 32768, 16384)])
 def test_prefill_then_generate_matches_oracle(opt, case):
