@@ -69,7 +69,9 @@ typedef struct lcsm_options {
                         columns into the scratch and transform each column as one contiguous
                         run (2U = 32768: as its even and odd bins, two 16384-point halves;
                         power of two >= 4; above 32768: never).  0: by shape -- from
-                        2U = 8192 while M*B*D >= 2^14, from 2U = 4096 while M*B*D >= 2^15 */
+                        2U = 2048 while M*B*D >= 2^14; with col_tile_form = 1 or
+                        half_state from 2U = 8192 while M*B*D >= 2^14, from 4096 while
+                        M*B*D >= 2^15 */
   int col_tile_form; /* how the tiles of the column-tile sizes reach contiguous columns.  0
                         (default): a column-major mirror of the state (LCSM_TILE_FFT_CM, see
                         below); 1: chunks transposed into the scratch and back for every

@@ -23,14 +23,17 @@ constexpr size_t kAlign = 256;
 constexpr int kAutoDirectMaxU = 32;
 constexpr int kDefaultLdsFftMaxN = 8192;   // 2U <= 8192: one LDS pass
 constexpr int kDefaultScratchMib = 512;    // multi-pass and column-tile FFT scratch cap
-// FFT tiles from 2U = 8192 up run on transposed column chunks when there are
-// at least 2^14 columns (M*B*D): there the row-panel tile's 16-byte row runs
-// (and above 8192 the three-pass tile's extra passes) cost more than the two
-// transposes; below that size, or with fewer columns, the row panels win.
-constexpr int kDefaultColFftMinN = 8192;
+// FFT tiles from 2U = 2048 up (to 32768) run as column tiles when there are
+// at least 2^14 columns (M*B*D): on the column-major mirror they read and
+// write contiguous runs, where the row-panel tile of 2U = 2048 holds one
+// workgroup per CU and 64-byte row runs (measured per smallest column size,
+// 1M / 55K / 18K columns: 2048 465 / 127.0 / 423 ms per generation, 4096 475
+// / 127.9 / 426, 1024 490 / 131.5 / 438).  With the transposed chunks
+// (col_tile_form = 1) the two transposes per tile make the column tiles pay
+// only from 2U = 8192, and 4096 from 2^15 columns.
+constexpr int kDefaultColFftMinN = 2048;
+constexpr int kTransposedColFftMinN = 8192;
 constexpr long long kAutoColMinCols = 1LL << 14;
-// and the 2U = 4096 tile too from this many columns (at 18K columns its row
-// panels are still ahead, at 55K and 1M the column tile)
 constexpr long long kAutoCol4096MinCols = 1LL << 15;
 constexpr int kMaxL = 1 << 19;             // FFT lengths up to 2^19 are built
 constexpr int kMaxLevels = 20;
@@ -102,9 +105,11 @@ int tile_kind(const Options& o, const Shape& s, int U) {
     dmax = ((long long)s.M * s.BD < lcsm::kWidePanelMinCols) ? 2 * kAutoDirectMaxU : kAutoDirectMaxU;
   if (U <= dmax) return LCSM_TILE_DIRECT;
   const long long cols = (long long)s.M * s.BD;
-  const int col_min = (o.col_auto && cols >= kAutoCol4096MinCols) ? 4096 : o.col_min_n;
+  const bool mirror = o.col_form == 0 && !o.half_state;
+  int col_min = o.col_min_n;
+  if (o.col_auto && !mirror) col_min = cols >= kAutoCol4096MinCols ? 4096 : kTransposedColFftMinN;
   if (2 * U >= col_min && 2 * U <= lcsm::kMaxColFftN && (!o.col_auto || cols >= kAutoColMinCols))
-    return (o.col_form == 0 && !o.half_state) ? LCSM_TILE_FFT_CM : LCSM_TILE_FFT_COL;
+    return mirror ? LCSM_TILE_FFT_CM : LCSM_TILE_FFT_COL;
   return (2 * U <= o.lds_fft_max_n) ? LCSM_TILE_FFT : LCSM_TILE_FFT_HBM;
 }
 

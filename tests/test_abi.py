@@ -158,32 +158,37 @@ def test_workspace_grows_with_fft_levels():
 
 
 def test_plan_tile_default_kinds_for_workloads():
-    # default at 18432 columns: direct up to U = 32, one LDS pass up to 2U = 4096,
-    # the column-tile sizes 2U = 8192, 16384 and 32768 (the last as two halves)
-    # on the column-major mirror, multi-pass above
+    # default at 18432 columns: direct up to U = 32, one LDS pass up to 2U = 1024,
+    # the column-tile sizes 2U = 2048 ... 32768 (the last as two halves) on the
+    # column-major mirror, multi-pass above
     L = 1 << 17
     kinds = {}
     for t in range(L - 1):
         _, U, _, k = lcsm.plan_tile(18, 1, 1024, L, t)
         kinds[U] = k
     assert all(kinds[1 << q] == lcsm.TILE_DIRECT for q in range(6))
-    assert all(kinds[1 << q] == lcsm.TILE_FFT for q in range(6, 12))
-    assert all(kinds[1 << q] == lcsm.TILE_FFT_CM for q in range(12, 15))
+    assert all(kinds[1 << q] == lcsm.TILE_FFT for q in range(6, 10))
+    assert all(kinds[1 << q] == lcsm.TILE_FFT_CM for q in range(10, 15))
     assert all(kinds[1 << q] == lcsm.TILE_FFT_HBM for q in range(15, 17))
-    # the transposed column chunks instead when asked for, and with half-state
+    # the transposed column chunks instead when asked for, and with half-state:
+    # from 2U = 8192 (4096 from 2^15 columns)
     for opts in ({"col_tile_form": 1}, {"half_state": 1}):
+        for q in range(10, 12):
+            assert lcsm.plan_tile(18, 1, 1024, L, (1 << q) - 1, opts)[3] == lcsm.TILE_FFT
         for q in range(12, 15):
             assert lcsm.plan_tile(18, 1, 1024, L, (1 << q) - 1, opts)[3] == lcsm.TILE_FFT_COL
+        for shape in ((18, 4, 768, 32768), (32, 16, 2048, 16384)):
+            assert lcsm.plan_tile(*shape, 2047, opts)[3] == lcsm.TILE_FFT_COL
+            assert lcsm.plan_tile(*shape, 1023, opts)[3] == lcsm.TILE_FFT
     # fewer than 2^14 columns (the 6144-column workload): no column tiles
     assert lcsm.plan_tile(1, 8, 768, 8192, 4095)[3] == lcsm.TILE_FFT
-    # from 2^15 columns the 2U = 4096 tile is a column tile too, not 2U = 2048
     for shape in ((18, 4, 768, 32768), (32, 16, 2048, 16384), (1, 1, 32768, 8192)):
-        assert lcsm.plan_tile(*shape, 2047)[3] == lcsm.TILE_FFT_CM
-        assert lcsm.plan_tile(*shape, 1023)[3] == lcsm.TILE_FFT
-    assert lcsm.plan_tile(1, 1, 32767, 8192, 2047)[3] == lcsm.TILE_FFT
+        assert lcsm.plan_tile(*shape, 1023)[3] == lcsm.TILE_FFT_CM
+        assert lcsm.plan_tile(*shape, 511)[3] == lcsm.TILE_FFT
+    assert lcsm.plan_tile(1, 1, 16383, 8192, 1023)[3] == lcsm.TILE_FFT
     # the column tiles when asked for: 2U from col_fft_min_n up to 32768
-    on = {"col_fft_min_n": 2048}
-    for q, want in ((9, lcsm.TILE_FFT), (10, lcsm.TILE_FFT_CM), (13, lcsm.TILE_FFT_CM),
+    on = {"col_fft_min_n": 4096}
+    for q, want in ((10, lcsm.TILE_FFT), (11, lcsm.TILE_FFT_CM), (13, lcsm.TILE_FFT_CM),
                     (14, lcsm.TILE_FFT_CM), (15, lcsm.TILE_FFT_HBM)):
         t = (1 << q) - 1
         assert lcsm.plan_tile(18, 1, 1024, L, t, on)[3] == want
