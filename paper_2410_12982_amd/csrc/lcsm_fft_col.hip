@@ -520,6 +520,152 @@ __global__ __launch_bounds__(kTThreads) void k_cm_merge(const float2* __restrict
   }
 }
 
+// The two mirror copies with 16-byte accesses, for shapes where a block of 64
+// pairs has its first columns in one 256-byte run of a state row and its
+// second columns in another (batch pairs with D a multiple of 64) or all of
+// them in one 512-byte run (neighbouring columns with B*D a multiple of 128):
+// a lane moves four pairs of a row, or two positions of a pair, at once.
+__device__ __forceinline__ void cm_block_cols(int p0, bool bpair, int D, int& a0, int& b0) {
+  if (bpair) {
+    const int q = p0 / D, d0 = p0 - q * D;
+    a0 = 2 * q * D + d0;
+    b0 = a0 + D;
+  } else {
+    a0 = 2 * p0;
+    b0 = -1;
+  }
+}
+
+// Pairs 4g .. 4g+3 of the block at row `row`: (a, b) of each.
+__device__ __forceinline__ void cm_load4(const float* __restrict__ row, int a0, int b0, int g,
+                                         float2 (&v)[4]) {
+  if (b0 >= 0) {
+    const float4 A = *reinterpret_cast<const float4*>(row + a0 + 4 * g);
+    const float4 B = *reinterpret_cast<const float4*>(row + b0 + 4 * g);
+    v[0] = make_float2(A.x, B.x);
+    v[1] = make_float2(A.y, B.y);
+    v[2] = make_float2(A.z, B.z);
+    v[3] = make_float2(A.w, B.w);
+  } else {
+    const float4 P = *reinterpret_cast<const float4*>(row + a0 + 8 * g);
+    const float4 Q = *reinterpret_cast<const float4*>(row + a0 + 8 * g + 4);
+    v[0] = make_float2(P.x, P.y);
+    v[1] = make_float2(P.z, P.w);
+    v[2] = make_float2(Q.x, Q.y);
+    v[3] = make_float2(Q.z, Q.w);
+  }
+}
+
+template <bool STORE>
+__device__ __forceinline__ void cm_store4(float* row, int a0, int b0, int g, const float2 (&v)[4]) {
+  if (b0 >= 0) {
+    float4* pa = reinterpret_cast<float4*>(row + a0 + 4 * g);
+    float4* pb = reinterpret_cast<float4*>(row + b0 + 4 * g);
+    float4 A = make_float4(v[0].x, v[1].x, v[2].x, v[3].x);
+    float4 B = make_float4(v[0].y, v[1].y, v[2].y, v[3].y);
+    if constexpr (!STORE) {
+      const float4 oa = *pa, ob = *pb;
+      A = make_float4(oa.x + A.x, oa.y + A.y, oa.z + A.z, oa.w + A.w);
+      B = make_float4(ob.x + B.x, ob.y + B.y, ob.z + B.z, ob.w + B.w);
+    }
+    *pa = A;
+    *pb = B;
+  } else {
+    float4* pp = reinterpret_cast<float4*>(row + a0 + 8 * g);
+    float4 P = make_float4(v[0].x, v[0].y, v[1].x, v[1].y);
+    float4 Q = make_float4(v[2].x, v[2].y, v[3].x, v[3].y);
+    if constexpr (!STORE) {
+      const float4 op = pp[0], oq = pp[1];
+      P = make_float4(op.x + P.x, op.y + P.y, op.z + P.z, op.w + P.w);
+      Q = make_float4(oq.x + Q.x, oq.y + Q.y, oq.z + Q.z, oq.w + Q.w);
+    }
+    pp[0] = P;
+    pp[1] = Q;
+  }
+}
+
+// k_cm_yin with 16-byte accesses.  Phase 1: lane (g = lane & 15, r) reads
+// four pairs of rows r, r+16, r+32, r+48; phase 2: each group of 32 lanes
+// writes the 64 positions of one pair as 32 float4 (two positions each).
+__global__ __launch_bounds__(kTThreads) void k_cm_yin4(const float* __restrict__ S, size_t lstride,
+                                                       float2* __restrict__ C, size_t cstride,
+                                                       int L, int BD, int D, int bpair, int row0,
+                                                       int row1) {
+  __shared__ float2 tile[kCmT][kCmT + 1];
+  const int m = (int)blockIdx.z;
+  const int p0 = (int)blockIdx.x * kCmT, r0 = row0 + (int)blockIdx.y * kCmT;
+  int a0, b0;
+  cm_block_cols(p0, bpair != 0, D, a0, b0);
+  const float* Sm = S + (size_t)m * lstride;
+  {
+    const int g = (int)threadIdx.x & 15, r16 = (int)threadIdx.x >> 4;
+#pragma unroll
+    for (int k = 0; k < kCmT / 16; ++k) {
+      const int r = r16 + 16 * k;
+      if (r0 + r < row1) {
+        float2 v[4];
+        cm_load4(Sm + (size_t)(r0 + r) * BD, a0, b0, g, v);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) tile[r][4 * g + j] = v[j];
+      }
+    }
+  }
+  __syncthreads();
+  float2* Cm = C + (size_t)m * cstride;
+  const int l = (int)threadIdx.x & 31, grp = (int)threadIdx.x >> 5;
+#pragma unroll
+  for (int k = 0; k < kCmT / 8; ++k) {
+    const int x = grp + 8 * k, t = r0 + 2 * l;
+    if (t + 1 < row1) {
+      const float2 u = tile[2 * l][x], w = tile[2 * l + 1][x];
+      *reinterpret_cast<float4*>(Cm + (size_t)(p0 + x) * L + t) = make_float4(u.x, u.y, w.x, w.y);
+    } else if (t < row1) {
+      Cm[(size_t)(p0 + x) * L + t] = tile[2 * l][x];
+    }
+  }
+}
+
+// k_cm_merge with 16-byte accesses (the reverse of k_cm_yin4).
+template <bool STORE>
+__global__ __launch_bounds__(kTThreads) void k_cm_merge4(const float2* __restrict__ C,
+                                                         size_t cstride, float* __restrict__ S,
+                                                         size_t lstride, int L, int BD, int D,
+                                                         int bpair, int row0, int row1) {
+  __shared__ float2 tile[kCmT][kCmT + 1];
+  const int m = (int)blockIdx.z;
+  const int p0 = (int)blockIdx.x * kCmT, r0 = row0 + (int)blockIdx.y * kCmT;
+  const float2* Cm = C + (size_t)m * cstride;
+  {
+    const int l = (int)threadIdx.x & 31, grp = (int)threadIdx.x >> 5;
+#pragma unroll
+    for (int k = 0; k < kCmT / 8; ++k) {
+      const int x = grp + 8 * k, t = r0 + 2 * l;
+      if (t + 1 < row1) {
+        const float4 v = *reinterpret_cast<const float4*>(Cm + (size_t)(p0 + x) * L + t);
+        tile[2 * l][x] = make_float2(v.x, v.y);
+        tile[2 * l + 1][x] = make_float2(v.z, v.w);
+      } else if (t < row1) {
+        tile[2 * l][x] = Cm[(size_t)(p0 + x) * L + t];
+      }
+    }
+  }
+  __syncthreads();
+  int a0, b0;
+  cm_block_cols(p0, bpair != 0, D, a0, b0);
+  float* Sm = S + (size_t)m * lstride;
+  const int g = (int)threadIdx.x & 15, r16 = (int)threadIdx.x >> 4;
+#pragma unroll
+  for (int k = 0; k < kCmT / 16; ++k) {
+    const int r = r16 + 16 * k;
+    if (r0 + r < row1) {
+      float2 v[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) v[j] = tile[r][4 * g + j];
+      cm_store4<STORE>(Sm + (size_t)(r0 + r) * BD, a0, b0, g, v);
+    }
+  }
+}
+
 // Spectral product of the transform in buf (padded LDS, one column) for a
 // pair: one channel (spectrum ha, plain P = Z H over bins k <= U and their
 // mirrors) or two (ha, hb: P[k] = Z[k] S[k] + conj(Z[N-k]) D[k]).  hv: ha
@@ -764,13 +910,24 @@ hipError_t launch_fft_col_tile(float* S, const float2* Hc, const float2* tw, con
   return hipSuccess;
 }
 
+// 16-byte mirror copies: every block of 64 pairs lies in whole aligned runs
+// (and L even keeps the two positions of a float4 in one pair's row).
+static bool cm_vec(const Shape& s, const CmShape& cm) {
+  if (s.L % 2 != 0) return false;
+  return cm.bpair ? s.D % kCmT == 0 : s.BD % (2 * kCmT) == 0;
+}
+
 hipError_t launch_cm_yin(const float* S, float2* C, const Shape& s, const CmShape& cm, int row0,
                          int row1, hipStream_t st) {
   if (row1 <= row0) return hipSuccess;
   const dim3 grid((unsigned)((cm.PC + kCmT - 1) / kCmT), (unsigned)((row1 - row0 + kCmT - 1) / kCmT),
                   (unsigned)s.M);
-  hipLaunchKernelGGL(k_cm_yin, grid, dim3(kTThreads), 0, st, S, (size_t)s.SL * s.BD, C,
-                     (size_t)cm.PC * s.L, s.L, cm.PC, s.BD, s.D, cm.bpair, row0, row1);
+  if (cm_vec(s, cm) && row0 % 2 == 0)
+    hipLaunchKernelGGL(k_cm_yin4, grid, dim3(kTThreads), 0, st, S, (size_t)s.SL * s.BD, C,
+                       (size_t)cm.PC * s.L, s.L, s.BD, s.D, cm.bpair, row0, row1);
+  else
+    hipLaunchKernelGGL(k_cm_yin, grid, dim3(kTThreads), 0, st, S, (size_t)s.SL * s.BD, C,
+                       (size_t)cm.PC * s.L, s.L, cm.PC, s.BD, s.D, cm.bpair, row0, row1);
   return hipGetLastError();
 }
 
@@ -779,7 +936,14 @@ hipError_t launch_cm_merge(const float2* C, float* S, const Shape& s, const CmSh
   if (row1 <= row0) return hipSuccess;
   const dim3 grid((unsigned)((cm.PC + kCmT - 1) / kCmT), (unsigned)((row1 - row0 + kCmT - 1) / kCmT),
                   (unsigned)s.M);
-  if (store)
+  const bool vec = cm_vec(s, cm) && row0 % 2 == 0;
+  if (vec && store)
+    hipLaunchKernelGGL(k_cm_merge4<true>, grid, dim3(kTThreads), 0, st, C, (size_t)cm.PC * s.L, S,
+                       (size_t)s.SL * s.BD, s.L, s.BD, s.D, cm.bpair, row0, row1);
+  else if (vec)
+    hipLaunchKernelGGL(k_cm_merge4<false>, grid, dim3(kTThreads), 0, st, C, (size_t)cm.PC * s.L, S,
+                       (size_t)s.SL * s.BD, s.L, s.BD, s.D, cm.bpair, row0, row1);
+  else if (store)
     hipLaunchKernelGGL(k_cm_merge<true>, grid, dim3(kTThreads), 0, st, C, (size_t)cm.PC * s.L, S,
                        (size_t)s.SL * s.BD, s.L, cm.PC, s.BD, s.D, cm.bpair, row0, row1);
   else
