@@ -75,6 +75,8 @@ def parse():
     p.add_argument("--direct-max-u", type=int, default=0, help="0 = library default")
     p.add_argument("--lds-fft-max-n", type=int, default=0, help="0 = library default")
     p.add_argument("--scratch-mib", type=int, default=0, help="0 = library default")
+    p.add_argument("--col-tile-form", type=int, default=0,
+                   help="1: column tiles on transposed chunks instead of the column-major mirror")
     p.add_argument("--col-fft-min-n", type=int, default=0,
                    help="smallest 2U of the column-chunk FFT tiles (0 = library default, "
                         "above 16384 = off)")
@@ -113,6 +115,16 @@ def parse():
     p.add_argument("--trace-from", metavar="DIR", default=None,
                    help="only summarise a rocprofv3 kernel trace under DIR per (kernel, U), "
                         "grouped as the per-launch pass groups launches")
+    p.add_argument("--bracket", default="",
+                   help="with --trace-from: comma-separated bench JSON outputs of the same command "
+                        "without the profiler (before and after), quoted beside the trace")
+    p.add_argument("--counters-from", metavar="DIR", default=None,
+                   help="only summarise rocprofv3 --pmc runs, one derived counter per DIR/<name>, "
+                        "per kernel into profiles/counters_<workload>.txt")
+    p.add_argument("--sweep-from", metavar="DIR", default=None,
+                   help="only tabulate bench JSON outputs DIR/sweep_<label>.json (one tile-kind "
+                        "option set each) per tile size into profiles/crossover_<workload>.txt")
+    p.add_argument("--command", default="", help="command line quoted in a written summary")
     p.add_argument("--copy-mib", type=int, default=1024, help="size the copy probe ran with")
     p.add_argument("--copy-scalar", action="store_true",
                    help="copy probe with 4-byte accesses per lane (a one-element offset keeps torch "
@@ -147,8 +159,8 @@ def launch_bytes(name, U, w):
 # Sources of the kernels a counter run of the timed region executes, and of
 # their dispatch (the data-dependent, synthetic-model and column-chunk
 # kernels never run there).
-COUNTED_SOURCES = ("lcsm_api.hip", "lcsm_direct.hip", "lcsm_fft.hip", "lcsm_fft_core.h",
-                   "lcsm_internal.h")
+COUNTED_SOURCES = ("lcsm_api.hip", "lcsm_direct.hip", "lcsm_fft.hip", "lcsm_fft_col.hip",
+                   "lcsm_fft_core.h", "lcsm_internal.h")
 
 
 def source_digest():
@@ -254,11 +266,21 @@ def tile_bytes(rows_c):
     return group_tiles(rows_c, lambda r: 1024.0 * float(r["Counter_Value"]))
 
 
+def short_name(name):
+    """Kernel name without namespaces and argument list."""
+    import re
+    name = re.sub(r"^void ", "", name).replace("(anonymous namespace)::", "").replace("lcsm::", "")
+    return re.sub(r"\(.*$", "", name)
+
+
 def trace_summary(args):
     """Per (kernel, U) launch durations from a rocprofv3 kernel trace
     (<dir>/run_kernel_trace.csv) of a bench command: the same grouping as the
-    per-launch pass (a column tile = its red cell + every chunk's dispatches),
-    with algorithmic GB/s and the fraction of 8 TB/s."""
+    per-launch pass (a column tile = its red cell + every chunk's dispatches;
+    a mirrored tile = its red cell, the mirror copies and the transform),
+    with algorithmic GB/s and the fraction of 8 TB/s; then the kernels with
+    the most time.  Written to profiles/kernels_<workload>.txt."""
+    import collections
     import csv
     import glob
 
@@ -269,8 +291,13 @@ def trace_summary(args):
         rows = list(csv.DictReader(f))
     per = group_tiles(rows, lambda r: (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3,
                       order_key="Start_Timestamp")
-    lines = [f"# per-launch durations from the kernel trace, workload {w.name} "
-             f"(M={w.M} B={w.B} D={w.D} L={w.L})",
+    lines = [f"# workload {w.name} (M={w.M} B={w.B} D={w.D} L={w.L}), library defaults",
+             "# rocprofv3 kernel trace; command (from a scratch directory, TMPDIR=/tmp):",
+             f"#   rocprofv3 --kernel-trace --stats --output-format csv -d <dir> -o run -- {args.command}",
+             f"#   then: python3 bench.py --trace-from <dir> --workload {w.name}",
+             f"# kernel sources digest {source_digest()}",
+             "# Per launch as the per-launch pass groups them (durations summed over a launch's "
+             "dispatches; every generation of the command, graph-replayed and per-launch):",
              "# kernel        U   launches    avg_us   total_ms  algorithmic_GB_s  frac_of_8TB_s"]
     for (name, U), v in sorted(per.items(), key=lambda kv: (kv[0][1] or 0, kv[0][0])):
         if U is None:
@@ -280,6 +307,116 @@ def trace_summary(args):
         gbs = launch_bytes(name, U, w) / (avg * 1e-6) / 1e9
         lines.append(f"{name:12s} {U:5d} {len(v):10d} {avg:9.2f} {sum(v) / 1e3:10.2f} "
                      f"{gbs:17.1f} {gbs / HBM_PEAK_GBS:14.4f}")
+    agg = collections.defaultdict(list)
+    for r in rows:
+        agg[short_name(r["Kernel_Name"])].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    total = sum(sum(v) for v in agg.values())
+    lines.append("# Kernels by total time (torch's input generation outside the timed region included):")
+    lines.append("#   calls     total_ms     avg_us    pct  kernel")
+    for k, v in sorted(agg.items(), key=lambda kv: -sum(kv[1]))[:30]:
+        lines.append(f"{len(v):9d} {sum(v) / 1e3:12.2f} {sum(v) / len(v):10.2f} "
+                     f"{100 * sum(v) / total:6.2f}  {k}")
+    for b in (x for x in args.bracket.split(",") if x):
+        with open(b) as f:
+            d = json.loads(f.read().strip().splitlines()[-1])
+        lines.append(f"# bench line of the same command without the profiler ({os.path.basename(b)}): "
+                     f"{d['ms_per_step']} ms per generation; per-launch pass (HIP events):")
+        for key, v in d.get("per_level_us", {}).items():
+            if not key.startswith("fused") or key in ("fused:U=1", "fused:U=32"):
+                lines.append(f"#   {key:18s} {v['avg_us']:10.2f} us  {v['GB_s']} GB/s")
+    prof = os.path.join(ROOT, "profiles")
+    os.makedirs(prof, exist_ok=True)
+    with open(os.path.join(prof, f"kernels_{w.name}.txt"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def counters_summary(args):
+    """Mean of each derived counter per kernel over its dispatches, from
+    rocprofv3 --pmc runs with one derived counter each (DIR/<counter>/...),
+    written to profiles/counters_<workload>.txt."""
+    import collections
+    import csv
+    import glob
+
+    import datagen
+    w = datagen.WORKLOADS[args.workload]
+    res = collections.defaultdict(dict)
+    names = []
+    for sub in sorted(os.listdir(args.counters_from)):
+        f = glob.glob(os.path.join(args.counters_from, sub, "**", "*counter_collection.csv"),
+                      recursive=True)
+        if not f:
+            continue
+        names.append(sub)
+        acc = collections.defaultdict(list)
+        with open(f[0]) as fh:
+            for r in csv.DictReader(fh):
+                acc[short_name(r["Kernel_Name"])].append(float(r["Counter_Value"]))
+        for k, v in acc.items():
+            res[k][sub] = (sum(v) / len(v), len(v))
+    lines = [f"# workload {w.name} (M={w.M} B={w.B} D={w.D} L={w.L}), library defaults",
+             "# rocprofv3 derived counters, one per run (mean over each kernel's dispatches):",
+             f"#   rocprofv3 --pmc <counter> --output-format csv -d <dir>/<counter> -o run -- {args.command}",
+             f"#   for <counter> in {' '.join(names)}; then: python3 bench.py --counters-from <dir> "
+             f"--workload {w.name}",
+             f"# kernel sources digest {source_digest()}",
+             "# VALUBusy: percent of the time the vector ALUs issue; VALUUtilization: active lanes "
+             "per VALU instruction; MfmaUtil: percent of the time the matrix cores are busy;",
+             "# OccupancyPercent: resident waves against the maximum; LdsUtil, LDSBankConflict: "
+             "LDS busy and bank-conflict cycles, percent.",
+             f"{'kernel':46s}" + "".join(f"{n[:16]:>17s}" for n in names) + "  dispatches"]
+    for k in sorted(res):
+        if "at::" in k or "elementwise" in k:
+            continue
+        n = max(x[1] for x in res[k].values())
+        lines.append(f"{k[:46]:46s}" + "".join(
+            f"{res[k][c][0]:17.1f}" if c in res[k] else f"{'-':>17s}" for c in names) + f"  {n:10d}")
+    prof = os.path.join(ROOT, "profiles")
+    os.makedirs(prof, exist_ok=True)
+    with open(os.path.join(prof, f"counters_{w.name}.txt"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def sweep_summary(args):
+    """Per tile size, the per-launch time and algorithmic GB/s of every tile
+    kind a sweep measured: DIR/sweep_<label>.json are bench outputs, each
+    with one tile-kind option set (its per-launch pass times every tile size
+    with the kind the options select).  Written to
+    profiles/crossover_<workload>.txt."""
+    import collections
+    import glob
+
+    import datagen
+    w = datagen.WORKLOADS[args.workload]
+    table = collections.defaultdict(dict)
+    labels = []
+    for path in sorted(glob.glob(os.path.join(args.sweep_from, f"sweep_{w.name}_*.json"))):
+        label = os.path.basename(path)[len(f"sweep_{w.name}_"):-5]
+        with open(path) as f:
+            d = json.loads(f.read().strip().splitlines()[-1])
+        labels.append((label, d["config"]["options"], d["ms_per_step"]))
+        for key, v in d.get("per_level_us", {}).items():
+            kind, u = key.split(":U=")
+            table[int(u)][f"{kind} ({label})"] = (v["avg_us"], v["GB_s"])
+    lines = [f"# workload {w.name} (M={w.M} B={w.B} D={w.D} L={w.L}): per-launch time of each tile "
+             "size (HIP events, the red cell included) under tile-kind option sets",
+             f"# command per set: python3 bench.py --workload {w.name} --steps 1 --warmup 1 "
+             "<options> --no-cpu-baseline --no-closed-loop --no-prefill --no-half-state --no-dd "
+             "--no-synth > <dir>/sweep_<workload>_<label>.json",
+             f"# then: python3 bench.py --sweep-from <dir> --workload {w.name}",
+             f"# kernel sources digest {source_digest()}"]
+    for label, opts, ms in labels:
+        lines.append(f"#   {label:14s} options {opts}: {ms} ms per generation")
+    lines.append("# U      kind (set): avg_us / algorithmic GB/s, fastest first")
+    for U in sorted(table):
+        cells = sorted(table[U].items(), key=lambda kv: kv[1][0])
+        lines.append(f"{U:6d}  " + "   ".join(f"{k}: {a:.2f} us / {g} GB/s" for k, (a, g) in cells))
+    prof = os.path.join(ROOT, "profiles")
+    os.makedirs(prof, exist_ok=True)
+    with open(os.path.join(prof, f"crossover_{w.name}.txt"), "w") as f:
+        f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
 
 
@@ -366,6 +503,12 @@ def main():
     if args.trace_from:
         trace_summary(args)
         return
+    if args.counters_from:
+        counters_summary(args)
+        return
+    if args.sweep_from:
+        sweep_summary(args)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
               "(this build has no multi-GPU path).", file=sys.stderr)
@@ -389,7 +532,8 @@ def main():
     opts = {k: v for k, v in (("direct_max_u", args.direct_max_u),
                               ("lds_fft_max_n", args.lds_fft_max_n),
                               ("scratch_mib", args.scratch_mib),
-                              ("col_fft_min_n", args.col_fft_min_n)) if v} or None
+                              ("col_fft_min_n", args.col_fft_min_n),
+                              ("col_tile_form", args.col_tile_form)) if v} or None
 
     print(f"# workload {w.name}: M={w.M} B={w.B} D={w.D} L={w.L} graph={args.graph}",
           file=sys.stderr, flush=True)
@@ -509,7 +653,8 @@ def counter_run(args, w, torch, datagen, lcsm):
     opts = {k: v for k, v in (("direct_max_u", args.direct_max_u),
                               ("lds_fft_max_n", args.lds_fft_max_n),
                               ("scratch_mib", args.scratch_mib),
-                              ("col_fft_min_n", args.col_fft_min_n)) if v} or None
+                              ("col_fft_min_n", args.col_fft_min_n),
+                              ("col_tile_form", args.col_tile_form)) if v} or None
     P = min(args.positions, w.L)
 
     def say(msg):
@@ -780,9 +925,16 @@ def baselines_timing(w, filters, y, ms_relaxed, kinds, lcsm, torch, dev, args, s
             for _ in range(args.baseline_warmup):
                 chain.replay()
             torch.cuda.synchronize()
+            # graph by graph, with a progress line after each (a lazy or eager
+            # generation of 131072 positions takes minutes); the timed region
+            # spans them all, the waits between graphs included
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record()
-            chain.replay()
+            for k, g in enumerate(chain.graphs):
+                g.replay()
+                torch.cuda.synchronize()
+                print(f"# baseline {kind}: graph {k + 1} of {len(chain.graphs)} "
+                      f"({chain.positions} positions each)", file=sys.stderr, flush=True)
             e1.record()
         torch.cuda.synchronize()
         bms = e0.elapsed_time(e1)

@@ -27,6 +27,11 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
     ("lcsm::k_fft_coltile2<16384, 0>", ("fft_col", 16384)),
     ("lcsm::k_rows_to_cols", ("fft_col", None)),
     ("lcsm::k_cols_to_rows<false>", ("fft_col", None)),
+    ("void lcsm::(anonymous namespace)::k_cm_tile<2048>(float2*, unsigned long)", ("fft_cm", 1024)),
+    ("lcsm::k_cm_tile2<16384, 1>", ("fft_cm", 16384)),
+    ("lcsm::k_cm_yin4(float const*)", ("fft_cm", None)),
+    ("lcsm::k_cm_merge4<true>", ("fft_cm", None)),
+    ("lcsm::k_cm_merge<false>", ("fft_cm", None)),
     ("at::native::vectorized_elementwise_kernel<4, ...>", None),
     ("lcsm::k_fft_spectra<1024>", None),
 ])
@@ -62,6 +67,17 @@ def test_tile_bytes_sums_a_column_tile_with_its_red_cell():
     assert per[("fused", 1)] == [1024.0, 2048.0]
     assert per[("fft_lds", 128)] == [7 * 1024.0]
     assert ("red", 0) not in per
+
+
+def test_tile_bytes_groups_a_mirrored_tile_with_its_copies():
+    """A mirrored tile launch: the red cell, the mirror's input copy, the
+    transform and the merge are one entry; a following fused step stays apart."""
+    order = [("lcsm::k_step_fused<0, true>", 0.5), ("lcsm::k_cm_yin4", 8.0),
+             ("lcsm::k_cm_tile<2048>", 40.0), ("lcsm::k_cm_merge4<true>", 9.0),
+             ("lcsm::k_step_fused<1, true>", 1.0)]
+    per = bench.tile_bytes([_row(i, n, v) for i, (n, v) in enumerate(order)])
+    assert per[("fft_cm", 1024)] == [1024.0 * (0.5 + 8 + 40 + 9)]
+    assert per[("fused", 1)] == [1024.0]
 
 
 def test_tile_bytes_keeps_a_lone_red_cell():
