@@ -220,32 +220,53 @@ def kernel_key(name):
         return ("fft_cm", int(m.group(1)))
     if "k_cm_yin" in name or "k_cm_merge" in name:
         return ("fft_cm", None)
+    # the three-pass tile: rows of N2 points, columns of N1 (2U = N1 N2)
+    m = re.search(r"k_fft_rows_(?:fwd|inv)<(\d+), (?:true|false)>", name)
+    if m:
+        return ("fft_hbm", ("N2", int(m.group(1))))
+    m = re.search(r"k_fft_mid_tile<(\d+)>", name)
+    if m:
+        return ("fft_hbm", ("N1", int(m.group(1))))
     return None
 
 
 def group_tiles(rows, value, order_key="Dispatch_Id"):
     """Per (kernel, U) key, one summed value per launch of the per-launch
-    pass, from profiler rows in dispatch order.  A column-chunk tile is one
-    launch made of several dispatches (the red cell before it, then
-    transpose, transform, transpose per chunk): their values are summed into
-    one entry per tile.  value(row) gives a row's number."""
+    pass, from profiler rows in dispatch order.  A tile made of several
+    dispatches -- a column tile (transposes and transform per chunk), a
+    mirrored tile (the mirror's copies and the transform) or a three-pass
+    tile (rows, columns, rows per chunk) -- is one launch together with the
+    red cell dispatched before it: their values are summed into one entry,
+    under the kind of its transform (the three-pass U from its row and
+    column lengths).  value(row) gives a row's number."""
     import collections
     per = collections.defaultdict(list)
     rows = sorted(rows, key=lambda r: int(r[order_key]))
-    tile, red = None, None  # open column tile [kind, U, value]; last red-cell dispatch's value
+    multi = ("fft_col", "fft_cm", "fft_hbm")
+    tile, red = None, None  # open multi-dispatch tile; last red-cell dispatch's value
+
+    def close(t):
+        if t["kind"] == "fft_hbm" and t["N1"] and t["N2"]:
+            t["U"] = t["N1"] * t["N2"] // 2
+        per[(t["kind"], t["U"])].append(t["v"])
+
     for r in rows:
         key = kernel_key(r["Kernel_Name"])
         v = value(r)
-        if key and key[0] in ("fft_col", "fft_cm"):
+        if key and key[0] in multi:
             if tile is None:
-                tile = [key[0], None, red or 0.0]
+                tile = {"kind": key[0], "U": None, "N1": 0, "N2": 0, "v": red or 0.0}
                 red = None
-            tile[2] += v
-            if key[1] is not None:
-                tile[1] = key[1]
+            tile["v"] += v
+            if key[0] == "fft_hbm" or (key[1] is not None and tile["kind"] != "fft_hbm"):
+                tile["kind"] = key[0]  # the transform names the launch's kind
+            if isinstance(key[1], tuple):
+                tile[key[1][0]] = key[1][1]
+            elif key[1] is not None:
+                tile["U"] = key[1]
             continue
         if tile is not None:
-            per[(tile[0], tile[1])].append(tile[2])
+            close(tile)
             tile = None
         if red is not None:
             per[("red", 0)].append(red)
@@ -255,7 +276,7 @@ def group_tiles(rows, value, order_key="Dispatch_Id"):
         elif key:
             per[key].append(v)
     if tile is not None:
-        per[(tile[0], tile[1])].append(tile[2])
+        close(tile)
     if red is not None:
         per[("red", 0)].append(red)
     return per
@@ -453,8 +474,8 @@ def traffic_from(args):
     except (OSError, ValueError):
         pass
     kernels = {}
-    for (name, U), v in sorted(per.items(), key=lambda kv: (kv[0][1], kv[0][0])):
-        if not v["FETCH_SIZE"] or not v["WRITE_SIZE"]:
+    for (name, U), v in sorted(per.items(), key=lambda kv: (kv[0][1] or 0, kv[0][0])):
+        if U is None or not v["FETCH_SIZE"] or not v["WRITE_SIZE"]:
             continue
         fb = sum(v["FETCH_SIZE"]) / len(v["FETCH_SIZE"])
         wb = sum(v["WRITE_SIZE"]) / len(v["WRITE_SIZE"])

@@ -32,6 +32,8 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
     ("lcsm::k_cm_yin4(float const*)", ("fft_cm", None)),
     ("lcsm::k_cm_merge4<true>", ("fft_cm", None)),
     ("lcsm::k_cm_merge<false>", ("fft_cm", None)),
+    ("lcsm::k_fft_rows_fwd<4096, true>", ("fft_hbm", ("N2", 4096))),
+    ("lcsm::k_fft_mid_tile<32>", ("fft_hbm", ("N1", 32))),
     ("at::native::vectorized_elementwise_kernel<4, ...>", None),
     ("lcsm::k_fft_spectra<1024>", None),
 ])
@@ -78,6 +80,21 @@ def test_tile_bytes_groups_a_mirrored_tile_with_its_copies():
     per = bench.tile_bytes([_row(i, n, v) for i, (n, v) in enumerate(order)])
     assert per[("fft_cm", 1024)] == [1024.0 * (0.5 + 8 + 40 + 9)]
     assert per[("fused", 1)] == [1024.0]
+
+
+def test_tile_bytes_three_pass_tile_after_a_mirror_copy():
+    """At a multiple of the mirror's T0 whose tile is a three-pass one (2U =
+    131072 = 32 x 4096): the red cell, the mirror's input copy and every
+    chunk's three passes are one launch of U = 65536."""
+    order = [("lcsm::k_step_fused<0, true>", 0.5), ("lcsm::k_cm_yin4", 8.0),
+             ("lcsm::k_fft_rows_fwd<4096, true>", 10.0), ("lcsm::k_fft_mid_tile<32>", 11.0),
+             ("lcsm::k_fft_rows_inv<4096, false>", 12.0), ("lcsm::k_fft_rows_fwd<4096, true>", 10.0),
+             ("lcsm::k_fft_mid_tile<32>", 11.0), ("lcsm::k_fft_rows_inv<4096, false>", 12.0),
+             ("lcsm::k_step_fused<1, true>", 1.0)]
+    per = bench.tile_bytes([_row(i, n, v) for i, (n, v) in enumerate(order)])
+    assert per[("fft_hbm", 65536)] == [1024.0 * (0.5 + 8 + 2 * (10 + 11 + 12))]
+    assert per[("fused", 1)] == [1024.0]
+    assert not any(k[1] is None for k in per)
 
 
 def test_tile_bytes_keeps_a_lone_red_cell():
