@@ -1005,7 +1005,7 @@ def dd_timing(w, ms_fixed, lcsm, torch, dev, args):
     import datagen
     try:
         lcsm.dd_workspace_bytes(w.M, w.B, w.D, w.L)
-    except lcsm.LcsmError as e:   # the largest tile is beyond the single-pass FFT
+    except lcsm.LcsmError as e:   # a shape the context rejects
         return {"skipped": str(e)}
     R = min(RING, w.L)
     y = datagen.y_torch(w, dev, 0, R)

@@ -40,12 +40,13 @@ typedef struct lcsm_dd lcsm_dd;
 /* Device bytes of the workspace (the inputs y and rho of every position:
  * 2*M*L*B*D fp32, the outputs' accumulators sharing y's rows, plus the FFT
  * twiddle table).  opt: direct_max_u (largest U done directly, default 32) and
- * lds_fft_max_n (largest 2U of the FFT tiles, power of two in [16, 8192],
- * default 8192) apply; scratch_mib, half_state and col_fft_min_n must be 0.
- * Host only.
- * Errors: LCSM_EINVAL for the shapes lcsm_workspace_bytes rejects, bad
- * options, or a length whose largest tile (the largest power of two U with
- * 2U < L) exceeds both limits. */
+ * lds_fft_max_n (largest transform of the FFT tiles, power of two in
+ * [16, 8192], default 8192) apply; scratch_mib, half_state and col_fft_min_n
+ * must be 0.  A tile with 2U above lds_fft_max_n = 2V runs as (U/V)^2 pairs
+ * of V-blocks whose 2V-point product spectra are summed per output block
+ * (same sums, more transforms).  Host only.
+ * Errors: LCSM_EINVAL for the shapes lcsm_workspace_bytes rejects or bad
+ * options. */
 int lcsm_dd_workspace_bytes(int M, int B, int D, int L, const lcsm_options* opt, size_t* bytes);
 
 /* Create a context at position 0 (all activations zero).  workspace: device

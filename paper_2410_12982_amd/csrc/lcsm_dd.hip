@@ -266,13 +266,13 @@ using DdTw = typename std::conditional<
     DdCfg<N>::TWL, fft::TwLds<N>,
     typename std::conditional<DdCfg<N>::TWH, fft::TwLdsHalf<N>, fft::TwGlobal>::type>::type;
 
-template <int N>
+template <int N, int NT>
 __device__ __forceinline__ DdTw<N> dd_make_tw(float2* lds, const float2* __restrict__ tw) {
   if constexpr (DdCfg<N>::TWL) {
-    fft::load_twiddles<N, DdCfg<N>::NT>(lds, tw);
+    fft::load_twiddles<N, NT>(lds, tw);
     return fft::TwLds<N>{lds};
   } else if constexpr (DdCfg<N>::TWH) {
-    fft::load_twiddles<N, DdCfg<N>::NT, N / 2>(lds, tw);
+    fft::load_twiddles<N, NT, N / 2>(lds, tw);
     return fft::TwLdsHalf<N>{lds};
   } else {
     return fft::TwGlobal{tw};
@@ -287,70 +287,101 @@ __device__ __forceinline__ void unpack(float2 xk, float2 xnk, float2& a, float2&
   b = make_float2(0.5f * d.y, -0.5f * d.x);
 }
 
-template <int N, bool SQ>
-__global__ __launch_bounds__(DdCfg<N>::NT) void k_dd_fft(float* __restrict__ Y,
+//
+// Tiles wider than the largest single-pass transform (U = K V, V = N / 2)
+// are split into V-blocks: fixed sub-blocks F_p = [fo + pV, fo + (p+1)V),
+// recent ones R_q = [lo + qV, ...), p, q < K.  The pair (p, q) contributes
+// its V-block convolution at offset (p + q) V of the destination, so output
+// block r = p + q (rows d0 + rV + j, j < 2V - 1) takes the sum over p of
+// the pairs' product spectra -- accumulated in registers, one inverse per r.
+// The square sums yF_p (*) rhoF_q over every ordered (p, q); the rectangle
+// yF_p (*) rhoR_q + rhoF_p (*) yR_q.  Blocks r and r + 1 overlap by V - 1
+// rows, so one launch (MB) covers every other r: r = r0 + 2 j.  K = 1 is
+// the plain tile (fo = U).
+// Threads of a workgroup: the block-split form keeps a third spectrum (the
+// running sum) in registers, so from N = 2048 on it takes 1024 threads.
+template <int N, bool MB>
+constexpr int dd_threads() {
+  return MB && N >= 2048 ? 1024 : DdCfg<N>::NT;
+}
+
+template <int N, bool SQ, bool MB>
+__global__ __launch_bounds__((dd_threads<N, MB>())) void k_dd_fft(float* __restrict__ Y,
                                                         const float* __restrict__ R,
                                                         const float2* __restrict__ tw, int L,
-                                                        int BD, int lo, int d0, int dlen,
-                                                        int ppl) {
-  constexpr int CW = DdCfg<N>::CW, NT = DdCfg<N>::NT, U = N / 2, HW = CW / 2;
+                                                        int BD, int fo, int lo, int d0, int dlen,
+                                                        int ppl, int lm, int K, int r0) {
+  constexpr int CW = DdCfg<N>::CW, NT = dd_threads<N, MB>(), U = N / 2, HW = CW / 2;
   __shared__ float2 buf[N * CW];
   __shared__ float2 twl[DdCfg<N>::TWN];
-  const auto twz = dd_make_tw<N>(twl, tw);
+  const auto twz = dd_make_tw<N, NT>(twl, tw);
   const int q = fft::xcd_logical((int)blockIdx.x, (int)gridDim.x);
-  const int m = q / ppl;
-  const int c0 = (q - m * ppl) * CW;
+  const int units = ppl * lm;  // (layer, panel) units per output block
+  const int rb = MB ? q / units : 0;
+  const int qu = MB ? q - rb * units : q;
+  const int m = qu / ppl;
+  const int c0 = (qu - m * ppl) * CW;
   const size_t rs = (size_t)BD;
   float* Ym = Y + (size_t)m * L * BD;
   const float* Rm = R + (size_t)m * L * BD;
 
-  // spectra of the fixed blocks [U, 2U) of the unit (bin kk <= U, column col)
-  constexpr int PUN = (U + 1) * CW;
+  constexpr int PUN = (U + 1) * CW;  // (bin kk <= U, column col) units
   constexpr int PU = (PUN + NT - 1) / NT;
-  fft::forward_from_global<N, CW, CW, NT, true>(buf, twz, [&](int row, int col) {
-    const int c = c0 + col;
-    if (c >= BD) return make_float2(0.f, 0.f);
-    const size_t e = (size_t)(U + row) * rs + c;
-    return make_float2(Ym[e], Rm[e]);
-  });
-  float2 yf[PU], rf[PU];
-#pragma unroll
-  for (int a = 0; a < PU; ++a) {
-    const int u = (int)threadIdx.x + a * NT;
-    yf[a] = rf[a] = make_float2(0.f, 0.f);
-    if (PUN % NT == 0 || u < PUN) {
-      const int kk = u / CW, col = u - kk * CW;
-      const int nk = (N - kk) & (N - 1);
-      unpack(buf[kk * CW + col], buf[nk * CW + col], yf[a], rf[a]);
-    }
-  }
-  float2 p[PU];  // product spectrum of the unit's column, scaled by 1/N
   constexpr float inv_n = 1.0f / (float)N;
-  if constexpr (SQ) {
-#pragma unroll
-    for (int a = 0; a < PU; ++a) {
-      const float2 v = cmul(yf[a], rf[a]);
-      p[a] = make_float2(v.x * inv_n, v.y * inv_n);
-    }
-  } else {
-    __syncthreads();  // every unit has read the fixed spectra
+  // the forward transform of the packed block y + i rho at rows base ..
+  // base + U - 1 of the unit's columns, into buf
+  auto forward_block = [&](int base) {
     fft::forward_from_global<N, CW, CW, NT, true>(buf, twz, [&](int row, int col) {
       const int c = c0 + col;
       if (c >= BD) return make_float2(0.f, 0.f);
-      const size_t e = (size_t)(lo + row) * rs + c;
+      const size_t e = (size_t)(base + row) * rs + c;
       return make_float2(Ym[e], Rm[e]);
     });
+  };
+  const int r = MB ? r0 + 2 * rb : 0;
+  const int pmin = MB ? (r - K + 1 > 0 ? r - K + 1 : 0) : 0;
+  const int pmax = MB ? (r < K - 1 ? r : K - 1) : 0;
+  float2 p[PU];  // product spectrum of the unit's column, scaled by 1/N
+#pragma unroll
+  for (int a = 0; a < PU; ++a) p[a] = make_float2(0.f, 0.f);
+  for (int pb = pmin; pb <= pmax; ++pb) {
+    const int qb = r - pb;
+    if (pb > pmin) __syncthreads();  // the previous pair's spectra have been read
+    // spectra of the fixed (sub-)block
+    forward_block(fo + pb * U);
+    float2 yf[PU], rf[PU];
 #pragma unroll
     for (int a = 0; a < PU; ++a) {
       const int u = (int)threadIdx.x + a * NT;
-      p[a] = make_float2(0.f, 0.f);
+      yf[a] = rf[a] = make_float2(0.f, 0.f);
       if (PUN % NT == 0 || u < PUN) {
         const int kk = u / CW, col = u - kk * CW;
         const int nk = (N - kk) & (N - 1);
-        float2 yr, rr;
-        unpack(buf[kk * CW + col], buf[nk * CW + col], yr, rr);
-        const float2 v = cadd(cmul(yf[a], rr), cmul(rf[a], yr));
-        p[a] = make_float2(v.x * inv_n, v.y * inv_n);
+        unpack(buf[kk * CW + col], buf[nk * CW + col], yf[a], rf[a]);
+      }
+    }
+    if (SQ && pb == qb) {
+#pragma unroll
+      for (int a = 0; a < PU; ++a) {
+        const float2 v = cmul(yf[a], rf[a]);
+        p[a].x = fmaf(v.x, inv_n, p[a].x);
+        p[a].y = fmaf(v.y, inv_n, p[a].y);
+      }
+    } else {
+      __syncthreads();  // every unit has read the fixed spectra
+      forward_block((SQ ? fo : lo) + qb * U);
+#pragma unroll
+      for (int a = 0; a < PU; ++a) {
+        const int u = (int)threadIdx.x + a * NT;
+        if (PUN % NT == 0 || u < PUN) {
+          const int kk = u / CW, col = u - kk * CW;
+          const int nk = (N - kk) & (N - 1);
+          float2 yr, rr;
+          unpack(buf[kk * CW + col], buf[nk * CW + col], yr, rr);
+          const float2 v = SQ ? cmul(yf[a], rr) : cadd(cmul(yf[a], rr), cmul(rf[a], yr));
+          p[a].x = fmaf(v.x, inv_n, p[a].x);
+          p[a].y = fmaf(v.y, inv_n, p[a].y);
+        }
       }
     }
   }
@@ -389,10 +420,13 @@ __global__ __launch_bounds__(DdCfg<N>::NT) void k_dd_fft(float* __restrict__ Y,
     }
   }
   __syncthreads();
+  // rows of output block r inside the destination (its linear convolution
+  // has N - 1 rows; row N - 1 of the inverse is zero up to rounding)
+  const int rlen = dlen - r * U < N - 1 ? dlen - r * U : N - 1;
   fft::inverse_to_global<N, HW, HW, NT, false>(buf, twz, [&](int row, int pr, float2 v) {
-    if (row >= dlen) return;
+    if (row >= rlen) return;
     const int c = c0 + 2 * pr;
-    float* dst = Ym + (size_t)(d0 + row) * rs;
+    float* dst = Ym + (size_t)(d0 + r * U + row) * rs;
     if (c < BD) dst[c] += v.x;
     if (c + 1 < BD) dst[c + 1] += v.y;
   });
@@ -447,15 +481,15 @@ int resolve(int M, int B, int D, int L, const lcsm_options* o, DdOptions* r) {
       r->fft_max_n = o->lds_fft_max_n;
     }
   }
-  const int Umax = largest_u(L);
-  if (Umax > r->direct_max_u && 2 * Umax > r->fft_max_n) return LCSM_EINVAL;
   return LCSM_OK;
 }
 
-// Largest FFT length of a context (0: every tile direct).
+// Largest FFT length of a context (0: every tile direct): 2U of its largest
+// FFT tile, capped at the single-pass limit (wider tiles run as V-blocks).
 int fft_nmax(int L, const DdOptions& o) {
   const int Umax = largest_u(L);
-  return Umax > o.direct_max_u ? 2 * Umax : 0;
+  if (Umax <= o.direct_max_u) return 0;
+  return 2 * Umax < o.fft_max_n ? 2 * Umax : o.fft_max_n;
 }
 
 size_t state_bytes(int M, int B, int D, int L) {
@@ -494,16 +528,35 @@ int dd_fail(lcsm_dd* c, int code, const char* what, hipError_t e) {
   return code;
 }
 
+// The FFT tile of side U for all layers: one 2U-point launch when 2U fits
+// the single-pass limit, else V-blocks (V = fft_max_n / 2, K = U / V) in two
+// launches, the even and then the odd output blocks r < 2K - 1 that start
+// inside the destination.
 template <bool SQ>
-hipError_t dd_fft(lcsm_dd* c, int N, int lo, int d0, int dlen) {
+hipError_t dd_fft(lcsm_dd* c, int U, int lo, int d0, int dlen) {
+  const int N = 2 * U <= c->opt.fft_max_n ? 2 * U : c->opt.fft_max_n;
+  const int V = N / 2, K = U / V;
+  // output blocks that start inside the destination (r V < dlen), at most 2K - 1
+  const int nb = (dlen + V - 1) / V < 2 * K - 1 ? (dlen + V - 1) / V : 2 * K - 1;
 #define LCSM_CASE(NN)                                                                             \
   case NN: {                                                                                      \
     constexpr int CW = lcsm::DdCfg<NN>::CW;                                                       \
     const int ppl = (c->BD + CW - 1) / CW;                                                        \
-    hipLaunchKernelGGL((lcsm::k_dd_fft<NN, SQ>), dim3((unsigned)(ppl * c->M)),                    \
-                       dim3(lcsm::DdCfg<NN>::NT), 0, c->stream, c->Y, c->R, c->tw, c->L, c->BD,   \
-                       lo, d0, dlen, ppl);                                                        \
-    return hipGetLastError();                                                                     \
+    if (K == 1) {                                                                                 \
+      hipLaunchKernelGGL((lcsm::k_dd_fft<NN, SQ, false>), dim3((unsigned)(ppl * c->M)),           \
+                         dim3(lcsm::DdCfg<NN>::NT), 0, c->stream, c->Y, c->R, c->tw, c->L, c->BD, \
+                         U, lo, d0, dlen, ppl, c->M, 1, 0);                                       \
+      return hipGetLastError();                                                                   \
+    }                                                                                             \
+    for (int r0 = 0; r0 < 2 && r0 < nb; ++r0) {                                                   \
+      const int nr = (nb - r0 + 1) / 2;                                                           \
+      hipLaunchKernelGGL((lcsm::k_dd_fft<NN, SQ, true>), dim3((unsigned)(nr * ppl * c->M)),       \
+                         dim3(lcsm::dd_threads<NN, true>()), 0, c->stream, c->Y, c->R, c->tw, c->L, c->BD, \
+                         U, lo, d0, dlen, ppl, c->M, K, r0);                                      \
+      const hipError_t e = hipGetLastError();                                                     \
+      if (e != hipSuccess) return e;                                                              \
+    }                                                                                             \
+    return hipSuccess;                                                                            \
   }
   switch (N) {
     LCSM_CASE(4)
@@ -527,7 +580,7 @@ hipError_t dd_fft(lcsm_dd* c, int N, int lo, int d0, int dlen) {
 // 2U-point FFT tile.
 hipError_t dd_tile(lcsm_dd* c, bool square, int U, int lo, int d0, int dlen) {
   if (U > c->opt.direct_max_u)
-    return square ? dd_fft<true>(c, 2 * U, lo, d0, dlen) : dd_fft<false>(c, 2 * U, lo, d0, dlen);
+    return square ? dd_fft<true>(c, U, lo, d0, dlen) : dd_fft<false>(c, U, lo, d0, dlen);
   const dim3 grid((unsigned)((c->BD + lcsm::kThreads - 1) / lcsm::kThreads),
                   (unsigned)((dlen + lcsm::kDdJ - 1) / lcsm::kDdJ), (unsigned)c->M);
 #define LCSM_DD_U(UU)                                                                              \

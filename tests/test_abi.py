@@ -320,9 +320,8 @@ def test_synth_init_validates_before_touching_the_device():
 
 
 def test_dd_workspace_and_validation():
-    """Data-dependent contexts: two state arrays; options checked; lengths
-    whose largest tile (largest U with 2U < L) fits neither the direct nor
-    the FFT limit rejected -- all host-side."""
+    """Data-dependent contexts: two state arrays; options checked; tiles
+    wider than one LDS pass accepted (run as block pairs) -- all host-side."""
     M, B, D, L = 2, 3, 16, 1000
     n = lcsm.dd_workspace_bytes(M, B, D, L)
     assert n >= 2 * 4 * M * L * B * D and n % 256 == 0
@@ -335,13 +334,15 @@ def test_dd_workspace_and_validation():
     o.reserved[1] = 5
     with pytest.raises(lcsm.LcsmError):
         lcsm.dd_workspace_bytes(M, B, D, L, o)
-    # L = 16384: largest tile U = 4096, 2U = 8192 fits one LDS pass; L = 16385 needs U = 8192
-    lcsm.dd_workspace_bytes(1, 1, 16, 16384)
-    with pytest.raises(lcsm.LcsmError):
-        lcsm.dd_workspace_bytes(1, 1, 16, 16385)
+    # tiles wider than one LDS pass run as block pairs: any length is accepted, and the
+    # twiddle table stops at the single-pass transform (8192 points, 64 KiB)
+    state = 2 * 4 * 131072 * 16
+    n = lcsm.dd_workspace_bytes(1, 1, 16, 131072)
+    assert state < n <= state + 8 * 2 * 8192 + 256
+    assert lcsm.dd_workspace_bytes(1, 1, 16, 16385) > lcsm.dd_workspace_bytes(1, 1, 16, 16384)
     lcsm.dd_workspace_bytes(1, 1, 16, 16385, {"direct_max_u": 8192})
-    with pytest.raises(lcsm.LcsmError):
-        lcsm.dd_workspace_bytes(1, 1, 16, 4096, {"lds_fft_max_n": 1024})   # U = 1024 > 32, 2048 > 1024
+    small = lcsm.dd_workspace_bytes(1, 1, 16, 4096, {"lds_fft_max_n": 1024})  # U = 1024: 2x2 blocks
+    assert small <= 2 * 4 * 4096 * 16 + 8 * 2 * 1024 + 256
     for shape in ((0, 1, 1, 8), (1, 1, 1, 0), (16385, 1, 1, 8)):
         with pytest.raises(lcsm.LcsmError):
             lcsm.dd_workspace_bytes(*shape)

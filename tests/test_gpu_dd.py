@@ -8,7 +8,12 @@ data max|z_gpu - z_ref| <= 1e-4 * max|z_ref| against the fp64 oracle
 (oracle/dd.py, itself pinned to the definition); on small-integer data the
 rounded outputs equal the exact int64 products; a fixed rho gives the
 ordinary convolution.  The option sets put every tile on the direct kernel,
-every tile above U = 1 on the FFT kernel, and the default crossover.
+every tile above U = 1 on the FFT kernel, and the default crossover; two
+more cap the FFT transform at 16 and 64 points, so that tiles of U = 16 ..
+512 run as pairs of 8- or 32-row blocks (up to 64 x 64 pairs, both output
+parities, clipped last blocks) -- the form the tiles wider than one LDS
+pass take on the 32768- and 131072-position workloads, which are checked
+at full size on sampled columns.
 """
 import numpy as np
 import pytest
@@ -25,6 +30,8 @@ OPTIONS = {
     "direct_all": {"direct_max_u": 1 << 20},
     "fft_from_2": {"direct_max_u": 1},
     "default": None,
+    "blocks_of_8": {"direct_max_u": 1, "lds_fft_max_n": 16},
+    "blocks_of_32": {"direct_max_u": 4, "lds_fft_max_n": 64},
 }
 
 
@@ -40,7 +47,7 @@ def _ctx(w, opt):
     return lcsm_mod().Dd(w.M, w.B, w.D, w.L, options=OPTIONS[opt])
 
 
-@pytest.mark.parametrize("opt", ["direct_all", "fft_from_2", "default"])
+@pytest.mark.parametrize("opt", ["direct_all", "fft_from_2", "default", "blocks_of_8", "blocks_of_32"])
 @pytest.mark.parametrize("shape", [(1, 1, 16, 300), (2, 3, 20, 1000), (3, 2, 33, 513),
                                    (1, 4, 64, 2048), (2, 1, 15, 400)])
 def test_dd_matches_oracle(opt, shape):
@@ -59,7 +66,7 @@ def test_dd_matches_oracle(opt, shape):
     assert err <= TOL
 
 
-@pytest.mark.parametrize("opt", ["direct_all", "fft_from_2"])
+@pytest.mark.parametrize("opt", ["direct_all", "fft_from_2", "blocks_of_8"])
 def test_dd_integer_data_rounds_to_exact(opt):
     M, B, D, L = 2, 2, 12, 700
     w = datagen.Workload("ddint", M, B, D, L, decay=1.0, seed=3)
@@ -112,15 +119,20 @@ def test_dd_errors():
     assert ex.value.code == lcsm.LCSM_EDONE
 
 
-@pytest.mark.parametrize("name", ["m1b8d768l8k", "m32b16d2048l16k"])
+@pytest.mark.parametrize("name", ["m1b8d768l8k", "m32b16d2048l16k", "m18b4d768l32k",
+                                  "m18b1d1024l128k"])
 def test_dd_workload_sizes_sampled_columns(name):
-    """The bench workload (largest tile 2U = 4096) and the largest length the
-    single-pass tiles allow (L = 16384, 2U = 8192) at full width, default
-    options; the columns are independent, so sampled ones are checked
-    against the definition over all L positions."""
+    """Full-width contexts with default options: the bench workload (largest
+    tile 2U = 4096), L = 16384 (2U = 8192, the largest single-pass tile), and
+    L = 32768 and 131072, whose tiles of U = 8192 .. 32768 run as 2x2 .. 8x8
+    pairs of 4096-row blocks.  The columns are independent, so sampled ones
+    are checked over all L positions: against the definition up to 16384
+    positions, beyond that against the oracle's whole-sequence fp64 FFT
+    convolution (z is the causal convolution of y and rho)."""
+    from oracle import conv
     from oracle.dd import product_naive
     w = datagen.WORKLOADS[name]
-    say(f"[dd workload] {name}")
+    say(f"[dd workload] {name} M={w.M} B={w.B} D={w.D} L={w.L}")
     ctx = lcsm_mod().Dd(w.M, w.B, w.D, w.L)
     cols = datagen.sample_columns(w, 8, seed=91)
     cm, cb, cd = (torch.as_tensor(cols[:, k], device=dev()) for k in range(3))
@@ -136,9 +148,16 @@ def test_dd_workload_sizes_sampled_columns(name):
         got.append(z[: t1 - t0, cm, cb, cd].cpu())
         ys.append(y[:, cm, cb, cd].cpu())
         rs.append(rho[:, cm, cb, cd].cpu())
+        if t0 % 16384 == 0 and t0:
+            say(f"  position {t0}")
     torch.cuda.synchronize()
+    ctx.close()
     zg = torch.cat(got).numpy()
-    zr = product_naive(torch.cat(ys).numpy(), torch.cat(rs).numpy())
+    yc, rc = torch.cat(ys).numpy(), torch.cat(rs).numpy()
+    if w.L <= 16384:
+        zr = product_naive(yc, rc)
+    else:
+        zr = conv.causal_conv_fft(yc.astype(np.float64), rc.astype(np.float64))
     err = rel_err(zg, zr)
     say(f"  sampled rel err {err:.3e}")
     assert err <= TOL
