@@ -397,7 +397,63 @@ def counters_summary(args):
     os.makedirs(prof, exist_ok=True)
     with open(os.path.join(prof, f"counters_{w.name}.txt"), "w") as f:
         f.write("\n".join(lines) + "\n")
+    # the same means as JSON, keyed by workload and stamped with the digest;
+    # entries of other workloads taken on the same sources are kept
+    path = os.path.join(prof, "counters.json")
+    try:
+        with open(path) as f:
+            data = json.load(f)
+    except (OSError, ValueError):
+        data = {}
+    if data.get("source_digest") != source_digest():
+        data = {"source_digest": source_digest(), "workloads": {}}
+    data["workloads"][w.name] = {
+        k: dict({c: round(v[0], 2) for c, v in res[k].items()},
+                dispatches=max(x[1] for x in res[k].values()))
+        for k in sorted(res) if "at::" not in k and "elementwise" not in k}
+    with open(path, "w") as f:
+        json.dump(data, f, indent=1, sort_keys=True)
     print("\n".join(lines))
+
+
+def group_kernels(kind, U):
+    """Predicate on short kernel names: the dispatches one launch of (kind, U)
+    is made of, as the per-launch pass groups them."""
+    n = 2 * U
+    if kind in ("fused", "red"):
+        return lambda k: k == f"k_step_fused<{U}, true>"
+    if kind == "direct":
+        return lambda k: k.startswith("k_direct_tile")
+    if kind == "fft_lds":
+        return lambda k: k.startswith(f"k_fft_tile<{n},")
+    if kind == "fft_cm":
+        tile = "k_cm_tile2<" if n == 32768 else f"k_cm_tile<{n}>"
+        return lambda k: k.startswith(tile) or k.startswith(("k_cm_yin", "k_cm_merge"))
+    if kind == "fft_col":
+        tile = "k_fft_coltile2" if n == 32768 else f"k_fft_coltile<{n}>"
+        return lambda k: k.startswith((tile, "k_rows_to_cols", "k_cols_to_rows"))
+    if kind == "fft_hbm":
+        return lambda k: k.startswith(("k_fft_rows_fwd", "k_fft_mid_tile", "k_fft_rows_inv"))
+    return lambda k: False
+
+
+def committed_counters(kernel, U, w):
+    """Derived-counter means of the dispatches of one (kernel, U) launch from
+    the committed counter profile, if it was taken on the current kernel
+    sources and this workload; else None."""
+    try:
+        with open(os.path.join(ROOT, "profiles", "counters.json")) as f:
+            data = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if data.get("source_digest") != source_digest():
+        return None
+    table = data.get("workloads", {}).get(w.name)
+    if not table:
+        return None
+    keep = group_kernels(kernel, U)
+    got = {k: v for k, v in table.items() if keep(k)}
+    return {"source": f"profiles/counters_{w.name}.txt", "kernels": got} if got else None
 
 
 def sweep_summary(args):
@@ -579,6 +635,10 @@ def main():
         # graph-replayed launch is bound by the launch, not by HBM
         if roofline["avg_launch_us"] < 2.0 * floor_us:
             roofline["bound"] = "launch"
+        # what the hardware counters say about those dispatches (vector-ALU
+        # and matrix-core busy, occupancy), when taken on these sources
+        kname, kU = roofline["kernel"].split(" U=")
+        roofline["counters"] = committed_counters(kname, int(kU), w)
 
     def release():
         # each leg's contexts hold tens of GB; give torch's cached blocks back

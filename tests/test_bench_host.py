@@ -141,3 +141,18 @@ def test_more_than_one_gpu_is_refused():
     assert r.returncode == 2
     assert "one GPU" in r.stderr
     assert r.stdout == ""
+
+
+def test_group_kernels_picks_the_dispatches_of_one_launch():
+    """The counter evidence quoted beside the roofline covers exactly the
+    dispatches one launch of (kind, U) is made of."""
+    g = bench.group_kernels("fft_cm", 1024)
+    assert g("k_cm_tile<2048>") and g("k_cm_yin4") and g("k_cm_merge4<true>") and g("k_cm_yin")
+    assert not g("k_cm_tile<4096>") and not g("k_fft_tile<2048, true, true, false, 8>")
+    assert bench.group_kernels("fft_cm", 16384)("k_cm_tile2<16384, 0>")
+    g = bench.group_kernels("fft_lds", 512)
+    assert g("k_fft_tile<1024, true, true, false, 8>") and not g("k_fft_tile<128, true, true, false, 8>")
+    g = bench.group_kernels("fused", 1)
+    assert g("k_step_fused<1, true>") and not g("k_step_fused<16, true>")
+    g = bench.group_kernels("fft_hbm", 32768)
+    assert g("k_fft_rows_fwd<1024, false>") and g("k_fft_mid_tile<16>") and not g("k_cm_yin4")
