@@ -449,6 +449,17 @@ __device__ __forceinline__ void cm_cols(int p, bool bpair, int D, int BD, int& a
   }
 }
 
+// Stored pair of the r-th workgroup of a layer in the mirrored tiles: with
+// batch pairs, the B/2 pairs of one channel (stored D apart) run on
+// consecutive workgroups, so they read that channel's filter spectrum while
+// it is in their XCD's L2; adjacent-column pairs keep their order.
+__device__ __forceinline__ int cm_pair_of(int r, bool bpair, int PC, int D) {
+  if (!bpair) return r;
+  const int h = PC / D;  // batch pairs per channel
+  const int d = r / h;
+  return (r - d * h) * D + d;
+}
+
 constexpr int kCmT = 64;  // transpose tile: 64 pairs x 64 positions
 
 // C[m][p][t] = (S[m][t][a], S[m][t][b]) for t in [row0, row1).  Grid (pair
@@ -728,7 +739,7 @@ __global__ __launch_bounds__(ColCfg<N>::NT, ColCfg<N>::MINB) void k_cm_tile(
     twz = TW{twl, twl + N / 64};
   }
   const int g = fft::xcd_logical((int)blockIdx.x, (int)gridDim.x);
-  const int m = g / PC, p = g - m * PC;
+  const int m = g / PC, p = cm_pair_of(g - m * PC, bpair != 0, PC, D);
   int a, b;
   cm_cols(p, bpair != 0, D, BD, a, b);
   const bool one = bpair != 0;
@@ -777,7 +788,7 @@ __global__ __launch_bounds__(ColCfg<NS>::NT, ColCfg<NS>::MINB) void k_cm_tile2(
   auto w2u = [&](int mm) { return cmul(tw[N + (mm & (CC - 1))], tw[32 + mm / CC]); };
   const int gl = fft::xcd_logical((int)blockIdx.x, (int)gridDim.x);
   const int g = g0 + gl;
-  const int m = g / PC, p = g - m * PC;
+  const int m = g / PC, p = cm_pair_of(g - m * PC, bpair != 0, PC, D);
   int a, b;
   cm_cols(p, bpair != 0, D, BD, a, b);
   const bool hasb = b >= 0;
