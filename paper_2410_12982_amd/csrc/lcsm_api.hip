@@ -623,6 +623,7 @@ int lcsm_run_noalloc(lcsm_ctx* c, int n, const float* y, size_t y_stride, float*
 struct lcsm_graph {
   lcsm_ctx* ctx;
   int n;
+  int mirrored;  // the context's mirrored positions after the recorded steps
   std::vector<hipGraph_t> graphs;
   std::vector<hipGraphExec_t> execs;
 };
@@ -693,6 +694,7 @@ int lcsm_graph_capture(lcsm_ctx* c, int flags, int n, const float* in, size_t in
     (void)hipGetLastError();
     return fail(c, LCSM_EDEVICE, "graph capture", e);
   }
+  g->mirrored = c->mirrored;
   *out = g;
   return LCSM_OK;
 }
@@ -704,7 +706,10 @@ int lcsm_graph_launch(lcsm_graph* g) {
     const hipError_t e = hipGraphLaunch(ex, c->stream);
     if (e != hipSuccess) return fail(c, LCSM_EDEVICE, "graph launch", e);
   }
+  // the host-side bookkeeping of the recorded steps' end (the graphs begin
+  // with a reset, so nothing before the launch carries over)
   c->t = g->n;
+  c->mirrored = g->mirrored;
   c->layers_done = 0;
   c->faulted = false;
   return LCSM_OK;

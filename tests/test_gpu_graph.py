@@ -153,3 +153,41 @@ def test_capture_argument_errors():
     assert torch.equal(z, z_ref)
     g.close()
     ctx.close()
+
+
+def test_launch_after_host_steps_continues_correctly():
+    """A replay starts with a reset whatever the context did before: host
+    steps past the recorded length, then the replay, then host steps from
+    there must equal an all-host run (the mirror's copy bookkeeping follows
+    the replay, not the host steps before it)."""
+    M, B, D, L = 2, 4, 48, 2048
+    w = datagen.Workload("graphm", M, B, D, L, decay=L / 4, seed=17)
+    opts = {"direct_max_u": 4, "col_fft_min_n": 16}   # mirrored tiles from U = 8
+    lcsm = lcsm_mod()
+    assert lcsm.plan_tile(M, B, D, L, 7, opts)[3] == lcsm.TILE_FFT_CM
+    say(f"[graph launch after host steps] M={M} B={B} D={D} L={L} opts={opts}")
+    y = datagen.y_torch(w, dev())
+    ctx = _ctx(w, opts)
+    z_ref = torch.empty_like(y)
+    with torch.cuda.stream(ctx.stream):
+        ctx.reset()
+        for t in range(L):
+            ctx.step(y[t], z_ref[t])
+    torch.cuda.synchronize()
+    n = 600
+    z = torch.full_like(y, float("nan"))
+    g = ctx.capture(y, z, n=n, seg=256)
+    with torch.cuda.stream(ctx.stream):
+        ctx.reset()
+        scratch = torch.empty_like(y[0])
+        for t in range(1500):                    # well past n, across mirror boundaries
+            ctx.step(y[t], scratch)
+    g.launch()
+    assert ctx.position == n
+    with torch.cuda.stream(ctx.stream):
+        for t in range(n, L):
+            ctx.step(y[t], z[t])
+    torch.cuda.synchronize()
+    assert torch.equal(z, z_ref)
+    g.close()
+    ctx.close()
