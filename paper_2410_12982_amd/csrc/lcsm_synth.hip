@@ -13,14 +13,17 @@
 //   the gray tiles of i = t+1 for all layers (the mixer's batched launch).
 //
 // The products are matrix-vector products over B <= 16 rows at a time: their
-// time is the weight read (4 bytes per weight, 2B flops), so they run on the
-// vector ALUs with coalesced weight rows, not on the matrix cores.  They are
+// time is the weight read (4 bytes per weight, 2B flops).  Small ones are
 // bound by how many loads are in flight, not by bytes: a workgroup takes one
 // output unit and splits its weight row over K/256 waves, one 1 KB piece per
 // wave (its 64 lanes in 16-byte parts), multiplied with the same pieces of
 // the B input rows; each wave reduces with butterfly shuffles and wave 0 sums
 // the waves' partials from LDS in wave order (deterministic), after which
-// lane r stores row r.
+// lane r stores row r.  With 8 and more rows against large weight matrices
+// that form is bound by re-reading the input rows for every unit, and the
+// products take the matrix cores instead (k_gemm16: 16 units per
+// workgroup, the 16 x 16 block of rows and units accumulated in four
+// registers per lane), which read the inputs once per 16 units.
 #include <math.h>
 #include <stdio.h>
 #include <string.h>
@@ -122,6 +125,85 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(const float* __restric
   }
 }
 
+// The same product on the matrix cores, for several batch rows: a
+// workgroup takes 16 output units and splits K over its waves; each wave
+// accumulates the 16 x 16 block (rows x units) of its K-slice with
+// v_mfma_f32_16x16x4f32, 16 k per step (lane l loads 4 consecutive k of
+// unit n0 + l%16 and of row l%16 at offset 4 (l/16); the four products of a
+// step take the four components, the same k on both operands).  The input
+// rows are then read once per 16 units instead of once per unit, and no
+// lane reductions are needed.  The waves' blocks are summed from LDS in
+// wave order (deterministic), then the same epilogue as k_gemv.  Rows past
+// nrows and units past N load clamped rows and are not stored; K is a
+// multiple of 4.
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+template <int MODE>
+__global__ __launch_bounds__(kGemvMaxThreads) void k_gemm16(const float* __restrict__ x,
+                                                            const float* __restrict__ W,
+                                                            const float* __restrict__ bias,
+                                                            float* __restrict__ out, int N, int K,
+                                                            int nrows, RedNext rn) {
+  __shared__ float part[kGemvMaxThreads / 64][256];
+  const int lane = (int)threadIdx.x & 63, wv = (int)threadIdx.x >> 6;
+  const int nw = (int)blockDim.x >> 6;
+  const int n0 = (int)blockIdx.x * 16;
+  const int j = lane & 15, q = lane >> 4;
+  const int un = n0 + j < N ? n0 + j : N - 1;   // unit whose weights this lane loads
+  const int xr = j < nrows ? j : nrows - 1;     // batch row whose inputs this lane loads
+  const float* wrow = W + (size_t)un * K + 4 * q;
+  const float* xrow = x + (size_t)xr * K + 4 * q;
+  // the wave's k-blocks of 16: a contiguous range
+  const int nkb = (K + 15) / 16;
+  const int per = (nkb + nw - 1) / nw;
+  const int kb0 = wv * per, kb1 = kb0 + per < nkb ? kb0 + per : nkb;
+  v4f acc = {0.f, 0.f, 0.f, 0.f};
+  // four k-blocks' loads in flight, then their 16 products
+  for (int kb = kb0; kb < kb1; kb += 4) {
+    float4 wf[4], xf[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int k = 16 * (kb + u);
+      wf[u] = xf[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (kb + u < kb1 && k + 4 * q < K) {
+        wf[u] = *reinterpret_cast<const float4*>(wrow + k);
+        xf[u] = *reinterpret_cast<const float4*>(xrow + k);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(xf[u].x, wf[u].x, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(xf[u].y, wf[u].y, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(xf[u].z, wf[u].z, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(xf[u].w, wf[u].w, acc, 0, 0, 0);
+    }
+  }
+  // lane (jj + 16 g) holds rows 4g .. 4g+3 of unit column jj
+#pragma unroll
+  for (int v = 0; v < 4; ++v) part[wv][(4 * q + v) * 16 + j] = acc[v];
+  __syncthreads();
+  for (int o = (int)threadIdx.x; o < 256; o += (int)blockDim.x) {
+    const int r = o >> 4, n = n0 + (o & 15);
+    if (r >= nrows || n >= N) continue;
+    float sacc = 0.f;
+    for (int w = 0; w < nw; ++w) sacc += part[w][o];
+    const float sv = sacc + bias[n];
+    const size_t e = (size_t)r * N + n;
+    if constexpr (MODE == kUp) {
+      out[e] = gelu(sv);
+    } else {
+      out[e] = sv;
+      if (rn.S) {
+        float* slot = rn.S + e;
+        rn.z[e] = fmaf(rn.h0[n], sv, *slot);
+        *slot = sv;
+      } else {
+        rn.last[e] = sv;
+      }
+    }
+  }
+}
+
 // Sampler and layer 0's red cell at position t: y = eps (+ last for t > 0),
 // z = fmaf(h0[d], y, slot), slot = y.
 __global__ __launch_bounds__(256) void k_synth_red0(const float* __restrict__ eps,
@@ -136,9 +218,27 @@ __global__ __launch_bounds__(256) void k_synth_red0(const float* __restrict__ ep
   slot_row[c] = y;
 }
 
+// Which form a product takes.  The matrix-core form reads the input rows
+// once per 16 units, which pays where the per-unit form is bound by those
+// reads (8 and more rows against large weight matrices: 16 rows x 2048 x
+// 4096 ran 3.1x faster); on the latency-bound small products of 4 and 8 rows
+// x 768 it was 4-37 % slower (fewer waves in flight).
+inline bool gemm16_for(int N, int K, int nrows) {
+  return nrows >= 8 && (int64_t)N * K >= ((int64_t)1 << 22);
+}
+
 template <int MODE>
 hipError_t gemv(const float* x, const float* W, const float* bias, float* out, int N, int K,
                 int nrows, const RedNext& rn, hipStream_t st) {
+  if (gemm16_for(N, K, nrows)) {
+    // 16 units per workgroup, about four k-blocks of 16 per wave, at most 16 waves
+    int nw = (K + 63) / 64;
+    if (nw > kGemvMaxThreads / 64) nw = kGemvMaxThreads / 64;
+    if (nw < 1) nw = 1;
+    hipLaunchKernelGGL((k_gemm16<MODE>), dim3((unsigned)((N + 15) / 16)), dim3((unsigned)(64 * nw)),
+                       0, st, x, W, bias, out, N, K, nrows, rn);
+    return hipGetLastError();
+  }
   int wpu = (K + 255) / 256;  // waves per unit: one 256-float piece each
   if (wpu > kGemvMaxThreads / 64) wpu = kGemvMaxThreads / 64;
   const dim3 grid((unsigned)N), block((unsigned)(64 * wpu));

@@ -9,6 +9,8 @@ input rule, ``oracle.block.mlp_chain``), max|a_gpu - a_ref| <= 1e-4 *
 max|a_ref|; with blocks that are the identity, the same against the oracle's
 linear model; with half-state storage, bit for bit the full-state outputs.
 """
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -53,10 +55,12 @@ def _make(w, filters=None, weights=None, options=None):
 
 
 @pytest.mark.parametrize("shape", [(1, 1, 16, 1024), (2, 3, 16, 300), (3, 2, 40, 1000),
-                                   (2, 17, 8, 200), (1, 4, 64, 2048)])
+                                   (2, 17, 8, 200), (1, 4, 64, 2048), (2, 9, 1500, 64)])
 def test_synth_matches_oracle(shape):
     """Includes the 16-channel 1024-position workload's shape, a ragged batch
-    (17 rows: two product launches of 16 and 1) and every tile kind."""
+    (17 rows: two product launches of 16 and 1), every tile kind, and products
+    on the matrix cores with ragged blocks (9 of 16 rows; 3000 and 1500
+    units and inputs, neither a multiple of 16)."""
     M, B, D, L = shape
     say(f"[synth] M={M} B={B} D={D} L={L}")
     w = datagen.Workload("synth", M, B, D, L, decay=L / 5, seed=50 + M + B)
@@ -108,12 +112,18 @@ def test_synth_half_state_equals_full_state_and_reset_repeats():
     assert np.array_equal(a_half, _gpu_run(half, eps, L))
 
 
-@pytest.mark.parametrize("name,n", [("m1b8d768l8k", 1024), ("m18b4d768l32k", 128)])
+@pytest.mark.parametrize("name,n", [("m1b8d768l8k", 1024), ("m18b4d768l32k", 128),
+                                    ("m32b16d2048l16k", 16)])
 def test_synth_workload_width_prefix(name, n):
     """The workloads' full widths (768 channels, 8 and 4 batch rows, 1 and 18
-    layers) over the first n positions of the generation."""
+    layers; 2048 channels, 16 batch rows, 32 layers: full 16-row matrix-core
+    blocks) over the first n positions of the generation."""
     w = datagen.WORKLOADS[name]
-    say(f"[synth prefix] {name} positions={n}")
+    if w.M * w.B * w.D >= 1 << 19:
+        # the products' widths are what is checked; a short context keeps the
+        # mixer's state (and its column-major mirror) small
+        w = dataclasses.replace(w, L=256)
+    say(f"[synth prefix] {name} M={w.M} B={w.B} D={w.D} L={w.L} positions={n}")
     # the generator's torch view (bit-identical to its numpy view) draws the
     # 42M weights of 18 layers in seconds; the oracle gets the same values
     weights = datagen.mlp_weights_torch(w, dev())
