@@ -252,10 +252,10 @@ __global__ __launch_bounds__(kThreads) void k_dd_direct_u(float* __restrict__ Y,
 // NT threads.
 template <int N>
 struct DdCfg {
-  static constexpr int CW = N <= 2048 ? 8 : (N <= 4096 ? 4 : 2);
+  static constexpr int CW = N <= 1024 ? 16 : (N <= 2048 ? 8 : (N <= 4096 ? 4 : 2));
   // at most 512 threads: the spectra held across the second transform need
   // more than the 128 registers a 1024-thread workgroup leaves
-  static constexpr int NT = N <= 128 ? 64 : (N <= 256 ? 128 : (N <= 512 ? 256 : 512));
+  static constexpr int NT = N <= 64 ? 64 : (N <= 128 ? 128 : (N <= 256 ? 256 : 512));
   static constexpr bool TWL = (size_t)N * 8 * (CW + 1) <= 163840;
   static constexpr bool TWH = !TWL && (size_t)N * 8 * CW + (size_t)N * 4 <= 163840;
   static constexpr int TWN = TWL ? N : (TWH ? N / 2 : 1);
