@@ -126,7 +126,9 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(const float* __restric
 }
 
 // The same product on the matrix cores, for several batch rows: a
-// workgroup takes 16 output units and splits K over its waves; each wave
+// workgroup takes 16 output units (or 8, with the block's other 8 columns
+// repeating them, where 16 would leave compute units idle) and splits K over
+// its waves; each wave
 // accumulates the 16 x 16 block (rows x units) of its K-slice with
 // v_mfma_f32_16x16x4f32, 16 k per step (lane l loads 4 consecutive k of
 // unit n0 + l%16 and of row l%16 at offset 4 (l/16); the four products of a
@@ -143,13 +145,14 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemm16(const float* __restr
                                                             const float* __restrict__ W,
                                                             const float* __restrict__ bias,
                                                             float* __restrict__ out, int N, int K,
-                                                            int nrows, RedNext rn) {
+                                                            int nrows, int ut, RedNext rn) {
   __shared__ float part[kGemvMaxThreads / 64][256];
   const int lane = (int)threadIdx.x & 63, wv = (int)threadIdx.x >> 6;
   const int nw = (int)blockDim.x >> 6;
-  const int n0 = (int)blockIdx.x * 16;
+  const int n0 = (int)blockIdx.x * ut;  // ut = 16 units per workgroup, or 8 (columns 8..15 repeat them)
   const int j = lane & 15, q = lane >> 4;
-  const int un = n0 + j < N ? n0 + j : N - 1;   // unit whose weights this lane loads
+  const int ju = j < ut ? j : j - ut;
+  const int un = n0 + ju < N ? n0 + ju : N - 1;  // unit whose weights this lane loads
   const int xr = j < nrows ? j : nrows - 1;     // batch row whose inputs this lane loads
   const float* wrow = W + (size_t)un * K + 4 * q;
   const float* xrow = x + (size_t)xr * K + 4 * q;
@@ -184,7 +187,7 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemm16(const float* __restr
   __syncthreads();
   for (int o = (int)threadIdx.x; o < 256; o += (int)blockDim.x) {
     const int r = o >> 4, n = n0 + (o & 15);
-    if (r >= nrows || n >= N) continue;
+    if (r >= nrows || (o & 15) >= ut || n >= N) continue;
     float sacc = 0.f;
     for (int w = 0; w < nw; ++w) sacc += part[w][o];
     const float sv = sacc + bias[n];
@@ -235,8 +238,11 @@ hipError_t gemv(const float* x, const float* W, const float* bias, float* out, i
     int nw = (K + 63) / 64;
     if (nw > kGemvMaxThreads / 64) nw = kGemvMaxThreads / 64;
     if (nw < 1) nw = 1;
-    hipLaunchKernelGGL((k_gemm16<MODE>), dim3((unsigned)((N + 15) / 16)), dim3((unsigned)(64 * nw)),
-                       0, st, x, W, bias, out, N, K, nrows, rn);
+    // 8 units per workgroup where 16 would leave CUs idle (the column blocks
+    // 8..15 then repeat units 0..7 and are not stored)
+    const int ut = (N + 15) / 16 >= 256 ? 16 : 8;
+    hipLaunchKernelGGL((k_gemm16<MODE>), dim3((unsigned)((N + ut - 1) / ut)),
+                       dim3((unsigned)(64 * nw)), 0, st, x, W, bias, out, N, K, nrows, ut, rn);
     return hipGetLastError();
   }
   int wpu = (K + 255) / 256;  // waves per unit: one 256-float piece each
