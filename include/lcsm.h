@@ -198,6 +198,21 @@ int lcsm_commit(lcsm_ctx* ctx);
  * Errors as lcsm_step; stops at the first. */
 int lcsm_run(lcsm_ctx* ctx, int n, const float* y, size_t y_stride, float* z, size_t z_stride);
 
+/* n consecutive lcsm_step_chain calls (the workloads' closed loop, Alg. 3's
+ * loop over positions with the built-in elementwise chain as its blocks and
+ * sampler): step k reads x + k*x_stride and writes z + k*z_stride (device
+ * pointers, strides in floats); the results equal those of the loop of
+ * single steps bit for bit.  The chain couples the layers of one (b, d)
+ * column only, and a direct tile of U <= 16 that starts inside an aligned
+ * block of 32 positions reads and writes rows of that block only; so with
+ * full-state storage, at most 30 layers and at most 8192 columns per layer
+ * (B*D), every stretch of such positions runs as one launch that keeps each
+ * column's block rows in registers, and only the larger tiles are launched
+ * on their own.  Other shapes take one position at a time.  Errors as
+ * lcsm_step_chain; stops at the first. */
+int lcsm_run_chain(lcsm_ctx* ctx, int n, const float* x, size_t x_stride, float* z,
+                   size_t z_stride);
+
 /* lcsm_run for callers that cannot allocate device memory (code under HIP
  * graph capture, serving loops or harnesses that forbid hipMalloc): the same
  * n steps, arguments, results (to fp32 rounding) and errors as lcsm_run,
@@ -228,8 +243,9 @@ int lcsm_run_noalloc(lcsm_ctx* ctx, int n, const float* y, size_t y_stride, floa
  * and writes
  *   z + (k mod z_ring) * z_stride         (device, [M][B][D] fp32),
  * strides in floats; in_ring / z_ring = 0 mean n (no wrap-around).  flags = 0
- * records lcsm_step (in = y_t); flags = LCSM_GRAPH_CHAIN records
- * lcsm_step_chain (in = x_t, the built-in tanh chain).  seg_positions = 0
+ * records lcsm_step (in = y_t); flags = LCSM_GRAPH_CHAIN records the chained
+ * steps as lcsm_run_chain runs them (in = x_t, the built-in tanh chain; the
+ * same results as lcsm_step_chain).  seg_positions = 0
  * selects LCSM_GRAPH_DEFAULT_SEG; at most LCSM_GRAPH_MAX_SEG.
  * Nothing runs on the device during the call; the context's stream must be
  * a created stream (not the null stream) that is not capturing, and the

@@ -431,6 +431,67 @@ int step_common(lcsm_ctx* c, const float* in, float* z, bool chain) {
   return LCSM_OK;
 }
 
+// n chained steps (as n calls of lcsm_step_chain, the same results bit for
+// bit).  Where the shape allows (chain_block_fits), each stretch of
+// positions inside one aligned block of kChainBlockW whose gray tiles are
+// direct with U <= kChainBlockW / 2 runs as one launch; the position that
+// ends a stretch has its FFT or larger tile launched as usual.  Otherwise
+// one position at a time.  Step k reads x slab (xs0 + k) mod xring and
+// writes z slab (zs0 + k) mod zring.
+bool chain_block_fits(const lcsm_ctx* c) {
+  const long long groups = ((long long)c->s.BD + lcsm::kChainBlockCols - 1) / lcsm::kChainBlockCols;
+  return !c->T && c->s.M <= lcsm::kChainBlockMaxM && groups <= lcsm::kChainBlockMaxGroups;
+}
+
+int chain_run(lcsm_ctx* c, int n, const float* x, size_t xst, int xring, int xs0, float* z,
+              size_t zst, int zring, int zs0) {
+  if (!c) return LCSM_EINVAL;
+  if (!x || !z) return fail(c, LCSM_EINVAL, "null input or output pointer", hipSuccess);
+  if (c->faulted) return LCSM_ESTATE;
+  if (c->layers_done != 0) return fail(c, LCSM_ESTATE, "step during a per-layer position", hipSuccess);
+  const bool block = chain_block_fits(c);
+  constexpr int W = lcsm::kChainBlockW;
+  int k = 0;
+  while (k < n) {
+    if (c->t >= c->s.L) return LCSM_EDONE;
+    if (!block) {
+      const int r = step_common(c, x + (size_t)((xs0 + k) % xring) * xst,
+                                z + (size_t)((zs0 + k) % zring) * zst, true);
+      if (r) return r;
+      ++k;
+      continue;
+    }
+    // the stretch: positions t0 .. t1-1, ending at the block's end, the end
+    // of the run, or the first position whose tile is not a small direct one
+    const int t0 = c->t;
+    const int bend = (t0 & ~(W - 1)) + W;
+    int t1 = t0;
+    bool tile_last = true;
+    while (t1 < c->s.L && t1 < bend && t1 - t0 < n - k) {
+      const int i = ++t1;  // the tile after position t1 - 1
+      if (i >= c->s.L) break;
+      const int U = lowbit(i);
+      if (2 * U >= W || tile_kind(c->opt, c->s, U) != LCSM_TILE_DIRECT) {
+        tile_last = false;
+        break;
+      }
+    }
+    hipError_t e = lcsm::launch_chain_block(x, xst, xring, (xs0 + k) % xring, z, zst, zring,
+                                            (zs0 + k) % zring, c->S, c->Hf, c->prev, c->s, t0, t1,
+                                            tile_last, c->stream);
+    if (e != hipSuccess) return fail(c, LCSM_EDEVICE, "chained-steps launch", e);
+    if (!tile_last) {
+      const int i = t1, U = lowbit(i);
+      const int dst_len = U < c->s.L - i ? U : c->s.L - i;
+      e = launch_tile(c, i, U, dst_len);
+      if (e != hipSuccess) return fail(c, LCSM_EDEVICE, "gray-tile launch", e);
+    }
+    k += t1 - t0;
+    c->t = t1;
+  }
+  return LCSM_OK;
+}
+
 }  // namespace
 
 namespace lcsm {
@@ -588,6 +649,13 @@ int lcsm_run(lcsm_ctx* c, int n, const float* y, size_t y_stride, float* z, size
   return LCSM_OK;
 }
 
+int lcsm_run_chain(lcsm_ctx* c, int n, const float* x, size_t x_stride, float* z, size_t z_stride) {
+  if (!c) return LCSM_EINVAL;
+  if (n < 0) return fail(c, LCSM_EINVAL, "negative step count", hipSuccess);
+  if (n == 0) return LCSM_OK;
+  return chain_run(c, n, x, x_stride, n, 0, z, z_stride, n, 0);
+}
+
 int lcsm_run_noalloc(lcsm_ctx* c, int n, const float* y, size_t y_stride, float* z,
                      size_t z_stride) {
   if (!c) return LCSM_EINVAL;
@@ -676,8 +744,12 @@ int lcsm_graph_capture(lcsm_ctx* c, int flags, int n, const float* in, size_t in
     if (e != hipSuccess) break;
     int r = LCSM_OK;
     if (p0 == 0) r = lcsm_reset(c);
-    for (int t = p0; r == LCSM_OK && t < p1; ++t)
-      r = step_common(c, in + (size_t)(t % ir) * in_stride, z + (size_t)(t % zr) * z_stride, chain);
+    if (chain) {
+      if (r == LCSM_OK) r = chain_run(c, p1 - p0, in, in_stride, ir, p0 % ir, z, z_stride, zr, p0 % zr);
+    } else {
+      for (int t = p0; r == LCSM_OK && t < p1; ++t)
+        r = step_common(c, in + (size_t)(t % ir) * in_stride, z + (size_t)(t % zr) * z_stride, false);
+    }
     hipGraph_t gr = nullptr;
     e = hipStreamEndCapture(c->stream, &gr);
     if (gr) g->graphs.push_back(gr);

@@ -14,6 +14,9 @@
 //
 // Gray tile (Eq. taus) for i = t+1, side U: for j < dst_len,
 //   S[i+j] += sum_{k<U} y[i-U+k] * h[U+j-k]     (lags 1..2U-1).
+#include <type_traits>
+#include <utility>
+
 #include "lcsm_internal.h"
 
 namespace lcsm {
@@ -226,6 +229,149 @@ __global__ __launch_bounds__(kThreads) void k_chain_fused(const float* __restric
   prev[c] = zl;
 }
 
+// The chained steps (lcsm_step_chain) of the positions [t0, t1) of one
+// aligned block of kChainBlockW positions (b = t0 rounded down to it), in
+// one launch, when every gray tile of the stretch is direct with
+// U <= kChainBlockW / 2 (the tile of the last position only when
+// tile_last).  Such a tile, of i = b + r + 1 with r + 1 < kChainBlockW,
+// reads y rows [i - U, i) and adds into rows [i, i + U), all inside
+// [b, b + kChainBlockW): the block's rows of a column stay in that column's
+// registers from the first position to the last, and no position of the
+// stretch moves a tile's operands through memory.
+//
+// A workgroup owns kChainBlockCols (b, d) columns of every layer.  Wave 0
+// walks the chain through the layers (y^m_t, z^m_t as k_chain_fused) on its
+// first kChainBlockCols lanes; wave w >= 1 holds layers 2(w-1) and
+// 2(w-1)+1, one per half.  Each lane of a layer wave keeps v[k] = state row
+// b + k of its column (y for positions already taken, the accumulator
+// otherwise) and the lags 1 .. kChainBlockW - 1 of its channel.  Per
+// position t = b + r: the layer waves hand acc_t and x_t over in LDS
+// (fetching x_{t+1}); wave 0 computes the chain and stores z_t and y_t; the
+// layer waves take y_t from LDS and do the tile of i = t+1 in registers,
+// with the arithmetic of k_step_fused<U, false> (per output, the fmaf chain
+// over the U inputs in increasing order, then added to the accumulator), so
+// the results equal the per-position steps bit for bit.  The two barriers
+// per position order LDS only: no wave reads global memory another wave of
+// the launch writes.  At the end the accumulator rows at and after t1 (a
+// stretch cut before its block ends) go back to the state.
+// f(std::integral_constant<int, 0>{}), ..., f(std::integral_constant<int, N-1>{}).
+template <class F, int... R>
+__device__ __forceinline__ void static_for_impl(F& f, std::integer_sequence<int, R...>) {
+  (f(std::integral_constant<int, R>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void static_for(F& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+__device__ __forceinline__ void chain_block_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// The tile of i = b + r + 1 (U = lowbit(r + 1)) on the register rows v.
+template <int R>
+__device__ __forceinline__ void chain_block_tile(float (&v)[kChainBlockW], const float (&hh)[kChainBlockW],
+                                                 int dst_len) {
+  constexpr int U = (R + 1) & -(R + 1);
+#pragma unroll
+  for (int j = 0; j < U; ++j) {
+    if (j < dst_len) {
+      float o = 0.f;
+#pragma unroll
+      for (int k = 0; k < U; ++k) o = fmaf(v[R + 1 - U + k], hh[U + j - k], o);
+      v[R + 1 + j] = v[R + 1 + j] + o;
+    }
+  }
+}
+
+__global__ __launch_bounds__(64 * (1 + (kChainBlockMaxM + 1) / 2)) void k_chain_block(
+    const float* __restrict__ x, size_t xst, int xring, int xs0, float* __restrict__ z,
+    size_t zst, int zring, int zs0, float* __restrict__ S, const float* __restrict__ Hf,
+    float* __restrict__ prev, int M, int L, int SL, int BD, int D, int t0, int t1,
+    int tile_last) {
+  constexpr int NC = kChainBlockCols, W = kChainBlockW;
+  __shared__ float xbuf[kChainBlockMaxM][NC];
+  __shared__ float abuf[kChainBlockMaxM][NC];
+  __shared__ float ybuf[kChainBlockMaxM][NC];
+  __shared__ float h0buf[kChainBlockMaxM][NC];
+  const int lane = (int)threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+  const int col = lane & (NC - 1);
+  const int c = (int)blockIdx.x * NC + col;
+  const bool live = c < BD;
+  const int cc = live ? c : BD - 1;
+  const int d = cc % D;
+  const size_t rs = (size_t)BD;
+  const int b = t0 & ~(W - 1);
+  const int r0 = t0 - b, r1 = t1 - b;
+  const int m = 2 * (wv - 1) + (lane >> 5);
+  const bool has = wv > 0 && m < M;
+  const int mc = has ? m : 0;
+  float* Sc = S + (size_t)mc * SL * BD + cc;
+  const float* hc = Hf + (size_t)mc * L * D + d;
+  const size_t xoff = (size_t)mc * BD + cc;
+  float v[W], hh[W];
+  float xn = 0.f;
+  if (has) {
+#pragma unroll
+    for (int k = 0; k < W; ++k) v[k] = Sc[(size_t)(b + k < L ? b + k : L - 1) * rs];
+    hh[0] = 0.f;
+#pragma unroll
+    for (int l = 1; l < W; ++l) {
+      const float hv = hc[(size_t)(l < L ? l : L - 1) * D];
+      hh[l] = l < L ? hv : 0.f;
+    }
+    h0buf[m][col] = hc[0];
+    xn = x[(size_t)(xs0 % xring) * xst + xoff];
+  } else {
+#pragma unroll
+    for (int k = 0; k < W; ++k) v[k] = hh[k] = 0.f;
+  }
+  float zl = 0.f;  // chain wave: z^{M-1}_{t-1}, then z^{m-1}_t
+  if (wv == 0) zl = prev[cc];  // unused at t = 0
+  auto position = [&](auto rc) {
+    constexpr int r = decltype(rc)::value;
+    if (r < r0 || r >= r1) return;
+    const int t = b + r;
+    if (has) {
+      abuf[m][col] = v[r];
+      xbuf[m][col] = xn;
+      if (r + 1 < r1) xn = x[(size_t)((xs0 + t + 1 - t0) % xring) * xst + xoff];
+    }
+    chain_block_sync();
+    if (wv == 0 && lane < NC) {
+      float* zt = z + (size_t)((zs0 + t - t0) % zring) * zst;
+      for (int q = 0; q < M; ++q) {
+        const float xv = xbuf[q][col];
+        const float yv = (q == 0 && t == 0) ? xv : fmaf(0.5f, tanhf(zl), xv);
+        const float zv = fmaf(h0buf[q][col], yv, abuf[q][col]);
+        if (live) {
+          zt[(size_t)q * BD + c] = zv;
+          S[(size_t)q * SL * BD + (size_t)t * rs + c] = yv;
+        }
+        ybuf[q][col] = yv;
+        zl = zv;
+      }
+    }
+    chain_block_sync();
+    if (has) {
+      v[r] = ybuf[m][col];
+      if constexpr (r + 1 < W) {
+        if (t + 1 < L && (r + 1 < r1 || tile_last)) chain_block_tile<r>(v, hh, L - (t + 1));
+      }
+    }
+  };
+  static_for<W>(position);
+  if (wv == 0 && lane < NC && live && r1 > r0) prev[c] = zl;
+  if (has && live) {
+#pragma unroll
+    for (int k = 0; k < W; ++k)
+      if (k >= r1 && b + k < L) Sc[(size_t)(b + k) * rs] = v[k];
+  }
+}
+
 // Red cell of one layer.
 __global__ __launch_bounds__(kThreads) void k_red_layer(const float* __restrict__ y,
                                                        float* __restrict__ z,
@@ -427,6 +573,19 @@ hipError_t launch_chain_fused(const float* x, float* z, float* S, const float* H
   }
 #undef LCSM_CHAIN_CASE
 #undef LCSM_CHAIN_K
+  return hipGetLastError();
+}
+
+hipError_t launch_chain_block(const float* x, size_t xst, int xring, int xs0, float* z,
+                              size_t zst, int zring, int zs0, float* S, const float* Hf,
+                              float* prev, const Shape& s, int t0, int t1, bool tile_last,
+                              hipStream_t st) {
+  if (s.M > kChainBlockMaxM || t1 <= t0 || (t0 & ~(kChainBlockW - 1)) != ((t1 - 1) & ~(kChainBlockW - 1)))
+    return hipErrorInvalidValue;
+  const int nw = 1 + (s.M + 1) / 2;
+  hipLaunchKernelGGL(k_chain_block, dim3((unsigned)((s.BD + kChainBlockCols - 1) / kChainBlockCols)),
+                     dim3((unsigned)(64 * nw)), 0, st, x, xst, xring, xs0, z, zst, zring, zs0, S, Hf,
+                     prev, s.M, s.L, s.SL, s.BD, s.D, t0, t1, tile_last ? 1 : 0);
   return hipGetLastError();
 }
 

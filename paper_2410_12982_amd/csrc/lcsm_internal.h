@@ -50,6 +50,24 @@ hipError_t launch_step_fused(const float* y, float* z, float* S, const float* Hf
 hipError_t launch_chain_fused(const float* x, float* z, float* S, const float* Hf, float* prev,
                               const Shape& s, int t, int U, int dst_len, hipStream_t st);
 
+// The chained steps of positions [t0, t1) in one launch, for a stretch that
+// lies inside one aligned block of kChainBlockW positions and whose gray
+// tiles are direct with U <= kChainBlockW / 2 (the last position's tile only
+// when tile_last).  Position t reads x slab (xs0 + t - t0) mod xring and
+// writes z slab (zs0 + t - t0) mod zring.  Full-state contexts with at most
+// kChainBlockMaxM layers; a workgroup takes kChainBlockCols columns of every
+// layer, and the launch is used while the columns fill at most
+// kChainBlockMaxGroups workgroups (one per compute unit: beyond that, the
+// serial chain of each workgroup makes one launch per position faster).
+constexpr int kChainBlockW = 32;
+constexpr int kChainBlockMaxM = 30;
+constexpr int kChainBlockCols = 32;
+constexpr int kChainBlockMaxGroups = 256;
+hipError_t launch_chain_block(const float* x, size_t xst, int xring, int xs0, float* z,
+                              size_t zst, int zring, int zs0, float* S, const float* Hf,
+                              float* prev, const Shape& s, int t0, int t1, bool tile_last,
+                              hipStream_t st);
+
 // Red cell of one layer at position t.
 hipError_t launch_red_layer(const float* y, float* z, float* S, const float* Hf, const Shape& s,
                             int layer, int t, hipStream_t st);

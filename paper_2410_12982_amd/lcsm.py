@@ -78,6 +78,7 @@ _SIGS = {
     "lcsm_advance": (ctypes.c_int, [_vp]),
     "lcsm_run": (ctypes.c_int, [_vp, ctypes.c_int, _vp, ctypes.c_size_t, _vp, ctypes.c_size_t]),
     "lcsm_run_noalloc": (ctypes.c_int, [_vp, ctypes.c_int, _vp, ctypes.c_size_t, _vp, ctypes.c_size_t]),
+    "lcsm_run_chain": (ctypes.c_int, [_vp, ctypes.c_int, _vp, ctypes.c_size_t, _vp, ctypes.c_size_t]),
     "lcsm_prefill": (ctypes.c_int, [_vp, ctypes.c_int, _vp, ctypes.c_size_t, _vp, ctypes.c_size_t]),
     "lcsm_reset": (ctypes.c_int, [_vp]),
     "lcsm_position": (ctypes.c_int, [_vp, _c_int_p]),
@@ -287,6 +288,20 @@ class Lcsm:
         _after_current(self.stream, self.device)
         self._check(_lib.lcsm_run(self._ctx, int(n), y.data_ptr(), slab, z.data_ptr(), slab),
                     "lcsm_run")
+        return z
+
+    def run_chain(self, x, z, n=None):
+        """n chained steps (lcsm_run_chain) reading x[k] and writing z[k] ([n, M, B, D])."""
+        shape = (self.M, self.B, self.D)
+        n = x.shape[0] if n is None else n
+        if x.shape[1:] != shape or z.shape[1:] != shape or x.shape[0] < n or z.shape[0] < n:
+            raise ValueError("x and z must be [n, M, B, D]")
+        if not (x.is_contiguous() and z.is_contiguous() and x.is_cuda and z.is_cuda):
+            raise ValueError("x and z must be contiguous CUDA tensors")
+        slab = self.M * self.B * self.D
+        _after_current(self.stream, self.device)
+        self._check(_lib.lcsm_run_chain(self._ctx, int(n), x.data_ptr(), slab, z.data_ptr(), slab),
+                    "lcsm_run_chain")
         return z
 
     def prefill(self, y, z, P=None):
