@@ -471,7 +471,7 @@ int chain_run(lcsm_ctx* c, int n, const float* x, size_t xst, int xring, int xs0
       const int i = ++t1;  // the tile after position t1 - 1
       if (i >= c->s.L) break;
       const int U = lowbit(i);
-      if (2 * U >= W || tile_kind(c->opt, c->s, U) != LCSM_TILE_DIRECT) {
+      if (U > W / 2 || tile_kind(c->opt, c->s, U) != LCSM_TILE_DIRECT) {
         tile_last = false;
         break;
       }
