@@ -129,6 +129,11 @@ def parse():
     p.add_argument("--copy-scalar", action="store_true",
                    help="copy probe with 4-byte accesses per lane (a one-element offset keeps torch "
                         "from vectorising) instead of 16-byte vector accesses")
+    p.add_argument("--closed-loop-once", action="store_true",
+                   help="one graph-replayed closed-loop generation with progress lines (the dispatches a "
+                        "kernel trace of the closed loop should see); no timing and no metric")
+    p.add_argument("--trace-name", default="kernels",
+                   help="--trace-from writes profiles/<name>_<workload>.txt")
     p.add_argument("--positions", type=int, default=0, metavar="P",
                    help="only run the first P positions of one generation from the host, printing "
                         "progress (for counter runs: few dispatches); prints no metric")
@@ -300,7 +305,7 @@ def trace_summary(args):
     per-launch pass (a column tile = its red cell + every chunk's dispatches;
     a mirrored tile = its red cell, the mirror copies and the transform),
     with algorithmic GB/s and the fraction of 8 TB/s; then the kernels with
-    the most time.  Written to profiles/kernels_<workload>.txt."""
+    the most time.  Written to profiles/<trace name>_<workload>.txt."""
     import collections
     import csv
     import glob
@@ -337,6 +342,12 @@ def trace_summary(args):
     for k, v in sorted(agg.items(), key=lambda kv: -sum(kv[1]))[:30]:
         lines.append(f"{len(v):9d} {sum(v) / 1e3:12.2f} {sum(v) / len(v):10.2f} "
                      f"{100 * sum(v) / total:6.2f}  {k}")
+    blk = agg.get("k_chain_block")
+    if blk:
+        lines.append(f"# chained-step block launches (the closed loop's positions inside blocks of 32): "
+                     f"{len(blk)} launches, {sum(blk) / len(blk):.2f} us each on average; with one "
+                     f"generation in the command, {w.L / len(blk):.2f} positions per launch and "
+                     f"{sum(blk) / w.L:.3f} us of block launch per position")
     for b in (x for x in args.bracket.split(",") if x):
         with open(b) as f:
             d = json.loads(f.read().strip().splitlines()[-1])
@@ -347,7 +358,7 @@ def trace_summary(args):
                 lines.append(f"#   {key:18s} {v['avg_us']:10.2f} us  {v['GB_s']} GB/s")
     prof = os.path.join(ROOT, "profiles")
     os.makedirs(prof, exist_ok=True)
-    with open(os.path.join(prof, f"kernels_{w.name}.txt"), "w") as f:
+    with open(os.path.join(prof, f"{args.trace_name}_{w.name}.txt"), "w") as f:
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
 
@@ -604,6 +615,9 @@ def main():
     if args.positions:
         counter_run(args, w, torch, datagen, lcsm)
         return
+    if args.closed_loop_once:
+        closed_loop_once(args, w, torch, datagen, lcsm)
+        return
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     opts = {k: v for k, v in (("direct_max_u", args.direct_max_u),
@@ -761,6 +775,38 @@ def counter_run(args, w, torch, datagen, lcsm):
             say(f"position {t + 1} of {P}")
     ctx.close()
     print(json.dumps({"counter_run": True, "workload": w.name, "positions": P}), flush=True)
+
+
+def closed_loop_once(args, w, torch, datagen, lcsm):
+    """One closed-loop generation as the closed-loop leg dispatches it
+    (recorded by the library as a chain of HIP graphs, then replayed once),
+    with a progress line after every phase.  No timing and no metric."""
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    def say(msg):
+        print(f"# {msg}", file=sys.stderr, flush=True)
+
+    say(f"closed-loop generation {w.name}")
+    filters = datagen.filters_torch(w, dev)
+    R = min(RING, w.L)
+    x = datagen.x_torch(w, dev, 0, R)
+    z = torch.empty_like(x)
+    stream = torch.cuda.Stream(dev)
+    torch.cuda.synchronize()
+    say("filters and input ring generated")
+    ctx = lcsm.Lcsm(filters, w.B, stream=stream)
+    torch.cuda.synchronize()
+    say("context initialised")
+    del filters
+    graph = ctx.capture(x, z, n=w.L, chain=True, seg=args.graph_seg)
+    say(f"generation recorded ({graph.segments} graphs)")
+    graph.launch()
+    torch.cuda.synchronize()
+    say("generation replayed")
+    graph.close()
+    ctx.close()
+    print(json.dumps({"closed_loop_once": True, "workload": w.name, "positions": w.L}), flush=True)
 
 
 def copy_probe(mib, torch, scalar=False):

@@ -156,3 +156,33 @@ def test_group_kernels_picks_the_dispatches_of_one_launch():
     assert g("k_step_fused<1, true>") and not g("k_step_fused<16, true>")
     g = bench.group_kernels("fft_hbm", 32768)
     assert g("k_fft_rows_fwd<1024, false>") and g("k_fft_mid_tile<16>") and not g("k_cm_yin4")
+
+
+def test_trace_summary_names_its_file_and_reports_block_launches(tmp_path, monkeypatch):
+    """A closed-loop trace is written under its own name, with the chained-step
+    block launches per launch and per position of the one generation."""
+    import types
+    csrc = os.path.join(ROOT, "paper_2410_12982_amd", "csrc")
+    fake = tmp_path / "paper_2410_12982_amd" / "csrc"
+    fake.mkdir(parents=True)
+    for f in bench.COUNTED_SOURCES:
+        with open(os.path.join(csrc, f), "rb") as src:
+            (fake / f).write_bytes(src.read())
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    tr = tmp_path / "trace"
+    tr.mkdir()
+    rows = ["Kernel_Name,Start_Timestamp,End_Timestamp"]
+    t = 1000
+    for us in (10, 12, 14):
+        rows.append(f'"lcsm::(anonymous namespace)::k_chain_block(float const*, int)",{t},{t + us * 1000}')
+        t += 100000
+    rows.append(f'"void lcsm::(anonymous namespace)::k_step_fused<32, false>(float const*)",{t},{t + 5000}')
+    (tr / "run_kernel_trace.csv").write_text("\n".join(rows) + "\n")
+    args = types.SimpleNamespace(trace_from=str(tr), workload="m1b1d16l1k", command="python3 bench.py",
+                                 bracket="", trace_name="closedloop")
+    bench.trace_summary(args)
+    out = (tmp_path / "profiles" / "closedloop_m1b1d16l1k.txt").read_text()
+    assert "3 launches, 12.00 us each" in out
+    assert f"{1024 / 3:.2f} positions per launch" in out
+    assert f"{36 / 1024:.3f} us of block launch per position" in out
+    assert not (tmp_path / "profiles" / "kernels_m1b1d16l1k.txt").exists()
