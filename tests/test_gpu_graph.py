@@ -65,24 +65,32 @@ def test_replay_equals_host_launches(shape, seg):
     ctx.close()
 
 
-@pytest.mark.parametrize("shape", [(1, 1, 16, 1024), (3, 2, 33, 300)])
-def test_replay_chain_equals_host_launches(shape):
+@pytest.mark.parametrize("shape,seg,ring", [((1, 1, 16, 1024), 128, 0), ((3, 2, 33, 300), 128, 0),
+                                            ((2, 2, 20, 700), 97, 48)])
+def test_replay_chain_equals_host_launches(shape, seg, ring):
+    """The recorded chained steps (the small steps of each 32-position block
+    in one launch) equal host-launched lcsm_step_chain bit for bit, on every
+    replay; with 97-position graphs and a 48-slab input and output ring the
+    graph boundaries and the ring's wrap fall inside blocks."""
     M, B, D, L = shape
-    say(f"[graph replay, chain] M={M} B={B} D={D} L={L}")
+    say(f"[graph replay, chain] M={M} B={B} D={D} L={L} seg={seg} ring={ring}")
     w = datagen.Workload("graphc", M, B, D, L, decay=200.0, seed=7)
-    x = datagen.x_torch(w, dev())
+    R = ring or L
+    x = datagen.x_torch(w, dev(), 0, R)
     ctx = _ctx(w)
     z_host = torch.empty_like(x)
     with torch.cuda.stream(ctx.stream):
         ctx.reset()
         for t in range(L):
-            ctx.step_chain(x[t], z_host[t])
+            ctx.step_chain(x[t % R], z_host[t % R])
     torch.cuda.synchronize()
     z = torch.full_like(x, float("nan"))
-    g = ctx.capture(x, z, chain=True, seg=128)
-    g.launch()
-    torch.cuda.synchronize()
-    assert torch.equal(z, z_host)
+    g = ctx.capture(x, z, n=L, chain=True, seg=seg)
+    for rep in range(2):
+        z.fill_(float("nan"))
+        g.launch()
+        torch.cuda.synchronize()
+        assert torch.equal(z, z_host), f"replay {rep} differs from host launches"
     g.close()
     ctx.close()
 
