@@ -154,3 +154,26 @@ def test_half_state_premise(L):
             assert s0 >= T and d0 >= T and d1 <= L
             assert d1 - T <= T             # rows p - T stay below T
     assert seen_swap
+
+
+@pytest.mark.parametrize("L", [64, 100, 1024, 4096 + 17])
+@pytest.mark.parametrize("W", [32])
+def test_small_tiles_stay_inside_their_block(L, W):
+    """The premise of running the positions of one aligned block of W
+    positions in one launch with the block's rows held in registers: in
+    every block [b, b + W), the tile of each step t except the block's last
+    has U <= W/2 and reads y and writes z only inside the block, and the
+    last step's tile (i = b + W) has U >= W; so a tile that reads or writes
+    a row of the block is either a small one of the block or a tile of
+    U >= W launched at a block boundary."""
+    for (i, U, s0, s1, d0, d1) in all_tiles(L):
+        t = i - 1
+        b = t - t % W
+        if i < b + W:
+            assert U <= W // 2
+            assert b <= s0 and s1 <= b + W and b <= d0 and d1 <= b + W
+        else:
+            assert i == b + W and U >= W and i % W == 0
+            # a large tile's inputs are whole earlier blocks, its outputs start
+            # at a block boundary
+            assert s0 % W == 0 and d0 % W == 0
