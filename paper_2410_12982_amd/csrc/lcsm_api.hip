@@ -401,12 +401,15 @@ int step_common(lcsm_ctx* c, const float* in, float* z, bool chain) {
   const int kind = tile_kind(c->opt, c->s, U);
   // the half-state swap tile runs on its own, after the red cells
   const bool swap = c->T && i == c->T;
-  // The chained step fuses its tiles only for a single layer: with several,
-  // the red cells run one thread per column through all layers, and the
-  // tiles go to the ordinary all-layer tile launch (parallel over layers).
-  const bool fuse = kind == LCSM_TILE_DIRECT && !swap &&
-                    (chain ? (U <= lcsm::kChainFusedMaxU && c->s.M <= lcsm::kChainFusedMaxM)
-                           : U <= lcsm::kFusedMaxU);
+  // The chained step fuses its tiles for a single layer; with several, the
+  // red cells run one thread per column through all layers, fusing only the
+  // U = 1 tile, and the other tiles go to the ordinary all-layer tile launch
+  // (parallel over layers).
+  const bool fuse =
+      kind == LCSM_TILE_DIRECT && !swap &&
+      (chain ? (U <= lcsm::kChainFusedMaxU &&
+                (c->s.M <= lcsm::kChainFusedMaxM || U <= lcsm::kChainFusedManyU))
+             : U <= lcsm::kFusedMaxU);
   float* S = state_base(c, t);
   hipError_t e;
   if (!chain && !swap && kind == LCSM_TILE_FFT && dst_len > 0 && 2 * U <= lcsm::kMaxRedFftN) {

@@ -30,11 +30,14 @@ struct Shape {
 
 // Largest tile side handled by the fused red+direct kernels, and by the
 // fused kernel of the built-in chain (one thread walks all layers there);
-// the chain fuses its tiles only up to kChainFusedMaxM layers (with more, the
-// all-layer tile launch runs them in parallel over layers).
+// the chain fuses its tiles up to kChainFusedMaxU only up to kChainFusedMaxM
+// layers, and with more layers only up to kChainFusedManyU (the U = 1 tile,
+// whose two operands per layer keep the all-layer walk bound by bandwidth;
+// larger ones go to the all-layer tile launch, parallel over layers).
 constexpr int kFusedMaxU = 64;
 constexpr int kChainFusedMaxU = 32;
 constexpr int kChainFusedMaxM = 1;
+constexpr int kChainFusedManyU = 1;
 // Output chunk of the generic direct tile kernel (U >= kDirectJ).
 constexpr int kDirectJ = 16;
 
