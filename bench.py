@@ -161,6 +161,58 @@ def launch_bytes(name, U, w):
     return tile_cols + 8 * (U + 1) * md
 
 
+def generation_bytes(w):
+    """Algorithmic HBM bytes of one whole generation of the fixed-filter path
+    (teacher-forced, or the closed loop, whose chain reads x_t in place of
+    y_t): per position the red cell (16 B per column) and the gray tile of
+    i = t+1 as launch_bytes counts it, with the library's default kind per U
+    (direct lags up to U = 32, and U = 64 below 2^14 columns; cached spectra
+    above) and the destination clipped at L."""
+    cols = w.M * w.B * w.D
+    md = w.M * w.D
+    dmax = 64 if cols < (1 << 14) else 32
+    total = 0
+    for t in range(w.L):
+        total += 16 * cols
+        i = t + 1
+        if i >= w.L:
+            continue
+        U = i & -i
+        total += (4 * (U - 1) + 8 * min(U, w.L - i)) * cols
+        total += (4 * (2 * U - 1) if U <= dmax else 8 * (U + 1)) * md
+    return total
+
+
+def dd_generation_bytes(w):
+    """Algorithmic HBM bytes of one generation with data-dependent filters
+    (Alg. 5, every power of two U dividing t+1): per position the red cell
+    reads y_t, rho_t and acc_t, writes z_t and stores y_t and rho_t (24 B per
+    column); a tile with 2U < t+1 reads its four blocks y[U,2U), rho[t-U+1, t],
+    rho[U,2U) and y[t-U+1, t] (16U B), the square one of t+1 = 2U its two
+    (8U B), and each reads and writes its destination rows acc[t+1, t+2U)
+    clipped at L (8 B per row)."""
+    cols = w.M * w.B * w.D
+    total = 0
+    for t in range(w.L):
+        total += 24 * cols
+        n = t + 1
+        U = 1
+        while 2 * U <= n:
+            if n % U == 0:
+                rows = min(t + 2 * U, w.L) - n
+                if rows > 0:
+                    total += ((16 if 2 * U < n else 8) * U + 8 * rows) * cols
+            U *= 2
+    return total
+
+
+def generation_roofline(nbytes, ms):
+    """A whole generation's algorithmic bytes against its measured time."""
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    return {"algorithmic_GB": round(nbytes / 1e9, 3), "GB_s": round(gbs, 1),
+            "frac_of_8TB_s": round(gbs / HBM_PEAK_GBS, 4)}
+
+
 # Sources of the kernels a counter run of the timed region executes, and of
 # their dispatch (the data-dependent, synthetic-model and column-chunk
 # kernels never run there).
@@ -718,6 +770,15 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
+    # every generation-shaped leg against its algorithmic bytes
+    gen = generation_bytes(w)
+    out["generation"] = generation_roofline(gen, ms)
+    if closed:
+        closed["generation"] = generation_roofline(gen, closed["ms_per_step"])
+    if half:
+        half["generation"] = generation_roofline(gen, half["ms_per_step"])
+    if dd:
+        dd["generation"] = generation_roofline(dd_generation_bytes(w), dd["ms_per_step"])
     if levels:
         out["per_level_us"] = levels
     if closed:

@@ -186,3 +186,31 @@ def test_trace_summary_names_its_file_and_reports_block_launches(tmp_path, monke
     assert f"{1024 / 3:.2f} positions per launch" in out
     assert f"{36 / 1024:.3f} us of block launch per position" in out
     assert not (tmp_path / "profiles" / "kernels_m1b1d16l1k.txt").exists()
+
+
+def test_generation_bytes_hand_counted():
+    """L = 4, one column: red cells 4 x 16 B; tiles i = 1 (U = 1: 8 B of
+    destination, lag 1), i = 2 (U = 2: one more input, 2 destination rows,
+    lags 1..3), i = 3 (U = 1).  28 + 48 + 28 + 16 = 120 B."""
+    w = datagen.Workload("tiny", 1, 1, 1, 4, decay=1.0, seed=0)
+    assert bench.generation_bytes(w) == 120
+    # the per-launch figures summed over the positions of a power-of-two run
+    w = datagen.Workload("small", 2, 3, 5, 64, decay=1.0, seed=0)
+    per = sum(bench.launch_bytes("fused", (t + 1) & -(t + 1), w) for t in range(w.L - 1))
+    assert bench.generation_bytes(w) == per + bench.launch_bytes("fused", 0, w)
+
+
+def test_dd_generation_bytes_hand_counted():
+    """L = 4, one column: red cells 4 x 24 B; t = 1 the square of U = 1
+    (two inputs, destination row 2: 16 B); t = 2 the tile of U = 1 (four
+    inputs, destination row 3: 24 B); t = 3 tiles whose rows lie past L
+    (nothing).  96 + 16 + 24 = 136 B."""
+    w = datagen.Workload("tiny", 1, 1, 1, 4, decay=1.0, seed=0)
+    assert bench.dd_generation_bytes(w) == 136
+    w2 = datagen.Workload("tiny2", 2, 3, 5, 4, decay=1.0, seed=0)
+    assert bench.dd_generation_bytes(w2) == 136 * 30
+
+
+def test_generation_roofline_arithmetic():
+    r = bench.generation_roofline(8e9, 2.0)     # 8 GB in 2 ms
+    assert r == {"algorithmic_GB": 8.0, "GB_s": 4000.0, "frac_of_8TB_s": 0.5}

@@ -6,7 +6,9 @@ of the result relies on: the metric, the step and warm-up counts, a value
 consistent with ms_per_step, the roofline object of the dominant launch (its
 achieved rate equal to its bytes over its duration, its fraction equal to
 achieved over peak) and the CPU baseline (the oracle, with its core count
-and sample)."""
+and sample), and the whole-generation figures of the timed region and
+the generation-shaped legs (their GB/s equal to the algorithmic bytes of a
+generation over its time)."""
 import json
 import os
 import subprocess
@@ -14,6 +16,8 @@ import sys
 
 import pytest
 
+import bench
+import datagen
 from gpu_harness import say
 
 pytestmark = pytest.mark.gpu
@@ -51,4 +55,13 @@ def test_bench_json_line_contract():
     assert cpu["kind"] == "oracle" and cpu["cores"] >= 1 and cpu["value"] > 0 and cpu["sample"]
     for leg in ("closed_loop", "prefill", "half_state", "data_dependent", "synthetic_model"):
         assert leg in d, leg
+    # whole generations against their algorithmic bytes
+    w = datagen.WORKLOADS["m1b1d16l1k"]
+    for obj, nbytes in ((d, bench.generation_bytes(w)), (d["closed_loop"], bench.generation_bytes(w)),
+                        (d["half_state"], bench.generation_bytes(w)),
+                        (d["data_dependent"], bench.dd_generation_bytes(w))):
+        g = obj["generation"]
+        gbs = nbytes / (obj["ms_per_step"] * 1e-3) / 1e9
+        assert abs(g["GB_s"] - gbs) <= 1e-3 * gbs + 0.1
+        assert abs(g["frac_of_8TB_s"] - gbs / 8000.0) <= 1e-4
     say(f"  {d['value']:.0f} tokens/s, dominant {rf['kernel']} ({rf['bound']})")
