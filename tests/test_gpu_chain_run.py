@@ -37,6 +37,8 @@ CASES = [
     ((2, 2, 24, 1200), {"half_state": 1}),                          # one position at a time
     ((34, 1, 8, 300), None),                                        # more layers than one launch takes
     ((1, 2, 4100, 200), None),                                      # more columns than one launch takes
+    ((2, 1, 8, 1), None),                                           # one position, no tile
+    ((1, 3, 8, 33), None),                                          # a last block of one position
 ]
 
 
