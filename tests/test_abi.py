@@ -237,6 +237,8 @@ def test_null_context_calls():
     assert lib.lcsm_advance(None) == lcsm.LCSM_EINVAL
     assert lib.lcsm_reset(None) == lcsm.LCSM_EINVAL
     assert lib.lcsm_run(None, 1, fake, 0, fake, 0) == lcsm.LCSM_EINVAL
+    assert lib.lcsm_run_chain(None, 1, fake, 0, fake, 0) == lcsm.LCSM_EINVAL
+    assert lib.lcsm_run_noalloc(None, 1, fake, 0, fake, 0) == lcsm.LCSM_EINVAL
     t = ctypes.c_int()
     assert lib.lcsm_position(None, ctypes.byref(t)) == lcsm.LCSM_EINVAL
     i, U, n, k = (ctypes.c_int() for _ in range(4))
