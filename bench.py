@@ -519,6 +519,17 @@ def committed_counters(kernel, U, w):
     return {"source": f"profiles/counters_{w.name}.txt", "kernels": got} if got else None
 
 
+def limiter_of(counters, valu_busy=60.0):
+    """Per kernel of a launch's committed counters: "vector ALU" where the
+    vector ALUs issue at least valu_busy percent of the time, else "memory"
+    (the matrix cores are idle in every mixer kernel)."""
+    if not counters:
+        return None
+    return {k: ("vector ALU" if v.get("VALUBusy", 0.0) >= valu_busy else "memory")
+            + f" (VALUBusy {v.get('VALUBusy', 0.0):.1f} %)"
+            for k, v in counters["kernels"].items()}
+
+
 def sweep_summary(args):
     """Per tile size, the per-launch time and algorithmic GB/s of every tile
     kind a sweep measured: DIR/sweep_<label>.json are bench outputs, each
@@ -705,6 +716,7 @@ def main():
         # and matrix-core busy, occupancy), when taken on these sources
         kname, kU = roofline["kernel"].split(" U=")
         roofline["counters"] = committed_counters(kname, int(kU), w)
+        roofline["limiter"] = limiter_of(roofline["counters"])
 
     def release():
         # each leg's contexts hold tens of GB; give torch's cached blocks back

@@ -214,3 +214,11 @@ def test_dd_generation_bytes_hand_counted():
 def test_generation_roofline_arithmetic():
     r = bench.generation_roofline(8e9, 2.0)     # 8 GB in 2 ms
     assert r == {"algorithmic_GB": 8.0, "GB_s": 4000.0, "frac_of_8TB_s": 0.5}
+
+
+def test_limiter_of_classifies_by_vector_alu_busy():
+    c = {"source": "x", "kernels": {"k_cm_tile<2048>": {"VALUBusy": 87.2}, "k_cm_yin4": {"VALUBusy": 6.9}}}
+    got = bench.limiter_of(c)
+    assert got["k_cm_tile<2048>"].startswith("vector ALU") and "87.2" in got["k_cm_tile<2048>"]
+    assert got["k_cm_yin4"].startswith("memory")
+    assert bench.limiter_of(None) is None
