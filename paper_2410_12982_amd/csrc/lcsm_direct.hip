@@ -359,6 +359,8 @@ __global__ __launch_bounds__(64 * (1 + (kChainBlockMaxM + 1) / 2)) void k_chain_
   auto tile_of = [&](int p) {
     return p >= r0 && p < r1 && p + 1 < W && b + p + 1 < L && (p + 1 < r1 || tile_last);
   };
+  // ring slabs of the current position's z and of the next position's x
+  int zsl = zs0 % zring, xsl = (xs0 + 1) % xring;
   auto position = [&](auto rc) {
     constexpr int r = decltype(rc)::value;
     if (r < r0 || r >= r1) return;
@@ -366,18 +368,22 @@ __global__ __launch_bounds__(64 * (1 + (kChainBlockMaxM + 1) / 2)) void k_chain_
     if (has) {
       abuf[m][col] = v[r];
       xbuf[m][col] = xn;
-      if (r + 1 < r1) xn = x[(size_t)((xs0 + t + 1 - t0) % xring) * xst + xoff];
+      if (r + 1 < r1) xn = x[(size_t)xsl * xst + xoff];
+      xsl = xsl + 1 == xring ? 0 : xsl + 1;
     }
     chain_block_sync();
     if (wv == 0) {
       if (lane < NC) {
-        float* zq = z + (size_t)((zs0 + t - t0) % zring) * zst + c;
+        float* zq = z + (size_t)zsl * zst + c;
         float* Sq = S + (size_t)t * rs + c;
         const size_t ls = (size_t)SL * BD;
+        // layer q's inputs read two layers ahead of the chain
+        const int q1 = M > 1 ? 1 : 0;
         float xv = xbuf[0][col], h0 = h0buf[0][col], av = abuf[0][col];
+        float xv1 = xbuf[q1][col], h01 = h0buf[q1][col], av1 = abuf[q1][col];
         for (int q = 0; q < M; ++q) {
-          const int qn = q + 1 < M ? q + 1 : q;
-          const float xv1 = xbuf[qn][col], h01 = h0buf[qn][col], av1 = abuf[qn][col];
+          const int qn = q + 2 < M ? q + 2 : M - 1;
+          const float xv2 = xbuf[qn][col], h02 = h0buf[qn][col], av2 = abuf[qn][col];
           const float yv = (q == 0 && t == 0) ? xv : fmaf(0.5f, chain_tanh(zl), xv);
           const float zv = fmaf(h0, yv, av);
           if (live) {
@@ -389,8 +395,12 @@ __global__ __launch_bounds__(64 * (1 + (kChainBlockMaxM + 1) / 2)) void k_chain_
           xv = xv1;
           h0 = h01;
           av = av1;
+          xv1 = xv2;
+          h01 = h02;
+          av1 = av2;
         }
       }
+      zsl = zsl + 1 == zring ? 0 : zsl + 1;
     } else if (has && r >= 1) {
       // the rest of the previous position's tile, beside the chain
       if constexpr (r >= 1) {
