@@ -257,14 +257,18 @@ __global__ __launch_bounds__(kThreads) void k_chain_fused(const float* __restric
 // b + k of its column (y for positions already taken, the accumulator
 // otherwise) and the lags 1 .. kChainBlockW - 1 of its channel.  Per
 // position t = b + r: the layer waves hand acc_t and x_t over in LDS
-// (fetching x_{t+1}); wave 0 computes the chain and stores z_t and y_t; the
-// layer waves take y_t from LDS and do the tile of i = t+1 in registers,
-// with the arithmetic of k_step_fused<U, false> (per output, the fmaf chain
-// over the U inputs in increasing order, then added to the accumulator), so
-// the results equal the per-position steps bit for bit.  The two barriers
-// per position order LDS only: no wave reads global memory another wave of
-// the launch writes.  At the end the accumulator rows at and after t1 (a
-// stretch cut before its block ends) go back to the state.
+// (fetching x_{t+1}); wave 0 computes the chain and leaves z_t and y_t in
+// LDS, while the layer waves add the other output rows of the previous
+// position's tile; then each layer wave stores its layers' z_t and y_t
+// (W0S, for at most kChainBlockWave0StoreM layers: wave 0 stores them as
+// it goes instead) and computes the first output row of the tile of i = t+1 (the next
+// accumulator).  The tile arithmetic is that of k_step_fused<U, false> (per
+// output, the fmaf chain over the U inputs in increasing order, then added
+// to the accumulator), so the results equal the per-position steps bit for
+// bit.  The two barriers per position order LDS only: no wave reads global
+// memory another wave of the launch writes.  At the end the accumulator rows
+// at and after t1 (a stretch cut before its block ends) go back to the state.
+
 // f(std::integral_constant<int, 0>{}), ..., f(std::integral_constant<int, N-1>{}).
 template <class F, int... R>
 __device__ __forceinline__ void static_for_impl(F& f, std::integer_sequence<int, R...>) {
@@ -310,6 +314,7 @@ __device__ __forceinline__ void chain_block_rest_rows(float (&v)[kChainBlockW],
   }
 }
 
+template <bool W0S>
 __global__ __launch_bounds__(64 * (1 + (kChainBlockMaxM + 1) / 2)) void k_chain_block(
     const float* __restrict__ x, size_t xst, int xring, int xs0, float* __restrict__ z,
     size_t zst, int zring, int zs0, float* __restrict__ S, const float* __restrict__ Hf,
@@ -319,6 +324,7 @@ __global__ __launch_bounds__(64 * (1 + (kChainBlockMaxM + 1) / 2)) void k_chain_
   __shared__ float xbuf[kChainBlockMaxM][NC];
   __shared__ float abuf[kChainBlockMaxM][NC];
   __shared__ float ybuf[kChainBlockMaxM][NC];
+  __shared__ float zbuf[kChainBlockMaxM][NC];
   __shared__ float h0buf[kChainBlockMaxM][NC];
   const int lane = (int)threadIdx.x & 63;
   const int wv = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
@@ -386,9 +392,13 @@ __global__ __launch_bounds__(64 * (1 + (kChainBlockMaxM + 1) / 2)) void k_chain_
           const float xv2 = xbuf[qn][col], h02 = h0buf[qn][col], av2 = abuf[qn][col];
           const float yv = (q == 0 && t == 0) ? xv : fmaf(0.5f, chain_tanh(zl), xv);
           const float zv = fmaf(h0, yv, av);
-          if (live) {
-            zq[(size_t)q * BD] = zv;
-            Sq[(size_t)q * ls] = yv;
+          if constexpr (W0S) {
+            if (live) {
+              zq[(size_t)q * BD] = zv;
+              Sq[(size_t)q * ls] = yv;
+            }
+          } else {
+            zbuf[q][col] = zv;
           }
           ybuf[q][col] = yv;
           zl = zv;
@@ -400,7 +410,6 @@ __global__ __launch_bounds__(64 * (1 + (kChainBlockMaxM + 1) / 2)) void k_chain_
           av1 = av2;
         }
       }
-      zsl = zsl + 1 == zring ? 0 : zsl + 1;
     } else if (has && r >= 1) {
       // the rest of the previous position's tile, beside the chain
       if constexpr (r >= 1) {
@@ -409,11 +418,19 @@ __global__ __launch_bounds__(64 * (1 + (kChainBlockMaxM + 1) / 2)) void k_chain_
     }
     chain_block_sync();
     if (has) {
-      v[r] = ybuf[m][col];
+      const float yv = ybuf[m][col];
+      if constexpr (!W0S) {
+        if (live) {
+          z[(size_t)zsl * zst + (size_t)m * BD + c] = zbuf[m][col];
+          Sc[(size_t)t * rs] = yv;
+        }
+      }
+      v[r] = yv;
       if constexpr (r + 1 < W) {
         if (tile_of(r)) chain_block_first_row<r>(v, hh);
       }
     }
+    zsl = zsl + 1 == zring ? 0 : zsl + 1;
   };
   static_for<W>(position);
   // the rest of the last position's tile
@@ -643,9 +660,13 @@ hipError_t launch_chain_block(const float* x, size_t xst, int xring, int xs0, fl
   if (s.M > kChainBlockMaxM || t1 <= t0 || (t0 & ~(kChainBlockW - 1)) != ((t1 - 1) & ~(kChainBlockW - 1)))
     return hipErrorInvalidValue;
   const int nw = 1 + (s.M + 1) / 2;
-  hipLaunchKernelGGL(k_chain_block, dim3((unsigned)((s.BD + kChainBlockCols - 1) / kChainBlockCols)),
-                     dim3((unsigned)(64 * nw)), 0, st, x, xst, xring, xs0, z, zst, zring, zs0, S, Hf,
-                     prev, s.M, s.L, s.SL, s.BD, s.D, t0, t1, tile_last ? 1 : 0);
+  const dim3 grid((unsigned)((s.BD + kChainBlockCols - 1) / kChainBlockCols)), block((unsigned)(64 * nw));
+  if (s.M <= kChainBlockWave0StoreM)
+    hipLaunchKernelGGL(k_chain_block<true>, grid, block, 0, st, x, xst, xring, xs0, z, zst, zring,
+                       zs0, S, Hf, prev, s.M, s.L, s.SL, s.BD, s.D, t0, t1, tile_last ? 1 : 0);
+  else
+    hipLaunchKernelGGL(k_chain_block<false>, grid, block, 0, st, x, xst, xring, xs0, z, zst, zring,
+                       zs0, S, Hf, prev, s.M, s.L, s.SL, s.BD, s.D, t0, t1, tile_last ? 1 : 0);
   return hipGetLastError();
 }
 

@@ -64,6 +64,7 @@ hipError_t launch_chain_fused(const float* x, float* z, float* S, const float* H
 // serial chain of each workgroup makes one launch per position faster).
 constexpr int kChainBlockW = 32;
 constexpr int kChainBlockMaxM = 30;
+constexpr int kChainBlockWave0StoreM = 4;  // up to this many layers the chain wave stores z and y
 constexpr int kChainBlockCols = 32;
 constexpr int kChainBlockMaxGroups = 256;
 hipError_t launch_chain_block(const float* x, size_t xst, int xring, int xs0, float* z,
