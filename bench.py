@@ -394,7 +394,7 @@ def trace_summary(args):
     for k, v in sorted(agg.items(), key=lambda kv: -sum(kv[1]))[:30]:
         lines.append(f"{len(v):9d} {sum(v) / 1e3:12.2f} {sum(v) / len(v):10.2f} "
                      f"{100 * sum(v) / total:6.2f}  {k}")
-    blk = agg.get("k_chain_block")
+    blk = [d for k, v in agg.items() if k.split("<")[0] == "k_chain_block" for d in v]
     if blk:
         lines.append(f"# chained-step block launches (the closed loop's positions inside blocks of 32): "
                      f"{len(blk)} launches, {sum(blk) / len(blk):.2f} us each on average; with one "

@@ -160,7 +160,8 @@ def test_group_kernels_picks_the_dispatches_of_one_launch():
 
 def test_trace_summary_names_its_file_and_reports_block_launches(tmp_path, monkeypatch):
     """A closed-loop trace is written under its own name, with the chained-step
-    block launches per launch and per position of the one generation."""
+    block launches (every instantiation) per launch and per position of the
+    one generation."""
     import types
     csrc = os.path.join(ROOT, "paper_2410_12982_amd", "csrc")
     fake = tmp_path / "paper_2410_12982_amd" / "csrc"
@@ -173,8 +174,9 @@ def test_trace_summary_names_its_file_and_reports_block_launches(tmp_path, monke
     tr.mkdir()
     rows = ["Kernel_Name,Start_Timestamp,End_Timestamp"]
     t = 1000
-    for us in (10, 12, 14):
-        rows.append(f'"lcsm::(anonymous namespace)::k_chain_block(float const*, int)",{t},{t + us * 1000}')
+    for us, tpl in ((10, ""), (12, "<false>"), (14, "<true>")):
+        rows.append(f'"void lcsm::(anonymous namespace)::k_chain_block{tpl}(float const*, int)",{t},'
+                    f'{t + us * 1000}')
         t += 100000
     rows.append(f'"void lcsm::(anonymous namespace)::k_step_fused<32, false>(float const*)",{t},{t + 5000}')
     (tr / "run_kernel_trace.csv").write_text("\n".join(rows) + "\n")
