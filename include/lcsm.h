@@ -150,9 +150,9 @@ int lcsm_step(lcsm_ctx* ctx, const float* y_t, float* z_t);
  *   y^0_0 = x^0_0,  y^0_t = 0.5 tanh(z^{M-1}_{t-1}) + x^0_t  (t >= 1),
  *   y^m_t = 0.5 tanh(z^{m-1}_t) + x^m_t                      (m >= 1).
  *   x_t  device [M][B][D] additive inputs;  z_t  device [M][B][D] outputs.
- * tanh is evaluated as 1 - 2/(1 + e^{2|x|}) with the sign of x (absolute
- * error below 2.4e-7).  The last layer's z_{t-1} is kept inside the
- * context.  Same errors as lcsm_step. */
+ * The rule is evaluated as y = (x + 1/2) - 1/(1 + e^{2z}), the same
+ * function (absolute error below 3.3e-7 for |x| <= 3).  The last layer's
+ * z_{t-1} is kept inside the context.  Same errors as lcsm_step. */
 int lcsm_step_chain(lcsm_ctx* ctx, const float* x_t, float* z_t);
 
 /* Red cell of one layer at the current position (the inner loop of Alg. 2 /

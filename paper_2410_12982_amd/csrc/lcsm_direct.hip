@@ -138,26 +138,19 @@ __global__ __launch_bounds__(kThreads) void k_step_fused(const float* __restrict
   }
 }
 
-// tanh of the chain's input rule, without branches: tanh|x| = 1 - 2/(1 + e^{2|x|})
-// from the hardware base-2 exponential and reciprocal (each within about one
-// ulp), the sign copied from x.  Absolute error below 2.4e-7 for every x (an
-// fp32 model of the formula with both hardware results off by one ulp either
-// way, against fp64 tanh, on 2.4M points over [-20, 20] and 1e-8 .. 32);
-// +-inf give +-1, NaN stays NaN.
-__device__ __forceinline__ float chain_tanh(float x) {
-  const float e = __builtin_amdgcn_exp2f(2.8853900817779268f * fabsf(x));  // 2 log2(e) |x|
-  return copysignf(fmaf(-2.f, __builtin_amdgcn_rcpf(1.f + e), 1.f), x);
+// The chain's input rule y = x + 0.5 tanh(z), evaluated as
+// (x + 1/2) - 1/(1 + e^{2z}) (the same function: 0.5 tanh(z) = 1/2 -
+// 1/(1 + e^{2z})) from the hardware base-2 exponential and reciprocal (each
+// within about one ulp): no branch, and x + 1/2 is off the serial chain.
+// Absolute error below 3.3e-7 for |x| <= 3 (an fp32 model of these steps
+// with both hardware results off by one ulp either way, against fp64, on
+// 1.2M points with z over [-20, 20] and 1e-8 .. 32 of either sign); z = +inf
+// gives x + 1/2, z = -inf x - 1/2, NaN stays NaN.
+__device__ __forceinline__ float chain_y(float x, float z) {
+  const float e = __builtin_amdgcn_exp2f(2.8853900817779268f * z);  // e^{2z}
+  return (x + 0.5f) - __builtin_amdgcn_rcpf(1.f + e);
 }
 
-// The chained input rule (lcsm_step_chain) fused with red cells and, for
-// 1 <= U <= kChainFusedMaxU, the gray tiles.  One thread per (b, d) column walks
-// the layers in order, since y^m_t depends on z^{m-1}_t.  Only the arithmetic
-// is sequential: the layers' loads (x, accumulator, h_0 and the tile's inputs,
-// lags and destination rows) do not depend on the chain, so they are issued
-// K layers at a time ahead of that chunk's stores, and a step costs about
-// M/K memory round trips instead of M.
-// Largest chunk for a tile side U (bounds the registers the chunk's loads
-// take); the launch uses the largest power of two not above it or M.
 template <int U>
 struct ChainChunk {
   static constexpr int value = U <= 2 ? 8 : (U <= 8 ? 4 : (U <= 16 ? 2 : 1));
@@ -215,7 +208,7 @@ __global__ __launch_bounds__(kThreads) void k_chain_fused(const float* __restric
       const int m = m0 + kk;
       if (m < M) {
         float* col = S + (size_t)m * SL * BD + c;
-        const float yv = (m == 0 && t == 0) ? xv[kk] : fmaf(0.5f, chain_tanh(zl), xv[kk]);
+        const float yv = (m == 0 && t == 0) ? xv[kk] : chain_y(xv[kk], zl);
         const float zv = fmaf(h0[kk], yv, acc[kk]);
         z[(size_t)m * BD + c] = zv;
         col[(size_t)t * rs] = yv;
@@ -321,10 +314,8 @@ __global__ __launch_bounds__(64 * (1 + (kChainBlockMaxM + 1) / 2)) void k_chain_
     float* __restrict__ prev, int M, int L, int SL, int BD, int D, int t0, int t1,
     int tile_last) {
   constexpr int NC = kChainBlockCols, W = kChainBlockW;
-  __shared__ float xbuf[kChainBlockMaxM][NC];
-  __shared__ float abuf[kChainBlockMaxM][NC];
-  __shared__ float ybuf[kChainBlockMaxM][NC];
-  __shared__ float zbuf[kChainBlockMaxM][NC];
+  __shared__ float2 axbuf[kChainBlockMaxM][NC];  // (acc_t, x_t)
+  __shared__ float2 yzbuf[kChainBlockMaxM][NC];  // (y_t, z_t)
   __shared__ float h0buf[kChainBlockMaxM][NC];
   const int lane = (int)threadIdx.x & 63;
   const int wv = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
@@ -372,8 +363,7 @@ __global__ __launch_bounds__(64 * (1 + (kChainBlockMaxM + 1) / 2)) void k_chain_
     if (r < r0 || r >= r1) return;
     const int t = b + r;
     if (has) {
-      abuf[m][col] = v[r];
-      xbuf[m][col] = xn;
+      axbuf[m][col] = make_float2(v[r], xn);
       if (r + 1 < r1) xn = x[(size_t)xsl * xst + xoff];
       xsl = xsl + 1 == xring ? 0 : xsl + 1;
     }
@@ -385,29 +375,27 @@ __global__ __launch_bounds__(64 * (1 + (kChainBlockMaxM + 1) / 2)) void k_chain_
         const size_t ls = (size_t)SL * BD;
         // layer q's inputs read two layers ahead of the chain
         const int q1 = M > 1 ? 1 : 0;
-        float xv = xbuf[0][col], h0 = h0buf[0][col], av = abuf[0][col];
-        float xv1 = xbuf[q1][col], h01 = h0buf[q1][col], av1 = abuf[q1][col];
+        float2 ax = axbuf[0][col], ax1 = axbuf[q1][col];
+        float h0 = h0buf[0][col], h01 = h0buf[q1][col];
         for (int q = 0; q < M; ++q) {
           const int qn = q + 2 < M ? q + 2 : M - 1;
-          const float xv2 = xbuf[qn][col], h02 = h0buf[qn][col], av2 = abuf[qn][col];
-          const float yv = (q == 0 && t == 0) ? xv : fmaf(0.5f, chain_tanh(zl), xv);
+          const float2 ax2 = axbuf[qn][col];
+          const float h02 = h0buf[qn][col];
+          const float xv = ax.y, av = ax.x;
+          const float yv = (q == 0 && t == 0) ? xv : chain_y(xv, zl);
           const float zv = fmaf(h0, yv, av);
           if constexpr (W0S) {
             if (live) {
               zq[(size_t)q * BD] = zv;
               Sq[(size_t)q * ls] = yv;
             }
-          } else {
-            zbuf[q][col] = zv;
           }
-          ybuf[q][col] = yv;
+          yzbuf[q][col] = make_float2(yv, zv);
           zl = zv;
-          xv = xv1;
+          ax = ax1;
           h0 = h01;
-          av = av1;
-          xv1 = xv2;
+          ax1 = ax2;
           h01 = h02;
-          av1 = av2;
         }
       }
     } else if (has && r >= 1) {
@@ -418,10 +406,11 @@ __global__ __launch_bounds__(64 * (1 + (kChainBlockMaxM + 1) / 2)) void k_chain_
     }
     chain_block_sync();
     if (has) {
-      const float yv = ybuf[m][col];
+      const float2 yz = yzbuf[m][col];
+      const float yv = yz.x;
       if constexpr (!W0S) {
         if (live) {
-          z[(size_t)zsl * zst + (size_t)m * BD + c] = zbuf[m][col];
+          z[(size_t)zsl * zst + (size_t)m * BD + c] = yz.y;
           Sc[(size_t)t * rs] = yv;
         }
       }
