@@ -109,7 +109,12 @@ __global__ __launch_bounds__(kThreads) void k_step_fused(const float* __restrict
   // values of the larger tiles held at once the compiler issues the loads in
   // small groups instead.
   constexpr bool PIN = U <= 16;
-  if constexpr (RED) asm volatile("" : "+v"(acc), "+v"(h0));
+  // y_t as well without the red cell: with nothing pinned there, the tile of
+  // U = 32 issued its lag loads one round trip each
+  if constexpr (RED)
+    asm volatile("" : "+v"(acc), "+v"(h0));
+  else
+    asm volatile("" : "+v"(yt));
   if constexpr (U > 0 && PIN) {
 #pragma unroll
     for (int l = 1; l < UJ + U; ++l) asm volatile("" : "+v"(hh[l]));
